@@ -1,0 +1,226 @@
+"""CPU oracle for the QuantWM hot path: TEST INFRASTRUCTURE ONLY.
+
+Thin ctypes wrappers over ``libquantwm_oracle.so`` (plain C in
+``quantwm_oracle.c``). Only ``tests/``, the package's ``smoke()`` check and the
+benchmark's CPU-baseline leg may import this module; the product path never
+does. Arrays are numpy float32 ``[B, N, H, d]`` holding values exact in the
+workload's element type; method-level tables are float32 too.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(_HERE, "quantwm_oracle.c")
+LIB = os.path.join(_HERE, "libquantwm_oracle.so")
+CFLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC", "-shared",
+          "-std=c11", "-Wall", "-Wextra"]
+
+
+def build() -> str:
+    tmp = LIB + ".tmp"
+    subprocess.run(["gcc", *CFLAGS, "-o", tmp, SRC, "-lm"], check=True)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+class OraCfg(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int), ("heads", ctypes.c_int), ("head_dim", ctypes.c_int),
+                ("n_centroids", ctypes.c_int), ("group_size", ctypes.c_int),
+                ("rank", ctypes.c_int), ("top_m", ctypes.c_int),
+                ("capacity", ctypes.c_longlong), ("table_bf16", ctypes.c_int)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            raise RuntimeError(f"oracle library missing: {LIB} (run __graft_entry__.build())")
+        _lib = ctypes.CDLL(LIB)
+        _lib.ora_cache_bytes.restype = ctypes.c_longlong
+        _lib.ora_round_bf16.restype = ctypes.c_double
+        _lib.ora_round_bf16.argtypes = [ctypes.c_double]
+        _lib.ora_round_f16.restype = ctypes.c_double
+        _lib.ora_round_f16.argtypes = [ctypes.c_double]
+        _lib.ora_f16_bits.restype = ctypes.c_uint16
+        _lib.ora_f16_bits.argtypes = [ctypes.c_double]
+        _lib.ora_f16_value.restype = ctypes.c_double
+        _lib.ora_f16_value.argtypes = [ctypes.c_uint16]
+    return _lib
+
+
+def cfg_of(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, bf16) -> OraCfg:
+    return OraCfg(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, int(bf16))
+
+
+def cfg_from_workload(wl, capacity=None) -> OraCfg:
+    return cfg_of(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank,
+                  wl.top_m, wl.capacity if capacity is None else capacity, wl.dtype == "bf16")
+
+
+def _p(a, ct=ctypes.c_float):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.POINTER(ct))
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise RuntimeError(f"oracle {what} failed with status {rc}")
+
+
+def set_threads(n: int):
+    lib().ora_set_threads(int(n))
+
+
+def max_threads() -> int:
+    return int(lib().ora_max_threads())
+
+
+def cache_bytes(cfg: OraCfg) -> int:
+    return int(lib().ora_cache_bytes(ctypes.byref(cfg)))
+
+
+def token_bytes(cfg: OraCfg):
+    kb, vb = ctypes.c_int(), ctypes.c_int()
+    _check(lib().ora_token_bytes(ctypes.byref(cfg), ctypes.byref(kb), ctypes.byref(vb)), "token_bytes")
+    return kb.value, vb.value
+
+
+def round_bf16(x: float) -> float:
+    return lib().ora_round_bf16(float(x))
+
+
+def round_f16(x: float) -> float:
+    return lib().ora_round_f16(float(x))
+
+
+def f16_bits(x: float) -> int:
+    return int(lib().ora_f16_bits(float(x)))
+
+
+def f16_value(bits: int) -> float:
+    return lib().ora_f16_value(int(bits))
+
+
+def int2_group(x, mu):
+    x, mu = _f32(x), _f32(mu)
+    n = x.shape[0]
+    codes = np.zeros(n, np.uint8)
+    zp, sc = ctypes.c_uint8(), ctypes.c_uint16()
+    xhat = np.zeros(n, np.float32)
+    lib().ora_int2_group(_p(x), _p(mu), n, _p(codes, ctypes.c_uint8), ctypes.byref(zp),
+                         ctypes.byref(sc), _p(xhat))
+    return codes, int(zp.value), int(sc.value), xhat
+
+
+def qsac_assign(k, mu, w, group_size, top_m):
+    k, mu, w = _f32(k), _f32(mu), _f32(w)
+    kc, d = mu.shape
+    cand = np.zeros(max(kc, 1), np.int32)
+    z = lib().ora_qsac_assign(_p(k), _p(mu), _p(w), kc, d, group_size, top_m, _p(cand, ctypes.c_int))
+    return int(z), cand[: min(top_m, kc)].copy()
+
+
+def nearest(x, mu):
+    x, mu = _f32(x), _f32(mu)
+    return int(lib().ora_nearest(_p(x), _p(mu), mu.shape[0], mu.shape[1]))
+
+
+def eigh(a):
+    a = np.ascontiguousarray(a, dtype=np.float64)
+    n = a.shape[0]
+    lam = np.zeros(n)
+    vt = np.zeros((n, n))
+    _check(lib().ora_eigh(_p(a, ctypes.c_double), n, _p(lam, ctypes.c_double),
+                          _p(vt, ctypes.c_double)), "eigh")
+    return lam, vt
+
+
+def calibrate(cfg: OraCfg, q_hist, k_cal, v_cal, kmeans_iters):
+    """Returns (mu_k, mu_v, w, u_t, lam) as float32 arrays."""
+    B, H, d, K, r = cfg.batch, cfg.heads, cfg.head_dim, cfg.n_centroids, cfg.rank
+    q_hist = _f32(q_hist) if q_hist is not None else np.zeros((B, 0, H, d), np.float32)
+    k_cal, v_cal = _f32(k_cal), _f32(v_cal)
+    mu_k = np.zeros((B, H, K, d), np.float32)
+    mu_v = np.zeros((B, H, K, d), np.float32)
+    w = np.zeros((B, H, d), np.float32)
+    u_t = np.zeros((B, H, max(r, 0), d), np.float32)
+    lam = np.zeros((B, H, max(r, 0)), np.float32)
+    rc = lib().ora_calibrate(ctypes.byref(cfg), _p(q_hist), ctypes.c_longlong(q_hist.shape[1]),
+                             _p(k_cal), _p(v_cal), ctypes.c_longlong(k_cal.shape[1]), kmeans_iters,
+                             _p(mu_k), _p(mu_v), _p(w), _p(u_t), _p(lam))
+    _check(rc, "calibrate")
+    return mu_k, mu_v, w, u_t, lam
+
+
+def new_cache(cfg: OraCfg) -> np.ndarray:
+    return np.zeros(cache_bytes(cfg), np.uint8)
+
+
+def append(cfg: OraCfg, tables, cache, n_cached, k_new, v_new, diagnostics=False):
+    """Writes slots [n_cached, n_cached + n) in place; returns diagnostics if asked."""
+    mu_k, mu_v, w, u_t = (_f32(t) for t in tables[:4])
+    k_new, v_new = _f32(k_new), _f32(v_new)
+    B, n, H = k_new.shape[0], k_new.shape[1], k_new.shape[2]
+    M = min(cfg.top_m, cfg.n_centroids)
+    coef = np.zeros((B, H, n, max(cfg.rank, 1)), np.float32) if diagnostics else None
+    kid = np.zeros((B, H, n), np.int32) if diagnostics else None
+    vid = np.zeros((B, H, n), np.int32) if diagnostics else None
+    cand = np.zeros((B, H, n, M), np.int32) if diagnostics else None
+    rc = lib().ora_append(ctypes.byref(cfg), _p(mu_k), _p(mu_v), _p(w), _p(u_t),
+                          _p(cache, ctypes.c_uint8), ctypes.c_longlong(n_cached),
+                          _p(k_new), _p(v_new), ctypes.c_longlong(n), _p(coef),
+                          _p(kid, ctypes.c_int), _p(vid, ctypes.c_int), _p(cand, ctypes.c_int))
+    _check(rc, "append")
+    if diagnostics:
+        return {"coef": coef[..., : cfg.rank], "k_ids": kid, "v_ids": vid, "cand": cand}
+    return None
+
+
+def decode(cfg: OraCfg, tables, cache, b, h, n):
+    mu_k, mu_v = _f32(tables[0]), _f32(tables[1])
+    d, r = cfg.head_dim, cfg.rank
+    k0 = np.zeros((n, d)); v = np.zeros((n, d)); ch = np.zeros((n, max(r, 1)))
+    rc = lib().ora_decode(ctypes.byref(cfg), _p(mu_k), _p(mu_v), _p(cache, ctypes.c_uint8), b, h,
+                          ctypes.c_longlong(n), _p(k0, ctypes.c_double), _p(ch, ctypes.c_double),
+                          _p(v, ctypes.c_double))
+    _check(rc, "decode")
+    return k0, ch[:, :r], v
+
+
+def attend(cfg: OraCfg, tables, cache, n_cache, q, q_start, frame_tokens, rows=None,
+           coef_override=None, want_logits=False):
+    """rows: int array [n_rows, 3] of (b, h, i); default all rows.
+
+    Returns (out [n_rows, d] fp64, lse [n_rows], logits [n_rows, n_cache] or None).
+    """
+    mu_k, mu_v, _, u_t = (_f32(t) for t in tables[:4])
+    q = _f32(q)
+    B, n_q, H, d = q.shape
+    if rows is None:
+        rows = np.array([(b, h, i) for b in range(B) for h in range(H) for i in range(n_q)], np.int32)
+    rows = np.ascontiguousarray(rows, dtype=np.int32).reshape(-1, 3)
+    nr = rows.shape[0]
+    out = np.zeros((nr, d)); lse = np.zeros(nr)
+    logits = np.zeros((nr, n_cache)) if want_logits else None
+    co = _f32(coef_override) if coef_override is not None else None
+    rc = lib().ora_attend(ctypes.byref(cfg), _p(mu_k), _p(mu_v), _p(u_t), _p(cache, ctypes.c_uint8),
+                          ctypes.c_longlong(n_cache), _p(q), ctypes.c_longlong(n_q),
+                          ctypes.c_longlong(q_start), int(frame_tokens), _p(co), nr,
+                          _p(rows, ctypes.c_int), _p(out, ctypes.c_double), _p(lse, ctypes.c_double),
+                          _p(logits, ctypes.c_double))
+    _check(rc, "attend")
+    return out, lse, logits

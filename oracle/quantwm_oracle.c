@@ -1,0 +1,638 @@
+/*
+ * QuantWM CPU oracle: TEST INFRASTRUCTURE ONLY (see quantwm_oracle.h).
+ *
+ * Build: gcc -O2 -ffp-contract=off -fno-fast-math -fopenmp -shared -fPIC.
+ * Contraction stays off so that every a*b+c below is two roundings.
+ *
+ * Readings of the paper that this file takes (each listed in the design doc):
+ *  - The quantiser range is extended to contain 0, so the INT2 zero-point always
+ *    lies in [0, 3] and can be bit-packed (Eq. 2 with App. D.1).
+ *  - The residual is quantised with the stored (FP16-rounded) scale.
+ *  - A group whose stored scale is 0 keeps all codes 0 (reconstruction = centroid).
+ *  - Eq. 10's range R_g is the literal max - min, without the 0 extension.
+ *  - Ties: the lower centroid id wins; eigenvalue ties keep the original order;
+ *    each eigenvector's largest-magnitude entry is made positive.
+ *  - Values take the nearest centroid (w = 1, M = 1) and no PSAC (App. D.1).
+ *  - PSAC coefficients are INT8, symmetric, one FP16 scale per row (max|C|/127).
+ *  - Cold start (no historical Queries): w = 1 and U_r = 0, so PSAC stores zero
+ *    rows (Appendix on the initialisation of historical statistics).
+ *  - K-means: Lloyd on the calibration tokens, initial centroids at tokens
+ *    floor(i*N/Kc), empty clusters keep their centroid, centroids are rounded to
+ *    the table type after every update.
+ */
+#include "quantwm_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ---------------------------------------------------------------- formats */
+
+/* Round to a binary format with p significand bits (hidden bit included) whose
+ * smallest normal exponent is emin; below it the spacing stays 2^(emin-p+1). */
+static double round_format(double x, int p, int emin) {
+  if (x == 0.0 || !isfinite(x)) return x;
+  int e;
+  frexp(x, &e); /* |x| in [2^(e-1), 2^e) */
+  int lsb = (e - 1) - (p - 1);
+  if (lsb < emin - (p - 1)) lsb = emin - (p - 1);
+  return ldexp(nearbyint(ldexp(x, -lsb)), lsb); /* default mode: ties to even */
+}
+
+double ora_round_bf16(double x) { return round_format(x, 8, -126); }
+
+double ora_round_f16(double x) {
+  double r = round_format(x, 11, -14);
+  if (fabs(r) > 65504.0) r = copysign(INFINITY, r);
+  return r;
+}
+
+static double round_f32(double x) { return (double)(float)x; }
+
+static double round_table(const ora_cfg* c, double x) {
+  return c->table_bf16 ? ora_round_bf16(x) : round_f32(x);
+}
+
+uint16_t ora_f16_bits(double v) {
+  uint16_t s = signbit(v) ? 0x8000u : 0u;
+  double a = fabs(v);
+  if (a == 0.0) return s;
+  if (isinf(a)) return (uint16_t)(s | 0x7C00u);
+  if (a < ldexp(1.0, -14)) return (uint16_t)(s | (uint16_t)ldexp(a, 24)); /* subnormal */
+  int e;
+  frexp(a, &e);
+  int exp_field = (e - 1) + 15;
+  int mant = (int)(ldexp(a, -(e - 1)) * 1024.0) - 1024;
+  return (uint16_t)(s | (exp_field << 10) | mant);
+}
+
+double ora_f16_value(uint16_t bits) {
+  int s = bits >> 15, ef = (bits >> 10) & 31, m = bits & 1023;
+  double v;
+  if (ef == 0) v = ldexp((double)m, -24);
+  else if (ef == 31) v = m ? NAN : INFINITY;
+  else v = ldexp((double)(1024 + m), ef - 15 - 10);
+  return s ? -v : v;
+}
+
+/* ----------------------------------------------------------------- layout */
+
+typedef struct {
+  int d, ng, zpb, r;
+  int k_bytes, v_bytes;
+  long long slots; /* capacity rounded up to 64 */
+  long long k_codes, k_ids, k_zp, k_scale, k_coef, k_cscale;
+  long long v_codes, v_ids, v_zp, v_scale;
+  long long total;
+} layout;
+
+static long long up256(long long x) { return (x + 255) / 256 * 256; }
+
+static int valid_cfg(const ora_cfg* c) {
+  if (!c || c->batch < 1 || c->heads < 1 || c->head_dim < 4 || c->head_dim % 4) return 0;
+  if (c->group_size < 1 || c->head_dim % c->group_size) return 0;
+  if (c->n_centroids < 1 || c->n_centroids > 256) return 0;
+  if (c->rank < 0 || c->rank > c->head_dim) return 0;
+  if (c->top_m < 1 || c->capacity < 0) return 0;
+  return 1;
+}
+
+static layout make_layout(const ora_cfg* c) {
+  layout L;
+  L.d = c->head_dim;
+  L.ng = c->head_dim / c->group_size;
+  L.zpb = (L.ng + 3) / 4;
+  L.r = c->rank;
+  L.slots = (c->capacity + 63) / 64 * 64;
+  long long bh = (long long)c->batch * c->heads, n = bh * L.slots, off = 0;
+#define SECTION(field, per_token) \
+  do { L.field = off; off = up256(off + n * (long long)(per_token)); } while (0)
+  SECTION(k_codes, L.d / 4);
+  SECTION(k_ids, 1);
+  SECTION(k_zp, L.zpb);
+  SECTION(k_scale, 2 * L.ng);
+  SECTION(k_coef, L.r);
+  SECTION(k_cscale, L.r > 0 ? 2 : 0);
+  SECTION(v_codes, L.d / 4);
+  SECTION(v_ids, 1);
+  SECTION(v_zp, L.zpb);
+  SECTION(v_scale, 2 * L.ng);
+#undef SECTION
+  L.total = off;
+  L.v_bytes = L.d / 4 + 1 + L.zpb + 2 * L.ng;
+  L.k_bytes = L.v_bytes + (L.r > 0 ? L.r + 2 : 0);
+  return L;
+}
+
+long long ora_cache_bytes(const ora_cfg* cfg) {
+  if (!valid_cfg(cfg)) return -1;
+  return make_layout(cfg).total;
+}
+
+int ora_token_bytes(const ora_cfg* cfg, int* k_bytes, int* v_bytes) {
+  if (!valid_cfg(cfg)) return -1;
+  layout L = make_layout(cfg);
+  *k_bytes = L.k_bytes;
+  *v_bytes = L.v_bytes;
+  return 0;
+}
+
+static void put16(uint8_t* p, uint16_t v) { p[0] = (uint8_t)(v & 255); p[1] = (uint8_t)(v >> 8); }
+static uint16_t get16(const uint8_t* p) { return (uint16_t)(p[0] | (p[1] << 8)); }
+
+/* ----------------------------------------------------- INT2 residual (O3) */
+
+static float clampf(float x, float lo, float hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+void ora_int2_group(const float* x, const float* mu, int n, uint8_t* codes,
+                    uint8_t* zero_point, uint16_t* scale_f16, float* xhat) {
+  /* Eq. 3: residual against the assigned centroid. */
+  float r[256];
+  float lo = 0.0f, hi = 0.0f; /* range extended to contain 0 */
+  for (int c = 0; c < n; ++c) {
+    r[c] = x[c] - mu[c];
+    if (r[c] < lo) lo = r[c];
+    if (r[c] > hi) hi = r[c];
+  }
+  /* Eq. 2 with q_min = 0, q_max = 2^2 - 1 = 3; the scale is stored as FP16. */
+  float s = (hi - lo) / 3.0f;
+  if (s > 65504.0f) s = 65504.0f;
+  double sh = ora_round_f16((double)s);
+  *scale_f16 = ora_f16_bits(sh);
+  float shf = (float)sh;
+  int z = 0;
+  if (shf != 0.0f) z = (int)clampf(rintf(0.0f - lo / shf), 0.0f, 3.0f);
+  *zero_point = (uint8_t)z;
+  for (int c = 0; c < n; ++c) {
+    int q = 0;
+    if (shf != 0.0f) q = (int)clampf(rintf(r[c] / shf) + (float)z, 0.0f, 3.0f); /* Eq. 1 */
+    codes[c] = (uint8_t)q;
+    xhat[c] = mu[c] + shf * (float)(q - z); /* Eq. 4: centroid + dequantised residual */
+  }
+}
+
+/* ------------------------------------------------------------ QSAC (O2) */
+
+/* Eq. 9: Query-aware distance, fp32, channels in order. */
+static float dq_distance(const float* k, const float* mu_j, const float* w, int d) {
+  float acc = 0.0f;
+  for (int c = 0; c < d; ++c) {
+    float t = k[c] - mu_j[c];
+    acc = acc + w[c] * (t * t);
+  }
+  return acc;
+}
+
+/* Eq. 10 and Eq. 12: sum over groups of W_g * R_g^2 with W_g = sum_{c in g} w_c. */
+static float qsac_score(const float* k, const float* mu_j, const float* Wg, int d, int G) {
+  float S = 0.0f;
+  for (int g = 0; g < d / G; ++g) {
+    float mx = -INFINITY, mn = INFINITY;
+    for (int c = g * G; c < (g + 1) * G; ++c) {
+      float r = k[c] - mu_j[c];
+      if (r > mx) mx = r;
+      if (r < mn) mn = r;
+    }
+    float R = mx - mn;
+    S = S + Wg[g] * (R * R);
+  }
+  return S;
+}
+
+static void group_weights(const float* w, int d, int G, float* Wg) {
+  for (int g = 0; g < d / G; ++g) {
+    float s = 0.0f;
+    for (int c = g * G; c < (g + 1) * G; ++c) s = s + w[c];
+    Wg[g] = s;
+  }
+}
+
+static int less_pair(float a, int ia, float b, int ib) { return a < b || (a == b && ia < ib); }
+
+int ora_qsac_assign(const float* k, const float* mu, const float* w, int n_centroids,
+                    int d, int group_size, int top_m, int* cand) {
+  float dist[256], Wg[256];
+  int taken[256] = {0};
+  int M = top_m < n_centroids ? top_m : n_centroids;
+  for (int j = 0; j < n_centroids; ++j) dist[j] = dq_distance(k, mu + (long long)j * d, w, d);
+  /* top-M candidate set C_i by (d_Q, id) */
+  for (int m = 0; m < M; ++m) {
+    int best = -1;
+    for (int j = 0; j < n_centroids; ++j)
+      if (!taken[j] && (best < 0 || less_pair(dist[j], j, dist[best], best))) best = j;
+    taken[best] = 1;
+    cand[m] = best;
+  }
+  group_weights(w, d, group_size, Wg);
+  int z = -1;
+  float Sz = 0.0f;
+  for (int m = 0; m < M; ++m) {
+    int j = cand[m];
+    float S = qsac_score(k, mu + (long long)j * d, Wg, d, group_size);
+    if (z < 0 || less_pair(S, j, Sz, z)) { z = j; Sz = S; }
+  }
+  return z;
+}
+
+int ora_nearest(const float* x, const float* mu, int n_centroids, int d) {
+  int best = 0;
+  float bd = 0.0f;
+  for (int j = 0; j < n_centroids; ++j) {
+    float acc = 0.0f;
+    for (int c = 0; c < d; ++c) {
+      float t = x[c] - mu[(long long)j * d + c];
+      acc = acc + t * t;
+    }
+    if (j == 0 || acc < bd) { best = j; bd = acc; }
+  }
+  return best;
+}
+
+/* ----------------------------------------------------------- calibration */
+
+int ora_eigh(const double* a_in, int n, double* lam, double* vecs_t) {
+  double* a = (double*)malloc(sizeof(double) * n * n);
+  double* v = (double*)malloc(sizeof(double) * n * n);
+  int* order = (int*)malloc(sizeof(int) * n);
+  if (!a || !v || !order) { free(a); free(v); free(order); return -2; }
+  memcpy(a, a_in, sizeof(double) * n * n);
+  for (int i = 0; i < n * n; ++i) v[i] = 0.0;
+  for (int i = 0; i < n; ++i) v[i * n + i] = 1.0;
+  double fro = 0.0;
+  for (int i = 0; i < n * n; ++i) fro += a[i] * a[i];
+  fro = sqrt(fro);
+  /* Cyclic Jacobi: rotate each off-diagonal pair to zero until the off-diagonal
+   * mass is negligible (Golub & Van Loan, Sec. 8.5). */
+  for (int sweep = 0; sweep < 100; ++sweep) {
+    double off = 0.0;
+    for (int p = 0; p < n; ++p)
+      for (int q = p + 1; q < n; ++q) off += a[p * n + q] * a[p * n + q];
+    if (sqrt(off) <= 1e-15 * fro || off == 0.0) break;
+    for (int p = 0; p < n - 1; ++p) {
+      for (int q = p + 1; q < n; ++q) {
+        double apq = a[p * n + q];
+        if (apq == 0.0) continue;
+        double theta = (a[q * n + q] - a[p * n + p]) / (2.0 * apq);
+        double t = (theta >= 0 ? 1.0 : -1.0) / (fabs(theta) + sqrt(theta * theta + 1.0));
+        double c = 1.0 / sqrt(t * t + 1.0), s = t * c;
+        for (int k = 0; k < n; ++k) { /* A <- A J (columns p, q) */
+          double akp = a[k * n + p], akq = a[k * n + q];
+          a[k * n + p] = c * akp - s * akq;
+          a[k * n + q] = s * akp + c * akq;
+        }
+        for (int k = 0; k < n; ++k) { /* A <- J^T A (rows p, q) */
+          double apk = a[p * n + k], aqk = a[q * n + k];
+          a[p * n + k] = c * apk - s * aqk;
+          a[q * n + k] = s * apk + c * aqk;
+        }
+        for (int k = 0; k < n; ++k) { /* V <- V J */
+          double vkp = v[k * n + p], vkq = v[k * n + q];
+          v[k * n + p] = c * vkp - s * vkq;
+          v[k * n + q] = s * vkp + c * vkq;
+        }
+      }
+    }
+  }
+  /* Eq. 15 orders lambda_1 >= ... >= lambda_d; equal values keep their index. */
+  for (int i = 0; i < n; ++i) order[i] = i;
+  for (int i = 1; i < n; ++i) {
+    int o = order[i], j = i - 1;
+    while (j >= 0 && a[order[j] * n + order[j]] < a[o * n + o]) { order[j + 1] = order[j]; --j; }
+    order[j + 1] = o;
+  }
+  for (int i = 0; i < n; ++i) {
+    int o = order[i];
+    lam[i] = a[o * n + o];
+    int arg = 0;
+    for (int k = 1; k < n; ++k)
+      if (fabs(v[k * n + o]) > fabs(v[arg * n + o])) arg = k;
+    double sg = v[arg * n + o] < 0 ? -1.0 : 1.0;
+    for (int k = 0; k < n; ++k) vecs_t[(long long)i * n + k] = sg * v[k * n + o];
+  }
+  free(a); free(v); free(order);
+  return 0;
+}
+
+static void kmeans(const ora_cfg* c, const float* x, long long xs, long long n, int iters,
+                   float* mu /* [Kc][d] */) {
+  int d = c->head_dim, K = c->n_centroids;
+  int* assign = (int*)malloc(sizeof(int) * (n > 0 ? n : 1));
+  double* sum = (double*)malloc(sizeof(double) * K * d);
+  long long* cnt = (long long*)malloc(sizeof(long long) * K);
+  float* row = (float*)malloc(sizeof(float) * d);
+  for (int j = 0; j < K; ++j) {
+    long long t = n > 0 ? ((long long)j * n) / K : 0;
+    for (int ch = 0; ch < d; ++ch) mu[(long long)j * d + ch] = n > 0 ? (float)round_table(c, x[t * xs + ch]) : 0.0f;
+  }
+  for (int it = 0; it < iters && n > 0; ++it) {
+    for (long long t = 0; t < n; ++t) {
+      for (int ch = 0; ch < d; ++ch) row[ch] = x[t * xs + ch];
+      assign[t] = ora_nearest(row, mu, K, d);
+    }
+    memset(sum, 0, sizeof(double) * K * d);
+    memset(cnt, 0, sizeof(long long) * K);
+    for (long long t = 0; t < n; ++t) {
+      int j = assign[t];
+      cnt[j] += 1;
+      for (int ch = 0; ch < d; ++ch) sum[(long long)j * d + ch] += (double)x[t * xs + ch];
+    }
+    for (int j = 0; j < K; ++j)
+      if (cnt[j] > 0)
+        for (int ch = 0; ch < d; ++ch)
+          mu[(long long)j * d + ch] = (float)round_table(c, sum[(long long)j * d + ch] / (double)cnt[j]);
+  }
+  free(assign); free(sum); free(cnt); free(row);
+}
+
+int ora_calibrate(const ora_cfg* cfg, const float* q_hist, long long n_hist,
+                  const float* k_cal, const float* v_cal, long long n_cal, int kmeans_iters,
+                  float* mu_k, float* mu_v, float* w, float* u_t, float* lam) {
+  if (!valid_cfg(cfg) || n_hist < 0 || n_cal < 0 || kmeans_iters < 0) return -1;
+  if ((n_hist > 0 && !q_hist) || (n_cal > 0 && (!k_cal || !v_cal))) return -1;
+  if (!mu_k || !mu_v || !w || (cfg->rank > 0 && (!u_t || !lam))) return -1;
+  const int d = cfg->head_dim, H = cfg->heads, K = cfg->n_centroids, r = cfg->rank;
+  const int nbh = cfg->batch * H;
+  int err = 0;
+#pragma omp parallel for schedule(dynamic)
+  for (int bh = 0; bh < nbh; ++bh) {
+    int b = bh / H, h = bh % H;
+    long long tok_stride = (long long)H * d;
+    float* wo = w + (long long)bh * d;
+    float* uo = u_t + (long long)bh * r * d;
+    float* lo = lam + (long long)bh * r;
+    /* Eq. 6: historical Query second moment, fp64, tokens in order. */
+    double* M = (double*)calloc((size_t)d * d, sizeof(double));
+    double* lam_all = (double*)malloc(sizeof(double) * d);
+    double* vec_t = (double*)malloc(sizeof(double) * d * d);
+    if (!M || !lam_all || !vec_t) { err = -2; free(M); free(lam_all); free(vec_t); continue; }
+    const float* qb = q_hist + (long long)b * n_hist * tok_stride + (long long)h * d;
+    for (long long t = 0; t < n_hist; ++t) {
+      const float* q = qb + t * tok_stride;
+      for (int i = 0; i < d; ++i)
+        for (int j = 0; j < d; ++j) M[i * d + j] += (double)q[i] * (double)q[j];
+    }
+    double tr = 0.0;
+    if (n_hist > 0) {
+      for (int i = 0; i < d * d; ++i) M[i] /= (double)n_hist;
+      for (int i = 0; i < d; ++i) tr += M[i * d + i];
+    }
+    if (n_hist == 0 || tr == 0.0) {
+      /* cold start: uniform sensitivity, PSAC inactive */
+      for (int c = 0; c < d; ++c) wo[c] = 1.0f;
+      for (long long i = 0; i < (long long)r * d; ++i) uo[i] = 0.0f;
+      for (int k = 0; k < r; ++k) lo[k] = 0.0f;
+    } else {
+      /* Eq. 8: w_c = M_cc / ((1/d) sum_c' M_c'c') */
+      for (int c = 0; c < d; ++c) wo[c] = (float)(M[c * d + c] / (tr / (double)d));
+      /* Eq. 15-16: top-r eigenvectors of M */
+      ora_eigh(M, d, lam_all, vec_t);
+      for (int k = 0; k < r; ++k) {
+        lo[k] = (float)lam_all[k];
+        for (int c = 0; c < d; ++c) uo[(long long)k * d + c] = (float)round_table(cfg, vec_t[(long long)k * d + c]);
+      }
+    }
+    free(M); free(lam_all); free(vec_t);
+    /* Eq. 3: centroids by K-means on the calibration tokens, Keys and Values apart. */
+    kmeans(cfg, k_cal + (long long)b * n_cal * tok_stride + (long long)h * d, tok_stride, n_cal,
+           kmeans_iters, mu_k + (long long)bh * K * d);
+    kmeans(cfg, v_cal + (long long)b * n_cal * tok_stride + (long long)h * d, tok_stride, n_cal,
+           kmeans_iters, mu_v + (long long)bh * K * d);
+  }
+  return err;
+}
+
+/* ------------------------------------------------------------- append */
+
+static void put_codes(uint8_t* dst, const uint8_t* q, int d) {
+  for (int i = 0; i < d / 4; ++i)
+    dst[i] = (uint8_t)(q[4 * i] | (q[4 * i + 1] << 2) | (q[4 * i + 2] << 4) | (q[4 * i + 3] << 6));
+}
+
+/* One token: centroid + per-group INT2 residual, written at slot pointers. */
+static void store_residual(const layout* L, int G, const float* x, const float* mu_z,
+                           uint8_t* codes_dst, uint8_t* zp_dst, uint8_t* scale_dst, float* xhat) {
+  uint8_t q[256];
+  memset(zp_dst, 0, (size_t)L->zpb);
+  for (int g = 0; g < L->ng; ++g) {
+    uint8_t zg;
+    uint16_t sg;
+    ora_int2_group(x + g * G, mu_z + g * G, G, q + g * G, &zg, &sg, xhat + g * G);
+    zp_dst[g / 4] |= (uint8_t)(zg << (2 * (g % 4)));
+    put16(scale_dst + 2 * g, sg);
+  }
+  put_codes(codes_dst, q, L->d);
+}
+
+int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const float* w,
+               const float* u_t, uint8_t* cache, long long n_cached,
+               const float* k_new, const float* v_new, long long n_new,
+               float* coef_f32, int* k_ids, int* v_ids, int* cand) {
+  if (!valid_cfg(cfg) || n_cached < 0 || n_new < 0) return -1;
+  if (n_cached + n_new > cfg->capacity) return -3;
+  if (n_new == 0) return 0;
+  if (!mu_k || !mu_v || !w || !cache || !k_new || !v_new || (cfg->rank > 0 && !u_t)) return -1;
+  const layout L = make_layout(cfg);
+  const int d = cfg->head_dim, H = cfg->heads, K = cfg->n_centroids, r = cfg->rank, G = cfg->group_size;
+  const int M = cfg->top_m < K ? cfg->top_m : K;
+  const int nbh = cfg->batch * H;
+#pragma omp parallel for schedule(dynamic)
+  for (int bh = 0; bh < nbh; ++bh) {
+    int b = bh / H, h = bh % H;
+    const float* muk = mu_k + (long long)bh * K * d;
+    const float* muv = mu_v + (long long)bh * K * d;
+    const float* wh = w + (long long)bh * d;
+    const float* uh = u_t + (long long)bh * r * d;
+    float xhat[256];
+    int cands[256];
+    for (long long t = 0; t < n_new; ++t) {
+      long long slot = (long long)bh * L.slots + n_cached + t;
+      long long src = (((long long)b * n_new + t) * H + h) * d;
+      const float* k = k_new + src;
+      const float* v = v_new + src;
+      long long diag = ((long long)bh * n_new + t);
+      /* QSAC: top-M by Eq. 9, then argmin of Eq. 12 */
+      int z = ora_qsac_assign(k, muk, wh, K, d, G, M, cands);
+      cache[L.k_ids + slot] = (uint8_t)z;
+      store_residual(&L, G, k, muk + (long long)z * d, cache + L.k_codes + slot * (d / 4),
+                     cache + L.k_zp + slot * L.zpb, cache + L.k_scale + slot * 2 * L.ng, xhat);
+      if (k_ids) k_ids[diag] = z;
+      if (cand) for (int m = 0; m < M; ++m) cand[diag * M + m] = cands[m];
+      if (r > 0) {
+        /* Eq. 13 and Eq. 16: C = (k - khat_0) U_r, fp64 */
+        float amax = 0.0f, Cf[256];
+        for (int kk = 0; kk < r; ++kk) {
+          double acc = 0.0;
+          for (int c = 0; c < d; ++c) acc += ((double)k[c] - (double)xhat[c]) * (double)uh[(long long)kk * d + c];
+          Cf[kk] = (float)acc;
+          if (fabsf(Cf[kk]) > amax) amax = fabsf(Cf[kk]);
+          if (coef_f32) coef_f32[diag * r + kk] = Cf[kk];
+        }
+        /* INT8 row with one FP16 scale (App. D.1) */
+        float s = amax / 127.0f;
+        if (s > 65504.0f) s = 65504.0f;
+        double sh = ora_round_f16((double)s);
+        float shf = (float)sh;
+        int8_t* code = (int8_t*)(cache + L.k_coef + slot * r);
+        for (int kk = 0; kk < r; ++kk)
+          code[kk] = (int8_t)(shf != 0.0f ? (int)clampf(rintf(Cf[kk] / shf), -127.0f, 127.0f) : 0);
+        put16(cache + L.k_cscale + slot * 2, ora_f16_bits(sh));
+      }
+      /* Values: nearest centroid, same residual path, no PSAC */
+      int zv = ora_nearest(v, muv, K, d);
+      cache[L.v_ids + slot] = (uint8_t)zv;
+      store_residual(&L, G, v, muv + (long long)zv * d, cache + L.v_codes + slot * (d / 4),
+                     cache + L.v_zp + slot * L.zpb, cache + L.v_scale + slot * 2 * L.ng, xhat);
+      if (v_ids) v_ids[diag] = zv;
+    }
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------- decode */
+
+static void load_residual(const layout* L, int G, const uint8_t* codes, const uint8_t* zp,
+                          const uint8_t* scale, const float* mu_z, double* out) {
+  for (int c = 0; c < L->d; ++c) {
+    int g = c / G;
+    int q = (codes[c / 4] >> (2 * (c % 4))) & 3;
+    int z = (zp[g / 4] >> (2 * (g % 4))) & 3;
+    float s = (float)ora_f16_value(get16(scale + 2 * g));
+    out[c] = (double)(mu_z[c] + s * (float)(q - z)); /* Eq. 4, fp32 as when encoding */
+  }
+}
+
+int ora_decode(const ora_cfg* cfg, const float* mu_k, const float* mu_v,
+               const uint8_t* cache, int b, int h, long long n,
+               double* k0, double* chat, double* v) {
+  if (!valid_cfg(cfg) || b < 0 || b >= cfg->batch || h < 0 || h >= cfg->heads || n < 0 || n > cfg->capacity)
+    return -1;
+  const layout L = make_layout(cfg);
+  const int d = cfg->head_dim, K = cfg->n_centroids, r = cfg->rank, G = cfg->group_size;
+  long long bh = (long long)b * cfg->heads + h;
+  for (long long t = 0; t < n; ++t) {
+    long long slot = bh * L.slots + t;
+    int zk = cache[L.k_ids + slot], zv = cache[L.v_ids + slot];
+    if (zk >= K || zv >= K) return -4;
+    if (k0)
+      load_residual(&L, G, cache + L.k_codes + slot * (d / 4), cache + L.k_zp + slot * L.zpb,
+                    cache + L.k_scale + slot * 2 * L.ng, mu_k + (bh * K + zk) * d, k0 + t * d);
+    if (v)
+      load_residual(&L, G, cache + L.v_codes + slot * (d / 4), cache + L.v_zp + slot * L.zpb,
+                    cache + L.v_scale + slot * 2 * L.ng, mu_v + (bh * K + zv) * d, v + t * d);
+    if (chat && r > 0) {
+      float s = (float)ora_f16_value(get16(cache + L.k_cscale + slot * 2));
+      const int8_t* code = (const int8_t*)(cache + L.k_coef + slot * r);
+      for (int kk = 0; kk < r; ++kk) chat[t * r + kk] = (double)((float)code[kk] * s);
+    }
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------- attend */
+
+static int cmp_rows(const void* a, const void* b) {
+  const int* x = (const int*)a;
+  const int* y = (const int*)b;
+  if (x[0] != y[0]) return x[0] - y[0];
+  if (x[1] != y[1]) return x[1] - y[1];
+  return x[2] - y[2];
+}
+
+int ora_attend(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const float* u_t,
+               const uint8_t* cache, long long n_cache, const float* q, long long n_q,
+               long long q_start, int frame_tokens, const float* coef_override,
+               int n_rows, const int* rows, double* out, double* lse, double* logits) {
+  if (!valid_cfg(cfg) || n_cache < 0 || n_cache > cfg->capacity || n_q < 0 || q_start < 0 ||
+      q_start > n_cache || frame_tokens < 1 || n_rows < 0)
+    return -1;
+  const int d = cfg->head_dim, H = cfg->heads, r = cfg->rank;
+  /* rows sorted by head so that each head's cache is decoded once; idx[4] keeps
+   * the caller's row number */
+  int* srt = (int*)malloc(sizeof(int) * 4 * (n_rows > 0 ? n_rows : 1));
+  for (int i = 0; i < n_rows; ++i) {
+    srt[4 * i] = rows[3 * i]; srt[4 * i + 1] = rows[3 * i + 1]; srt[4 * i + 2] = rows[3 * i + 2];
+    srt[4 * i + 3] = i;
+    if (rows[3 * i] < 0 || rows[3 * i] >= cfg->batch || rows[3 * i + 1] < 0 || rows[3 * i + 1] >= H ||
+        rows[3 * i + 2] < 0 || rows[3 * i + 2] >= n_q) { free(srt); return -1; }
+  }
+  qsort(srt, (size_t)n_rows, sizeof(int) * 4, cmp_rows);
+  double* K0 = (double*)malloc(sizeof(double) * (n_cache > 0 ? n_cache : 1) * d);
+  double* V = (double*)malloc(sizeof(double) * (n_cache > 0 ? n_cache : 1) * d);
+  double* Ch = (double*)malloc(sizeof(double) * (n_cache > 0 ? n_cache : 1) * (r > 0 ? r : 1));
+  if (!K0 || !V || !Ch) { free(srt); free(K0); free(V); free(Ch); return -2; }
+  const double inv_sqrt_d = 1.0 / sqrt((double)d);
+  int i0 = 0, status = 0;
+  while (i0 < n_rows) {
+    int b = srt[4 * i0], h = srt[4 * i0 + 1], i1 = i0;
+    while (i1 < n_rows && srt[4 * i1] == b && srt[4 * i1 + 1] == h) ++i1;
+    long long bh = (long long)b * H + h;
+    if (ora_decode(cfg, mu_k, mu_v, cache, b, h, n_cache, K0, Ch, V)) { status = -4; break; }
+    /* operands of the attention product, in the table type (BF16 per App. D.1) */
+    for (long long t = 0; t < n_cache * d; ++t) { K0[t] = round_table(cfg, K0[t]); V[t] = round_table(cfg, V[t]); }
+    for (long long t = 0; t < n_cache * r; ++t)
+      Ch[t] = coef_override ? (double)coef_override[bh * n_cache * r + t] : round_table(cfg, Ch[t]);
+#pragma omp parallel for schedule(dynamic)
+    for (int ri = i0; ri < i1; ++ri) {
+      long long i = srt[4 * ri + 2];
+      int dst = srt[4 * ri + 3];
+      const float* qi = q + (((long long)b * n_q + i) * H + h) * d;
+      double u[256];
+      for (int kk = 0; kk < r; ++kk) {
+        double acc = 0.0;
+        for (int c = 0; c < d; ++c) acc += (double)qi[c] * (double)u_t[(bh * r + kk) * d + c];
+        u[kk] = round_table(cfg, acc); /* qU_r enters the product in the table type */
+      }
+      double* L = (double*)malloc(sizeof(double) * (n_cache > 0 ? n_cache : 1));
+      double m = -INFINITY;
+      for (long long j = 0; j < n_cache; ++j) {
+        int visible = j < q_start || (j - q_start) / frame_tokens <= i / frame_tokens;
+        if (!visible) { L[j] = -INFINITY; continue; }
+        /* Eq. 5 with Eq. 17: (q khat_0 + (q U_r) c) / sqrt(d) */
+        double acc = 0.0;
+        for (int c = 0; c < d; ++c) acc += (double)qi[c] * K0[j * d + c];
+        for (int kk = 0; kk < r; ++kk) acc += u[kk] * Ch[j * r + kk];
+        L[j] = acc * inv_sqrt_d;
+        if (L[j] > m) m = L[j];
+      }
+      double l = 0.0;
+      double* o = out + (long long)dst * d;
+      for (int c = 0; c < d; ++c) o[c] = 0.0;
+      if (m > -INFINITY) {
+        for (long long j = 0; j < n_cache; ++j) {
+          if (L[j] == -INFINITY) continue;
+          double p = exp(L[j] - m);
+          l += p;
+          for (int c = 0; c < d; ++c) o[c] += p * V[j * d + c];
+        }
+        for (int c = 0; c < d; ++c) o[c] /= l;
+        lse[dst] = m + log(l);
+      } else {
+        lse[dst] = -INFINITY;
+      }
+      if (logits) memcpy(logits + (long long)dst * n_cache, L, sizeof(double) * n_cache);
+      free(L);
+    }
+    i0 = i1;
+  }
+  free(srt); free(K0); free(V); free(Ch);
+  return status;
+}
+
+int ora_max_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+void ora_set_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}

@@ -1,0 +1,103 @@
+/*
+ * QuantWM CPU oracle: TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, single-unit-at-a-time CPU implementation of what the QuantWM
+ * hot path computes, written from the paper (arxiv 2609.26425, Sections 2, 4.1,
+ * 4.2 and Appendix D.1). Only tests/, the package's smoke check and the
+ * benchmark's CPU-baseline leg may load it. It shares no code with the HIP
+ * library; the two only agree on the packed byte format of the cache.
+ *
+ * Precision. Attention, second moments, eigendecomposition and PSAC
+ * coefficients are computed in fp64. Every decision that turns a float into an
+ * integer (the Eq. 9 distance, the Eq. 12 score, the INT2 quantiser of Eq. 1-2,
+ * the INT8 coefficient codes, the K-means assignment) is taken in fp32, the
+ * precision of the GPU kernels, evaluated in the order the equations are written
+ * (IEEE division, round-to-nearest-even, no contraction).
+ *
+ * Layouts. Activations are float32 arrays [B, N, H, d] (token-major) holding
+ * values that are exact in the workload's element type. Method-level tables are
+ * float32 arrays: centroids [B, H, Kc, d], sensitivities w [B, H, d], principal
+ * basis U_r^T [B, H, r, d] (row k = k-th eigenvector), eigenvalues [B, H, r].
+ *
+ * Every function returns 0 on success and a negative number on a bad argument.
+ */
+#ifndef QUANTWM_ORACLE_H
+#define QUANTWM_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+  int batch, heads, head_dim;  /* B, H, d */
+  int n_centroids;             /* Kc <= 256 (uint8 centroid ids, App. D.1) */
+  int group_size;              /* G: INT2 residual group along channels */
+  int rank;                    /* r: PSAC rank (0 disables PSAC) */
+  int top_m;                   /* M: QSAC candidate count (Sec. 4.1) */
+  long long capacity;          /* cache slots per (b, h) */
+  int table_bf16;              /* 1: centroids, U_r and attention operands are BF16 */
+} ora_cfg;
+
+/* Packed cache size in bytes and the per-token-head byte counts (K and V). */
+long long ora_cache_bytes(const ora_cfg* cfg);
+int ora_token_bytes(const ora_cfg* cfg, int* k_bytes, int* v_bytes);
+
+/* Number conversions the format fixes (round to nearest, ties to even). */
+double ora_round_bf16(double x);
+double ora_round_f16(double x);  /* IEEE binary16, subnormals kept, overflow -> inf */
+uint16_t ora_f16_bits(double exact_f16_value);
+double ora_f16_value(uint16_t bits);
+
+/* Eq. 1-2 with b = 2 on one residual group, plus Eq. 4 reconstruction. */
+void ora_int2_group(const float* x, const float* mu, int n, uint8_t* codes,
+                    uint8_t* zero_point, uint16_t* scale_f16, float* xhat);
+
+/* Eq. 9-12 on one Key token. cand receives the top-M ids in (d_Q, id) order. */
+int ora_qsac_assign(const float* k, const float* mu, const float* w, int n_centroids,
+                    int d, int group_size, int top_m, int* cand);
+
+/* Plain nearest centroid (Euclidean), ties to the lower id. */
+int ora_nearest(const float* x, const float* mu, int n_centroids, int d);
+
+/* Eq. 6, Eq. 8 and Eq. 15, plus Lloyd K-means centroids (Eq. 3). */
+int ora_calibrate(const ora_cfg* cfg, const float* q_hist, long long n_hist,
+                  const float* k_cal, const float* v_cal, long long n_cal, int kmeans_iters,
+                  float* mu_k, float* mu_v, float* w, float* u_t, float* lam);
+
+/* Cyclic Jacobi eigendecomposition of a symmetric n x n matrix (fp64).
+ * Returns eigenvalues descending in lam and eigenvectors as rows of vecs_t. */
+int ora_eigh(const double* a, int n, double* lam, double* vecs_t);
+
+/* QSAC + INT2 residual + PSAC for Keys, nearest centroid + INT2 for Values,
+ * written into cache slots [n_cached, n_cached + n_new) of every (b, h).
+ * coef_f32 [B,H,n_new,r], k_ids/v_ids [B,H,n_new] and cand [B,H,n_new,M] are
+ * optional diagnostics (NULL to skip). */
+int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const float* w,
+               const float* u_t, uint8_t* cache, long long n_cached,
+               const float* k_new, const float* v_new, long long n_new,
+               float* coef_f32, int* k_ids, int* v_ids, int* cand);
+
+/* Decode slots [0, n) of head (b, h): Khat_0 (Eq. 4), INT8-decoded C, Vhat. */
+int ora_decode(const ora_cfg* cfg, const float* mu_k, const float* mu_v,
+               const uint8_t* cache, int b, int h, long long n,
+               double* k0, double* chat, double* v);
+
+/* Attention of selected Query rows over the packed cache (Eq. 5 with Eq. 17).
+ * rows holds (b, h, i) triples. coef_override [B,H,n_cache,r] replaces the
+ * decoded coefficients when non-NULL. logits [n_rows, n_cache] is optional and
+ * holds -inf where a key is masked. A row with no visible key gets O = 0 and
+ * lse = -inf. */
+int ora_attend(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const float* u_t,
+               const uint8_t* cache, long long n_cache, const float* q, long long n_q,
+               long long q_start, int frame_tokens, const float* coef_override,
+               int n_rows, const int* rows, double* out, double* lse, double* logits);
+
+int ora_max_threads(void);
+void ora_set_threads(int n);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
