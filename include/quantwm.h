@@ -1,0 +1,165 @@
+/*
+ * quantwm.h: C ABI of libquantwm.so, the QuantWM hot path for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * QuantWM (arxiv 2609.26425) keeps the KV cache of a causal video world model
+ * as BF16 centroids plus group-wise INT2 residuals (Eq. 3-4). Keys pick their
+ * centroid by quantization-sensitivity-aware clustering (QSAC, Sec. 4.1,
+ * Eq. 6-12). A low-rank compensation along the top historical Query directions
+ * (PSAC, Sec. 4.2, Eq. 13-17) corrects the logits. Packed storage follows
+ * App. D.1.
+ *
+ * Conventions for every entry point:
+ *  - Pointers named *device* point to GPU memory that the caller allocated and
+ *    owns. The library never allocates device memory and keeps no state between
+ *    calls, except the per-thread message behind quantwm_last_error().
+ *  - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued
+ *    asynchronously on it; outputs are valid once the stream has reached that
+ *    point. Calls that touch the same buffers must be ordered on one stream.
+ *  - Activations are contiguous token-major [B, N, H, d] tensors of the config's
+ *    dtype (BF16 or FP32); all device pointers must be 16-byte aligned.
+ *  - Arguments are validated on the host before anything is enqueued; a failed
+ *    check returns a non-zero status, enqueues nothing, and sets the message.
+ *    Non-finite inputs are outside the domain. A device fault surfaces at the
+ *    caller's next synchronisation.
+ */
+#ifndef QUANTWM_H
+#define QUANTWM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  QWM_OK = 0,
+  QWM_ERR_INVALID_ARG = 1, /* null/misaligned pointer, negative size, bad range */
+  QWM_ERR_UNSUPPORTED = 2, /* a shape this build has no kernel for */
+  QWM_ERR_CAPACITY = 3,    /* tokens would exceed the cache capacity */
+  QWM_ERR_HIP = 4          /* a HIP runtime call or a launch failed */
+} quantwm_status;
+
+typedef enum { QWM_F32 = 0, QWM_BF16 = 1 } quantwm_dtype;
+
+typedef struct {
+  int32_t batch;       /* B: independent rollouts */
+  int32_t heads;       /* H */
+  int32_t head_dim;    /* d: 64 or 128 */
+  int32_t n_centroids; /* Kc in [1, 256]; ids are uint8 (App. D.1) */
+  int32_t group_size;  /* G: INT2 residual group along channels; 16, 32 or 64, divides d */
+  int32_t rank;        /* r: PSAC rank in [0, 32]; 0 disables PSAC (Eq. 16) */
+  int32_t top_m;       /* M: QSAC candidates in [1, 8] (Sec. 4.1; the paper uses 4) */
+  int32_t dtype;       /* quantwm_dtype of Q/K/V/O, centroids and U_r */
+  int64_t capacity;    /* cache slots per (b, h) */
+} quantwm_config;
+
+/* ------------------------------------------------------------------ sizes */
+
+/* Bytes of the packed K+V cache for cfg (0 if cfg is invalid). Layout: ten
+ * sections, each starting on a 256-byte boundary, each [B*H][slots][bytes per
+ * token] with slots = capacity rounded up to 64:
+ *   K codes    d/4 bytes: channel c in bits 2(c%4) of byte c/4 (four INT2 codes per byte)
+ *   K ids      1 byte: centroid id (uint8)
+ *   K zp       ceil(d/G/4) bytes: group g in bits 2(g%4) of byte g/4 (INT2 zero-points)
+ *   K scale    2*d/G bytes: IEEE binary16 group scales, little-endian
+ *   K coef     r bytes: INT8 PSAC coefficients
+ *   K cscale   2 bytes (0 if r = 0): binary16 row scale of the coefficients
+ *   V codes, V ids, V zp, V scale: as for K (Values carry no PSAC row).
+ * A token's reconstruction is centroid + scale * (code - zero_point) (Eq. 4)
+ * and its coefficients are code * cscale (Eq. 16, App. D.1). */
+size_t quantwm_cache_bytes(const quantwm_config* cfg);
+
+/* Packed bytes per token-head for Keys and Values. Returns a status. */
+quantwm_status quantwm_token_bytes(const quantwm_config* cfg, int32_t* k_bytes, int32_t* v_bytes);
+
+/* Bytes of the calibration block: one slab per (b, h) of calib_slab_bytes. */
+size_t quantwm_calib_bytes(const quantwm_config* cfg);
+
+/* Byte offsets of the fields inside one (b, h) slab of the calibration block:
+ *   mu_k, mu_v  [Kc][d] dtype   Key / Value centroids (Eq. 3)
+ *   a_k         [Kc][d] f32     -2 * w_c * mu_k[j][c]   (search constants of Eq. 9)
+ *   b_k         [Kc]    f32     sum_c w_c * mu_k[j][c]^2
+ *   a_v, b_v                    the same for Values with w = 1
+ *   w           [d]     f32     channel sensitivities (Eq. 8)
+ *   wg          [d/G]   f32     per-group sums of w (Eq. 12)
+ *   u_t         [r][d]  dtype   U_r transposed: row k is the k-th eigenvector (Eq. 15)
+ *   lam         [r]     f32     the matching eigenvalues (0 at cold start) */
+typedef struct {
+  int64_t slab_bytes;
+  int64_t mu_k, mu_v, a_k, b_k, a_v, b_v, w, wg, u_t, lam;
+} quantwm_calib_layout;
+quantwm_status quantwm_calib_offsets(const quantwm_config* cfg, quantwm_calib_layout* out);
+
+/* Device workspace bytes that quantwm_calibrate needs for these token counts. */
+size_t quantwm_calibrate_workspace_bytes(const quantwm_config* cfg, int64_t n_hist, int64_t n_calib);
+
+/* ------------------------------------------------------------ calibration */
+
+/* Builds the calibration block from method-level tables (all device):
+ * mu_k, mu_v [B,H,Kc,d] dtype; w [B,H,d] f32; u_t [B,H,r,d] dtype (NULL allowed
+ * when r = 0); lam [B,H,r] f32 or NULL (then stored as 0). It derives the
+ * search constants and group sums (Eq. 9, Eq. 12) on the device. */
+quantwm_status quantwm_calib_pack(const quantwm_config* cfg, const void* mu_k, const void* mu_v,
+                                  const float* w, const void* u_t, const float* lam,
+                                  void* calib, void* stream);
+
+/* QSAC/PSAC statistics and centroids for every (b, h):
+ *  - Eq. 6: M = (1/n_hist) sum q q^T over q_hist [B,n_hist,H,d] (fp64 on the device);
+ *  - Eq. 8: w_c = M_cc / (tr(M)/d);
+ *  - Eq. 15: U_r = top-r eigenvectors of M (host fp64 Jacobi; sorted by
+ *    eigenvalue, each vector's largest-magnitude entry positive);
+ *  - Eq. 3: centroids by deterministic Lloyd K-means (kmeans_iters rounds) on
+ *    k_calib / v_calib [B,n_calib,H,d], starting from tokens floor(j*n/Kc).
+ * n_hist == 0 is the cold start: w = 1 and U_r = 0, so PSAC stores zero rows.
+ * Needs n_calib >= 1 and a device workspace of
+ * quantwm_calibrate_workspace_bytes(). The call synchronises `stream` (it reads
+ * M back to the host). */
+quantwm_status quantwm_calibrate(const quantwm_config* cfg, const void* q_hist, int64_t n_hist,
+                                 const void* k_calib, const void* v_calib, int64_t n_calib,
+                                 int32_t kmeans_iters, void* calib, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------- hot path */
+
+/* Quantize-on-append (Sec. 4.1-4.2, App. D.1) of n_new new tokens per (b, h)
+ * into cache slots [n_cached, n_cached + n_new):
+ *  - Keys: QSAC picks z = argmin of Eq. 12 over the top-M centroids by Eq. 9;
+ *    the residual is quantised per group to INT2 with an FP16 scale and an INT2
+ *    zero-point (Eq. 1-2, range extended to contain 0); PSAC stores
+ *    C = (k - khat_0) U_r (Eq. 13, 16) as INT8 with an FP16 row scale.
+ *  - Values: nearest centroid and the same INT2 residual, no PSAC.
+ * k_new, v_new: [B,n_new,H,d] dtype. coef_f32_out: optional [B,H,n_new,r] f32
+ * copy of C before INT8 rounding. n_new == 0 is a no-op. Needs
+ * n_cached + n_new <= capacity. */
+quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void* cache,
+                              int64_t n_cached, const void* k_new, const void* v_new,
+                              int64_t n_new, float* coef_f32_out, void* stream);
+
+/* Attention of a Query chunk over the packed cache (Eq. 5 with Eq. 17):
+ * L = (q . khat_0 + (q U_r) . chat) / sqrt(d), softmax over visible keys, times
+ * vhat. Query i sits at absolute position q_start + i; key j is visible iff
+ * j < q_start, or (j - q_start)/F <= i/F (block-causal by frames of
+ * F = frame_tokens). q: [B,n_q,H,d] dtype; out: [B,n_q,H,d] dtype;
+ * lse_out: optional [B,H,n_q] f32 natural-log sum-exp (-inf for a row with no
+ * visible key, whose O is 0). Needs 0 <= q_start <= n_cache <= capacity.
+ * n_q == 0 is a no-op. Keys and Values are dequantised in registers; the cache
+ * is only ever read in packed form. */
+quantwm_status quantwm_attend(const quantwm_config* cfg, const void* calib, const void* cache,
+                              int64_t n_cache, const void* q, int64_t n_q, int64_t q_start,
+                              int32_t frame_tokens, void* out, float* lse_out, void* stream);
+
+/* Test hook: the scaled logits of quantwm_attend, [B,H,n_q,n_cache] f32,
+ * -inf where masked. Same tile code as quantwm_attend. */
+quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, const void* cache,
+                              int64_t n_cache, const void* q, int64_t n_q, int64_t q_start,
+                              int32_t frame_tokens, float* logits_out, void* stream);
+
+/* Message for the last non-OK status on the calling thread ("" if none). */
+const char* quantwm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

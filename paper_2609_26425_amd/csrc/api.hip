@@ -1,0 +1,312 @@
+// C ABI of libquantwm.so: host-side validation, size queries and launches.
+// Every check runs before anything is enqueued; nothing here allocates device
+// memory.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "qwm_common.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+quantwm_status fail(quantwm_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+quantwm_status fail(quantwm_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return s;
+}
+
+quantwm_status ok() {
+  g_error.clear();
+  return QWM_OK;
+}
+
+quantwm_status hip_fail(hipError_t e, const char* what) {
+  return fail(QWM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// Shape support of this build; INVALID for nonsense, UNSUPPORTED for shapes
+// that are meaningful but have no kernel here.
+quantwm_status check_cfg(const quantwm_config* c) {
+  if (!c) return fail(QWM_ERR_INVALID_ARG, "config is null");
+  if (c->batch < 1 || c->heads < 1) return fail(QWM_ERR_INVALID_ARG, "batch and heads must be >= 1");
+  if (c->head_dim < 1 || c->group_size < 1 || c->head_dim % c->group_size)
+    return fail(QWM_ERR_INVALID_ARG, "group_size must divide head_dim");
+  if (c->n_centroids < 1 || c->n_centroids > 256)
+    return fail(QWM_ERR_INVALID_ARG, "n_centroids must be in [1, 256] (uint8 ids)");
+  if (c->rank < 0 || c->rank > c->head_dim) return fail(QWM_ERR_INVALID_ARG, "rank must be in [0, head_dim]");
+  if (c->top_m < 1) return fail(QWM_ERR_INVALID_ARG, "top_m must be >= 1");
+  if (c->capacity < 0) return fail(QWM_ERR_INVALID_ARG, "capacity must be >= 0");
+  if (c->dtype != QWM_F32 && c->dtype != QWM_BF16) return fail(QWM_ERR_INVALID_ARG, "dtype must be F32 or BF16");
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(QWM_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c->group_size != 16 && c->group_size != 32 && c->group_size != 64)
+    return fail(QWM_ERR_UNSUPPORTED, "group_size must be 16, 32 or 64");
+  if (c->rank > 32) return fail(QWM_ERR_UNSUPPORTED, "rank must be <= 32");
+  if (c->top_m > 8) return fail(QWM_ERR_UNSUPPORTED, "top_m must be <= 8");
+  return QWM_OK;
+}
+
+quantwm_status check_dev(const void* p, const char* name, bool required = true) {
+  if (!p) return required ? fail(QWM_ERR_INVALID_ARG, "%s is null", name) : QWM_OK;
+  if (!aligned16(p)) return fail(QWM_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return QWM_OK;
+}
+
+#define QWM_TRY(x)                         \
+  do {                                     \
+    quantwm_status _s = (x);               \
+    if (_s != QWM_OK) return _s;           \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* quantwm_last_error(void) { return g_error.c_str(); }
+
+size_t quantwm_cache_bytes(const quantwm_config* cfg) {
+  if (check_cfg(cfg) != QWM_OK) return 0;
+  return size_t(qwm::cache_layout(*cfg).total);
+}
+
+quantwm_status quantwm_token_bytes(const quantwm_config* cfg, int32_t* k_bytes, int32_t* v_bytes) {
+  QWM_TRY(check_cfg(cfg));
+  if (!k_bytes || !v_bytes) return fail(QWM_ERR_INVALID_ARG, "output pointer is null");
+  const qwm::CacheLayout L = qwm::cache_layout(*cfg);
+  *k_bytes = L.k_bytes;
+  *v_bytes = L.v_bytes;
+  return ok();
+}
+
+size_t quantwm_calib_bytes(const quantwm_config* cfg) {
+  if (check_cfg(cfg) != QWM_OK) return 0;
+  return size_t(qwm::calib_layout(*cfg).slab_bytes) * cfg->batch * cfg->heads;
+}
+
+quantwm_status quantwm_calib_offsets(const quantwm_config* cfg, quantwm_calib_layout* out) {
+  QWM_TRY(check_cfg(cfg));
+  if (!out) return fail(QWM_ERR_INVALID_ARG, "output pointer is null");
+  *out = qwm::calib_layout(*cfg);
+  return ok();
+}
+
+size_t quantwm_calibrate_workspace_bytes(const quantwm_config* cfg, int64_t n_hist, int64_t n_calib) {
+  if (check_cfg(cfg) != QWM_OK || n_hist < 0 || n_calib < 0) return 0;
+  const size_t bh = size_t(cfg->batch) * cfg->heads, d = cfg->head_dim;
+  const size_t m = qwm::align256(int64_t(bh * d * d * sizeof(double)));
+  const size_t as = qwm::align256(int64_t(bh * size_t(n_calib) * sizeof(int32_t)));
+  return m + as;
+}
+
+quantwm_status quantwm_calib_pack(const quantwm_config* cfg, const void* mu_k, const void* mu_v, const float* w,
+                                  const void* u_t, const float* lam, void* calib, void* stream) {
+  QWM_TRY(check_cfg(cfg));
+  QWM_TRY(check_dev(mu_k, "mu_k"));
+  QWM_TRY(check_dev(mu_v, "mu_v"));
+  QWM_TRY(check_dev(w, "w"));
+  QWM_TRY(check_dev(u_t, "u_t", false));
+  QWM_TRY(check_dev(lam, "lam", false));
+  QWM_TRY(check_dev(calib, "calib"));
+  if (cfg->rank > 0 && !u_t) return fail(QWM_ERR_INVALID_ARG, "u_t is null with rank > 0");
+  const hipError_t e = qwm::launch_pack_tables(*cfg, mu_k, mu_v, w, u_t, lam, static_cast<uint8_t*>(calib),
+                                               static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "calib_pack launch");
+  return ok();
+}
+
+quantwm_status quantwm_calibrate(const quantwm_config* cfg, const void* q_hist, int64_t n_hist, const void* k_calib,
+                                 const void* v_calib, int64_t n_calib, int32_t kmeans_iters, void* calib,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  QWM_TRY(check_cfg(cfg));
+  if (n_hist < 0 || n_calib < 1 || kmeans_iters < 0)
+    return fail(QWM_ERR_INVALID_ARG, "need n_hist >= 0, n_calib >= 1, kmeans_iters >= 0");
+  QWM_TRY(check_dev(q_hist, "q_hist", n_hist > 0));
+  QWM_TRY(check_dev(k_calib, "k_calib"));
+  QWM_TRY(check_dev(v_calib, "v_calib"));
+  QWM_TRY(check_dev(calib, "calib"));
+  QWM_TRY(check_dev(workspace, "workspace"));
+  if (workspace_bytes < quantwm_calibrate_workspace_bytes(cfg, n_hist, n_calib))
+    return fail(QWM_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes,
+                quantwm_calibrate_workspace_bytes(cfg, n_hist, n_calib));
+  const quantwm_config& c = *cfg;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const quantwm_calib_layout C = qwm::calib_layout(c);
+  const int bh = c.batch * c.heads, d = c.head_dim, r = c.rank, e = qwm::elem_bytes(c);
+  uint8_t* cal = static_cast<uint8_t*>(calib);
+  double* m_dev = static_cast<double*>(workspace);
+  int32_t* assign = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) +
+                                               qwm::align256(int64_t(size_t(bh) * d * d * sizeof(double))));
+  hipError_t he;
+
+  // Eq. 6 on the device, then Eq. 8 and Eq. 15 on the host in fp64.
+  std::vector<double> M(size_t(bh) * d * d, 0.0);
+  if (n_hist > 0) {
+    if ((he = qwm::launch_second_moment(c, q_hist, n_hist, m_dev, s)) != hipSuccess) return hip_fail(he, "moment");
+    if ((he = hipMemcpyAsync(M.data(), m_dev, M.size() * sizeof(double), hipMemcpyDeviceToHost, s)) != hipSuccess)
+      return hip_fail(he, "moment readback");
+    if ((he = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(he, "moment sync");
+  }
+  std::vector<float> w(size_t(bh) * d), lam(size_t(bh) * (r > 0 ? r : 1));
+  std::vector<uint8_t> ut(size_t(bh) * (r > 0 ? r : 1) * d * e, 0);
+  std::vector<double> ev(d), vt(size_t(d) * d);
+  for (int i = 0; i < bh; ++i) {
+    const double* Mi = M.data() + size_t(i) * d * d;
+    double tr = 0.0;
+    for (int k = 0; k < d; ++k) tr += Mi[size_t(k) * d + k];
+    float* wi = w.data() + size_t(i) * d;
+    if (n_hist == 0 || tr == 0.0) {  // cold start: uniform sensitivity, PSAC inactive
+      for (int k = 0; k < d; ++k) wi[k] = 1.0f;
+      for (int k = 0; k < r; ++k) lam[size_t(i) * r + k] = 0.0f;
+      continue;
+    }
+    for (int k = 0; k < d; ++k) wi[k] = (float)(Mi[size_t(k) * d + k] / (tr / (double)d));
+    qwm::host_eigh(Mi, d, ev.data(), vt.data());
+    for (int k = 0; k < r; ++k) {
+      lam[size_t(i) * r + k] = (float)ev[k];
+      for (int cc = 0; cc < d; ++cc) {
+        const double x = vt[size_t(k) * d + cc];
+        uint8_t* dst = ut.data() + ((size_t(i) * r + k) * d + cc) * e;
+        if (e == 4) {
+          const float f = (float)x;
+          std::memcpy(dst, &f, 4);
+        } else {  // bf16, one rounding from fp64 (nearest, ties to even)
+          uint64_t u;
+          std::memcpy(&u, &x, 8);
+          u += ((uint64_t(1) << 44) - 1) + ((u >> 45) & 1);
+          u &= ~((uint64_t(1) << 45) - 1);
+          double y;
+          std::memcpy(&y, &u, 8);
+          const float f = (float)y;
+          uint32_t fb;
+          std::memcpy(&fb, &f, 4);
+          const uint16_t hb = uint16_t(fb >> 16);
+          std::memcpy(dst, &hb, 2);
+        }
+      }
+    }
+  }
+  auto put = [&](int64_t off, const void* src, size_t row) -> hipError_t {
+    if (row == 0) return hipSuccess;
+    return hipMemcpy2DAsync(cal + off, size_t(C.slab_bytes), src, row, row, size_t(bh), hipMemcpyHostToDevice, s);
+  };
+  if ((he = put(C.w, w.data(), size_t(d) * 4)) != hipSuccess) return hip_fail(he, "w upload");
+  if (r > 0) {
+    if ((he = put(C.u_t, ut.data(), size_t(r) * d * e)) != hipSuccess) return hip_fail(he, "u_t upload");
+    if ((he = put(C.lam, lam.data(), size_t(r) * 4)) != hipSuccess) return hip_fail(he, "lam upload");
+  }
+  // Eq. 3: Key and Value centroids by Lloyd K-means on the calibration tokens.
+  if ((he = qwm::launch_kmeans(c, k_calib, n_calib, kmeans_iters, cal, C.mu_k, assign, s)) != hipSuccess)
+    return hip_fail(he, "kmeans (K)");
+  if ((he = qwm::launch_kmeans(c, v_calib, n_calib, kmeans_iters, cal, C.mu_v, assign, s)) != hipSuccess)
+    return hip_fail(he, "kmeans (V)");
+  if ((he = qwm::launch_derive_constants(c, cal, s)) != hipSuccess) return hip_fail(he, "derive");
+  // the host staging buffers die with this call
+  if ((he = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(he, "calibrate sync");
+  return ok();
+}
+
+quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void* cache, int64_t n_cached,
+                              const void* k_new, const void* v_new, int64_t n_new, float* coef_f32_out,
+                              void* stream) {
+  QWM_TRY(check_cfg(cfg));
+  if (n_cached < 0 || n_new < 0) return fail(QWM_ERR_INVALID_ARG, "token counts must be >= 0");
+  if (n_cached + n_new > cfg->capacity)
+    return fail(QWM_ERR_CAPACITY, "n_cached + n_new = %lld exceeds capacity %lld", (long long)(n_cached + n_new),
+                (long long)cfg->capacity);
+  if (n_new == 0) return ok();
+  QWM_TRY(check_dev(calib, "calib"));
+  QWM_TRY(check_dev(cache, "cache"));
+  QWM_TRY(check_dev(k_new, "k_new"));
+  QWM_TRY(check_dev(v_new, "v_new"));
+  if (coef_f32_out && (reinterpret_cast<uintptr_t>(coef_f32_out) & 3))
+    return fail(QWM_ERR_INVALID_ARG, "coef_f32_out is not 4-byte aligned");
+  if (n_new > (int64_t(1) << 31) - 256) return fail(QWM_ERR_UNSUPPORTED, "n_new too large for one call");
+  const quantwm_calib_layout C = qwm::calib_layout(*cfg);
+  qwm::AppendArgs a;
+  a.calib = static_cast<const uint8_t*>(calib);
+  a.slab = C.slab_bytes;
+  a.o_mu_k = C.mu_k; a.o_mu_v = C.mu_v; a.o_a_k = C.a_k; a.o_b_k = C.b_k;
+  a.o_a_v = C.a_v; a.o_b_v = C.b_v; a.o_wg = C.wg; a.o_u_t = C.u_t;
+  a.cache = static_cast<uint8_t*>(cache);
+  a.L = qwm::cache_layout(*cfg);
+  a.k = k_new; a.v = v_new;
+  a.n_new = n_new; a.n_cached = n_cached;
+  a.heads = cfg->heads; a.n_centroids = cfg->n_centroids; a.rank = cfg->rank; a.top_m = cfg->top_m;
+  a.coef_out = coef_f32_out;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  const bool bf = cfg->dtype == QWM_BF16;
+  if (cfg->head_dim == 64) e = bf ? qwm::launch_append_bf16_64(a, cfg->group_size, cfg->batch, s)
+                                  : qwm::launch_append_f32_64(a, cfg->group_size, cfg->batch, s);
+  else e = bf ? qwm::launch_append_bf16_128(a, cfg->group_size, cfg->batch, s)
+              : qwm::launch_append_f32_128(a, cfg->group_size, cfg->batch, s);
+  if (e != hipSuccess) return hip_fail(e, "append launch");
+  return ok();
+}
+
+static quantwm_status attend_common(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
+                                    const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
+                                    float* lse_out, float* logits_out, void* stream) {
+  QWM_TRY(check_cfg(cfg));
+  if (n_cache < 0 || n_q < 0 || q_start < 0) return fail(QWM_ERR_INVALID_ARG, "sizes must be >= 0");
+  if (n_cache > cfg->capacity) return fail(QWM_ERR_CAPACITY, "n_cache exceeds capacity");
+  if (q_start > n_cache) return fail(QWM_ERR_INVALID_ARG, "q_start > n_cache");
+  if (frame_tokens < 1) return fail(QWM_ERR_INVALID_ARG, "frame_tokens must be >= 1");
+  if (n_q == 0) return ok();
+  QWM_TRY(check_dev(calib, "calib"));
+  QWM_TRY(check_dev(cache, "cache"));
+  QWM_TRY(check_dev(q, "q"));
+  if (logits_out) {
+    if (reinterpret_cast<uintptr_t>(logits_out) & 3) return fail(QWM_ERR_INVALID_ARG, "logits_out misaligned");
+  } else {
+    QWM_TRY(check_dev(out, "out"));
+    if (lse_out && (reinterpret_cast<uintptr_t>(lse_out) & 3)) return fail(QWM_ERR_INVALID_ARG, "lse_out misaligned");
+  }
+  if ((n_q + 255) / 256 > 0x7fffffff) return fail(QWM_ERR_UNSUPPORTED, "n_q too large");
+  const int elem = qwm::elem_bytes(*cfg);
+  const bool tables = qwm::attend_tables_fit(cfg->head_dim, elem, cfg->rank, cfg->n_centroids);
+  const quantwm_calib_layout C = qwm::calib_layout(*cfg);
+  qwm::AttendArgs a;
+  a.calib = static_cast<const uint8_t*>(calib);
+  a.slab = C.slab_bytes;
+  a.o_mu_k = C.mu_k; a.o_mu_v = C.mu_v; a.o_u_t = C.u_t;
+  a.cache = static_cast<const uint8_t*>(cache);
+  a.L = qwm::cache_layout(*cfg);
+  a.q = q; a.out = out; a.lse = lse_out; a.logits = logits_out;
+  a.n_cache = n_cache; a.n_q = n_q; a.q_start = q_start;
+  a.frame_tokens = frame_tokens; a.heads = cfg->heads; a.n_centroids = cfg->n_centroids; a.rank = cfg->rank;
+  a.tables_in_lds = tables ? 1 : 0;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool lg = logits_out != nullptr;
+  const hipError_t e = cfg->dtype == QWM_BF16 ? qwm::launch_attend_bf16(a, cfg->head_dim, cfg->batch, lg, s)
+                                              : qwm::launch_attend_f32(a, cfg->head_dim, cfg->batch, lg, s);
+  if (e != hipSuccess) return hip_fail(e, "attend launch");
+  return ok();
+}
+
+quantwm_status quantwm_attend(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
+                              const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
+                              float* lse_out, void* stream) {
+  return attend_common(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, out, lse_out, nullptr, stream);
+}
+
+quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
+                              const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, float* logits_out,
+                              void* stream) {
+  if (!logits_out && n_q > 0) return fail(QWM_ERR_INVALID_ARG, "logits_out is null");
+  return attend_common(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, nullptr, nullptr, logits_out,
+                       stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,334 @@
+// Quantize-on-append for gfx950: QSAC centroid choice (Sec. 4.1, Eq. 9-12),
+// group-wise INT2 residual (Eq. 1-4, App. D.1) and PSAC coefficients
+// (Sec. 4.2, Eq. 13 and 16) for Keys; nearest centroid + INT2 residual for
+// Values.
+//
+// Mapping: one token-head per lane, 256 tokens of one (b, h) per workgroup. The
+// candidate search is the dominant cost (Kc * d multiply-adds per token for K
+// and again for V). It uses the expanded distance
+//     d'_j = b_j + sum_c a_jc k_c,  a_jc = -2 w_c mu_jc,  b_j = sum_c w_c mu_jc^2,
+// which equals Eq. 9 minus the centroid-independent sum_c w_c k_c^2, so it has
+// the same ordering in exact arithmetic at one FMA per term. a and b are
+// wave-uniform and arrive through scalar loads, so the vector ALU does nothing
+// but FMAs in the inner loop. Everything that turns a float into an integer
+// (the Eq. 12 score, the INT2 and INT8 codes) follows the equations' operation
+// order in fp32 with IEEE division and round-to-nearest-even.
+#include "qwm_common.h"
+
+#include <type_traits>
+
+namespace qwm {
+namespace {
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E) step S.
+// Keeps register-array indices static where #pragma unroll gives up on large bodies.
+template <int B, int E, int S = 1, typename F>
+__device__ inline void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + S, E, S>(f);
+  }
+}
+
+__device__ inline float ld(const float* p) { return *p; }
+__device__ inline float ld(const bf16* p) { return (float)*p; }
+
+template <typename T, int D>
+__device__ inline void load_row(const T* __restrict__ src, float (&x)[D]) {
+  if constexpr (sizeof(T) == 2) {
+    const uint4* p = reinterpret_cast<const uint4*>(src);
+#pragma unroll
+    for (int i = 0; i < D / 8; ++i) {
+      uint4 u = p[i];
+      uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        x[8 * i + 2 * k] = __uint_as_float(w[k] << 16);
+        x[8 * i + 2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+      }
+    }
+  } else {
+    const float4* p = reinterpret_cast<const float4*>(src);
+#pragma unroll
+    for (int i = 0; i < D / 4; ++i) {
+      float4 u = p[i];
+      x[4 * i] = u.x; x[4 * i + 1] = u.y; x[4 * i + 2] = u.z; x[4 * i + 3] = u.w;
+    }
+  }
+}
+
+__device__ inline float f16_round(float s) {
+  // FP16 storage of a scale (App. D.1): saturate, then round to nearest even.
+  s = fminf(s, 65504.0f);
+  return (float)(_Float16)s;
+}
+
+__device__ inline uint16_t f16_bits(float exact) {
+  return __builtin_bit_cast(uint16_t, (_Float16)exact);
+}
+
+// Code of one channel given its group's stored scale s and zero-point z (Eq. 1).
+__device__ inline int quant_code(float x, float mu, float s, int z) {
+  if (s == 0.0f) return 0;
+  return (int)fminf(fmaxf(rintf((x - mu) / s) + (float)z, 0.0f), 3.0f);
+}
+
+// Residual of one token against centroid row mu_row, group by group (Eq. 1-2
+// with q_min = 0, q_max = 3, the range extended to contain 0, the residual
+// quantised with the stored FP16 scale). The fp32 reconstruction
+// mu + s (q - z) (Eq. 4) of each channel goes to `each(c, xhat)`. Centroid
+// values stream in chunks of 16 (re-read from L1 in the second pass) so that
+// only the token itself stays resident in registers.
+template <typename T, int D, int G, typename F>
+__device__ inline void quant_token(float (&x)[D], const T* __restrict__ mu_row, uint32_t (&cw)[D / 16],
+                                   int (&zg)[D / G], float (&sg)[D / G], F each) {
+  constexpr int CH = G < 16 ? G : 16;
+#pragma unroll
+  for (int w = 0; w < D / 16; ++w) cw[w] = 0;
+  static_for<0, D / G>([&](auto gi) {
+    constexpr int g = decltype(gi)::value;
+    float lo = 0.0f, hi = 0.0f;
+    static_for<0, G, CH>([&](auto ci) {
+      constexpr int c0 = decltype(ci)::value;
+      float mu[CH];
+      load_row<T, CH>(mu_row + g * G + c0, mu);
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        const float r = x[g * G + c0 + c] - mu[c];
+        lo = r < lo ? r : lo;
+        hi = r > hi ? r : hi;
+      }
+    });
+    const float s = f16_round((hi - lo) / 3.0f);
+    int z = 0;
+    if (s != 0.0f) z = (int)fminf(fmaxf(rintf(0.0f - lo / s), 0.0f), 3.0f);
+    zg[g] = z;
+    sg[g] = s;
+    static_for<0, G, CH>([&](auto ci) {
+      constexpr int c0 = decltype(ci)::value;
+      float mu[CH];
+      load_row<T, CH>(mu_row + g * G + c0, mu);
+      static_for<0, CH>([&](auto cc) {
+        constexpr int ch = g * G + c0 + decltype(cc)::value;
+        const float m = mu[decltype(cc)::value];
+        const int q = quant_code(x[ch], m, s, z);
+        cw[ch / 16] |= uint32_t(q) << (2 * (ch % 16));
+        each(std::integral_constant<int, ch>{}, m + s * (float)(q - z));
+      });
+    });
+  });
+}
+
+template <int D, int G>
+__device__ inline void store_residual(uint8_t* __restrict__ codes, uint8_t* __restrict__ zp_dst,
+                                      uint8_t* __restrict__ scale_dst, const uint32_t (&cw)[D / 16],
+                                      const int (&zg)[D / G], const float (&sg)[D / G]) {
+  constexpr int NG = D / G;
+  uint4* cp = reinterpret_cast<uint4*>(codes);
+#pragma unroll
+  for (int i = 0; i < D / 64; ++i) cp[i] = make_uint4(cw[4 * i], cw[4 * i + 1], cw[4 * i + 2], cw[4 * i + 3]);
+  uint32_t z = 0;
+#pragma unroll
+  for (int g = 0; g < NG; ++g) z |= uint32_t(zg[g]) << (2 * g);
+  zp_dst[0] = uint8_t(z & 255);
+  if constexpr (NG > 4) zp_dst[1] = uint8_t(z >> 8);
+  uint16_t* sp = reinterpret_cast<uint16_t*>(scale_dst);
+#pragma unroll
+  for (int g = 0; g < NG; ++g) sp[g] = f16_bits(sg[g]);
+}
+
+// Bubble (dist, id) into a list kept sorted by (dist, id); ids arrive in
+// increasing order, so a strict comparison keeps the lower id first on ties.
+template <int MM>
+__device__ inline void topm_insert(float (&bd)[MM], int (&bi)[MM], float dv, int iv) {
+#pragma unroll
+  for (int p = 0; p < MM; ++p) {
+    const bool lt = dv < bd[p];
+    const float td = lt ? bd[p] : dv;
+    const int ti = lt ? bi[p] : iv;
+    bd[p] = lt ? dv : bd[p];
+    bi[p] = lt ? iv : bi[p];
+    dv = td;
+    iv = ti;
+  }
+}
+
+template <typename T, int D, int G, int RP, int MM>
+__global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
+  constexpr int NG = D / G;
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const bool active = t < a.n_new;
+  const int64_t tt = active ? t : a.n_new - 1;  // idle lanes recompute a real token and store nothing
+  const int64_t bh = int64_t(b) * a.heads + h;
+  const uint8_t* slab = a.calib + bh * a.slab;
+  const float* __restrict__ ak = reinterpret_cast<const float*>(slab + a.o_a_k);
+  const float* __restrict__ bk = reinterpret_cast<const float*>(slab + a.o_b_k);
+  const float* __restrict__ av = reinterpret_cast<const float*>(slab + a.o_a_v);
+  const float* __restrict__ bv = reinterpret_cast<const float*>(slab + a.o_b_v);
+  const float* __restrict__ wg = reinterpret_cast<const float*>(slab + a.o_wg);
+  const T* __restrict__ muk = reinterpret_cast<const T*>(slab + a.o_mu_k);
+  const T* __restrict__ muv = reinterpret_cast<const T*>(slab + a.o_mu_v);
+  const T* __restrict__ ut = reinterpret_cast<const T*>(slab + a.o_u_t);
+  const int Kc = a.n_centroids;
+  const int64_t src = ((int64_t(b) * a.n_new + tt) * a.heads + h) * D;
+  const int64_t slot = bh * a.L.slots + a.n_cached + tt;
+
+  float x[D];
+  load_row<T, D>(reinterpret_cast<const T*>(a.k) + src, x);
+
+  // ---- QSAC candidate search (Eq. 9, expanded form), top-M by (d', id)
+  float bd[MM];
+  int bi[MM];
+#pragma unroll
+  for (int p = 0; p < MM; ++p) { bd[p] = __builtin_inff(); bi[p] = 0x7fffffff; }
+  for (int j = 0; j < Kc; j += 4) {
+    float acc[4];
+    int row[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      row[u] = min(j + u, Kc - 1);
+      acc[u] = bk[row[u]];
+    }
+#pragma unroll
+    for (int c = 0; c < D; ++c)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] = __builtin_fmaf(ak[row[u] * D + c], x[c], acc[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (j + u < Kc) topm_insert<MM>(bd, bi, acc[u], j + u);
+  }
+
+  // ---- QSAC score (Eq. 10, 12) over the M candidates; ties to the lower id
+  const int M = a.top_m < Kc ? a.top_m : Kc;
+  int z = 0;
+  float zs = __builtin_inff();
+  static_for<0, MM>([&](auto mi) {
+    constexpr int m = decltype(mi)::value;
+    if (m >= M) return;
+    const int j = bi[m];
+    const T* mrow = muk + int64_t(j) * D;
+    float S = 0.0f;
+    static_for<0, NG>([&](auto gi) {
+      constexpr int g = decltype(gi)::value;
+      float mx = -__builtin_inff(), mn = __builtin_inff();
+#pragma unroll
+      for (int c0 = 0; c0 < G; c0 += 16) {
+        float mu[16];
+        load_row<T, 16>(mrow + g * G + c0, mu);
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+          const float r = x[g * G + c0 + c] - mu[c];
+          mx = r > mx ? r : mx;
+          mn = r < mn ? r : mn;
+        }
+      }
+      const float R = mx - mn;
+      S = S + wg[g] * (R * R);
+    });
+    if (S < zs || (S == zs && j < z)) { zs = S; z = j; }
+  });
+
+  // ---- INT2 residual against mu_z; the key registers become E = k - khat_0 (Eq. 13)
+  {
+    uint32_t cw[D / 16];
+    int zg[NG];
+    float sg[NG];
+    quant_token<T, D, G>(x, muk + int64_t(z) * D, cw, zg, sg, [&](auto ci, float xhat) {
+      constexpr int c = decltype(ci)::value;
+      x[c] = x[c] - xhat;
+    });
+    if (active) {
+      store_residual<D, G>(a.cache + a.L.k_codes + slot * (D / 4), a.cache + a.L.k_zp + slot * a.L.zpb,
+                           a.cache + a.L.k_scale + slot * 2 * NG, cw, zg, sg);
+      a.cache[a.L.k_ids + slot] = uint8_t(z);
+    }
+  }
+  // ---- PSAC: C = E U_r (Eq. 16), INT8 with one FP16 row scale (App. D.1).
+  // The rows of U_r are wave-uniform (scalar loads); C goes through LDS so that
+  // the rank loop stays a runtime loop.
+  if constexpr (RP > 0) {
+    __shared__ float cbuf[RP][256];
+    const int r = a.rank;
+    float amax = 0.0f;
+    for (int k = 0; k < r; ++k) {
+      float acc = 0.0f;
+      const T* urow = ut + int64_t(k) * D;
+#pragma unroll
+      for (int c = 0; c < D; ++c) acc = __builtin_fmaf(x[c], ld(urow + c), acc);
+      cbuf[k][threadIdx.x] = acc;
+      amax = fmaxf(amax, fabsf(acc));
+    }
+    const float s = f16_round(amax / 127.0f);
+    if (active) {
+      int8_t* code = reinterpret_cast<int8_t*>(a.cache + a.L.k_coef + slot * r);
+      float* co = a.coef_out ? a.coef_out + (bh * a.n_new + tt) * r : nullptr;
+      for (int k = 0; k < r; ++k) {
+        const float ck = cbuf[k][threadIdx.x];
+        code[k] = int8_t(s != 0.0f ? (int)fminf(fmaxf(rintf(ck / s), -127.0f), 127.0f) : 0);
+        if (co) co[k] = ck;
+      }
+      *reinterpret_cast<uint16_t*>(a.cache + a.L.k_cscale + slot * 2) = f16_bits(s);
+    }
+  }
+
+  // ---- Values: nearest centroid (w = 1), same residual path, no PSAC
+  load_row<T, D>(reinterpret_cast<const T*>(a.v) + src, x);
+  int zv = 0;
+  float dv = __builtin_inff();
+  for (int j = 0; j < Kc; j += 4) {
+    float acc[4];
+    int row[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      row[u] = min(j + u, Kc - 1);
+      acc[u] = bv[row[u]];
+    }
+#pragma unroll
+    for (int c = 0; c < D; ++c)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] = __builtin_fmaf(av[row[u] * D + c], x[c], acc[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (j + u < Kc && acc[u] < dv) { dv = acc[u]; zv = j + u; }
+  }
+  {
+    uint32_t cw[D / 16];
+    int zg[NG];
+    float sg[NG];
+    quant_token<T, D, G>(x, muv + int64_t(zv) * D, cw, zg, sg, [](auto, float) {});
+    if (active) {
+      store_residual<D, G>(a.cache + a.L.v_codes + slot * (D / 4), a.cache + a.L.v_zp + slot * a.L.zpb,
+                           a.cache + a.L.v_scale + slot * 2 * NG, cw, zg, sg);
+      a.cache[a.L.v_ids + slot] = uint8_t(zv);
+    }
+  }
+}
+
+template <typename T, int D, int G>
+hipError_t launch_dg(const AppendArgs& a, int batch, hipStream_t s) {
+  const dim3 grid((unsigned)((a.n_new + 255) / 256), (unsigned)a.heads, (unsigned)batch);
+  const bool psac = a.rank > 0;
+  const bool wide = a.top_m > 4;
+  if (psac && wide) hipLaunchKernelGGL((append_kernel<T, D, G, 32, 8>), grid, dim3(256), 0, s, a);
+  else if (psac) hipLaunchKernelGGL((append_kernel<T, D, G, 32, 4>), grid, dim3(256), 0, s, a);
+  else if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 0, 8>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((append_kernel<T, D, G, 0, 4>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// This file is compiled once per (element type, head_dim): QWM_APPEND_T and
+// QWM_APPEND_D select the instantiations and the launcher's name.
+#define QWM_CAT2(a, b, c) a##b##_##c
+#define QWM_CAT(a, b, c) QWM_CAT2(a, b, c)
+hipError_t QWM_CAT(launch_append_, QWM_APPEND_TN, QWM_APPEND_D)(const AppendArgs& a, int g, int batch,
+                                                                 hipStream_t s) {
+  if (g == 16) return launch_dg<QWM_APPEND_T, QWM_APPEND_D, 16>(a, batch, s);
+  if (g == 32) return launch_dg<QWM_APPEND_T, QWM_APPEND_D, 32>(a, batch, s);
+  if (g == 64) return launch_dg<QWM_APPEND_T, QWM_APPEND_D, 64>(a, batch, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace qwm

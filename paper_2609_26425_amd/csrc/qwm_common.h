@@ -1,0 +1,125 @@
+// Shared host/device definitions of the QuantWM HIP library: packed-cache and
+// calibration-block layouts, element types and kernel argument blocks.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/quantwm.h"
+
+namespace qwm {
+
+typedef __bf16 bf16;
+
+// Packed cache layout (App. D.1 storage, section order fixed by quantwm.h).
+struct CacheLayout {
+  int d, ng, zpb, r;
+  int k_bytes, v_bytes;
+  int64_t slots;  // per (b, h): capacity rounded up to 64
+  int64_t k_codes, k_ids, k_zp, k_scale, k_coef, k_cscale;
+  int64_t v_codes, v_ids, v_zp, v_scale;
+  int64_t total;
+};
+
+inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+inline CacheLayout cache_layout(const quantwm_config& c) {
+  CacheLayout L;
+  L.d = c.head_dim;
+  L.ng = c.head_dim / c.group_size;
+  L.zpb = (L.ng + 3) / 4;
+  L.r = c.rank;
+  L.slots = (c.capacity + 63) / 64 * 64;
+  const int64_t rows = int64_t(c.batch) * c.heads * L.slots;
+  int64_t at = 0;
+  auto take = [&](int64_t per_token) { int64_t o = at; at = align256(at + rows * per_token); return o; };
+  L.k_codes = take(L.d / 4);
+  L.k_ids = take(1);
+  L.k_zp = take(L.zpb);
+  L.k_scale = take(2 * L.ng);
+  L.k_coef = take(L.r);
+  L.k_cscale = take(L.r > 0 ? 2 : 0);
+  L.v_codes = take(L.d / 4);
+  L.v_ids = take(1);
+  L.v_zp = take(L.zpb);
+  L.v_scale = take(2 * L.ng);
+  L.total = at;
+  L.v_bytes = L.d / 4 + 1 + L.zpb + 2 * L.ng;
+  L.k_bytes = L.v_bytes + (L.r > 0 ? L.r + 2 : 0);
+  return L;
+}
+
+inline int elem_bytes(const quantwm_config& c) { return c.dtype == QWM_BF16 ? 2 : 4; }
+
+inline quantwm_calib_layout calib_layout(const quantwm_config& c) {
+  quantwm_calib_layout L;
+  const int64_t d = c.head_dim, K = c.n_centroids, r = c.rank, e = elem_bytes(c);
+  int64_t at = 0;
+  auto take = [&](int64_t bytes) { int64_t o = at; at = align256(at + bytes); return o; };
+  L.mu_k = take(K * d * e);
+  L.mu_v = take(K * d * e);
+  L.a_k = take(K * d * 4);
+  L.b_k = take(K * 4);
+  L.a_v = take(K * d * 4);
+  L.b_v = take(K * 4);
+  L.w = take(d * 4);
+  L.wg = take((d / c.group_size) * 4);
+  L.u_t = take(r * d * e);
+  L.lam = take(r * 4);
+  L.slab_bytes = at;
+  return L;
+}
+
+// ------------------------------------------------------------ kernel args
+
+struct AppendArgs {
+  const uint8_t* calib;
+  int64_t slab;
+  int64_t o_mu_k, o_mu_v, o_a_k, o_b_k, o_a_v, o_b_v, o_wg, o_u_t;
+  uint8_t* cache;
+  CacheLayout L;
+  const void* k;
+  const void* v;
+  int64_t n_new, n_cached;
+  int heads, n_centroids, rank, top_m;
+  float* coef_out;
+};
+
+struct AttendArgs {
+  const uint8_t* calib;
+  int64_t slab;
+  int64_t o_mu_k, o_mu_v, o_u_t;
+  const uint8_t* cache;
+  CacheLayout L;
+  const void* q;
+  void* out;
+  float* lse;
+  float* logits;
+  int64_t n_cache, n_q, q_start;
+  int frame_tokens, heads, n_centroids, rank;
+  int tables_in_lds;
+};
+
+// Launchers (one translation unit per element type).
+hipError_t launch_append_f32_64(const AppendArgs& a, int g, int batch, hipStream_t s);
+hipError_t launch_append_f32_128(const AppendArgs& a, int g, int batch, hipStream_t s);
+hipError_t launch_append_bf16_64(const AppendArgs& a, int g, int batch, hipStream_t s);
+hipError_t launch_append_bf16_128(const AppendArgs& a, int g, int batch, hipStream_t s);
+hipError_t launch_attend_f32(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s);
+hipError_t launch_attend_bf16(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s);
+size_t attend_lds_bytes(int d, int elem, int rank, int n_centroids, bool tables_in_lds);
+bool attend_tables_fit(int d, int elem, int rank, int n_centroids);
+
+hipError_t launch_derive_constants(const quantwm_config& c, uint8_t* calib, hipStream_t s);
+hipError_t launch_pack_tables(const quantwm_config& c, const void* mu_k, const void* mu_v,
+                              const float* w, const void* u_t, const float* lam, uint8_t* calib,
+                              hipStream_t s);
+hipError_t launch_second_moment(const quantwm_config& c, const void* q, int64_t n, double* m_out,
+                                hipStream_t s);
+hipError_t launch_kmeans(const quantwm_config& c, const void* x, int64_t n, int iters, uint8_t* calib,
+                         int64_t o_mu, int32_t* assign_ws, hipStream_t s);
+
+// Host fp64 symmetric eigensolver: eigenvalues descending, eigenvectors as rows.
+void host_eigh(const double* a, int n, double* lam, double* vecs_t);
+
+}  // namespace qwm

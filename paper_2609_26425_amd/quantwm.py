@@ -1,0 +1,165 @@
+"""ctypes binding of libquantwm.so: the QuantWM hot path on MI355X (gfx950).
+
+Argument marshalling only: torch tensors become device pointers, the current
+torch stream becomes the hipStream_t, and a non-zero status raises
+QuantwmError. Every step of the path runs in the library's HIP kernels; there
+is no fallback, and a missing library is an ImportError.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libquantwm.so")
+
+F32, BF16 = 0, 1
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_HIP = 0, 1, 2, 3, 4
+
+
+class QuantwmError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"quantwm status {status}: {message}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    """Mirror of quantwm_config."""
+    _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("n_centroids", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("rank", ctypes.c_int32), ("top_m", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("capacity", ctypes.c_int64)]
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == BF16 else torch.float32
+
+
+class CalibLayout(ctypes.Structure):
+    """Mirror of quantwm_calib_layout (byte offsets inside one (b, h) slab)."""
+    _fields_ = [(n, ctypes.c_int64) for n in
+                ("slab_bytes", "mu_k", "mu_v", "a_k", "b_k", "a_v", "b_v", "w", "wg", "u_t", "lam")]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with paper_2609_26425_amd/build.py "
+                          "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    C = ctypes.POINTER(Config)
+    sig = {
+        "quantwm_cache_bytes": (SZ, [C]),
+        "quantwm_token_bytes": (I32, [C, ctypes.POINTER(I32), ctypes.POINTER(I32)]),
+        "quantwm_calib_bytes": (SZ, [C]),
+        "quantwm_calib_offsets": (I32, [C, ctypes.POINTER(CalibLayout)]),
+        "quantwm_calibrate_workspace_bytes": (SZ, [C, I64, I64]),
+        "quantwm_calib_pack": (I32, [C, P, P, P, P, P, P, P]),
+        "quantwm_calibrate": (I32, [C, P, I64, P, P, I64, I32, P, P, SZ, P]),
+        "quantwm_append": (I32, [C, P, P, I64, P, P, I64, P, P]),
+        "quantwm_attend": (I32, [C, P, P, I64, P, I64, I64, I32, P, P, P]),
+        "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I32, P, P]),
+        "quantwm_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype, fn.argtypes = res, args
+    return lib
+
+
+_lib = _load()
+
+EXPORTED = ("quantwm_cache_bytes", "quantwm_token_bytes", "quantwm_calib_bytes", "quantwm_calib_offsets",
+            "quantwm_calibrate_workspace_bytes", "quantwm_calib_pack", "quantwm_calibrate",
+            "quantwm_append", "quantwm_attend", "quantwm_logits", "quantwm_last_error")
+
+
+def library():
+    return _lib
+
+
+def make_config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, dtype) -> Config:
+    dt = {"bf16": BF16, "f32": F32, BF16: BF16, F32: F32}[dtype]
+    return Config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, dt, capacity)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch.Tensor or None")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        if not torch.cuda.is_available():
+            return None
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _check(status):
+    if status != OK:
+        raise QuantwmError(status, (_lib.quantwm_last_error() or b"").decode())
+
+
+def quantwm_last_error() -> str:
+    return (_lib.quantwm_last_error() or b"").decode()
+
+
+def quantwm_cache_bytes(cfg: Config) -> int:
+    return int(_lib.quantwm_cache_bytes(ctypes.byref(cfg)))
+
+
+def quantwm_token_bytes(cfg: Config):
+    k, v = ctypes.c_int32(), ctypes.c_int32()
+    _check(_lib.quantwm_token_bytes(ctypes.byref(cfg), ctypes.byref(k), ctypes.byref(v)))
+    return k.value, v.value
+
+
+def quantwm_calib_bytes(cfg: Config) -> int:
+    return int(_lib.quantwm_calib_bytes(ctypes.byref(cfg)))
+
+
+def quantwm_calib_offsets(cfg: Config) -> CalibLayout:
+    out = CalibLayout()
+    _check(_lib.quantwm_calib_offsets(ctypes.byref(cfg), ctypes.byref(out)))
+    return out
+
+
+def quantwm_calibrate_workspace_bytes(cfg: Config, n_hist: int, n_calib: int) -> int:
+    return int(_lib.quantwm_calibrate_workspace_bytes(ctypes.byref(cfg), n_hist, n_calib))
+
+
+def quantwm_calib_pack(cfg, mu_k, mu_v, w, u_t, lam, calib, stream=None):
+    _check(_lib.quantwm_calib_pack(ctypes.byref(cfg), _ptr(mu_k), _ptr(mu_v), _ptr(w), _ptr(u_t), _ptr(lam),
+                                   _ptr(calib), _stream(stream)))
+
+
+def quantwm_calibrate(cfg, q_hist, n_hist, k_calib, v_calib, n_calib, kmeans_iters, calib, workspace,
+                      stream=None):
+    _check(_lib.quantwm_calibrate(ctypes.byref(cfg), _ptr(q_hist), n_hist, _ptr(k_calib), _ptr(v_calib), n_calib,
+                                  kmeans_iters, _ptr(calib), _ptr(workspace),
+                                  0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                  _stream(stream)))
+
+
+def quantwm_append(cfg, calib, cache, n_cached, k_new, v_new, n_new, coef_f32_out=None, stream=None):
+    _check(_lib.quantwm_append(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cached, _ptr(k_new), _ptr(v_new),
+                               n_new, _ptr(coef_f32_out), _stream(stream)))
+
+
+def quantwm_attend(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, out, lse_out=None, stream=None):
+    _check(_lib.quantwm_attend(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cache, _ptr(q), n_q, q_start,
+                               frame_tokens, _ptr(out), _ptr(lse_out), _stream(stream)))
+
+
+def quantwm_logits(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, logits_out, stream=None):
+    _check(_lib.quantwm_logits(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cache, _ptr(q), n_q, q_start,
+                               frame_tokens, _ptr(logits_out), _stream(stream)))

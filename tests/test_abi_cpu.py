@@ -1,0 +1,78 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every entry point that include/quantwm.h declares, and its size queries and
+argument validation behave as documented (no kernel is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_2609_26425_amd import quantwm as qw
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "quantwm.h")).read()
+    return sorted(set(re.findall(r"\b(quantwm_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_symbols_are_exported():
+    names = declared_symbols()
+    assert len(names) >= 10
+    lib = ctypes.CDLL(qw.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in quantwm.h but not exported"
+    assert set(names) == set(qw.EXPORTED)
+
+
+@pytest.mark.parametrize("shape", [(1, 2, 64, 16, 32, 4, 4, 1024, "f32"), (1, 12, 128, 64, 32, 8, 4, 13200, "bf16"),
+                                   (1, 40, 128, 128, 32, 16, 4, 32760, "bf16"),
+                                   (4, 30, 128, 256, 64, 32, 4, 24960, "bf16"), (2, 3, 128, 37, 32, 12, 3, 1000, "bf16"),
+                                   (1, 2, 64, 24, 16, 20, 8, 700, "bf16"), (1, 2, 128, 5, 64, 0, 1, 513, "bf16")])
+def test_sizes_agree_with_the_oracle_format(shape):
+    B, H, d, K, G, r, M, cap, dt = shape
+    cfg = qw.make_config(B, H, d, K, G, r, M, cap, dt)
+    ocfg = oracle.cfg_of(B, H, d, K, G, r, M, cap, dt == "bf16")
+    assert qw.quantwm_cache_bytes(cfg) == oracle.cache_bytes(ocfg)
+    assert qw.quantwm_token_bytes(cfg) == oracle.token_bytes(ocfg)
+    L = qw.quantwm_calib_offsets(cfg)
+    assert qw.quantwm_calib_bytes(cfg) == L.slab_bytes * B * H
+    offs = [L.mu_k, L.mu_v, L.a_k, L.b_k, L.a_v, L.b_v, L.w, L.wg, L.u_t, L.lam]
+    assert all(o % 256 == 0 for o in offs) and offs == sorted(offs) and L.slab_bytes % 256 == 0
+
+
+def test_validation_without_a_gpu():
+    good = qw.make_config(1, 2, 128, 16, 32, 8, 4, 100, "bf16")
+    for bad, status in [(qw.make_config(1, 2, 96, 16, 32, 8, 4, 100, "bf16"), qw.ERR_UNSUPPORTED),
+                        (qw.make_config(1, 2, 128, 300, 32, 8, 4, 100, "bf16"), qw.ERR_INVALID_ARG),
+                        (qw.make_config(1, 2, 128, 16, 48, 8, 4, 100, "bf16"), qw.ERR_INVALID_ARG),
+                        (qw.make_config(1, 2, 128, 16, 32, 40, 4, 100, "bf16"), qw.ERR_UNSUPPORTED),
+                        (qw.make_config(1, 2, 128, 16, 32, 8, 9, 100, "bf16"), qw.ERR_UNSUPPORTED),
+                        (qw.make_config(0, 2, 128, 16, 32, 8, 4, 100, "bf16"), qw.ERR_INVALID_ARG)]:
+        with pytest.raises(qw.QuantwmError) as e:
+            qw.quantwm_token_bytes(bad)
+        assert e.value.status == status
+        assert qw.quantwm_cache_bytes(bad) == 0
+    # checks that fire before any device work
+    with pytest.raises(qw.QuantwmError) as e:
+        qw._check(qw.library().quantwm_append(ctypes.byref(good), None, None, 90, None, None, 20, None, None))
+    assert e.value.status == qw.ERR_CAPACITY
+    with pytest.raises(qw.QuantwmError) as e:
+        qw._check(qw.library().quantwm_append(ctypes.byref(good), None, None, 0, None, None, 5, None, None))
+    assert e.value.status == qw.ERR_INVALID_ARG and "calib" in qw.quantwm_last_error()
+    with pytest.raises(qw.QuantwmError) as e:
+        qw._check(qw.library().quantwm_append(ctypes.byref(good), ctypes.c_void_p(0x1008), ctypes.c_void_p(0x2000),
+                                              0, ctypes.c_void_p(0x3000), ctypes.c_void_p(0x4000), 5, None, None))
+    assert "aligned" in qw.quantwm_last_error()
+    with pytest.raises(qw.QuantwmError) as e:
+        qw._check(qw.library().quantwm_attend(ctypes.byref(good), None, None, 50, None, 4, 60, 1, None, None, None))
+    assert e.value.status == qw.ERR_INVALID_ARG
+    with pytest.raises(qw.QuantwmError) as e:
+        qw._check(qw.library().quantwm_attend(ctypes.byref(good), None, None, 50, None, 4, 10, 0, None, None, None))
+    assert "frame_tokens" in qw.quantwm_last_error()
+    # empty calls are OK no-ops and touch nothing
+    assert qw.library().quantwm_append(ctypes.byref(good), None, None, 0, None, None, 0, None, None) == qw.OK
+    assert qw.library().quantwm_attend(ctypes.byref(good), None, None, 0, None, 0, 0, 1, None, None, None) == qw.OK
+    assert qw.quantwm_last_error() == ""

@@ -1,0 +1,359 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bar (ids and codes exact except counted fp32 near-ties; PSAC coefficients
+within 1e-4 relative; logits within 1e-3 relative; outputs within 2e-2 max-abs
+for bf16). Small cases run the oracle on every head; the benchmark workloads run
+the GPU at full size in the benchmark's launch configuration, with every head
+replicating one of a few oracle-computed source heads (tests/harness.py).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import harness
+import oracle
+import packed
+import synth
+
+pytestmark = pytest.mark.gpu
+
+from paper_2609_26425_amd import quantwm as qw  # noqa: E402  (fails loudly if the library is missing)
+
+DEV = "cuda:0"
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def tdev(x, dtype):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV).to(dtype)
+
+
+def gpu_config(wl, capacity=None):
+    return qw.make_config(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank,
+                          wl.top_m, wl.n_cache if capacity is None else capacity, wl.dtype)
+
+
+def gpu_calib_from_tables(cfg, tables):
+    mu_k, mu_v, w, u_t, lam = tables
+    dt = cfg.torch_dtype
+    calib = torch.empty(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=DEV)
+    qw.quantwm_calib_pack(cfg, tdev(mu_k, dt), tdev(mu_v, dt), tdev(w, torch.float32),
+                          tdev(u_t, dt) if cfg.rank > 0 else None, tdev(lam, torch.float32) if cfg.rank > 0 else None,
+                          calib)
+    return calib
+
+
+def gpu_append_all(wl, cfg, calib, k_full, v_full):
+    dt = cfg.torch_dtype
+    cache = torch.zeros(qw.quantwm_cache_bytes(cfg), dtype=torch.uint8, device=DEV)
+    coef = torch.zeros((wl.batch, wl.heads, wl.n_cache, max(wl.rank, 1)), dtype=torch.float32, device=DEV)
+    kd, vd = tdev(k_full, dt), tdev(v_full, dt)
+    for start, n in wl.chunks():
+        kc = kd[:, start:start + n].contiguous()
+        vc = vd[:, start:start + n].contiguous()
+        co = torch.zeros((wl.batch, wl.heads, n, max(wl.rank, 1)), dtype=torch.float32, device=DEV) \
+            if wl.rank > 0 else None
+        qw.quantwm_append(cfg, calib, cache, start, kc, vc, n, co)
+        if co is not None:
+            coef[:, :, start:start + n] = co
+    torch.cuda.synchronize()
+    return cache.cpu().numpy(), coef[..., :wl.rank].cpu().numpy()
+
+
+def check_append(case, gpu_cache, gpu_coef):
+    wl = case.wl
+    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.n_cache)
+    mu_k, mu_v, w = case.tables[0][0], case.tables[1][0], case.tables[2][0]
+    M = min(wl.top_m, wl.n_centroids)
+    stats = {"tokens": 0, "k_ties": 0, "v_ties": 0, "coef_half": 0, "cscale_f16": 0}
+    for bh in range(wl.batch * wl.heads):
+        s = int(case.src_of[bh])
+        g = packed.fields(gpu_cache, lay, bh, 0, wl.n_cache)
+        o = packed.fields(case.cache, case.lay, s, 0, wl.n_cache)
+        stats["tokens"] += wl.n_cache
+        kmis = np.nonzero(g["k_ids"] != o["k_ids"])[0]
+        for t in kmis:
+            assert harness.qsac_near_tie(case.k[0, t, s], mu_k[s], w[s], M), \
+                f"head {bh} token {t}: K centroid {g['k_ids'][t]} vs oracle {o['k_ids'][t]} is not a near-tie"
+        vmis = np.nonzero(g["v_ids"] != o["v_ids"])[0]
+        for t in vmis:
+            assert harness.nearest_near_tie(case.v[0, t, s], mu_v[s]), \
+                f"head {bh} token {t}: V centroid {g['v_ids'][t]} vs oracle {o['v_ids'][t]} is not a near-tie"
+        stats["k_ties"] += len(kmis)
+        stats["v_ties"] += len(vmis)
+        kok = np.ones(wl.n_cache, bool); kok[kmis] = False
+        vok = np.ones(wl.n_cache, bool); vok[vmis] = False
+        for f in ("k_codes", "k_zp", "k_scale"):
+            bad = np.nonzero((g[f][kok] != o[f][kok]).reshape(kok.sum(), -1).any(1))[0]
+            assert len(bad) == 0, f"head {bh}: {f} differs at tokens {np.nonzero(kok)[0][bad][:8]}"
+        for f in ("v_codes", "v_zp", "v_scale"):
+            bad = np.nonzero((g[f][vok] != o[f][vok]).reshape(vok.sum(), -1).any(1))[0]
+            assert len(bad) == 0, f"head {bh}: {f} differs at tokens {np.nonzero(vok)[0][bad][:8]}"
+        if wl.rank > 0:
+            b, h = divmod(bh, wl.heads)
+            Cg = gpu_coef[b, h][kok].astype(np.float64)
+            Co = case.diag["coef"][0, s][kok].astype(np.float64)
+            tol = 1e-4 * np.abs(Co).max(1) + 1e-7
+            err = np.abs(Cg - Co).max(1)
+            assert np.all(err <= tol), f"head {bh}: PSAC coefficient error {err.max()} > 1e-4 relative"
+            sc_g, sc_o = g["k_cscale"][kok], o["k_cscale"][kok]
+            amax = np.abs(Co).max(1).astype(np.float32) / np.float32(127.0)
+            sbad = sc_g != sc_o
+            assert np.all(harness.f16_boundary(amax[sbad])), f"head {bh}: coefficient scale differs off a tie"
+            stats["cscale_f16"] += int(sbad.sum())
+            cg, co_ = g["k_coef"][kok].astype(np.int32), o["k_coef"][kok].astype(np.int32)
+            same_scale = ~sbad
+            diff = (cg != co_) & same_scale[:, None]
+            if diff.any():
+                sval = np.array([np.uint16(x).view(np.float16) for x in sc_o], np.float64)
+                ratio = Co / np.where(sval > 0, sval, 1.0)[:, None]
+                ok = (np.abs(cg - co_) == 1) & harness.near_half(ratio, 1e-3)
+                assert np.all(ok[diff]), f"head {bh}: INT8 coefficient codes differ off a .5 tie"
+                stats["coef_half"] += int(diff.sum())
+    assert stats["k_ties"] + stats["v_ties"] <= max(4, 2e-3 * stats["tokens"]), stats
+    return stats
+
+
+def gpu_attend(wl, cfg, calib, cache_np, q_full):
+    dt = cfg.torch_dtype
+    cache = torch.from_numpy(cache_np).to(DEV)
+    q = tdev(q_full, dt)
+    out = torch.empty_like(q)
+    lse = torch.empty((wl.batch, wl.heads, wl.n_q), dtype=torch.float32, device=DEV)
+    qw.quantwm_attend(cfg, calib, cache, wl.n_cache, q, wl.n_q, wl.q_start, wl.frame_tokens, out, lse)
+    torch.cuda.synchronize()
+    return out.float().cpu().numpy(), lse.cpu().numpy()
+
+
+def check_attend(case, out, lse, rows):
+    wl = case.wl
+    src_rows = np.array([(0, int(case.src_of[b * wl.heads + h]), i) for b, h, i in rows], np.int32)
+    uniq, inv = np.unique(src_rows, axis=0, return_inverse=True)
+    o_out, o_lse, _ = oracle.attend(case.cfg, case.tables, case.cache, wl.n_cache, case.q, wl.q_start,
+                                    wl.frame_tokens, rows=uniq)
+    o_out, o_lse = o_out[inv.ravel()], o_lse[inv.ravel()]
+    g_out = out[rows[:, 0], rows[:, 2], rows[:, 1], :]
+    g_lse = lse[rows[:, 0], rows[:, 1], rows[:, 2]]
+    tol = 2e-2 if wl.dtype == "bf16" else 1e-4
+    err = np.abs(g_out - o_out)
+    assert err.max() <= tol, f"attention output max-abs error {err.max():.3g} > {tol} (mean {err.mean():.3g})"
+    fin = np.isfinite(o_lse)
+    assert np.array_equal(np.isfinite(g_lse), fin)
+    assert np.all(np.abs(g_lse[fin] - o_lse[fin]) <= harness.lse_tol(o_lse[fin])), \
+        f"lse error {np.abs(g_lse[fin] - o_lse[fin]).max():.3g}"
+    return float(err.max()), float(err.mean())
+
+
+def check_logits(case, cfg, calib, cache_np, q_full, n_q_rows):
+    """Logits hook on the first n_q_rows Queries of every head (full key range)."""
+    wl = case.wl
+    dt = cfg.torch_dtype
+    n_q = min(n_q_rows, wl.n_q)
+    q = tdev(np.ascontiguousarray(q_full[:, :n_q]), dt)
+    cache = torch.from_numpy(cache_np).to(DEV)
+    lg = torch.empty((wl.batch, wl.heads, n_q, wl.n_cache), dtype=torch.float32, device=DEV)
+    qw.quantwm_logits(cfg, calib, cache, wl.n_cache, q, n_q, wl.q_start, wl.frame_tokens, lg)
+    torch.cuda.synchronize()
+    lg = lg.cpu().numpy()
+    rows = np.array([(0, s, i) for s in range(len(case.sources)) for i in range(n_q)], np.int32)
+    _, _, o_lg = oracle.attend(case.cfg, case.tables, case.cache, wl.n_cache, np.ascontiguousarray(case.q[:, :n_q]),
+                               wl.q_start, wl.frame_tokens, rows=rows, want_logits=True)
+    worst = 0.0
+    for bh in range(wl.batch * wl.heads):
+        b, h = divmod(bh, wl.heads)
+        s = int(case.src_of[bh])
+        for i in range(n_q):
+            ref = o_lg[s * n_q + i]
+            got = lg[b, h, i]
+            vis = np.isfinite(ref)
+            assert np.array_equal(vis, np.isfinite(got)), f"mask differs at head {bh} row {i}"
+            e = np.abs(got[vis] - ref[vis]).max() / max(np.abs(ref[vis]).max(), 1e-30)
+            worst = max(worst, e)
+            assert e <= 1e-3, f"logits error {e:.3g} at head {bh} row {i}"
+    return worst
+
+
+# ------------------------------------------------------------------ cases
+
+RAGGED = synth.Workload(name="ragged", dtype="bf16", batch=2, heads=3, head_dim=128, n_cache=1000, n_q=300,
+                        q_start=700, frame_tokens=50, n_centroids=37, group_size=32, rank=12, top_m=3, q_rank=8,
+                        n_out=4, out_scale=10.0, n_hist=500, chunk=300, seed=7)
+D64 = synth.Workload(name="d64-g16-m8", dtype="bf16", batch=1, heads=2, head_dim=64, n_cache=700, n_q=130,
+                     q_start=570, frame_tokens=1, n_centroids=24, group_size=16, rank=20, top_m=8, q_rank=6,
+                     n_out=2, out_scale=10.0, n_hist=400, chunk=350, seed=8)
+NOPSAC = synth.Workload(name="g64-r0-m1", dtype="bf16", batch=1, heads=2, head_dim=128, n_cache=513, n_q=257,
+                        q_start=256, frame_tokens=64, n_centroids=5, group_size=64, rank=0, top_m=1, q_rank=4,
+                        n_out=2, out_scale=20.0, n_hist=300, chunk=513, seed=9)
+
+SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC]
+FULL = ["mg2-12h", "lingbot-40h", "batched-4x30h", "rollout-30k", "rollout-120k"]
+
+_cases = {}
+
+
+def case_for(wl, max_sources=6):
+    key = (wl.name, max_sources)
+    if key not in _cases:
+        _say(f"[oracle] building case {wl.name} ({max_sources} source heads)")
+        _cases[key] = harness.build_oracle_case(wl, max_sources)
+    return _cases[key]
+
+
+def run_case(wl, max_sources, n_heads_rows, row_step, logits_rows):
+    _say(f"[case] {wl.name}")
+    case = case_for(wl, max_sources)
+    cfg = gpu_config(wl)
+    tables = harness.full_tables(case)
+    calib = gpu_calib_from_tables(cfg, tables)
+    _say(f"[gpu] append {wl.name}")
+    g_cache, g_coef = gpu_append_all(wl, cfg, calib, harness.full_inputs(case, "k"), harness.full_inputs(case, "v"))
+    st = check_append(case, g_cache, g_coef)
+    _say(f"[ok] append {wl.name}: {st}")
+    ora_full = harness.full_oracle_cache(case)
+    q_full = harness.full_inputs(case, "q")
+    _say(f"[gpu] attend {wl.name}")
+    out, lse = gpu_attend(wl, cfg, calib, ora_full, q_full)
+    rows = harness.sample_rows(wl, n_heads_rows, row_step)
+    mx, mean = check_attend(case, out, lse, rows)
+    _say(f"[ok] attend {wl.name}: max-abs {mx:.3g} mean-abs {mean:.3g} over {len(rows)} rows")
+    if logits_rows:
+        worst = check_logits(case, cfg, calib, ora_full, q_full, logits_rows)
+        _say(f"[ok] logits {wl.name}: worst relative error {worst:.3g}")
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=[w.name for w in SMALL])
+def test_small_parity(wl):
+    run_case(wl, max_sources=64, n_heads_rows=64, row_step=1, logits_rows=wl.n_q)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_parity(name):
+    wl = synth.WORKLOADS[name]
+    run_case(wl, max_sources=3, n_heads_rows=6, row_step=37, logits_rows=16)
+
+
+# ------------------------------------------------------------ calibration
+
+def _gpu_calibrate(case):
+    wl = case.wl
+    cfg = gpu_config(wl)
+    dt = cfg.torch_dtype
+    nc = min(wl.chunk, wl.n_cache)
+    qh = harness._gen_sources(wl, case.sources, "qhist", wl.n_hist)
+    src = {"q": qh, "k": np.ascontiguousarray(case.k[:, :nc]), "v": np.ascontiguousarray(case.v[:, :nc])}
+    full = {}
+    for key, arr in src.items():
+        o = np.empty((wl.batch, arr.shape[1], wl.heads, wl.head_dim), np.float32)
+        for bh in range(wl.batch * wl.heads):
+            b, h = divmod(bh, wl.heads)
+            o[b, :, h, :] = arr[0, :, case.src_of[bh], :]
+        full[key] = tdev(o, dt)
+    calib = torch.zeros(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=DEV)
+    ws = torch.empty(qw.quantwm_calibrate_workspace_bytes(cfg, wl.n_hist, nc), dtype=torch.uint8, device=DEV)
+    qw.quantwm_calibrate(cfg, full["q"], wl.n_hist, full["k"], full["v"], nc, wl.kmeans_iters, calib, ws)
+    torch.cuda.synchronize()
+    return cfg, calib.cpu().numpy()
+
+
+def _slab_field(cfg, buf, bh, name, count, dtype):
+    L = qw.quantwm_calib_offsets(cfg)
+    off = bh * L.slab_bytes + getattr(L, name)
+    nbytes = count * np.dtype(dtype).itemsize
+    return np.frombuffer(buf[off:off + nbytes].tobytes(), dtype=dtype)
+
+
+@pytest.mark.parametrize("name", ["tiny-f32", "ragged", "mg2-12h"])
+def test_calibrate_parity(name):
+    wl = {"ragged": RAGGED}.get(name) or synth.WORKLOADS[name]
+    case = case_for(wl, 64 if name != "mg2-12h" else 3)
+    cfg, buf = _gpu_calibrate(case)
+    d, K, r = wl.head_dim, wl.n_centroids, wl.rank
+    bf = wl.dtype == "bf16"
+    for bh in range(wl.batch * wl.heads):
+        s = int(case.src_of[bh])
+        if bf:
+            mk = _slab_field(cfg, buf, bh, "mu_k", K * d, np.uint16).astype(np.uint32) << 16
+            mv = _slab_field(cfg, buf, bh, "mu_v", K * d, np.uint16).astype(np.uint32) << 16
+            mk, mv = mk.view(np.float32), mv.view(np.float32)
+        else:
+            mk = _slab_field(cfg, buf, bh, "mu_k", K * d, np.float32)
+            mv = _slab_field(cfg, buf, bh, "mu_v", K * d, np.float32)
+        np.testing.assert_array_equal(mk.reshape(K, d), case.tables[0][0, s], err_msg=f"mu_k head {bh}")
+        np.testing.assert_array_equal(mv.reshape(K, d), case.tables[1][0, s], err_msg=f"mu_v head {bh}")
+        w = _slab_field(cfg, buf, bh, "w", d, np.float32)
+        np.testing.assert_array_equal(w, case.tables[2][0, s], err_msg=f"w head {bh}")
+        if r > 0:
+            lam = _slab_field(cfg, buf, bh, "lam", r, np.float32)
+            np.testing.assert_allclose(lam, case.tables[4][0, s], rtol=1e-6)
+            if bf:
+                u = (_slab_field(cfg, buf, bh, "u_t", r * d, np.uint16).astype(np.uint32) << 16).view(np.float32)
+            else:
+                u = _slab_field(cfg, buf, bh, "u_t", r * d, np.float32)
+            u = u.reshape(r, d).astype(np.float64)
+            uo = case.tables[3][0, s].astype(np.float64)
+            tol = 2.0 ** -8 if bf else 1e-5
+            assert np.all(np.abs(u - uo) <= tol * np.abs(uo) + 1e-6), f"U_r head {bh}"
+    _say(f"[ok] calibrate {name}")
+
+
+def test_calibrate_cold_start():
+    wl = synth.WORKLOADS["tiny-f32"]
+    cfg = gpu_config(wl)
+    k = tdev(synth.tensor(wl, "k", 64), torch.float32)
+    calib = torch.zeros(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=DEV)
+    ws = torch.empty(qw.quantwm_calibrate_workspace_bytes(cfg, 0, 64), dtype=torch.uint8, device=DEV)
+    qw.quantwm_calibrate(cfg, None, 0, k, k, 64, 3, calib, ws)
+    torch.cuda.synchronize()
+    buf = calib.cpu().numpy()
+    for bh in range(wl.heads):
+        assert np.all(_slab_field(cfg, buf, bh, "w", wl.head_dim, np.float32) == 1.0)
+        assert not _slab_field(cfg, buf, bh, "u_t", wl.rank * wl.head_dim, np.float32).any()
+
+
+# ------------------------------------------------------------ edge cases
+
+def test_empty_calls_are_noops():
+    wl = RAGGED
+    case = case_for(wl, 64)
+    cfg = gpu_config(wl)
+    calib = gpu_calib_from_tables(cfg, harness.full_tables(case))
+    cache = torch.zeros(qw.quantwm_cache_bytes(cfg), dtype=torch.uint8, device=DEV)
+    k = torch.zeros((wl.batch, 1, wl.heads, wl.head_dim), dtype=torch.bfloat16, device=DEV)
+    qw.quantwm_append(cfg, calib, cache, 0, k, k, 0)
+    out = torch.zeros_like(k)
+    qw.quantwm_attend(cfg, calib, cache, 0, k, 0, 0, 1, out)
+    torch.cuda.synchronize()
+    assert not cache.any()
+
+
+def test_attend_empty_cache_gives_zero_and_neg_inf_lse():
+    wl = RAGGED
+    case = case_for(wl, 64)
+    cfg = gpu_config(wl)
+    calib = gpu_calib_from_tables(cfg, harness.full_tables(case))
+    cache = torch.zeros(qw.quantwm_cache_bytes(cfg), dtype=torch.uint8, device=DEV)
+    q = tdev(harness.full_inputs(case, "q")[:, :40], torch.bfloat16)
+    out = torch.ones_like(q)
+    lse = torch.zeros((wl.batch, wl.heads, 40), dtype=torch.float32, device=DEV)
+    qw.quantwm_attend(cfg, calib, cache, 0, q, 40, 0, 1, out, lse)
+    torch.cuda.synchronize()
+    assert not out.float().any() and torch.isneginf(lse).all()
+
+
+def test_capacity_and_argument_errors():
+    wl = RAGGED
+    cfg = gpu_config(wl)
+    calib = torch.zeros(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=DEV)
+    cache = torch.zeros(qw.quantwm_cache_bytes(cfg), dtype=torch.uint8, device=DEV)
+    k = torch.zeros((wl.batch, 10, wl.heads, wl.head_dim), dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(qw.QuantwmError) as e:
+        qw.quantwm_append(cfg, calib, cache, wl.n_cache - 5, k, k, 10)
+    assert e.value.status == qw.ERR_CAPACITY
+    with pytest.raises(qw.QuantwmError) as e:
+        qw.quantwm_attend(cfg, calib, cache, 10, k, 10, 11, 1, k)
+    assert e.value.status == qw.ERR_INVALID_ARG
