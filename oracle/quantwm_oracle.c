@@ -15,7 +15,7 @@
  *  - Values take the nearest centroid (w = 1, M = 1) and no PSAC (App. D.1).
  *  - PSAC coefficients are INT8, symmetric, one FP16 scale per row (max|C|/127).
  *  - Cold start (no historical Queries): w = 1 and U_r = 0, so PSAC stores zero
- *    rows (Appendix on the initialisation of historical statistics).
+ *    rows (App. C.3).
  *  - K-means: Lloyd on the calibration tokens, initial centroids at tokens
  *    floor(i*N/Kc), empty clusters keep their centroid, centroids are rounded to
  *    the table type after every update.
