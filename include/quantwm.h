@@ -52,7 +52,7 @@ typedef struct {
   int32_t rank;        /* r: PSAC rank in [0, 32]; 0 disables PSAC (Eq. 16) */
   int32_t top_m;       /* M: QSAC candidates in [1, 8] (Sec. 4.1; the paper uses 4) */
   int32_t dtype;       /* quantwm_dtype of Q/K/V/O, centroids and U_r */
-  int64_t capacity;    /* cache slots per (b, h) */
+  int64_t capacity;    /* cache slots per (b, h), at most 2^26 */
 } quantwm_config;
 
 /* ------------------------------------------------------------------ sizes */

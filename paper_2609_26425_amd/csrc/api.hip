@@ -54,6 +54,8 @@ quantwm_status check_cfg(const quantwm_config* c) {
     return fail(QWM_ERR_UNSUPPORTED, "group_size must be 16, 32 or 64");
   if (c->rank > 32) return fail(QWM_ERR_UNSUPPORTED, "rank must be <= 32");
   if (c->top_m > 8) return fail(QWM_ERR_UNSUPPORTED, "top_m must be <= 8");
+  if (c->capacity > (int64_t(1) << 26))  // kernels address a head's slots with 32-bit offsets
+    return fail(QWM_ERR_UNSUPPORTED, "capacity must be <= 2^26 slots per (b, h)");
   return QWM_OK;
 }
 

@@ -16,6 +16,8 @@
 // Softmax is online (running max and sum per Query, base-2 exponentials).
 #include "qwm_common.h"
 
+#include <type_traits>
+
 namespace qwm {
 namespace {
 
@@ -50,20 +52,101 @@ __device__ inline void vset(V& v, int j, T x) {
 // Row of the 32x32 accumulator held by accumulator slot i of a lane in half hf.
 __device__ inline constexpr int acc_row(int i, int hf) { return (i / 4) * 8 + hf * 4 + (i % 4); }
 
-__device__ inline float bf16_bits_to_f(uint32_t hi16) { return __uint_as_float(hi16 << 16); }
+template <typename T, int N>
+__device__ inline void load_vals(const T* p, float (&out)[N]) {
+  if constexpr (sizeof(T) == 2) {
+    static_assert(N % 8 == 0 || N == 4, "bf16 loads of 8 or 4 values");
+    if constexpr (N == 4) {
+      const uint2 u = *reinterpret_cast<const uint2*>(p);
+      out[0] = __uint_as_float(u.x << 16); out[1] = __uint_as_float(u.x & 0xffff0000u);
+      out[2] = __uint_as_float(u.y << 16); out[3] = __uint_as_float(u.y & 0xffff0000u);
+    } else {
+#pragma unroll
+      for (int i = 0; i < N / 8; ++i) {
+        const uint4 u = reinterpret_cast<const uint4*>(p)[i];
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          out[8 * i + 2 * k] = __uint_as_float(w[k] << 16);
+          out[8 * i + 2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < N; ++i) out[i] = p[i];
+  }
+}
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+template <typename T, int N>
+__device__ inline void store_vals(T* p, const float (&x)[N]) {
+  if constexpr (sizeof(T) == 2) {
+    static_assert(N % 8 == 0, "bf16 stores of 8 values");
+#pragma unroll
+    for (int i = 0; i < N / 8; ++i) {
+      bf16x8 v;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = (bf16)x[8 * i + k];
+      reinterpret_cast<bf16x8*>(p)[i] = v;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < N; ++i) p[i] = x[i];
+  }
+}
+
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// Stores with 8-byte alignment only (rows whose stride is an odd multiple of 8 B).
+template <typename T, int N>
+__device__ inline void store_vals8(T* p, const float (&x)[N]) {
+  if constexpr (sizeof(T) == 2) {
+    static_assert(N % 4 == 0, "bf16 stores of 4 values");
+#pragma unroll
+    for (int i = 0; i < N / 4; ++i) {
+      bf16x4 v;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] = (bf16)x[4 * i + k];
+      reinterpret_cast<bf16x4*>(p)[i] = v;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < N; ++i) p[i] = x[i];
+  }
+}
+
+template <typename T>
+__device__ inline void store_pair(T* p, float a, float b) {
+  if constexpr (sizeof(T) == 2) {
+    bf16x2 v;
+    v[0] = (bf16)a;
+    v[1] = (bf16)b;
+    *reinterpret_cast<bf16x2*>(p) = v;
+  } else {
+    p[0] = a;
+    p[1] = b;
+  }
+}
 
 constexpr int NW = 8, BQ = 32 * NW, KT = 64, NT = 64 * NW;
 
+// LDS row strides (elements), chosen so that the matrix-core operand reads are
+// free of bank conflicts: K tile rows of 272 B (16-byte reads), V^T rows of
+// 136 B and chat rows of (r + 4) * 2 B (8-byte reads), and centroid-table rows
+// padded by 16 B so that lanes looking up different centroids spread over banks.
 template <typename T, int D, int RP>
 struct Lds {
-  static constexpr int PK = sizeof(T) == 2 ? 8 : 1;  // row padding (elements)
-  static constexpr int KS = D + PK;                  // K tile row stride
-  static constexpr int CS = (RP > 0 ? RP : 1) + (sizeof(T) == 2 ? 4 : 1);
-  static constexpr int VS = KT + PK;                 // V^T tile row stride
+  static constexpr bool H = sizeof(T) == 2;
+  static constexpr int KS = D + (H ? 8 : 1);
+  static constexpr int CS = (RP > 0 ? RP : 1) + (H ? 4 : 1);
+  static constexpr int VS = KT + (H ? 4 : 1);
+  static constexpr int TS = D + (H ? 8 : 4);
   static constexpr int tile_elems = KT * KS + KT * CS + D * VS;
 };
 
-template <typename T, int D, int RP, bool LOGITS>
+template <typename T, int D, int RP, bool LOGITS, bool TAB>
 __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   typedef Mfma<T> MF;
   typedef typename MF::V V;
@@ -72,11 +155,12 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
   T* smem = reinterpret_cast<T*>(smem_raw);
   const int Kc = a.n_centroids;
+  // LDS: [mu_K table][mu_V table] (TAB) then two tile buffers, each
+  // [K tile][chat tile][V^T tile]. Every LDS pointer is formed as smem + offset
+  // where it is used, so the compiler keeps LDS addressing (ds_read/ds_write).
   T* tabK = smem;
-  T* tabV = smem + (a.tables_in_lds ? Kc * D : 0);
-  T* ktile = smem + (a.tables_in_lds ? 2 * Kc * D : 0);
-  T* ctile = ktile + KT * LY::KS;
-  T* vtile = ctile + KT * LY::CS;
+  T* tabV = smem + Kc * LY::TS;
+  const int tile0 = TAB ? 2 * Kc * LY::TS : 0;
 
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, l32 = lane % 32, hf = lane / 32;
   const int h = blockIdx.y, b = blockIdx.z;
@@ -92,13 +176,15 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   const int G = D / L.ng;
 
   // ---- stage the centroid tables of this head (App. D.1: BF16 centroids)
-  if (a.tables_in_lds) {
-    const int n16 = Kc * D * int(sizeof(T)) / 16;
+  if constexpr (TAB) {
+    constexpr int PER_ROW = D * int(sizeof(T)) / 16;  // 16-byte chunks per centroid row
     const uint4* sk = reinterpret_cast<const uint4*>(gtabK);
     const uint4* sv = reinterpret_cast<const uint4*>(gtabV);
-    uint4* dk = reinterpret_cast<uint4*>(tabK);
-    uint4* dv = reinterpret_cast<uint4*>(tabV);
-    for (int i = tid; i < n16; i += NT) { dk[i] = sk[i]; dv[i] = sv[i]; }
+    for (int i = tid; i < Kc * PER_ROW; i += NT) {
+      const int row = i / PER_ROW, ch = i % PER_ROW;
+      *reinterpret_cast<uint4*>(tabK + row * LY::TS + ch * (16 / int(sizeof(T)))) = sk[i];
+      *reinterpret_cast<uint4*>(tabV + row * LY::TS + ch * (16 / int(sizeof(T)))) = sv[i];
+    }
   }
 
   // ---- Query fragment (B operand: k = channel, column = Query)
@@ -144,7 +230,6 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   int64_t lim = qvalid ? qs + (qi / F + 1) * F : nc;  // this lane's Query sees keys j < lim
   if (lim > nc) lim = nc;
 
-  const float kscale = 1.4426950408889634f / sqrtf((float)D);  // log2(e) / sqrt(d)
   float m_run = -__builtin_inff(), l_run = 0.0f;
   f32x16 oacc[D / 32];
 #pragma unroll
@@ -152,90 +237,154 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) oacc[cb][i] = 0.0f;
 
-  constexpr int CHK = D * KT / NT;       // K channels per thread
+  constexpr int CHK = D * KT / NT;        // K channels per thread (one key)
   constexpr int CHV = D * KT / (2 * NT);  // V channels per thread (two keys)
+  constexpr int RCH = 8;                  // PSAC ranks per thread
+  constexpr int RPT = RP > 0 ? RP / RCH : 1;
+  const int kkey = tid / (D / CHK), kch0 = (tid % (D / CHK)) * CHK, kg = kch0 / G;
+  const int vkp = tid % (KT / 2), vch0 = (tid / (KT / 2)) * CHV, vg = vch0 / G;
+  const int ckey = tid / RPT, cr0 = (tid % RPT) * RCH;
+  const bool crole = RP > 0 && tid < KT * RPT && cr0 < r;
+  const bool r8 = (r & 7) == 0;
 
-  for (int64_t k0 = 0; k0 < kend; k0 += KT) {
-    __syncthreads();
-    // ---- dequantise the tile into LDS
-    {  // Keys: thread -> (key, CHK consecutive channels inside one group)
-      const int key = tid / (D / CHK), ch0 = (tid % (D / CHK)) * CHK;
-      const int64_t tok = k0 + key;
-      T* dst = ktile + key * LY::KS + ch0;
-      if (tok < nc) {
-        const int64_t slot = slot0 + tok;
-        const int g = ch0 / G;
-        int id = cache[L.k_ids + slot];
-        id = id < Kc ? id : Kc - 1;
-        const int z = (cache[L.k_zp + slot * L.zpb + g / 4] >> (2 * (g % 4))) & 3;
-        const float s = (float)*reinterpret_cast<const _Float16*>(cache + L.k_scale + slot * 2 * L.ng + 2 * g);
-        uint32_t cw;
-        if constexpr (CHK == 16) cw = *reinterpret_cast<const uint32_t*>(cache + L.k_codes + slot * (D / 4) + ch0 / 4);
-        else cw = *reinterpret_cast<const uint16_t*>(cache + L.k_codes + slot * (D / 4) + ch0 / 4);
-        const T* mu = (a.tables_in_lds ? tabK : gtabK) + id * D + ch0;
-#pragma unroll
-        for (int c = 0; c < CHK; ++c) {
-          const int q = (cw >> (2 * c)) & 3;
-          dst[c] = T(__builtin_fmaf(s, (float)(q - z), (float)mu[c]));
-        }
-      } else {
-#pragma unroll
-        for (int c = 0; c < CHK; ++c) dst[c] = T(0.0f);
+  // ---- packed tile fields of this thread, loaded one tile ahead of use
+  uint32_t k_cw = 0, c_lo = 0, c_hi = 0, v_cw[2] = {0, 0};
+  int k_id = 0, k_z = 0, v_id[2] = {0, 0}, v_z[2] = {0, 0};
+  float k_s = 0.0f, c_s = 0.0f, v_s[2] = {0.0f, 0.0f};
+  bool k_ok = true, c_ok = crole, v_ok[2] = {true, true};
+  // per-head field bases (wave-uniform) and 32-bit token offsets inside the head
+  const uint8_t* __restrict__ kcb = cache + L.k_codes + slot0 * (D / 4) + kch0 / 4;
+  const uint8_t* __restrict__ kib = cache + L.k_ids + slot0;
+  const uint8_t* __restrict__ kzb = cache + L.k_zp + slot0 * L.zpb + kg / 4;
+  const uint8_t* __restrict__ ksb = cache + L.k_scale + slot0 * 2 * L.ng + 2 * kg;
+  const uint8_t* __restrict__ ccb = cache + L.k_coef + slot0 * r + cr0;
+  const uint8_t* __restrict__ csb = cache + L.k_cscale + slot0 * 2;
+  const uint8_t* __restrict__ vcb = cache + L.v_codes + slot0 * (D / 4) + vch0 / 4;
+  const uint8_t* __restrict__ vib = cache + L.v_ids + slot0;
+  const uint8_t* __restrict__ vzb = cache + L.v_zp + slot0 * L.zpb + vg / 4;
+  const uint8_t* __restrict__ vsb = cache + L.v_scale + slot0 * 2 * L.ng + 2 * vg;
+  const uint32_t zpb = L.zpb, sstride = 2 * L.ng, ncu = uint32_t(nc);
+
+  // FULL: every key of the tile is < n_cache, so no per-thread guards.
+  auto load_raw = [&](auto full_tag, uint32_t k0) {
+    constexpr bool FULL = decltype(full_tag)::value;
+    {
+      const uint32_t tok = k0 + kkey;
+      if (!FULL) k_ok = tok < ncu;
+      if (FULL || k_ok) {
+        const int id = kib[tok];
+        k_id = id < Kc ? id : Kc - 1;
+        k_z = (kzb[tok * zpb] >> (2 * (kg % 4))) & 3;
+        k_s = (float)*reinterpret_cast<const _Float16*>(ksb + tok * sstride);
+        if constexpr (CHK == 16) k_cw = *reinterpret_cast<const uint32_t*>(kcb + tok * (D / 4));
+        else k_cw = *reinterpret_cast<const uint16_t*>(kcb + tok * (D / 4));
       }
     }
-    if constexpr (RP > 0) {  // INT8 PSAC rows -> code * cscale
-      constexpr int RCH = 8;
-      if (tid < KT * (RP / RCH)) {
-        const int key = tid / (RP / RCH), r0 = (tid % (RP / RCH)) * RCH;
-        const int64_t tok = k0 + key;
-        T* dst = ctile + key * LY::CS + r0;
-        if (tok < nc) {
-          const int64_t slot = slot0 + tok;
-          const float cs = (float)*reinterpret_cast<const _Float16*>(cache + L.k_cscale + slot * 2);
-          const int8_t* cp = reinterpret_cast<const int8_t*>(cache + L.k_coef + slot * r);
-#pragma unroll
-          for (int k = 0; k < RCH; ++k) dst[k] = T(r0 + k < r ? (float)cp[r0 + k] * cs : 0.0f);
+    if constexpr (RP > 0) {
+      const uint32_t tok = k0 + ckey;
+      c_ok = crole && (FULL || tok < ncu);
+      if (c_ok) {
+        c_s = (float)*reinterpret_cast<const _Float16*>(csb + tok * 2);
+        const uint8_t* cp = ccb + tok * uint32_t(r);
+        if (r8) {
+          const uint2 u = *reinterpret_cast<const uint2*>(cp);
+          c_lo = u.x;
+          c_hi = u.y;
         } else {
+          uint32_t w[2] = {0, 0};
 #pragma unroll
-          for (int k = 0; k < RCH; ++k) dst[k] = T(0.0f);
+          for (int k = 0; k < RCH; ++k)
+            if (cr0 + k < r) w[k / 4] |= uint32_t(cp[k]) << (8 * (k % 4));
+          c_lo = w[0];
+          c_hi = w[1];
         }
       }
     }
-    {  // Values: thread -> (key pair, CHV channels), written transposed
-      const int kp = tid % (KT / 2), ch0 = (tid / (KT / 2)) * CHV;
-      float vv[2][CHV];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const uint32_t tok = k0 + 2 * vkp + e;
+      if (!FULL) v_ok[e] = tok < ncu;
+      if (FULL || v_ok[e]) {
+        const int id = vib[tok];
+        v_id[e] = id < Kc ? id : Kc - 1;
+        v_z[e] = (vzb[tok * zpb] >> (2 * (vg % 4))) & 3;
+        v_s[e] = (float)*reinterpret_cast<const _Float16*>(vsb + tok * sstride);
+        if constexpr (CHV == 8) v_cw[e] = *reinterpret_cast<const uint16_t*>(vcb + tok * (D / 4));
+        else v_cw[e] = vcb[tok * (D / 4)];
+      }
+    }
+  };
+
+  // ---- rebuild khat_0 = mu + s (q - z) (Eq. 4), chat = code * cscale and vhat
+  // into tile buffer `buf` (keys past n_cache become zeros)
+  auto dequant = [&](auto full_tag, int buf) {
+    constexpr bool FULL = decltype(full_tag)::value;
+    T* kt = smem + tile0 + buf * LY::tile_elems;
+    T* ct = kt + KT * LY::KS;
+    T* vt = ct + KT * LY::CS;
+    {
+      float x[CHK];
+      float mu[CHK];
+      if constexpr (TAB) load_vals<T, CHK>(tabK + k_id * LY::TS + kch0, mu);
+      else load_vals<T, CHK>(gtabK + k_id * D + kch0, mu);
+#pragma unroll
+      for (int c = 0; c < CHK; ++c) {
+        x[c] = __builtin_fmaf(k_s, (float)(int((k_cw >> (2 * c)) & 3) - k_z), mu[c]);
+        if (!FULL && !k_ok) x[c] = 0.0f;
+      }
+      store_vals<T, CHK>(kt + kkey * LY::KS + kch0, x);
+    }
+    if constexpr (RP > 0) {
+      if (tid < KT * RPT) {
+        float x[RCH];
+#pragma unroll
+        for (int k = 0; k < RCH; ++k) {
+          const int8_t code = int8_t(((k < 4 ? c_lo : c_hi) >> (8 * (k % 4))) & 255);
+          x[k] = c_ok && cr0 + k < r ? (float)code * c_s : 0.0f;
+        }
+        store_vals8<T, RCH>(ct + ckey * LY::CS + cr0, x);
+      }
+    }
+    {
+      float x0[CHV], x1[CHV];
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const int64_t tok = k0 + 2 * kp + e;
-        if (tok < nc) {
-          const int64_t slot = slot0 + tok;
-          const int g = ch0 / G;
-          int id = cache[L.v_ids + slot];
-          id = id < Kc ? id : Kc - 1;
-          const int z = (cache[L.v_zp + slot * L.zpb + g / 4] >> (2 * (g % 4))) & 3;
-          const float s = (float)*reinterpret_cast<const _Float16*>(cache + L.v_scale + slot * 2 * L.ng + 2 * g);
-          uint32_t cw;
-          if constexpr (CHV == 8) cw = *reinterpret_cast<const uint16_t*>(cache + L.v_codes + slot * (D / 4) + ch0 / 4);
-          else cw = cache[L.v_codes + slot * (D / 4) + ch0 / 4];
-          const T* mu = (a.tables_in_lds ? tabV : gtabV) + id * D + ch0;
+        float* x = e == 0 ? x0 : x1;
+        float mu[CHV];
+        if constexpr (TAB) load_vals<T, CHV>(tabV + v_id[e] * LY::TS + vch0, mu);
+        else load_vals<T, CHV>(gtabV + v_id[e] * D + vch0, mu);
 #pragma unroll
-          for (int c = 0; c < CHV; ++c) {
-            const int q = (cw >> (2 * c)) & 3;
-            vv[e][c] = __builtin_fmaf(s, (float)(q - z), (float)mu[c]);
-          }
-        } else {
-#pragma unroll
-          for (int c = 0; c < CHV; ++c) vv[e][c] = 0.0f;
+        for (int c = 0; c < CHV; ++c) {
+          x[c] = __builtin_fmaf(v_s[e], (float)(int((v_cw[e] >> (2 * c)) & 3) - v_z[e]), mu[c]);
+          if (!FULL && !v_ok[e]) x[c] = 0.0f;
         }
       }
 #pragma unroll
-      for (int c = 0; c < CHV; ++c) {
-        T* dst = vtile + (ch0 + c) * LY::VS + 2 * kp;
-        dst[0] = T(vv[0][c]);
-        dst[1] = T(vv[1][c]);
-      }
+      for (int c = 0; c < CHV; ++c) store_pair<T>(vt + (vch0 + c) * LY::VS + 2 * vkp, x0[c], x1[c]);
     }
+  };
+
+  const int64_t ntile = (kend + KT - 1) / KT;
+  const int64_t nfull = nc / KT;  // tiles [0, nfull) hold no key past n_cache
+  using Full = std::integral_constant<bool, true>;
+  using Tail = std::integral_constant<bool, false>;
+  if (ntile > 0) {
+    if (nfull > 0) { load_raw(Full{}, 0u); dequant(Full{}, 0); }
+    else { load_raw(Tail{}, 0u); dequant(Tail{}, 0); }
+    if (ntile > 1) {
+      if (nfull > 1) load_raw(Full{}, uint32_t(KT));
+      else load_raw(Tail{}, uint32_t(KT));
+    }
+  }
+  const float mscale = 1.4426950408889634f / sqrtf((float)D);  // logits are exponentiated as 2^(S log2(e)/sqrt(d))
+
+  for (int64_t it = 0; it < ntile; ++it) {
+    const int64_t k0 = it * KT;
+    // buffer it&1 is complete and every wave is done with buffer (it+1)&1
     __syncthreads();
+    const T* kt = smem + tile0 + int(it & 1) * LY::tile_elems;
+    const T* ct = kt + KT * LY::KS;
+    const T* vt = ct + KT * LY::CS;
 
     // ---- logits tile S^T (keys x Queries) on matrix cores
     f32x16 sacc[2];
@@ -243,23 +392,39 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) sacc[kb][i] = 0.0f;
-      const T* krow = ktile + (kb * 32 + l32) * LY::KS;
+    }
 #pragma unroll
-      for (int st = 0; st < D / KSTEP; ++st) {
+    for (int st = 0; st < D / KSTEP; ++st) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const T* krow = kt + (kb * 32 + l32) * LY::KS;
         V av;
         if constexpr (KPL == 8) av = *reinterpret_cast<const V*>(krow + st * KSTEP + hf * KPL);
         else av = krow[st * KSTEP + hf];
         sacc[kb] = MF::run(av, qreg[st], sacc[kb]);
       }
-      if constexpr (RP > 0) {
-        const T* crow = ctile + (kb * 32 + l32) * LY::CS;
+    }
+    if constexpr (RP > 0) {
 #pragma unroll
-        for (int st = 0; st < RP / KSTEP; ++st) {
+      for (int st = 0; st < RP / KSTEP; ++st) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          const T* crow = ct + (kb * 32 + l32) * LY::CS;
           V av;
 #pragma unroll
           for (int j = 0; j < KPL; ++j) vset(av, j, crow[acc_row(st * KPL + j, hf)]);
           sacc[kb] = MF::run(av, ureg[st], sacc[kb]);
         }
+      }
+    }
+
+    // ---- next tile into the other buffer while the matrix cores run
+    if (it + 1 < ntile) {
+      if (it + 1 < nfull) dequant(Full{}, int((it + 1) & 1));
+      else dequant(Tail{}, int((it + 1) & 1));
+      if (it + 2 < ntile) {
+        if (it + 2 < nfull) load_raw(Full{}, uint32_t(k0 + 2 * KT));
+        else load_raw(Tail{}, uint32_t(k0 + 2 * KT));
       }
     }
 
@@ -275,58 +440,61 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
             if (j < nc) lrow[j] = j < lim ? sacc[kb][i] * inv : -__builtin_inff();
           }
       }
-      continue;
-    }
-
-    // ---- online softmax (base 2); masked keys -> -inf
-    const bool need_mask = k0 + KT > kfull;
-    float mt = -__builtin_inff();
+    } else {
+      // ---- online softmax on raw logits; masked keys -> -inf
+      if (k0 + KT > kfull) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float v = sacc[kb][i] * kscale;
-        if (need_mask && k0 + kb * 32 + acc_row(i, hf) >= lim) v = -__builtin_inff();
-        sacc[kb][i] = v;
-        mt = fmaxf(mt, v);
+          for (int i = 0; i < 16; ++i)
+            if (k0 + kb * 32 + acc_row(i, hf) >= lim) sacc[kb][i] = -__builtin_inff();
       }
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    const float m_use = m_new == -__builtin_inff() ? 0.0f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    m_run = m_new;
-    float lsum = 0.0f;
+      float mt = -__builtin_inff();
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = __builtin_amdgcn_exp2f(sacc[kb][i] - m_use);
-        sacc[kb][i] = p;
-        lsum += p;
+        for (int i = 0; i < 16; ++i) mt = fmaxf(mt, sacc[kb][i]);
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float m_new = fmaxf(m_run, mt);
+      if (__any(m_new > m_run)) {  // rescale only when some row's running max moved
+        const float alpha = m_new == -__builtin_inff() ? 1.0f : __builtin_amdgcn_exp2f((m_run - m_new) * mscale);
+        l_run *= alpha;
+#pragma unroll
+        for (int cb = 0; cb < D / 32; ++cb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) oacc[cb][i] *= alpha;
+        m_run = m_new;
       }
-    l_run = l_run * alpha + lsum;
+      const float mc = m_run == -__builtin_inff() ? 0.0f : -m_run * mscale;
+      float lpart[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int cb = 0; cb < D / 32; ++cb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[cb][i] *= alpha;
-
-    // ---- O^T += Vhat^T P^T (B operand = this lane's probabilities)
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int t = 0; t < 32 / KSTEP; ++t) {
-        V bv;
-#pragma unroll
-        for (int j = 0; j < KPL; ++j) vset(bv, j, T(sacc[kb][t * KPL + j]));
-#pragma unroll
-        for (int cb = 0; cb < D / 32; ++cb) {
-          const T* vrow = vtile + (cb * 32 + l32) * LY::VS + kb * 32;
-          V av;
-#pragma unroll
-          for (int j = 0; j < KPL; ++j) vset(av, j, vrow[acc_row(t * KPL + j, hf)]);
-          oacc[cb] = MF::run(av, bv, oacc[cb]);
+        for (int i = 0; i < 16; ++i) {
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][i], mscale, mc));
+          sacc[kb][i] = p;
+          lpart[i % 4] += p;
         }
-      }
+      l_run += (lpart[0] + lpart[1]) + (lpart[2] + lpart[3]);
+
+      // ---- O^T += Vhat^T P^T (B operand = this lane's probabilities)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int t = 0; t < 32 / KSTEP; ++t) {
+          V bv;
+#pragma unroll
+          for (int j = 0; j < KPL; ++j) vset(bv, j, T(sacc[kb][t * KPL + j]));
+#pragma unroll
+          for (int cb = 0; cb < D / 32; ++cb) {
+            const T* vrow = vt + (cb * 32 + l32) * LY::VS + kb * 32;
+            V av;
+#pragma unroll
+            for (int j = 0; j < KPL; ++j) vset(av, j, vrow[acc_row(t * KPL + j, hf)]);
+            oacc[cb] = MF::run(av, bv, oacc[cb]);
+          }
+        }
+    }
   }
 
   if constexpr (!LOGITS) {
@@ -339,7 +507,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) orow[cb * 32 + acc_row(i, hf)] = T(oacc[cb][i] * inv);
       if (a.lse && hf == 0)
-        a.lse[bh * a.n_q + qi] = l_tot > 0.0f ? m_run * 0.6931471805599453f + logf(l_tot) : -__builtin_inff();
+        a.lse[bh * a.n_q + qi] = l_tot > 0.0f ? m_run / sqrtf((float)D) + logf(l_tot) : -__builtin_inff();
     }
   }
 }
@@ -350,23 +518,26 @@ size_t lds_bytes_t(int rank, int kc, bool tables) {
   if (rank == 0) tile = Lds<T, D, 0>::tile_elems;
   else if (rank <= 16) tile = Lds<T, D, 16>::tile_elems;
   else tile = Lds<T, D, 32>::tile_elems;
-  return (tile + (tables ? size_t(2) * kc * D : 0)) * sizeof(T);
+  constexpr size_t TS = Lds<T, D, 0>::TS;
+  return (2 * tile + (tables ? size_t(2) * kc * TS : 0)) * sizeof(T);  // two tile buffers
+}
+
+template <typename T, int D, int RP, bool LOGITS, bool TAB>
+hipError_t launch_k(const AttendArgs& a, const dim3& grid, size_t lds, hipStream_t s) {
+  const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, LOGITS, TAB>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attend_kernel<T, D, RP, LOGITS, TAB>), grid, dim3(NT), lds, s, a);
+  return hipGetLastError();
 }
 
 template <typename T, int D, int RP>
 hipError_t launch_r(const AttendArgs& a, int batch, bool logits, hipStream_t s) {
   const dim3 grid((unsigned)((a.n_q + BQ - 1) / BQ), (unsigned)a.heads, (unsigned)batch);
-  const size_t lds = lds_bytes_t<T, D>(a.rank, a.n_centroids, a.tables_in_lds != 0);
-  if (logits) {
-    hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, true>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL((attend_kernel<T, D, RP, true>), grid, dim3(NT), lds, s, a);
-  } else {
-    hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, false>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL((attend_kernel<T, D, RP, false>), grid, dim3(NT), lds, s, a);
-  }
-  return hipGetLastError();
+  const bool tab = a.tables_in_lds != 0;
+  const size_t lds = lds_bytes_t<T, D>(a.rank, a.n_centroids, tab);
+  if (logits) return tab ? launch_k<T, D, RP, true, true>(a, grid, lds, s) : launch_k<T, D, RP, true, false>(a, grid, lds, s);
+  return tab ? launch_k<T, D, RP, false, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false>(a, grid, lds, s);
 }
 
 template <typename T, int D>
