@@ -79,25 +79,27 @@ __device__ inline void load_vals(const T* p, float (&out)[N]) {
 }
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32.
+__device__ inline uint32_t pack_bf16(float a, float b) {
+  const f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
 
 template <typename T, int N>
 __device__ inline void store_vals(T* p, const float (&x)[N]) {
   if constexpr (sizeof(T) == 2) {
     static_assert(N % 8 == 0, "bf16 stores of 8 values");
 #pragma unroll
-    for (int i = 0; i < N / 8; ++i) {
-      bf16x8 v;
-#pragma unroll
-      for (int k = 0; k < 8; ++k) v[k] = (bf16)x[8 * i + k];
-      reinterpret_cast<bf16x8*>(p)[i] = v;
-    }
+    for (int i = 0; i < N / 8; ++i)
+      reinterpret_cast<uint4*>(p)[i] = make_uint4(pack_bf16(x[8 * i], x[8 * i + 1]), pack_bf16(x[8 * i + 2], x[8 * i + 3]),
+                                                  pack_bf16(x[8 * i + 4], x[8 * i + 5]), pack_bf16(x[8 * i + 6], x[8 * i + 7]));
   } else {
 #pragma unroll
     for (int i = 0; i < N; ++i) p[i] = x[i];
   }
 }
-
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 // Stores with 8-byte alignment only (rows whose stride is an odd multiple of 8 B).
 template <typename T, int N>
@@ -105,12 +107,8 @@ __device__ inline void store_vals8(T* p, const float (&x)[N]) {
   if constexpr (sizeof(T) == 2) {
     static_assert(N % 4 == 0, "bf16 stores of 4 values");
 #pragma unroll
-    for (int i = 0; i < N / 4; ++i) {
-      bf16x4 v;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) v[k] = (bf16)x[4 * i + k];
-      reinterpret_cast<bf16x4*>(p)[i] = v;
-    }
+    for (int i = 0; i < N / 4; ++i)
+      reinterpret_cast<uint2*>(p)[i] = make_uint2(pack_bf16(x[4 * i], x[4 * i + 1]), pack_bf16(x[4 * i + 2], x[4 * i + 3]));
   } else {
 #pragma unroll
     for (int i = 0; i < N; ++i) p[i] = x[i];
@@ -120,13 +118,32 @@ __device__ inline void store_vals8(T* p, const float (&x)[N]) {
 template <typename T>
 __device__ inline void store_pair(T* p, float a, float b) {
   if constexpr (sizeof(T) == 2) {
-    bf16x2 v;
-    v[0] = (bf16)a;
-    v[1] = (bf16)b;
-    *reinterpret_cast<bf16x2*>(p) = v;
+    *reinterpret_cast<uint32_t*>(p) = pack_bf16(a, b);
   } else {
     p[0] = a;
     p[1] = b;
+  }
+}
+
+// INT2 codes of N consecutive channels (channel c in bits 2c of cw) as floats.
+// The four 2-bit fields of every byte are spread into four words of bytes, so
+// each code converts with one v_cvt_f32_ubyteN.
+template <int N>
+__device__ inline void codes_to_float(uint32_t cw, float (&q)[N]) {
+  const uint32_t w[4] = {cw & 0x03030303u, (cw >> 2) & 0x03030303u, (cw >> 4) & 0x03030303u,
+                         (cw >> 6) & 0x03030303u};
+#pragma unroll
+  for (int c = 0; c < N; ++c) q[c] = (float)((w[c % 4] >> (8 * (c / 4))) & 0xffu);
+}
+
+// Builds a bf16x8 MFMA operand from 8 floats with paired conversions.
+template <typename V>
+__device__ inline V pack_operand(const float* x) {
+  if constexpr (sizeof(V) == 16) {
+    const uint4 u = make_uint4(pack_bf16(x[0], x[1]), pack_bf16(x[2], x[3]), pack_bf16(x[4], x[5]), pack_bf16(x[6], x[7]));
+    return __builtin_bit_cast(V, u);
+  } else {
+    return x[0];
   }
 }
 
@@ -251,7 +268,6 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   uint32_t k_cw = 0, c_lo = 0, c_hi = 0, v_cw[2] = {0, 0};
   int k_id = 0, k_z = 0, v_id[2] = {0, 0}, v_z[2] = {0, 0};
   float k_s = 0.0f, c_s = 0.0f, v_s[2] = {0.0f, 0.0f};
-  bool k_ok = true, c_ok = crole, v_ok[2] = {true, true};
   // per-head field bases (wave-uniform) and 32-bit token offsets inside the head
   const uint8_t* __restrict__ kcb = cache + L.k_codes + slot0 * (D / 4) + kch0 / 4;
   const uint8_t* __restrict__ kib = cache + L.k_ids + slot0;
@@ -265,25 +281,30 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   const uint8_t* __restrict__ vsb = cache + L.v_scale + slot0 * 2 * L.ng + 2 * vg;
   const uint32_t zpb = L.zpb, sstride = 2 * L.ng, ncu = uint32_t(nc);
 
-  // FULL: every key of the tile is < n_cache, so no per-thread guards.
+  // FULL: every key of the tile is < n_cache, so no per-thread guards. A key
+  // past n_cache (tail tiles only) gets centroid 0, scale 0 and code 0: a finite
+  // placeholder whose logit the mask turns into -inf, so it never contributes.
   auto load_raw = [&](auto full_tag, uint32_t k0) {
     constexpr bool FULL = decltype(full_tag)::value;
     {
       const uint32_t tok = k0 + kkey;
-      if (!FULL) k_ok = tok < ncu;
-      if (FULL || k_ok) {
+      if (FULL || tok < ncu) {
         const int id = kib[tok];
         k_id = id < Kc ? id : Kc - 1;
         k_z = (kzb[tok * zpb] >> (2 * (kg % 4))) & 3;
         k_s = (float)*reinterpret_cast<const _Float16*>(ksb + tok * sstride);
         if constexpr (CHK == 16) k_cw = *reinterpret_cast<const uint32_t*>(kcb + tok * (D / 4));
         else k_cw = *reinterpret_cast<const uint16_t*>(kcb + tok * (D / 4));
+      } else {
+        k_id = 0; k_z = 0; k_s = 0.0f; k_cw = 0;
       }
     }
     if constexpr (RP > 0) {
       const uint32_t tok = k0 + ckey;
-      c_ok = crole && (FULL || tok < ncu);
-      if (c_ok) {
+      c_s = 0.0f;
+      c_lo = 0;
+      c_hi = 0;
+      if (crole && (FULL || tok < ncu)) {
         c_s = (float)*reinterpret_cast<const _Float16*>(csb + tok * 2);
         const uint8_t* cp = ccb + tok * uint32_t(r);
         if (r8) {
@@ -303,45 +324,42 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const uint32_t tok = k0 + 2 * vkp + e;
-      if (!FULL) v_ok[e] = tok < ncu;
-      if (FULL || v_ok[e]) {
+      if (FULL || tok < ncu) {
         const int id = vib[tok];
         v_id[e] = id < Kc ? id : Kc - 1;
         v_z[e] = (vzb[tok * zpb] >> (2 * (vg % 4))) & 3;
         v_s[e] = (float)*reinterpret_cast<const _Float16*>(vsb + tok * sstride);
         if constexpr (CHV == 8) v_cw[e] = *reinterpret_cast<const uint16_t*>(vcb + tok * (D / 4));
         else v_cw[e] = vcb[tok * (D / 4)];
+      } else {
+        v_id[e] = 0; v_z[e] = 0; v_s[e] = 0.0f; v_cw[e] = 0;
       }
     }
   };
 
   // ---- rebuild khat_0 = mu + s (q - z) (Eq. 4), chat = code * cscale and vhat
-  // into tile buffer `buf` (keys past n_cache become zeros)
-  auto dequant = [&](auto full_tag, int buf) {
-    constexpr bool FULL = decltype(full_tag)::value;
+  // into tile buffer `buf`. s (q - z) is exact in fp32, so the fma rounds once,
+  // exactly like mu + s (q - z).
+  auto dequant = [&](int buf) {
     T* kt = smem + tile0 + buf * LY::tile_elems;
     T* ct = kt + KT * LY::KS;
     T* vt = ct + KT * LY::CS;
     {
-      float x[CHK];
-      float mu[CHK];
+      float q[CHK], mu[CHK], x[CHK];
+      codes_to_float<CHK>(k_cw, q);
       if constexpr (TAB) load_vals<T, CHK>(tabK + k_id * LY::TS + kch0, mu);
       else load_vals<T, CHK>(gtabK + k_id * D + kch0, mu);
+      const float zf = (float)k_z;
 #pragma unroll
-      for (int c = 0; c < CHK; ++c) {
-        x[c] = __builtin_fmaf(k_s, (float)(int((k_cw >> (2 * c)) & 3) - k_z), mu[c]);
-        if (!FULL && !k_ok) x[c] = 0.0f;
-      }
+      for (int c = 0; c < CHK; ++c) x[c] = __builtin_fmaf(k_s, q[c] - zf, mu[c]);
       store_vals<T, CHK>(kt + kkey * LY::KS + kch0, x);
     }
     if constexpr (RP > 0) {
       if (tid < KT * RPT) {
         float x[RCH];
 #pragma unroll
-        for (int k = 0; k < RCH; ++k) {
-          const int8_t code = int8_t(((k < 4 ? c_lo : c_hi) >> (8 * (k % 4))) & 255);
-          x[k] = c_ok && cr0 + k < r ? (float)code * c_s : 0.0f;
-        }
+        for (int k = 0; k < RCH; ++k)
+          x[k] = (float)int8_t(((k < 4 ? c_lo : c_hi) >> (8 * (k % 4))) & 255) * c_s;
         store_vals8<T, RCH>(ct + ckey * LY::CS + cr0, x);
       }
     }
@@ -350,14 +368,13 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         float* x = e == 0 ? x0 : x1;
-        float mu[CHV];
+        float q[CHV], mu[CHV];
+        codes_to_float<CHV>(v_cw[e], q);
         if constexpr (TAB) load_vals<T, CHV>(tabV + v_id[e] * LY::TS + vch0, mu);
         else load_vals<T, CHV>(gtabV + v_id[e] * D + vch0, mu);
+        const float zf = (float)v_z[e];
 #pragma unroll
-        for (int c = 0; c < CHV; ++c) {
-          x[c] = __builtin_fmaf(v_s[e], (float)(int((v_cw[e] >> (2 * c)) & 3) - v_z[e]), mu[c]);
-          if (!FULL && !v_ok[e]) x[c] = 0.0f;
-        }
+        for (int c = 0; c < CHV; ++c) x[c] = __builtin_fmaf(v_s[e], q[c] - zf, mu[c]);
       }
 #pragma unroll
       for (int c = 0; c < CHV; ++c) store_pair<T>(vt + (vch0 + c) * LY::VS + 2 * vkp, x0[c], x1[c]);
@@ -369,8 +386,9 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   using Full = std::integral_constant<bool, true>;
   using Tail = std::integral_constant<bool, false>;
   if (ntile > 0) {
-    if (nfull > 0) { load_raw(Full{}, 0u); dequant(Full{}, 0); }
-    else { load_raw(Tail{}, 0u); dequant(Tail{}, 0); }
+    if (nfull > 0) load_raw(Full{}, 0u);
+    else load_raw(Tail{}, 0u);
+    dequant(0);
     if (ntile > 1) {
       if (nfull > 1) load_raw(Full{}, uint32_t(KT));
       else load_raw(Tail{}, uint32_t(KT));
@@ -420,8 +438,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 
     // ---- next tile into the other buffer while the matrix cores run
     if (it + 1 < ntile) {
-      if (it + 1 < nfull) dequant(Full{}, int((it + 1) & 1));
-      else dequant(Tail{}, int((it + 1) & 1));
+      dequant(int((it + 1) & 1));
       if (it + 2 < ntile) {
         if (it + 2 < nfull) load_raw(Full{}, uint32_t(k0 + 2 * KT));
         else load_raw(Tail{}, uint32_t(k0 + 2 * KT));
@@ -482,9 +499,10 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int t = 0; t < 32 / KSTEP; ++t) {
-          V bv;
+          float pv[KPL];
 #pragma unroll
-          for (int j = 0; j < KPL; ++j) vset(bv, j, T(sacc[kb][t * KPL + j]));
+          for (int j = 0; j < KPL; ++j) pv[j] = sacc[kb][t * KPL + j];
+          const V bv = pack_operand<V>(pv);
 #pragma unroll
           for (int cb = 0; cb < D / 32; ++cb) {
             const T* vrow = vt + (cb * 32 + l32) * LY::VS + kb * 32;
@@ -495,6 +513,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
           }
         }
     }
+
   }
 
   if constexpr (!LOGITS) {
