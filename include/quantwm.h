@@ -85,10 +85,12 @@ size_t quantwm_calib_bytes(const quantwm_config* cfg);
  *   w           [d]     f32     channel sensitivities (Eq. 8)
  *   wg          [d/G]   f32     per-group sums of w (Eq. 12)
  *   u_t         [r][d]  dtype   U_r transposed: row k is the k-th eigenvector (Eq. 15)
- *   lam         [r]     f32     the matching eigenvalues (0 at cold start) */
+ *   lam         [r]     f32     the matching eigenvalues (0 at cold start)
+ *   u_dr        [d][rs] f32     U_r itself (the transpose of u_t), ranks zero-padded to
+ *                               rs = 16 (r <= 16) or 32 (r <= 32), for per-channel use */
 typedef struct {
   int64_t slab_bytes;
-  int64_t mu_k, mu_v, a_k, b_k, a_v, b_v, w, wg, u_t, lam;
+  int64_t mu_k, mu_v, a_k, b_k, a_v, b_v, w, wg, u_t, lam, u_dr;
 } quantwm_calib_layout;
 quantwm_status quantwm_calib_offsets(const quantwm_config* cfg, quantwm_calib_layout* out);
 

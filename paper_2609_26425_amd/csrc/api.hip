@@ -239,7 +239,7 @@ quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void
   a.calib = static_cast<const uint8_t*>(calib);
   a.slab = C.slab_bytes;
   a.o_mu_k = C.mu_k; a.o_mu_v = C.mu_v; a.o_a_k = C.a_k; a.o_b_k = C.b_k;
-  a.o_a_v = C.a_v; a.o_b_v = C.b_v; a.o_wg = C.wg; a.o_u_t = C.u_t;
+  a.o_a_v = C.a_v; a.o_b_v = C.b_v; a.o_wg = C.wg; a.o_u_t = C.u_t; a.o_u_dr = C.u_dr;
   a.cache = static_cast<uint8_t*>(cache);
   a.L = qwm::cache_layout(*cfg);
   a.k = k_new; a.v = v_new;

@@ -68,65 +68,98 @@ __device__ inline uint16_t f16_bits(float exact) {
 }
 
 // Code of one channel given its group's stored scale s and zero-point z (Eq. 1).
+// Branch-free: a zero scale divides by 1 and the result is then discarded.
 __device__ inline int quant_code(float x, float mu, float s, int z) {
-  if (s == 0.0f) return 0;
-  return (int)fminf(fmaxf(rintf((x - mu) / s) + (float)z, 0.0f), 3.0f);
+  const float sd = s != 0.0f ? s : 1.0f;
+  const int q = (int)fminf(fmaxf(rintf((x - mu) / sd) + (float)z, 0.0f), 3.0f);
+  return s != 0.0f ? q : 0;
+}
+
+// rint(x/s) for N residuals x = xv - mu with the IEEE quotient of Eq. 1, without
+// N full divisions. t = x * RN(1/s) lies within 3 * 2^-24 * |x/s| of RN(x/s);
+// every residual satisfies |x/s| <= 3.01 here (the range spans 3 steps), so the
+// two differ by less than 2^-20 and round to the same integer unless t is
+// within 2^-19 of a half-integer (or |t| > 4, out of this bound). If any lane
+// of the wave meets such a case the whole chunk takes the exact division.
+template <int N>
+__device__ inline void round_quotients(const float (&xv)[N], const float (&mu)[N], float s, float inv,
+                                       float (&t)[N]) {
+  bool near = false;
+#pragma unroll
+  for (int c = 0; c < N; ++c) {
+    const float q = (xv[c] - mu[c]) * inv;
+    const float k = rintf(q);
+    near |= fabsf(q - k) > 0.5f - 0x1p-19f || fabsf(q) > 4.0f;
+    t[c] = k;
+  }
+  if (__any(near)) {
+    const float sd = s != 0.0f ? s : 1.0f;
+#pragma unroll
+    for (int c = 0; c < N; ++c) t[c] = rintf((xv[c] - mu[c]) / sd);
+  }
 }
 
 // Residual of one token against centroid row mu_row, group by group (Eq. 1-2
 // with q_min = 0, q_max = 3, the range extended to contain 0, the residual
-// quantised with the stored FP16 scale). The fp32 reconstruction
-// mu + s (q - z) (Eq. 4) of each channel goes to `each(c, xhat)`. Centroid
-// values stream in chunks of 16 (re-read from L1 in the second pass) so that
-// only the token itself stays resident in registers.
+// quantised with the stored FP16 scale). Token and centroid values stream from
+// memory 16 channels at a time in two passes (range, then codes). Codes are
+// stored as they are made; `each(c, e)` receives e = x_c - (mu_c + s (q_c - z))
+// for every channel c in order (Eq. 4, Eq. 13).
 template <typename T, int D, int G, typename F>
-__device__ inline void quant_token(float (&x)[D], const T* __restrict__ mu_row, uint32_t (&cw)[D / 16],
-                                   int (&zg)[D / G], float (&sg)[D / G], F each) {
+__device__ inline void quant_stream(const T* __restrict__ xrow, const T* __restrict__ mrow,
+                                    uint8_t* __restrict__ codes, bool active, int (&zg)[D / G],
+                                    float (&sg)[D / G], F each) {
   constexpr int CH = G < 16 ? G : 16;
-#pragma unroll
-  for (int w = 0; w < D / 16; ++w) cw[w] = 0;
   static_for<0, D / G>([&](auto gi) {
     constexpr int g = decltype(gi)::value;
+    // keep each group's loads inside the group: hoisting them all ahead would
+    // hold every chunk in registers at once
+    __builtin_amdgcn_sched_barrier(0);
     float lo = 0.0f, hi = 0.0f;
     static_for<0, G, CH>([&](auto ci) {
-      constexpr int c0 = decltype(ci)::value;
-      float mu[CH];
-      load_row<T, CH>(mu_row + g * G + c0, mu);
+      constexpr int c0 = g * G + decltype(ci)::value;
+      float xv[CH], mu[CH];
+      load_row<T, CH>(xrow + c0, xv);
+      load_row<T, CH>(mrow + c0, mu);
 #pragma unroll
       for (int c = 0; c < CH; ++c) {
-        const float r = x[g * G + c0 + c] - mu[c];
+        const float r = xv[c] - mu[c];
         lo = r < lo ? r : lo;
         hi = r > hi ? r : hi;
       }
     });
     const float s = f16_round((hi - lo) / 3.0f);
-    int z = 0;
-    if (s != 0.0f) z = (int)fminf(fmaxf(rintf(0.0f - lo / s), 0.0f), 3.0f);
+    const float sd = s != 0.0f ? s : 1.0f;
+    const int z = s != 0.0f ? (int)fminf(fmaxf(rintf(0.0f - lo / sd), 0.0f), 3.0f) : 0;
+    const float inv = s != 0.0f ? 1.0f / s : 0.0f;
     zg[g] = z;
     sg[g] = s;
     static_for<0, G, CH>([&](auto ci) {
-      constexpr int c0 = decltype(ci)::value;
-      float mu[CH];
-      load_row<T, CH>(mu_row + g * G + c0, mu);
-      static_for<0, CH>([&](auto cc) {
-        constexpr int ch = g * G + c0 + decltype(cc)::value;
-        const float m = mu[decltype(cc)::value];
-        const int q = quant_code(x[ch], m, s, z);
-        cw[ch / 16] |= uint32_t(q) << (2 * (ch % 16));
-        each(std::integral_constant<int, ch>{}, m + s * (float)(q - z));
-      });
+      constexpr int c0 = g * G + decltype(ci)::value;
+      float xv[CH], mu[CH];
+      load_row<T, CH>(xrow + c0, xv);
+      load_row<T, CH>(mrow + c0, mu);
+      float t[CH];
+      round_quotients<CH>(xv, mu, s, inv, t);
+      uint32_t cw = 0;
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        const int q = s != 0.0f ? (int)fminf(fmaxf(t[c] + (float)z, 0.0f), 3.0f) : 0;  // Eq. 1
+        cw |= uint32_t(q) << (2 * c);
+        each(c0 + c, xv[c] - (mu[c] + s * (float)(q - z)));
+      }
+      if (active) {
+        if constexpr (CH == 16) *reinterpret_cast<uint32_t*>(codes + c0 / 4) = cw;
+        else *reinterpret_cast<uint16_t*>(codes + c0 / 4) = uint16_t(cw);
+      }
     });
   });
 }
 
 template <int D, int G>
-__device__ inline void store_residual(uint8_t* __restrict__ codes, uint8_t* __restrict__ zp_dst,
-                                      uint8_t* __restrict__ scale_dst, const uint32_t (&cw)[D / 16],
-                                      const int (&zg)[D / G], const float (&sg)[D / G]) {
+__device__ inline void store_meta(uint8_t* __restrict__ zp_dst, uint8_t* __restrict__ scale_dst,
+                                  const int (&zg)[D / G], const float (&sg)[D / G]) {
   constexpr int NG = D / G;
-  uint4* cp = reinterpret_cast<uint4*>(codes);
-#pragma unroll
-  for (int i = 0; i < D / 64; ++i) cp[i] = make_uint4(cw[4 * i], cw[4 * i + 1], cw[4 * i + 2], cw[4 * i + 3]);
   uint32_t z = 0;
 #pragma unroll
   for (int g = 0; g < NG; ++g) z |= uint32_t(zg[g]) << (2 * g);
@@ -154,7 +187,7 @@ __device__ inline void topm_insert(float (&bd)[MM], int (&bi)[MM], float dv, int
 }
 
 template <typename T, int D, int G, int RP, int MM>
-__global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void append_kernel(const AppendArgs a) {
   constexpr int NG = D / G;
   const int t = blockIdx.x * 256 + threadIdx.x;
   const int h = blockIdx.y, b = blockIdx.z;
@@ -169,7 +202,7 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
   const float* __restrict__ wg = reinterpret_cast<const float*>(slab + a.o_wg);
   const T* __restrict__ muk = reinterpret_cast<const T*>(slab + a.o_mu_k);
   const T* __restrict__ muv = reinterpret_cast<const T*>(slab + a.o_mu_v);
-  const T* __restrict__ ut = reinterpret_cast<const T*>(slab + a.o_u_t);
+  const float* __restrict__ udr = reinterpret_cast<const float*>(slab + a.o_u_dr);
   const int Kc = a.n_centroids;
   const int64_t src = ((int64_t(b) * a.n_new + tt) * a.heads + h) * D;
   const int64_t slot = bh * a.L.slots + a.n_cached + tt;
@@ -229,46 +262,50 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
     if (S < zs || (S == zs && j < z)) { zs = S; z = j; }
   });
 
-  // ---- INT2 residual against mu_z; the key registers become E = k - khat_0 (Eq. 13)
+  // ---- INT2 residual against mu_z, with PSAC accumulated channel by channel:
+  // E_c = k_c - khat_0,c (Eq. 13), C_k += E_c U_ck (Eq. 16). From here on the
+  // key is re-read 16 channels at a time (L1 hits), so only the r accumulators
+  // stay resident. INT8 rows with one FP16 scale (App. D.1).
   {
-    uint32_t cw[D / 16];
+    const T* krow = reinterpret_cast<const T*>(a.k) + src;
+    const T* mrow = muk + int64_t(z) * D;
+    float C[RP > 0 ? RP : 1];
+#pragma unroll
+    for (int k = 0; k < (RP > 0 ? RP : 1); ++k) C[k] = 0.0f;
     int zg[NG];
     float sg[NG];
-    quant_token<T, D, G>(x, muk + int64_t(z) * D, cw, zg, sg, [&](auto ci, float xhat) {
-      constexpr int c = decltype(ci)::value;
-      x[c] = x[c] - xhat;
-    });
+    quant_stream<T, D, G>(krow, mrow, a.cache + a.L.k_codes + slot * (D / 4), active, zg, sg,
+                          [&](int c, float e) {
+                            if constexpr (RP > 0) {
+                              const float* urow = udr + c * RP;
+#pragma unroll
+                              for (int k = 0; k < RP; ++k) C[k] = __builtin_fmaf(e, urow[k], C[k]);
+                            }
+                          });
     if (active) {
-      store_residual<D, G>(a.cache + a.L.k_codes + slot * (D / 4), a.cache + a.L.k_zp + slot * a.L.zpb,
-                           a.cache + a.L.k_scale + slot * 2 * NG, cw, zg, sg);
+      store_meta<D, G>(a.cache + a.L.k_zp + slot * a.L.zpb, a.cache + a.L.k_scale + slot * 2 * NG, zg, sg);
       a.cache[a.L.k_ids + slot] = uint8_t(z);
     }
-  }
-  // ---- PSAC: C = E U_r (Eq. 16), INT8 with one FP16 row scale (App. D.1).
-  // The rows of U_r are wave-uniform (scalar loads); C goes through LDS so that
-  // the rank loop stays a runtime loop.
-  if constexpr (RP > 0) {
-    __shared__ float cbuf[RP][256];
-    const int r = a.rank;
-    float amax = 0.0f;
-    for (int k = 0; k < r; ++k) {
-      float acc = 0.0f;
-      const T* urow = ut + int64_t(k) * D;
+    if constexpr (RP > 0) {
+      const int r = a.rank;
+      float amax = 0.0f;
 #pragma unroll
-      for (int c = 0; c < D; ++c) acc = __builtin_fmaf(x[c], ld(urow + c), acc);
-      cbuf[k][threadIdx.x] = acc;
-      amax = fmaxf(amax, fabsf(acc));
-    }
-    const float s = f16_round(amax / 127.0f);
-    if (active) {
-      int8_t* code = reinterpret_cast<int8_t*>(a.cache + a.L.k_coef + slot * r);
-      float* co = a.coef_out ? a.coef_out + (bh * a.n_new + tt) * r : nullptr;
-      for (int k = 0; k < r; ++k) {
-        const float ck = cbuf[k][threadIdx.x];
-        code[k] = int8_t(s != 0.0f ? (int)fminf(fmaxf(rintf(ck / s), -127.0f), 127.0f) : 0);
-        if (co) co[k] = ck;
+      for (int k = 0; k < RP; ++k)
+        if (k < r) amax = fmaxf(amax, fabsf(C[k]));
+      const float s = f16_round(amax / 127.0f);
+      const float sd = s != 0.0f ? s : 1.0f;
+      if (active) {
+        int8_t* code = reinterpret_cast<int8_t*>(a.cache + a.L.k_coef + slot * r);
+        float* co = a.coef_out ? a.coef_out + (bh * a.n_new + tt) * r : nullptr;
+#pragma unroll
+        for (int k = 0; k < RP; ++k) {
+          if (k < r) {
+            code[k] = int8_t(s != 0.0f ? (int)fminf(fmaxf(rintf(C[k] / sd), -127.0f), 127.0f) : 0);
+            if (co) co[k] = C[k];
+          }
+        }
+        *reinterpret_cast<uint16_t*>(a.cache + a.L.k_cscale + slot * 2) = f16_bits(s);
       }
-      *reinterpret_cast<uint16_t*>(a.cache + a.L.k_cscale + slot * 2) = f16_bits(s);
     }
   }
 
@@ -293,13 +330,12 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
       if (j + u < Kc && acc[u] < dv) { dv = acc[u]; zv = j + u; }
   }
   {
-    uint32_t cw[D / 16];
     int zg[NG];
     float sg[NG];
-    quant_token<T, D, G>(x, muv + int64_t(zv) * D, cw, zg, sg, [](auto, float) {});
+    quant_stream<T, D, G>(reinterpret_cast<const T*>(a.v) + src, muv + int64_t(zv) * D,
+                          a.cache + a.L.v_codes + slot * (D / 4), active, zg, sg, [](int, float) {});
     if (active) {
-      store_residual<D, G>(a.cache + a.L.v_codes + slot * (D / 4), a.cache + a.L.v_zp + slot * a.L.zpb,
-                           a.cache + a.L.v_scale + slot * 2 * NG, cw, zg, sg);
+      store_meta<D, G>(a.cache + a.L.v_zp + slot * a.L.zpb, a.cache + a.L.v_scale + slot * 2 * NG, zg, sg);
       a.cache[a.L.v_ids + slot] = uint8_t(zv);
     }
   }
@@ -308,12 +344,18 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
 template <typename T, int D, int G>
 hipError_t launch_dg(const AppendArgs& a, int batch, hipStream_t s) {
   const dim3 grid((unsigned)((a.n_new + 255) / 256), (unsigned)a.heads, (unsigned)batch);
-  const bool psac = a.rank > 0;
+  const int rp = a.rank == 0 ? 0 : (a.rank <= 16 ? 16 : 32);  // the [d][rs] stride of U_r
   const bool wide = a.top_m > 4;
-  if (psac && wide) hipLaunchKernelGGL((append_kernel<T, D, G, 32, 8>), grid, dim3(256), 0, s, a);
-  else if (psac) hipLaunchKernelGGL((append_kernel<T, D, G, 32, 4>), grid, dim3(256), 0, s, a);
-  else if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 0, 8>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((append_kernel<T, D, G, 0, 4>), grid, dim3(256), 0, s, a);
+  if (rp == 32) {
+    if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 32, 8>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((append_kernel<T, D, G, 32, 4>), grid, dim3(256), 0, s, a);
+  } else if (rp == 16) {
+    if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 16, 8>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((append_kernel<T, D, G, 16, 4>), grid, dim3(256), 0, s, a);
+  } else {
+    if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 0, 8>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((append_kernel<T, D, G, 0, 4>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -21,11 +21,12 @@ __device__ inline bf16 to_bf16_rn(double x) {
 __device__ inline void store_rn(float* p, double x) { *p = (float)x; }
 __device__ inline void store_rn(bf16* p, double x) { *p = to_bf16_rn(x); }
 
-// Eq. 12 group sums W_g and the expanded-distance constants of Eq. 9:
-// a_jc = -2 (w_c mu_jc), b_j = sum_c (w_c mu_jc) mu_jc; Values use w = 1.
+// Eq. 12 group sums W_g, the expanded-distance constants of Eq. 9
+// (a_jc = -2 (w_c mu_jc), b_j = sum_c (w_c mu_jc) mu_jc; Values use w = 1) and
+// U_r in [d][r] order for the append kernel's per-channel PSAC accumulation.
 template <typename T>
 __global__ __launch_bounds__(256) void derive_kernel(uint8_t* calib, quantwm_calib_layout C, int d, int G,
-                                                     int Kc) {
+                                                     int Kc, int r) {
   uint8_t* slab = calib + int64_t(blockIdx.x) * C.slab_bytes;
   const float* w = reinterpret_cast<const float*>(slab + C.w);
   float* wg = reinterpret_cast<float*>(slab + C.wg);
@@ -45,6 +46,13 @@ __global__ __launch_bounds__(256) void derive_kernel(uint8_t* calib, quantwm_cal
     const float mkv = ldf(mk + i), mvv = ldf(mv + i);
     ak[i] = -2.0f * (w[c] * mkv);
     av[i] = -2.0f * mvv;
+  }
+  const T* ut = reinterpret_cast<const T*>(slab + C.u_t);
+  float* udr = reinterpret_cast<float*>(slab + C.u_dr);
+  const int rs = r == 0 ? 0 : (r <= 16 ? 16 : 32);
+  for (int i = threadIdx.x; i < rs * d; i += 256) {
+    const int c = i / rs, k = i % rs;
+    udr[i] = k < r ? ldf(ut + k * d + c) : 0.0f;
   }
   for (int j = threadIdx.x; j < Kc; j += 256) {
     float sk = 0.0f, sv = 0.0f;
@@ -191,9 +199,11 @@ hipError_t launch_derive_constants(const quantwm_config& c, uint8_t* calib, hipS
   const quantwm_calib_layout C = calib_layout(c);
   const dim3 grid((unsigned)(c.batch * c.heads));
   if (c.dtype == QWM_BF16)
-    hipLaunchKernelGGL(derive_kernel<bf16>, grid, dim3(256), 0, s, calib, C, c.head_dim, c.group_size, c.n_centroids);
+    hipLaunchKernelGGL(derive_kernel<bf16>, grid, dim3(256), 0, s, calib, C, c.head_dim, c.group_size, c.n_centroids,
+                       c.rank);
   else
-    hipLaunchKernelGGL(derive_kernel<float>, grid, dim3(256), 0, s, calib, C, c.head_dim, c.group_size, c.n_centroids);
+    hipLaunchKernelGGL(derive_kernel<float>, grid, dim3(256), 0, s, calib, C, c.head_dim, c.group_size, c.n_centroids,
+                       c.rank);
   return hipGetLastError();
 }
 

@@ -51,6 +51,9 @@ inline CacheLayout cache_layout(const quantwm_config& c) {
 
 inline int elem_bytes(const quantwm_config& c) { return c.dtype == QWM_BF16 ? 2 : 4; }
 
+// Row stride of the [d][rs] copy of U_r: ranks padded with zeros to 16 or 32.
+inline int rank_stride(const quantwm_config& c) { return c.rank == 0 ? 0 : (c.rank <= 16 ? 16 : 32); }
+
 inline quantwm_calib_layout calib_layout(const quantwm_config& c) {
   quantwm_calib_layout L;
   const int64_t d = c.head_dim, K = c.n_centroids, r = c.rank, e = elem_bytes(c);
@@ -66,6 +69,7 @@ inline quantwm_calib_layout calib_layout(const quantwm_config& c) {
   L.wg = take((d / c.group_size) * 4);
   L.u_t = take(r * d * e);
   L.lam = take(r * 4);
+  L.u_dr = take(int64_t(rank_stride(c)) * d * 4);
   L.slab_bytes = at;
   return L;
 }
@@ -75,7 +79,7 @@ inline quantwm_calib_layout calib_layout(const quantwm_config& c) {
 struct AppendArgs {
   const uint8_t* calib;
   int64_t slab;
-  int64_t o_mu_k, o_mu_v, o_a_k, o_b_k, o_a_v, o_b_v, o_wg, o_u_t;
+  int64_t o_mu_k, o_mu_v, o_a_k, o_b_k, o_a_v, o_b_v, o_wg, o_u_t, o_u_dr;
   uint8_t* cache;
   CacheLayout L;
   const void* k;

@@ -39,7 +39,7 @@ class Config(ctypes.Structure):
 class CalibLayout(ctypes.Structure):
     """Mirror of quantwm_calib_layout (byte offsets inside one (b, h) slab)."""
     _fields_ = [(n, ctypes.c_int64) for n in
-                ("slab_bytes", "mu_k", "mu_v", "a_k", "b_k", "a_v", "b_v", "w", "wg", "u_t", "lam")]
+                ("slab_bytes", "mu_k", "mu_v", "a_k", "b_k", "a_v", "b_v", "w", "wg", "u_t", "lam", "u_dr")]
 
 
 def _load():

@@ -39,7 +39,7 @@ def test_sizes_agree_with_the_oracle_format(shape):
     assert qw.quantwm_token_bytes(cfg) == oracle.token_bytes(ocfg)
     L = qw.quantwm_calib_offsets(cfg)
     assert qw.quantwm_calib_bytes(cfg) == L.slab_bytes * B * H
-    offs = [L.mu_k, L.mu_v, L.a_k, L.b_k, L.a_v, L.b_v, L.w, L.wg, L.u_t, L.lam]
+    offs = [L.mu_k, L.mu_v, L.a_k, L.b_k, L.a_v, L.b_v, L.w, L.wg, L.u_t, L.lam, L.u_dr]
     assert all(o % 256 == 0 for o in offs) and offs == sorted(offs) and L.slab_bytes % 256 == 0
 
 
