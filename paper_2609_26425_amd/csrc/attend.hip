@@ -1,15 +1,15 @@
 // Chunked attention over the packed 2-bit cache for gfx950 (Eq. 5 with the
 // PSAC correction of Eq. 17), Keys and Values dequantised on chip.
 //
-// Per workgroup: one (b, h) and BQ = 256 Queries (8 waves x 32). The centroid
-// tables of the head are staged in LDS once. For every 64-key tile the workgroup
-// reads the packed tile (codes, ids, zero-points, scales, INT8 coefficients)
-// from HBM, rebuilds
+// Per workgroup: one (b, h) and BQ = 256 Queries. The centroid tables of the
+// head are staged in LDS once. For every 64-key tile four producer waves read
+// the packed tile (codes, ids, zero-points, scales, INT8 coefficients) from HBM
+// and rebuild
 //     khat_0 = mu_z + s (q - z)   (Eq. 4, fp32, then the MFMA type)
 //     chat   = code * cscale      (INT8 PSAC row)
 //     vhat   = nu_z + s (q - z)
-// into LDS (K row-major, V transposed), and every wave then computes its logits
-// tile with matrix cores as S^T = [khat_0 | chat] [q | qU_r]^T over an augmented
+// into LDS (K row-major, V transposed, double-buffered), while eight consumer
+// waves (32 Queries each) compute the previous tile's logits with matrix cores as S^T = [khat_0 | chat] [q | qU_r]^T over an augmented
 // depth d + r, so (qU)c is added to qk^T before the softmax. With S^T each lane
 // holds one Query column, so the exponentials feed the P.V product straight
 // from the accumulator registers and O^T = Vhat^T P^T accumulates in registers.
@@ -125,15 +125,39 @@ __device__ inline void store_pair(T* p, float a, float b) {
   }
 }
 
-// INT2 codes of N consecutive channels (channel c in bits 2c of cw) as floats.
-// The four 2-bit fields of every byte are spread into four words of bytes, so
-// each code converts with one v_cvt_f32_ubyteN.
+// max of x over lanes i and i ^ 32 (v_permlane32_swap: no LDS round trip)
+__device__ inline float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+// (x & m) | o in one v_and_or_b32; written as asm so that the compiler does not
+// fold the mask into per-field extractions.
+__device__ inline uint32_t and_or(uint32_t x, uint32_t m, uint32_t o) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(m), "v"(o));
+  return r;
+}
+
+// x[c] = mu[c] + s (code_c - z) for the N consecutive channels of one code word
+// (channel c in bits 2c). Each code is placed in a binary16 half as 1024 + code
+// (exponent 10: one unit per ulp), so one packed f16 subtraction of 1024 + z
+// yields two exact (code - z), and v_fma_mix_f32 takes them and the binary16
+// scale as fp32 operands: one rounding, the same value as fma(s, code - z, mu).
 template <int N>
-__device__ inline void codes_to_float(uint32_t cw, float (&q)[N]) {
-  const uint32_t w[4] = {cw & 0x03030303u, (cw >> 2) & 0x03030303u, (cw >> 4) & 0x03030303u,
-                         (cw >> 6) & 0x03030303u};
+__device__ inline void dequant_codes(uint32_t cw, _Float16 s, uint32_t zz, const float (&mu)[N], float (&x)[N]) {
+  static_assert(N == 16 || N == 8, "16 or 8 channels per code word");
+  const f16x2 zh = __builtin_bit_cast(f16x2, zz);
+  // N == 8: channels 4..7 move to bits 16..23, so half k pairs channels k and k + N/2
+  const uint32_t w = N == 16 ? cw : ((cw & 0xffu) | ((cw & 0xff00u) << 8));
 #pragma unroll
-  for (int c = 0; c < N; ++c) q[c] = (float)((w[c % 4] >> (8 * (c / 4))) & 0xffu);
+  for (int k = 0; k < N / 2; ++k) {
+    const f16x2 d = __builtin_bit_cast(f16x2, and_or(w >> (2 * k), 0x00030003u, 0x64006400u)) - zh;
+    x[k] = __builtin_fmaf((float)s, (float)d.x, mu[k]);
+    x[k + N / 2] = __builtin_fmaf((float)s, (float)d.y, mu[k + N / 2]);
+  }
 }
 
 // Builds a bf16x8 MFMA operand from 8 floats with paired conversions.
@@ -147,7 +171,11 @@ __device__ inline V pack_operand(const float* x) {
   }
 }
 
-constexpr int NW = 8, BQ = 32 * NW, KT = 64, NT = 64 * NW;
+// Workgroup: NC consumer waves (32 Queries each: logits, softmax, P.V on the
+// matrix cores) and NP producer waves (read and dequantise the packed tiles).
+// Waves w and w + 4 share a SIMD, so every SIMD runs one producer beside two
+// consumers: the producer's vector work overlaps the consumers' matrix work.
+constexpr int NC = 8, NP = 4, BQ = 32 * NC, KT = 64, NT = 64 * (NC + NP), PT = 64 * NP;
 
 // LDS row strides (elements), chosen so that the matrix-core operand reads are
 // free of bank conflicts: K tile rows of 272 B (16-byte reads), V^T rows of
@@ -191,6 +219,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   const int64_t slot0 = bh * L.slots;
   const int r = a.rank;
   const int G = D / L.ng;
+  const bool producer = wave >= NC;
 
   // ---- stage the centroid tables of this head (App. D.1: BF16 centroids)
   if constexpr (TAB) {
@@ -204,305 +233,346 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     }
   }
 
-  // ---- Query fragment (B operand: k = channel, column = Query)
-  const int64_t qa = int64_t(blockIdx.x) * BQ;
-  const int64_t qi = qa + wave * 32 + l32;
-  const bool qvalid = qi < a.n_q;
-  const T* qrow = reinterpret_cast<const T*>(a.q) + ((int64_t(b) * a.n_q + (qvalid ? qi : 0)) * a.heads + h) * D;
-  V qreg[D / KSTEP];
-#pragma unroll
-  for (int st = 0; st < D / KSTEP; ++st) {
-#pragma unroll
-    for (int j = 0; j < KPL; ++j) vset(qreg[st], j, qvalid ? qrow[st * KSTEP + hf * KPL + j] : T(0.0f));
-  }
-
-  // ---- u = q U_r on matrix cores (A operand: rows = ranks of U_r^T)
-  V ureg[RP > 0 ? RP / KSTEP : 1];
-  if constexpr (RP > 0) {
-    f32x16 uacc;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) uacc[i] = 0.0f;
-#pragma unroll
-    for (int st = 0; st < D / KSTEP; ++st) {
-      V av;
-#pragma unroll
-      for (int j = 0; j < KPL; ++j)
-        vset(av, j, l32 < r ? gU[int64_t(l32) * D + st * KSTEP + hf * KPL + j] : T(0.0f));
-      uacc = MF::run(av, qreg[st], uacc);
-    }
-    // slot i holds rank acc_row(i, hf): round to the MFMA type (the operand of Eq. 17)
-#pragma unroll
-    for (int st = 0; st < RP / KSTEP; ++st)
-#pragma unroll
-      for (int j = 0; j < KPL; ++j) vset(ureg[st], j, T(uacc[st * KPL + j]));
-  }
-
   // ---- key range of this workgroup
   const int64_t F = a.frame_tokens, qs = a.q_start, nc = a.n_cache;
+  const int64_t qa = int64_t(blockIdx.x) * BQ;
   const int64_t qb = qa + BQ < a.n_q ? qa + BQ : a.n_q;
   int64_t kend = LOGITS ? nc : qs + ((qb - 1) / F + 1) * F;
   if (kend > nc) kend = nc;
   int64_t kfull = qs + (qa / F + 1) * F;  // keys below are visible to every Query of the workgroup
   if (kfull > nc) kfull = nc;
-  int64_t lim = qvalid ? qs + (qi / F + 1) * F : nc;  // this lane's Query sees keys j < lim
-  if (lim > nc) lim = nc;
+  const int64_t ntile = (kend + KT - 1) / KT;
+  const int64_t nfull = nc / KT;  // tiles [0, nfull) hold no key past n_cache
 
-  float m_run = -__builtin_inff(), l_run = 0.0f;
-  f32x16 oacc[D / 32];
-#pragma unroll
-  for (int cb = 0; cb < D / 32; ++cb)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) oacc[cb][i] = 0.0f;
-
-  constexpr int CHK = D * KT / NT;        // K channels per thread (one key)
-  constexpr int CHV = D * KT / (2 * NT);  // V channels per thread (two keys)
-  constexpr int RCH = 8;                  // PSAC ranks per thread
+  // ======================= producer state (waves NC .. NC+NP-1)
+  const int ptid = producer ? tid - NC * 64 : 0;
+  constexpr int CHK = D * KT / PT;        // K channels per producer thread (one key)
+  constexpr int NSUB = CHK / 16;          // 16-channel pieces
+  constexpr int CHV = D * KT / (2 * PT);  // V channels per producer thread (two keys)
+  constexpr int RCH = RP > 0 ? RP * KT / PT : 1;  // PSAC ranks per producer thread
   constexpr int RPT = RP > 0 ? RP / RCH : 1;
-  const int kkey = tid / (D / CHK), kch0 = (tid % (D / CHK)) * CHK, kg = kch0 / G;
-  const int vkp = tid % (KT / 2), vch0 = (tid / (KT / 2)) * CHV, vg = vch0 / G;
-  const int ckey = tid / RPT, cr0 = (tid % RPT) * RCH;
-  const bool crole = RP > 0 && tid < KT * RPT && cr0 < r;
-  const bool r8 = (r & 7) == 0;
+  const int kkey = ptid / (D / CHK), kch0 = (ptid % (D / CHK)) * CHK;
+  const int vkp = ptid % (KT / 2), vch0 = (ptid / (KT / 2)) * CHV, vg = vch0 / G;
+  const int ckey = ptid / RPT, cr0 = (ptid % RPT) * RCH;
+  const bool crole = RP > 0 && cr0 < r;
+  const bool raligned = r % RCH == 0;
 
-  // ---- packed tile fields of this thread, loaded one tile ahead of use
-  uint32_t k_cw = 0, c_lo = 0, c_hi = 0, v_cw[2] = {0, 0};
-  int k_id = 0, k_z = 0, v_id[2] = {0, 0}, v_z[2] = {0, 0};
-  float k_s = 0.0f, c_s = 0.0f, v_s[2] = {0.0f, 0.0f};
-  // per-head field bases (wave-uniform) and 32-bit token offsets inside the head
-  const uint8_t* __restrict__ kcb = cache + L.k_codes + slot0 * (D / 4) + kch0 / 4;
-  const uint8_t* __restrict__ kib = cache + L.k_ids + slot0;
-  const uint8_t* __restrict__ kzb = cache + L.k_zp + slot0 * L.zpb + kg / 4;
-  const uint8_t* __restrict__ ksb = cache + L.k_scale + slot0 * 2 * L.ng + 2 * kg;
-  const uint8_t* __restrict__ ccb = cache + L.k_coef + slot0 * r + cr0;
-  const uint8_t* __restrict__ csb = cache + L.k_cscale + slot0 * 2;
-  const uint8_t* __restrict__ vcb = cache + L.v_codes + slot0 * (D / 4) + vch0 / 4;
-  const uint8_t* __restrict__ vib = cache + L.v_ids + slot0;
-  const uint8_t* __restrict__ vzb = cache + L.v_zp + slot0 * L.zpb + vg / 4;
-  const uint8_t* __restrict__ vsb = cache + L.v_scale + slot0 * 2 * L.ng + 2 * vg;
+  // packed tile fields of this thread, loaded one tile ahead of use
+  // zero-points are kept as (1024 + z) in both binary16 halves (dequant_codes)
+  uint32_t k_cw[NSUB], c_w[2] = {0, 0}, v_cw[2] = {0, 0};
+  int k_id = 0, v_id[2] = {0, 0};
+  uint32_t k_z[NSUB], v_z[2] = {0x64006400u, 0x64006400u};
+  _Float16 k_s[NSUB], v_s[2] = {0, 0};
+  float c_s = 0.0f;
+#pragma unroll
+  for (int u = 0; u < NSUB; ++u) { k_cw[u] = 0; k_z[u] = 0x64006400u; k_s[u] = 0; }
+  // Packed fields are read with buffer loads: one resource per field of this
+  // head (base = its first slot), this thread's byte offset inside a tile as the
+  // vector offset (fixed for all tiles) and the tile's byte offset as the scalar
+  // offset, so advancing a tile costs no vector instruction.
   const uint32_t zpb = L.zpb, sstride = 2 * L.ng, ncu = uint32_t(nc);
+  auto field = [&](int64_t off, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(cache + off + slot0 * bytes), 0,
+                                             int(uint32_t(L.slots) * bytes), 0x00020000);
+  };
+  const auto r_kc = field(L.k_codes, D / 4), r_ki = field(L.k_ids, 1), r_kz = field(L.k_zp, zpb),
+             r_ks = field(L.k_scale, sstride), r_vc = field(L.v_codes, D / 4), r_vi = field(L.v_ids, 1),
+             r_vz = field(L.v_zp, zpb), r_vs = field(L.v_scale, sstride);
+  const auto r_cc = field(L.k_coef, uint32_t(r)), r_cs = field(L.k_cscale, 2);
+  const int o_kc = kkey * (D / 4) + kch0 / 4, o_kz = kkey * zpb, o_ks = kkey * sstride;
+  const int o_cc = ckey * r + cr0, o_cs = ckey * 2;
+  const int o_vc = 2 * vkp * (D / 4) + vch0 / 4, o_vz = 2 * vkp * zpb + vg / 4, o_vs = 2 * vkp * sstride + 2 * vg;
 
   // FULL: every key of the tile is < n_cache, so no per-thread guards. A key
   // past n_cache (tail tiles only) gets centroid 0, scale 0 and code 0: a finite
   // placeholder whose logit the mask turns into -inf, so it never contributes.
   auto load_raw = [&](auto full_tag, uint32_t k0) {
     constexpr bool FULL = decltype(full_tag)::value;
-    {
-      const uint32_t tok = k0 + kkey;
-      if (FULL || tok < ncu) {
-        const int id = kib[tok];
-        k_id = id < Kc ? id : Kc - 1;
-        k_z = (kzb[tok * zpb] >> (2 * (kg % 4))) & 3;
-        k_s = (float)*reinterpret_cast<const _Float16*>(ksb + tok * sstride);
-        if constexpr (CHK == 16) k_cw = *reinterpret_cast<const uint32_t*>(kcb + tok * (D / 4));
-        else k_cw = *reinterpret_cast<const uint16_t*>(kcb + tok * (D / 4));
-      } else {
-        k_id = 0; k_z = 0; k_s = 0.0f; k_cw = 0;
+    const int k0i = int(k0);
+    if (FULL || k0 + kkey < ncu) {
+      const int id = __builtin_amdgcn_raw_buffer_load_b8(r_ki, kkey, k0i, 0);
+      k_id = id < Kc ? id : Kc - 1;
+#pragma unroll
+      for (int u = 0; u < NSUB; ++u) {
+        const int g = (kch0 + 16 * u) / G;
+        const uint32_t zb = __builtin_amdgcn_raw_buffer_load_b8(r_kz, o_kz + g / 4, k0i * int(zpb), 0);
+        k_z[u] = (0x6400u + ((zb >> (2 * (g % 4))) & 3)) * 0x00010001u;
+        k_s[u] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_ks, o_ks + 2 * g, k0i * int(sstride), 0));
       }
+      if constexpr (NSUB == 2) {
+        const auto cw = __builtin_amdgcn_raw_buffer_load_b64(r_kc, o_kc, k0i * (D / 4), 0);
+        k_cw[0] = cw[0];
+        k_cw[NSUB - 1] = cw[1];
+      } else {
+        k_cw[0] = __builtin_amdgcn_raw_buffer_load_b32(r_kc, o_kc, k0i * (D / 4), 0);
+      }
+    } else {
+      k_id = 0;
+#pragma unroll
+      for (int u = 0; u < NSUB; ++u) { k_cw[u] = 0; k_z[u] = 0x64006400u; k_s[u] = 0; }
     }
     if constexpr (RP > 0) {
-      const uint32_t tok = k0 + ckey;
       c_s = 0.0f;
-      c_lo = 0;
-      c_hi = 0;
-      if (crole && (FULL || tok < ncu)) {
-        c_s = (float)*reinterpret_cast<const _Float16*>(csb + tok * 2);
-        const uint8_t* cp = ccb + tok * uint32_t(r);
-        if (r8) {
-          const uint2 u = *reinterpret_cast<const uint2*>(cp);
-          c_lo = u.x;
-          c_hi = u.y;
+      c_w[0] = 0;
+      c_w[1] = 0;
+      if (crole && (FULL || k0 + ckey < ncu)) {
+        c_s = (float)__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_cs, o_cs, k0i * 2, 0));
+        if (raligned) {
+          if constexpr (RCH == 8) {
+            const auto u = __builtin_amdgcn_raw_buffer_load_b64(r_cc, o_cc, k0i * r, 0);
+            c_w[0] = u[0];
+            c_w[1] = u[1];
+          } else {
+            c_w[0] = __builtin_amdgcn_raw_buffer_load_b32(r_cc, o_cc, k0i * r, 0);
+          }
         } else {
-          uint32_t w[2] = {0, 0};
 #pragma unroll
           for (int k = 0; k < RCH; ++k)
-            if (cr0 + k < r) w[k / 4] |= uint32_t(cp[k]) << (8 * (k % 4));
-          c_lo = w[0];
-          c_hi = w[1];
+            if (cr0 + k < r) c_w[k / 4] |= uint32_t(__builtin_amdgcn_raw_buffer_load_b8(r_cc, o_cc + k, k0i * r, 0)) << (8 * (k % 4));
         }
       }
     }
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      const uint32_t tok = k0 + 2 * vkp + e;
-      if (FULL || tok < ncu) {
-        const int id = vib[tok];
+      if (FULL || k0 + 2 * vkp + e < ncu) {
+        const int id = __builtin_amdgcn_raw_buffer_load_b8(r_vi, 2 * vkp + e, k0i, 0);
         v_id[e] = id < Kc ? id : Kc - 1;
-        v_z[e] = (vzb[tok * zpb] >> (2 * (vg % 4))) & 3;
-        v_s[e] = (float)*reinterpret_cast<const _Float16*>(vsb + tok * sstride);
-        if constexpr (CHV == 8) v_cw[e] = *reinterpret_cast<const uint16_t*>(vcb + tok * (D / 4));
-        else v_cw[e] = vcb[tok * (D / 4)];
+        const uint32_t zb = __builtin_amdgcn_raw_buffer_load_b8(r_vz, o_vz + e * int(zpb), k0i * int(zpb), 0);
+        v_z[e] = (0x6400u + ((zb >> (2 * (vg % 4))) & 3)) * 0x00010001u;
+        v_s[e] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_vs, o_vs + e * int(sstride), k0i * int(sstride), 0));
+        if constexpr (CHV == 16) v_cw[e] = __builtin_amdgcn_raw_buffer_load_b32(r_vc, o_vc + e * (D / 4), k0i * (D / 4), 0);
+        else v_cw[e] = __builtin_amdgcn_raw_buffer_load_b16(r_vc, o_vc + e * (D / 4), k0i * (D / 4), 0);
       } else {
-        v_id[e] = 0; v_z[e] = 0; v_s[e] = 0.0f; v_cw[e] = 0;
+        v_id[e] = 0; v_z[e] = 0x64006400u; v_s[e] = 0; v_cw[e] = 0;
       }
     }
   };
 
-  // ---- rebuild khat_0 = mu + s (q - z) (Eq. 4), chat = code * cscale and vhat
-  // into tile buffer `buf`. s (q - z) is exact in fp32, so the fma rounds once,
+  // rebuild khat_0 = mu + s (q - z) (Eq. 4), chat = code * cscale and vhat into
+  // tile buffer `buf`. s (q - z) is exact in fp32, so the fma rounds once,
   // exactly like mu + s (q - z).
   auto dequant = [&](int buf) {
     T* kt = smem + tile0 + buf * LY::tile_elems;
     T* ct = kt + KT * LY::KS;
     T* vt = ct + KT * LY::CS;
-    {
-      float q[CHK], mu[CHK], x[CHK];
-      codes_to_float<CHK>(k_cw, q);
-      if constexpr (TAB) load_vals<T, CHK>(tabK + k_id * LY::TS + kch0, mu);
-      else load_vals<T, CHK>(gtabK + k_id * D + kch0, mu);
-      const float zf = (float)k_z;
 #pragma unroll
-      for (int c = 0; c < CHK; ++c) x[c] = __builtin_fmaf(k_s, q[c] - zf, mu[c]);
-      store_vals<T, CHK>(kt + kkey * LY::KS + kch0, x);
+    for (int u = 0; u < NSUB; ++u) {
+      float mu[16], x[16];
+      if constexpr (TAB) load_vals<T, 16>(tabK + k_id * LY::TS + kch0 + 16 * u, mu);
+      else load_vals<T, 16>(gtabK + k_id * D + kch0 + 16 * u, mu);
+      dequant_codes<16>(k_cw[u], k_s[u], k_z[u], mu, x);
+      store_vals<T, 16>(kt + kkey * LY::KS + kch0 + 16 * u, x);
     }
     if constexpr (RP > 0) {
-      if (tid < KT * RPT) {
+      if (ptid < KT * RPT) {
         float x[RCH];
 #pragma unroll
-        for (int k = 0; k < RCH; ++k)
-          x[k] = (float)int8_t(((k < 4 ? c_lo : c_hi) >> (8 * (k % 4))) & 255) * c_s;
+        for (int k = 0; k < RCH; ++k) x[k] = (float)int8_t((c_w[k / 4] >> (8 * (k % 4))) & 255) * c_s;
         store_vals8<T, RCH>(ct + ckey * LY::CS + cr0, x);
       }
     }
     {
       float x0[CHV], x1[CHV];
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        float* x = e == 0 ? x0 : x1;
-        float q[CHV], mu[CHV];
-        codes_to_float<CHV>(v_cw[e], q);
-        if constexpr (TAB) load_vals<T, CHV>(tabV + v_id[e] * LY::TS + vch0, mu);
-        else load_vals<T, CHV>(gtabV + v_id[e] * D + vch0, mu);
-        const float zf = (float)v_z[e];
-#pragma unroll
-        for (int c = 0; c < CHV; ++c) x[c] = __builtin_fmaf(v_s[e], q[c] - zf, mu[c]);
+      float mu0[CHV], mu1[CHV];
+      if constexpr (TAB) {
+        load_vals<T, CHV>(tabV + v_id[0] * LY::TS + vch0, mu0);
+        load_vals<T, CHV>(tabV + v_id[1] * LY::TS + vch0, mu1);
+      } else {
+        load_vals<T, CHV>(gtabV + v_id[0] * D + vch0, mu0);
+        load_vals<T, CHV>(gtabV + v_id[1] * D + vch0, mu1);
       }
+      dequant_codes<CHV>(v_cw[0], v_s[0], v_z[0], mu0, x0);
+      dequant_codes<CHV>(v_cw[1], v_s[1], v_z[1], mu1, x1);
 #pragma unroll
       for (int c = 0; c < CHV; ++c) store_pair<T>(vt + (vch0 + c) * LY::VS + 2 * vkp, x0[c], x1[c]);
     }
   };
 
-  const int64_t ntile = (kend + KT - 1) / KT;
-  const int64_t nfull = nc / KT;  // tiles [0, nfull) hold no key past n_cache
   using Full = std::integral_constant<bool, true>;
   using Tail = std::integral_constant<bool, false>;
-  if (ntile > 0) {
-    if (nfull > 0) load_raw(Full{}, 0u);
-    else load_raw(Tail{}, 0u);
-    dequant(0);
-    if (ntile > 1) {
-      if (nfull > 1) load_raw(Full{}, uint32_t(KT));
-      else load_raw(Tail{}, uint32_t(KT));
+  auto prefetch = [&](int64_t t) {
+    if (t < nfull) load_raw(Full{}, uint32_t(t * KT));
+    else load_raw(Tail{}, uint32_t(t * KT));
+  };
+
+  // ======================= consumer state (waves 0 .. NC-1)
+  const int64_t qi = qa + (producer ? 0 : wave) * 32 + l32;
+  const bool qvalid = !producer && qi < a.n_q;
+  V qreg[D / KSTEP];
+  V ureg[RP > 0 ? RP / KSTEP : 1];
+  float m_run = -__builtin_inff(), l_run = 0.0f;
+  f32x16 oacc[D / 32];
+  int64_t lim = nc;
+  if (!producer) {
+    // Query fragment (B operand: k = channel, column = Query)
+    const T* qrow = reinterpret_cast<const T*>(a.q) + ((int64_t(b) * a.n_q + (qvalid ? qi : 0)) * a.heads + h) * D;
+#pragma unroll
+    for (int st = 0; st < D / KSTEP; ++st) {
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) vset(qreg[st], j, qvalid ? qrow[st * KSTEP + hf * KPL + j] : T(0.0f));
     }
+    // u = q U_r on matrix cores (A operand: rows = ranks of U_r^T)
+    if constexpr (RP > 0) {
+      f32x16 uacc;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) uacc[i] = 0.0f;
+#pragma unroll
+      for (int st = 0; st < D / KSTEP; ++st) {
+        V av;
+#pragma unroll
+        for (int j = 0; j < KPL; ++j)
+          vset(av, j, l32 < r ? gU[int64_t(l32) * D + st * KSTEP + hf * KPL + j] : T(0.0f));
+        uacc = MF::run(av, qreg[st], uacc);
+      }
+      // slot i holds rank acc_row(i, hf): round to the MFMA type (the operand of Eq. 17)
+#pragma unroll
+      for (int st = 0; st < RP / KSTEP; ++st)
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) vset(ureg[st], j, T(uacc[st * KPL + j]));
+    }
+#pragma unroll
+    for (int cb = 0; cb < D / 32; ++cb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) oacc[cb][i] = 0.0f;
+    if (qvalid) lim = qs + (qi / F + 1) * F;  // this lane's Query sees keys j < lim
+    if (lim > nc) lim = nc;
   }
   const float mscale = 1.4426950408889634f / sqrtf((float)D);  // logits are exponentiated as 2^(S log2(e)/sqrt(d))
 
-  for (int64_t it = 0; it < ntile; ++it) {
+  // Producers and consumers run separate loops with one barrier per tile each,
+  // so neither keeps the other's registers live.
+  if (producer) {
+    // Producers issue first: their vector work fills the matrix-core phases of
+    // the consumers, and a late tile would stall all eight consumers.
+    __builtin_amdgcn_s_setprio(2);
+    if (ntile > 0) {
+      prefetch(0);
+      dequant(0);
+      if (ntile > 1) prefetch(1);
+    }
+    for (int64_t it = 0; it < ntile; ++it) {
+      // buffer it&1 is complete and every consumer is done with buffer (it+1)&1
+      __syncthreads();
+      if (it + 1 < ntile) {
+        dequant(int((it + 1) & 1));
+        if (it + 2 < ntile) prefetch(it + 2);
+      }
+    }
+    return;
+  }
+
+  // Lazy rescaling: the running max m_run is raised only when a logit exceeds it
+  // by more than tau (2^8 in probability), so probabilities stay below 256 and
+  // the rescale of O is rare after the first tiles. O / l and lse are exact for
+  // any m_run, so this changes no result beyond rounding.
+  const float tau = 8.0f / mscale;
+
+  // Tiles below kfull need no mask: they run as a separate instance of the tile
+  // code without the mask branches, so nothing splits its instruction stream.
+  auto tile = [&](int64_t it, auto mask_tag) {
+    constexpr bool MASKED = decltype(mask_tag)::value;
     const int64_t k0 = it * KT;
-    // buffer it&1 is complete and every wave is done with buffer (it+1)&1
     __syncthreads();
     const T* kt = smem + tile0 + int(it & 1) * LY::tile_elems;
     const T* ct = kt + KT * LY::KS;
     const T* vt = ct + KT * LY::CS;
 
-    // ---- logits tile S^T (keys x Queries) on matrix cores
-    f32x16 sacc[2];
+    // logits S^T of the 32 keys k0 + 32 kb + row (rows x Queries) on matrix cores
+    auto logits_half = [&](int kb) {
+      f32x16 acc;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+      for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+      const T* krow = kt + (kb * 32 + l32) * LY::KS;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) sacc[kb][i] = 0.0f;
-    }
-#pragma unroll
-    for (int st = 0; st < D / KSTEP; ++st) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const T* krow = kt + (kb * 32 + l32) * LY::KS;
+      for (int st = 0; st < D / KSTEP; ++st) {
         V av;
         if constexpr (KPL == 8) av = *reinterpret_cast<const V*>(krow + st * KSTEP + hf * KPL);
         else av = krow[st * KSTEP + hf];
-        sacc[kb] = MF::run(av, qreg[st], sacc[kb]);
+        acc = MF::run(av, qreg[st], acc);
       }
-    }
-    if constexpr (RP > 0) {
+      if constexpr (RP > 0) {
+        const T* crow = ct + (kb * 32 + l32) * LY::CS;
 #pragma unroll
-      for (int st = 0; st < RP / KSTEP; ++st) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          const T* crow = ct + (kb * 32 + l32) * LY::CS;
+        for (int st = 0; st < RP / KSTEP; ++st) {
           V av;
 #pragma unroll
           for (int j = 0; j < KPL; ++j) vset(av, j, crow[acc_row(st * KPL + j, hf)]);
-          sacc[kb] = MF::run(av, ureg[st], sacc[kb]);
+          acc = MF::run(av, ureg[st], acc);
         }
       }
-    }
-
-    // ---- next tile into the other buffer while the matrix cores run
-    if (it + 1 < ntile) {
-      dequant(int((it + 1) & 1));
-      if (it + 2 < ntile) {
-        if (it + 2 < nfull) load_raw(Full{}, uint32_t(k0 + 2 * KT));
-        else load_raw(Tail{}, uint32_t(k0 + 2 * KT));
-      }
-    }
+      return acc;
+    };
 
     if constexpr (LOGITS) {
-      if (qvalid) {
-        const float inv = 1.0f / sqrtf((float)D);
-        float* lrow = a.logits + (bh * a.n_q + qi) * nc;
+      const float inv = 1.0f / sqrtf((float)D);
+      float* lrow = a.logits + (bh * a.n_q + (qvalid ? qi : 0)) * nc;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb) {
+        // every lane takes part in the matrix-core product: its operand reads
+        // feed the whole wave, so they may not sit under a per-lane condition
+        const f32x16 sv = logits_half(kb);
+        if (qvalid) {
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const int64_t j = k0 + kb * 32 + acc_row(i, hf);
-            if (j < nc) lrow[j] = j < lim ? sacc[kb][i] * inv : -__builtin_inff();
+            if (j < nc) lrow[j] = j < lim ? sv[i] * inv : -__builtin_inff();
           }
+        }
       }
     } else {
-      // ---- online softmax on raw logits; masked keys -> -inf
-      if (k0 + KT > kfull) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+      // masked keys (only in tiles past kfull) -> -inf
+      auto mask_half = [&](f32x16& sv, int kb) {
+        if constexpr (MASKED) {
 #pragma unroll
           for (int i = 0; i < 16; ++i)
-            if (k0 + kb * 32 + acc_row(i, hf) >= lim) sacc[kb][i] = -__builtin_inff();
-      }
-      float mt = -__builtin_inff();
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mt = fmaxf(mt, sacc[kb][i]);
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
-      const float m_new = fmaxf(m_run, mt);
-      if (__any(m_new > m_run)) {  // rescale only when some row's running max moved
-        const float alpha = m_new == -__builtin_inff() ? 1.0f : __builtin_amdgcn_exp2f((m_run - m_new) * mscale);
-        l_run *= alpha;
-#pragma unroll
-        for (int cb = 0; cb < D / 32; ++cb)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) oacc[cb][i] *= alpha;
-        m_run = m_new;
-      }
-      const float mc = m_run == -__builtin_inff() ? 0.0f : -m_run * mscale;
-      float lpart[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][i], mscale, mc));
-          sacc[kb][i] = p;
-          lpart[i % 4] += p;
+            if (k0 + kb * 32 + acc_row(i, hf) >= lim) sv[i] = -__builtin_inff();
         }
-      l_run += (lpart[0] + lpart[1]) + (lpart[2] + lpart[3]);
-
-      // ---- O^T += Vhat^T P^T (B operand = this lane's probabilities)
+      };
+      // raise m_run if the tile's max exceeds it by more than tau
+      auto raise_max = [&](const f32x16& sa, const f32x16& sb) {
+        float mt = -__builtin_inff();
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+        for (int i = 0; i < 16; ++i) mt = fmaxf(mt, fmaxf(sa[i], sb[i]));
+        mt = max_halves(mt);
+        if (__any(mt > m_run + tau)) {
+          const float m_new = fmaxf(m_run, mt);
+          const float alpha = m_new == -__builtin_inff() ? 1.0f : __builtin_amdgcn_exp2f((m_run - m_new) * mscale);
+          l_run *= alpha;
+#pragma unroll
+          for (int cb = 0; cb < D / 32; ++cb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) oacc[cb][i] *= alpha;
+          m_run = m_new;
+        }
+      };
+      auto probs = [&](f32x16& sv) {
+        const float mc = m_run == -__builtin_inff() ? 0.0f : -m_run * mscale;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sv[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[i], mscale, mc));
+        if constexpr (KPL == 1) {
+          float lpart[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int i = 0; i < 16; ++i) lpart[i % 4] += sv[i];
+          l_run += (lpart[0] + lpart[1]) + (lpart[2] + lpart[3]);
+        }
+      };
+      // O^T += Vhat^T P^T over the 32 keys of half kb (B operand = this lane's probabilities)
+      auto pv_half = [&](const f32x16& pv32, int kb) {
 #pragma unroll
         for (int t = 0; t < 32 / KSTEP; ++t) {
           float pv[KPL];
 #pragma unroll
-          for (int j = 0; j < KPL; ++j) pv[j] = sacc[kb][t * KPL + j];
+          for (int j = 0; j < KPL; ++j) pv[j] = pv32[t * KPL + j];
           const V bv = pack_operand<V>(pv);
+          if constexpr (KPL == 8) {
+            // row sum of the probabilities as rounded for the product: two per v_dot2_f32_bf16
+            const bf16x2 one = {bf16(1.0f), bf16(1.0f)};
+            const uint4 pw = __builtin_bit_cast(uint4, bv);
+            const uint32_t w[4] = {pw.x, pw.y, pw.z, pw.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[j]), one, l_run, false);
+          }
 #pragma unroll
           for (int cb = 0; cb < D / 32; ++cb) {
             const T* vrow = vt + (cb * 32 + l32) * LY::VS + kb * 32;
@@ -512,21 +582,37 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
             oacc[cb] = MF::run(av, bv, oacc[cb]);
           }
         }
-    }
+      };
 
-  }
+      f32x16 s0 = logits_half(0);
+      f32x16 s1 = logits_half(1);
+      mask_half(s0, 0);
+      mask_half(s1, 1);
+      raise_max(s0, s1);
+      probs(s0);
+      probs(s1);
+      pv_half(s0, 0);
+      pv_half(s1, 1);
+    }
+  };
+  const int64_t nclean = kfull / KT < ntile ? kfull / KT : ntile;
+  int64_t it = 0;
+  for (; it < nclean; ++it) tile(it, std::integral_constant<bool, false>{});
+  for (; it < ntile; ++it) tile(it, std::integral_constant<bool, true>{});
 
   if constexpr (!LOGITS) {
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
-    if (qvalid) {
-      const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
-      T* orow = reinterpret_cast<T*>(a.out) + ((int64_t(b) * a.n_q + qi) * a.heads + h) * D;
+    if (!producer) {
+      const float l_tot = l_run + __shfl_xor(l_run, 32);
+      if (qvalid) {
+        const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+        T* orow = reinterpret_cast<T*>(a.out) + ((int64_t(b) * a.n_q + qi) * a.heads + h) * D;
 #pragma unroll
-      for (int cb = 0; cb < D / 32; ++cb)
+        for (int cb = 0; cb < D / 32; ++cb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) orow[cb * 32 + acc_row(i, hf)] = T(oacc[cb][i] * inv);
-      if (a.lse && hf == 0)
-        a.lse[bh * a.n_q + qi] = l_tot > 0.0f ? m_run / sqrtf((float)D) + logf(l_tot) : -__builtin_inff();
+          for (int i = 0; i < 16; ++i) orow[cb * 32 + acc_row(i, hf)] = T(oacc[cb][i] * inv);
+        if (a.lse && hf == 0)
+          a.lse[bh * a.n_q + qi] = l_tot > 0.0f ? m_run / sqrtf((float)D) + logf(l_tot) : -__builtin_inff();
+      }
     }
   }
 }
