@@ -65,6 +65,26 @@ def append_flops(wl, n_new) -> float:
     return wl.batch * wl.heads * n_new * (4 * wl.n_centroids * d + 2 * d * wl.rank + 28 * d)
 
 
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary of this
+    workload, or None when there is none or the kernel source has changed since
+    the counters were taken (the summary records the source's SHA-256)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"attend_append_{workload}_traffic.md")
+    src = os.path.join(ROOT, "paper_2609_26425_amd", "csrc", f"{kernel}.hip")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.split(":")[0].strip().startswith(kernel + "_"):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if fields.get(f"{kernel}_source_sha256") != digest or f"{kernel}_traffic_bytes_per_launch" not in fields:
+        return None
+    return int(fields[f"{kernel}_traffic_bytes_per_launch"])
+
+
 def cpu_baseline(wl):
     """The oracle as it stands, timed on a bounded sample of the same step."""
     import oracle
@@ -125,6 +145,9 @@ def main():
     ap.add_argument("--workload", default="lingbot-40h", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--copies", type=int, default=3, help="rotated input/cache copies (defeats the 256 MiB MALL)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run one plain 1 GiB device copy kernel (read 1 GiB, write 1 GiB) outside the timed "
+                         "region, as the scale for FETCH_SIZE / WRITE_SIZE counter runs")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (heads shard with no exchange; "
@@ -183,6 +206,13 @@ def main():
         if ev is not None:
             ev[2].record()
 
+    if args.copy_probe:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)  # elementwise kernel: 1 GiB read, 1 GiB written
+        torch.cuda.synchronize()
+        del src, dst
+
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for i in range(args.warmup):
         step(i)
@@ -224,7 +254,9 @@ def main():
         "append_hbm_frac": app_gbps / PEAK_HBM_GBPS,
         "append_valu_frac": app_tflops / PEAK_FP32_VALU_TFLOPS,
         "roofline": {"kernel": "attend", "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": measured_traffic("attend", wl.name)},
+        "append_traffic": measured_traffic("append", wl.name),
         "copies": args.copies,
     }
     if not args.no_cpu_baseline:
