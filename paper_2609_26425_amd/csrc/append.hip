@@ -104,11 +104,12 @@ __device__ inline void round_quotients(const float (&xv)[N], const float (&mu)[N
 // quantised with the stored FP16 scale). Token and centroid values stream from
 // memory 16 channels at a time in two passes (range, then codes). Codes are
 // stored as they are made; `each(c, e)` receives e = x_c - (mu_c + s (q_c - z))
-// for every channel c in order (Eq. 4, Eq. 13).
-template <typename T, int D, int G, typename F>
+// for every channel c in order (Eq. 4, Eq. 13), and `chunk(c0)` follows the
+// last channel of every chunk of CH channels starting at c0.
+template <typename T, int D, int G, typename F, typename FC>
 __device__ inline void quant_stream(const T* __restrict__ xrow, const T* __restrict__ mrow,
                                     uint8_t* __restrict__ codes, bool active, int (&zg)[D / G],
-                                    float (&sg)[D / G], F each) {
+                                    float (&sg)[D / G], F each, FC chunk) {
   constexpr int CH = G < 16 ? G : 16;
   static_for<0, D / G>([&](auto gi) {
     constexpr int g = decltype(gi)::value;
@@ -152,6 +153,7 @@ __device__ inline void quant_stream(const T* __restrict__ xrow, const T* __restr
         if constexpr (CH == 16) *reinterpret_cast<uint32_t*>(codes + c0 / 4) = cw;
         else *reinterpret_cast<uint16_t*>(codes + c0 / 4) = uint16_t(cw);
       }
+      chunk(c0);
     });
   });
 }
@@ -274,14 +276,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     for (int k = 0; k < (RP > 0 ? RP : 1); ++k) C[k] = 0.0f;
     int zg[NG];
     float sg[NG];
-    quant_stream<T, D, G>(krow, mrow, a.cache + a.L.k_codes + slot * (D / 4), active, zg, sg,
-                          [&](int c, float e) {
-                            if constexpr (RP > 0) {
-                              const float* urow = udr + c * RP;
+    // The errors of one chunk go to this thread's LDS row, and a rolled loop over
+    // the chunk's channels adds e_c U_r[c, :] to C. Written as straight-line code,
+    // the compiler hoisted the wave-uniform loads of all d x RP entries of U_r
+    // and spilled them.
+    constexpr int CHK = G < 16 ? G : 16, ES = CHK + 1;
+    __shared__ float s_err[RP > 0 ? 256 * ES : 1];
+    float* my_err = s_err + threadIdx.x * ES;
+    quant_stream<T, D, G>(
+        krow, mrow, a.cache + a.L.k_codes + slot * (D / 4), active, zg, sg,
+        [&](int c, float e) {
+          if constexpr (RP > 0) my_err[c % CHK] = e;
+        },
+        [&](int c0) {
+          if constexpr (RP > 0) {
+#pragma nounroll
+            for (int c = 0; c < CHK; ++c) {
+              const float e = my_err[c];
+              const float* urow = udr + (c0 + c) * RP;
 #pragma unroll
-                              for (int k = 0; k < RP; ++k) C[k] = __builtin_fmaf(e, urow[k], C[k]);
-                            }
-                          });
+              for (int k = 0; k < RP; ++k) C[k] = __builtin_fmaf(e, urow[k], C[k]);
+            }
+          }
+        });
     if (active) {
       store_meta<D, G>(a.cache + a.L.k_zp + slot * a.L.zpb, a.cache + a.L.k_scale + slot * 2 * NG, zg, sg);
       a.cache[a.L.k_ids + slot] = uint8_t(z);
@@ -333,7 +350,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     int zg[NG];
     float sg[NG];
     quant_stream<T, D, G>(reinterpret_cast<const T*>(a.v) + src, muv + int64_t(zv) * D,
-                          a.cache + a.L.v_codes + slot * (D / 4), active, zg, sg, [](int, float) {});
+                          a.cache + a.L.v_codes + slot * (D / 4), active, zg, sg, [](int, float) {}, [](int) {});
     if (active) {
       store_meta<D, G>(a.cache + a.L.v_zp + slot * a.L.zpb, a.cache + a.L.v_scale + slot * 2 * NG, zg, sg);
       a.cache[a.L.v_ids + slot] = uint8_t(zv);
