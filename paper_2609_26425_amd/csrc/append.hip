@@ -264,6 +264,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     if (S < zs || (S == zs && j < z)) { zs = S; z = j; }
   });
 
+  // ---- Values: nearest centroid (w = 1). Both searches run before the first
+  // store, so the compiler may keep their table loads on the scalar path.
+  load_row<T, D>(reinterpret_cast<const T*>(a.v) + src, x);
+  int zv = 0;
+  float dv = __builtin_inff();
+  for (int j = 0; j < Kc; j += 4) {
+    float acc[4];
+    int row[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      row[u] = min(j + u, Kc - 1);
+      acc[u] = bv[row[u]];
+    }
+#pragma unroll
+    for (int c = 0; c < D; ++c)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] = __builtin_fmaf(av[row[u] * D + c], x[c], acc[u]);
+    // branch-free update: a divergent branch here turns the table loads of the
+    // loop into per-lane vector loads
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const bool better = (j + u < Kc) & (acc[u] < dv);
+      dv = better ? acc[u] : dv;
+      zv = better ? j + u : zv;
+    }
+  }
   // ---- INT2 residual against mu_z, with PSAC accumulated channel by channel:
   // E_c = k_c - khat_0,c (Eq. 13), C_k += E_c U_ck (Eq. 16). From here on the
   // key is re-read 16 channels at a time (L1 hits), so only the r accumulators
@@ -326,26 +352,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     }
   }
 
-  // ---- Values: nearest centroid (w = 1), same residual path, no PSAC
-  load_row<T, D>(reinterpret_cast<const T*>(a.v) + src, x);
-  int zv = 0;
-  float dv = __builtin_inff();
-  for (int j = 0; j < Kc; j += 4) {
-    float acc[4];
-    int row[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      row[u] = min(j + u, Kc - 1);
-      acc[u] = bv[row[u]];
-    }
-#pragma unroll
-    for (int c = 0; c < D; ++c)
-#pragma unroll
-      for (int u = 0; u < 4; ++u) acc[u] = __builtin_fmaf(av[row[u] * D + c], x[c], acc[u]);
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (j + u < Kc && acc[u] < dv) { dv = acc[u]; zv = j + u; }
-  }
+  // ---- Values: the same residual path as Keys, no PSAC
   {
     int zg[NG];
     float sg[NG];
