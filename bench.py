@@ -191,6 +191,8 @@ def main():
     outs = [torch.empty_like(q) for _ in range(args.copies)]
     qs = [q.clone() for _ in range(args.copies)]
     lse = torch.empty((wl.batch, wl.heads, wl.n_q), dtype=torch.float32, device=dev)
+    ws_bytes = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q)
+    attend_ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
     del k_all, v_all
     torch.cuda.synchronize()
 
@@ -202,7 +204,7 @@ def main():
         if ev is not None:
             ev[1].record()
         qw.quantwm_attend(cfg, calib, caches[c], wl.n_cache, qs[c], wl.n_q, wl.q_start, wl.frame_tokens,
-                          outs[c], lse)
+                          outs[c], lse, attend_ws)
         if ev is not None:
             ev[2].record()
 
@@ -258,6 +260,7 @@ def main():
                      "traffic": measured_traffic("attend", wl.name)},
         "append_traffic": measured_traffic("append", wl.name),
         "copies": args.copies,
+        "attend_workspace_bytes": ws_bytes,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)

@@ -139,6 +139,14 @@ quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void
                               int64_t n_cached, const void* k_new, const void* v_new,
                               int64_t n_new, float* coef_f32_out, void* stream);
 
+/* Device workspace bytes that quantwm_attend can use for these sizes (0 when
+ * it has no use for one). With it, a launch that would give the GPU fewer than
+ * two workgroups per compute unit splits every Query block's key range over
+ * several workgroups and merges their partial softmax results (the log-sum-exp
+ * merge of Eq. 5 over disjoint key sets); the result is the same up to rounding.
+ * The size depends on the current device's compute-unit count. */
+size_t quantwm_attend_workspace_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_q);
+
 /* Attention of a Query chunk over the packed cache (Eq. 5 with Eq. 17):
  * L = (q . khat_0 + (q U_r) . chat) / sqrt(d), softmax over visible keys, times
  * vhat. Query i sits at absolute position q_start + i; key j is visible iff
@@ -147,10 +155,14 @@ quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void
  * lse_out: optional [B,H,n_q] f32 natural-log sum-exp (-inf for a row with no
  * visible key, whose O is 0). Needs 0 <= q_start <= n_cache <= capacity.
  * n_q == 0 is a no-op. Keys and Values are dequantised in registers; the cache
- * is only ever read in packed form. */
+ * is only ever read in packed form. workspace: optional device scratch of
+ * workspace_bytes, 256-byte aligned, owned by the caller and not read back (NULL,
+ * or fewer bytes than quantwm_attend_workspace_bytes(), means no split). Calls
+ * that share a workspace must be ordered on one stream. */
 quantwm_status quantwm_attend(const quantwm_config* cfg, const void* calib, const void* cache,
                               int64_t n_cache, const void* q, int64_t n_q, int64_t q_start,
-                              int32_t frame_tokens, void* out, float* lse_out, void* stream);
+                              int32_t frame_tokens, void* out, float* lse_out, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /* Test hook: the scaled logits of quantwm_attend, [B,H,n_q,n_cache] f32,
  * -inf where masked. Same tile code as quantwm_attend. */

@@ -257,9 +257,36 @@ quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void
   return ok();
 }
 
+// Compute units of the current device (256 on MI355X; 256 when no device answers,
+// so that sizes agree between a host-only query and the launch).
+static int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  return cus;
+}
+
+static size_t attend_split_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_q, int* splits) {
+  const int ns = qwm::attend_splits(n_q, cfg->heads, cfg->batch, n_cache, device_cus());
+  if (splits) *splits = ns;
+  if (ns <= 1) return 0;
+  const size_t rows = size_t(ns) * cfg->batch * cfg->heads * size_t(n_q);
+  const size_t o_bytes = (rows * cfg->head_dim * 4 + 255) / 256 * 256;
+  return o_bytes + rows * 2 * 4;
+}
+
+size_t quantwm_attend_workspace_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_q) {
+  if (check_cfg(cfg) != QWM_OK || n_cache < 0 || n_q <= 0) return 0;
+  return attend_split_bytes(cfg, n_cache, n_q, nullptr);
+}
+
 static quantwm_status attend_common(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
                                     const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
-                                    float* lse_out, float* logits_out, void* stream) {
+                                    float* lse_out, float* logits_out, void* workspace, size_t workspace_bytes,
+                                    void* stream) {
   QWM_TRY(check_cfg(cfg));
   if (n_cache < 0 || n_q < 0 || q_start < 0) return fail(QWM_ERR_INVALID_ARG, "sizes must be >= 0");
   if (n_cache > cfg->capacity) return fail(QWM_ERR_CAPACITY, "n_cache exceeds capacity");
@@ -289,6 +316,21 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   a.n_cache = n_cache; a.n_q = n_q; a.q_start = q_start;
   a.frame_tokens = frame_tokens; a.heads = cfg->heads; a.n_centroids = cfg->n_centroids; a.rank = cfg->rank;
   a.tables_in_lds = tables ? 1 : 0;
+  a.n_split = 1;
+  a.part_o = nullptr;
+  a.part_ml = nullptr;
+  if (!logits_out && workspace) {
+    if (reinterpret_cast<uintptr_t>(workspace) & 255) return fail(QWM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    int ns = 1;
+    const size_t need = attend_split_bytes(cfg, n_cache, n_q, &ns);
+    if (ns > 1 && workspace_bytes >= need) {
+      const size_t rows = size_t(ns) * cfg->batch * cfg->heads * size_t(n_q);
+      a.n_split = ns;
+      a.part_o = static_cast<float*>(workspace);
+      a.part_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + (rows * cfg->head_dim * 4 + 255) / 256 * 256);
+    }
+  }
+  if ((n_q + 255) / 256 * int64_t(a.n_split) > 0x7fffffff) return fail(QWM_ERR_UNSUPPORTED, "n_q too large");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool lg = logits_out != nullptr;
   const hipError_t e = cfg->dtype == QWM_BF16 ? qwm::launch_attend_bf16(a, cfg->head_dim, cfg->batch, lg, s)
@@ -299,8 +341,9 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
 
 quantwm_status quantwm_attend(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
                               const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
-                              float* lse_out, void* stream) {
-  return attend_common(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, out, lse_out, nullptr, stream);
+                              float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
+  return attend_common(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, out, lse_out, nullptr, workspace,
+                       workspace_bytes, stream);
 }
 
 quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
@@ -308,7 +351,7 @@ quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, cons
                               void* stream) {
   if (!logits_out && n_q > 0) return fail(QWM_ERR_INVALID_ARG, "logits_out is null");
   return attend_common(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, nullptr, nullptr, logits_out,
-                       stream);
+                       nullptr, 0, stream);
 }
 
 }  // extern "C"

@@ -233,15 +233,20 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     }
   }
 
-  // ---- key range of this workgroup
+  // ---- key range of this workgroup: Query block blockIdx.x / n_split, and the
+  // split-th of n_split equal runs of its key tiles
   const int64_t F = a.frame_tokens, qs = a.q_start, nc = a.n_cache;
-  const int64_t qa = int64_t(blockIdx.x) * BQ;
+  const int split = int(blockIdx.x) % a.n_split;
+  const int64_t qa = int64_t(blockIdx.x / a.n_split) * BQ;
   const int64_t qb = qa + BQ < a.n_q ? qa + BQ : a.n_q;
   int64_t kend = LOGITS ? nc : qs + ((qb - 1) / F + 1) * F;
   if (kend > nc) kend = nc;
   int64_t kfull = qs + (qa / F + 1) * F;  // keys below are visible to every Query of the workgroup
   if (kfull > nc) kfull = nc;
-  const int64_t ntile = (kend + KT - 1) / KT;
+  const int64_t ntile_all = (kend + KT - 1) / KT;
+  const int64_t per_split = (ntile_all + a.n_split - 1) / a.n_split;
+  const int64_t t0 = split * per_split < ntile_all ? split * per_split : ntile_all;
+  const int64_t ntile = t0 + per_split < ntile_all ? t0 + per_split : ntile_all;  // this split: tiles [t0, ntile)
   const int64_t nfull = nc / KT;  // tiles [0, nfull) hold no key past n_cache
 
   // ======================= producer state (waves NC .. NC+NP-1)
@@ -445,12 +450,12 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     // Producers issue first: their vector work fills the matrix-core phases of
     // the consumers, and a late tile would stall all eight consumers.
     __builtin_amdgcn_s_setprio(2);
-    if (ntile > 0) {
-      prefetch(0);
-      dequant(0);
-      if (ntile > 1) prefetch(1);
+    if (t0 < ntile) {
+      prefetch(t0);
+      dequant(int(t0 & 1));
+      if (t0 + 1 < ntile) prefetch(t0 + 1);
     }
-    for (int64_t it = 0; it < ntile; ++it) {
+    for (int64_t it = t0; it < ntile; ++it) {
       // buffer it&1 is complete and every consumer is done with buffer (it+1)&1
       __syncthreads();
       if (it + 1 < ntile) {
@@ -596,13 +601,28 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     }
   };
   const int64_t nclean = kfull / KT < ntile ? kfull / KT : ntile;
-  int64_t it = 0;
+  int64_t it = t0;
   for (; it < nclean; ++it) tile(it, std::integral_constant<bool, false>{});
   for (; it < ntile; ++it) tile(it, std::integral_constant<bool, true>{});
 
   if constexpr (!LOGITS) {
-    if (!producer) {
-      const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    if (a.n_split > 1) {
+      // partial result of this split: unnormalised O, the running max (raw logit
+      // units) and the sum; attend_combine merges the splits
+      if (qvalid) {
+        const int64_t row = (int64_t(split) * a.heads * gridDim.z + bh) * a.n_q + qi;
+        float* po = a.part_o + row * D;
+#pragma unroll
+        for (int cb = 0; cb < D / 32; ++cb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) po[cb * 32 + acc_row(i, hf)] = oacc[cb][i];
+        if (hf == 0) {
+          a.part_ml[2 * row] = m_run;
+          a.part_ml[2 * row + 1] = l_tot;
+        }
+      }
+    } else {
       if (qvalid) {
         const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
         T* orow = reinterpret_cast<T*>(a.out) + ((int64_t(b) * a.n_q + qi) * a.heads + h) * D;
@@ -615,6 +635,42 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       }
     }
   }
+}
+
+// Merges the n_split partial results of every Query: with M the largest running
+// max and w_s = 2^((m_s - M) log2(e) / sqrt(d)), O = sum w_s O_s / sum w_s l_s
+// and lse = M / sqrt(d) + log(sum w_s l_s). One wave per Query, D / 64 channels
+// per lane.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void attend_combine(const AttendArgs a) {
+  const int64_t qi = int64_t(blockIdx.x) * 4 + threadIdx.x / 64;
+  const int lane = threadIdx.x % 64;
+  const int h = blockIdx.y, b = blockIdx.z;
+  if (qi >= a.n_q) return;
+  const int64_t bh = int64_t(b) * a.heads + h;
+  const int64_t plane = int64_t(a.heads) * gridDim.z * a.n_q;  // rows per split
+  const float mscale = 1.4426950408889634f / sqrtf((float)D);
+  float M = -__builtin_inff();
+  for (int sp = 0; sp < a.n_split; ++sp) M = fmaxf(M, a.part_ml[2 * (sp * plane + bh * a.n_q + qi)]);
+  constexpr int PL = D / 64;
+  float o[PL];
+#pragma unroll
+  for (int j = 0; j < PL; ++j) o[j] = 0.0f;
+  float L = 0.0f;
+  for (int sp = 0; sp < a.n_split; ++sp) {
+    const int64_t row = sp * plane + bh * a.n_q + qi;
+    const float m = a.part_ml[2 * row], l = a.part_ml[2 * row + 1];
+    if (!(l > 0.0f)) continue;  // this split saw no visible key of this Query
+    const float w = __builtin_amdgcn_exp2f((m - M) * mscale);
+    L += w * l;
+#pragma unroll
+    for (int j = 0; j < PL; ++j) o[j] += w * a.part_o[row * D + j * 64 + lane];
+  }
+  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+  T* orow = reinterpret_cast<T*>(a.out) + ((int64_t(b) * a.n_q + qi) * a.heads + h) * D;
+#pragma unroll
+  for (int j = 0; j < PL; ++j) orow[j * 64 + lane] = T(o[j] * inv);
+  if (a.lse && lane == 0) a.lse[bh * a.n_q + qi] = L > 0.0f ? M / sqrtf((float)D) + logf(L) : -__builtin_inff();
 }
 
 template <typename T, int D>
@@ -638,11 +694,15 @@ hipError_t launch_k(const AttendArgs& a, const dim3& grid, size_t lds, hipStream
 
 template <typename T, int D, int RP>
 hipError_t launch_r(const AttendArgs& a, int batch, bool logits, hipStream_t s) {
-  const dim3 grid((unsigned)((a.n_q + BQ - 1) / BQ), (unsigned)a.heads, (unsigned)batch);
+  const dim3 grid((unsigned)((a.n_q + BQ - 1) / BQ * a.n_split), (unsigned)a.heads, (unsigned)batch);
   const bool tab = a.tables_in_lds != 0;
   const size_t lds = lds_bytes_t<T, D>(a.rank, a.n_centroids, tab);
   if (logits) return tab ? launch_k<T, D, RP, true, true>(a, grid, lds, s) : launch_k<T, D, RP, true, false>(a, grid, lds, s);
-  return tab ? launch_k<T, D, RP, false, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false>(a, grid, lds, s);
+  const hipError_t e = tab ? launch_k<T, D, RP, false, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false>(a, grid, lds, s);
+  if (e != hipSuccess || a.n_split == 1) return e;
+  hipLaunchKernelGGL((attend_combine<T, D>), dim3((unsigned)((a.n_q + 3) / 4), (unsigned)a.heads, (unsigned)batch),
+                     dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 template <typename T, int D>
@@ -661,6 +721,18 @@ size_t attend_lds_bytes(int d, int elem, int rank, int n_centroids, bool tables)
                                 : lds_bytes_t<bf16, 128>(rank, n_centroids, tables);
   return d == 64 ? lds_bytes_t<float, 64>(rank, n_centroids, tables)
                  : lds_bytes_t<float, 128>(rank, n_centroids, tables);
+}
+
+int attend_splits(int64_t n_q, int heads, int batch, int64_t n_cache, int cus) {
+  // Split the key range only when the launch gives fewer than two workgroups
+  // per compute unit: up to 4 per CU, at least 8 tiles per split, at most 16.
+  const int64_t wgs = (n_q + BQ - 1) / BQ * heads * batch;
+  if (wgs <= 0 || wgs >= 2 * int64_t(cus)) return 1;
+  int64_t ns = (4 * int64_t(cus) + wgs - 1) / wgs;
+  const int64_t by_tiles = ((n_cache + KT - 1) / KT) / 8;
+  if (ns > by_tiles) ns = by_tiles;
+  if (ns > 16) ns = 16;
+  return ns < 1 ? 1 : int(ns);
 }
 
 bool attend_tables_fit(int d, int elem, int rank, int n_centroids) {

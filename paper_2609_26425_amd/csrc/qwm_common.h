@@ -102,6 +102,9 @@ struct AttendArgs {
   int64_t n_cache, n_q, q_start;
   int frame_tokens, heads, n_centroids, rank;
   int tables_in_lds;
+  int n_split;    // workgroups per Query block, each over its share of the key tiles
+  float* part_o;  // [n_split][B*H][n_q][d] unnormalised partial outputs (n_split > 1)
+  float* part_ml; // [n_split][B*H][n_q][2] running max (raw logits) and sum per partial
 };
 
 // Launchers (one translation unit per element type).
@@ -112,6 +115,7 @@ hipError_t launch_append_bf16_128(const AppendArgs& a, int g, int batch, hipStre
 hipError_t launch_attend_f32(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s);
 hipError_t launch_attend_bf16(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s);
 size_t attend_lds_bytes(int d, int elem, int rank, int n_centroids, bool tables_in_lds);
+int attend_splits(int64_t n_q, int heads, int batch, int64_t n_cache, int cus);
 bool attend_tables_fit(int d, int elem, int rank, int n_centroids);
 
 hipError_t launch_derive_constants(const quantwm_config& c, uint8_t* calib, hipStream_t s);

@@ -58,7 +58,8 @@ def _load():
         "quantwm_calib_pack": (I32, [C, P, P, P, P, P, P, P]),
         "quantwm_calibrate": (I32, [C, P, I64, P, P, I64, I32, P, P, SZ, P]),
         "quantwm_append": (I32, [C, P, P, I64, P, P, I64, P, P]),
-        "quantwm_attend": (I32, [C, P, P, I64, P, I64, I64, I32, P, P, P]),
+        "quantwm_attend_workspace_bytes": (SZ, [C, I64, I64]),
+        "quantwm_attend": (I32, [C, P, P, I64, P, I64, I64, I32, P, P, P, SZ, P]),
         "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I32, P, P]),
         "quantwm_last_error": (ctypes.c_char_p, []),
     }
@@ -72,7 +73,8 @@ _lib = _load()
 
 EXPORTED = ("quantwm_cache_bytes", "quantwm_token_bytes", "quantwm_calib_bytes", "quantwm_calib_offsets",
             "quantwm_calibrate_workspace_bytes", "quantwm_calib_pack", "quantwm_calibrate",
-            "quantwm_append", "quantwm_attend", "quantwm_logits", "quantwm_last_error")
+            "quantwm_append", "quantwm_attend_workspace_bytes", "quantwm_attend", "quantwm_logits",
+            "quantwm_last_error")
 
 
 def library():
@@ -155,9 +157,16 @@ def quantwm_append(cfg, calib, cache, n_cached, k_new, v_new, n_new, coef_f32_ou
                                n_new, _ptr(coef_f32_out), _stream(stream)))
 
 
-def quantwm_attend(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, out, lse_out=None, stream=None):
+def quantwm_attend_workspace_bytes(cfg: Config, n_cache: int, n_q: int) -> int:
+    return int(_lib.quantwm_attend_workspace_bytes(ctypes.byref(cfg), n_cache, n_q))
+
+
+def quantwm_attend(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, out, lse_out=None, workspace=None,
+                   stream=None):
     _check(_lib.quantwm_attend(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cache, _ptr(q), n_q, q_start,
-                               frame_tokens, _ptr(out), _ptr(lse_out), _stream(stream)))
+                               frame_tokens, _ptr(out), _ptr(lse_out), _ptr(workspace),
+                               0 if workspace is None else workspace.numel() * workspace.element_size(),
+                               _stream(stream)))
 
 
 def quantwm_logits(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, logits_out, stream=None):

@@ -67,12 +67,27 @@ def test_validation_without_a_gpu():
                                               0, ctypes.c_void_p(0x3000), ctypes.c_void_p(0x4000), 5, None, None))
     assert "aligned" in qw.quantwm_last_error()
     with pytest.raises(qw.QuantwmError) as e:
-        qw._check(qw.library().quantwm_attend(ctypes.byref(good), None, None, 50, None, 4, 60, 1, None, None, None))
+        qw._check(qw.library().quantwm_attend(ctypes.byref(good), None, None, 50, None, 4, 60, 1, None, None, None, 0, None))
     assert e.value.status == qw.ERR_INVALID_ARG
     with pytest.raises(qw.QuantwmError) as e:
-        qw._check(qw.library().quantwm_attend(ctypes.byref(good), None, None, 50, None, 4, 10, 0, None, None, None))
+        qw._check(qw.library().quantwm_attend(ctypes.byref(good), None, None, 50, None, 4, 10, 0, None, None, None, 0, None))
     assert "frame_tokens" in qw.quantwm_last_error()
     # empty calls are OK no-ops and touch nothing
     assert qw.library().quantwm_append(ctypes.byref(good), None, None, 0, None, None, 0, None, None) == qw.OK
-    assert qw.library().quantwm_attend(ctypes.byref(good), None, None, 0, None, 0, 0, 1, None, None, None) == qw.OK
+    assert qw.library().quantwm_attend(ctypes.byref(good), None, None, 0, None, 0, 0, 1, None, None, None, 0, None) == qw.OK
     assert qw.quantwm_last_error() == ""
+
+
+def test_attend_workspace_sizes():
+    """A launch that under-fills the GPU asks for split workspace; a full one does not."""
+    # 40 heads x 7 Query blocks of 256 = 280 workgroups < 2 per CU on 256 CUs -> 4 splits
+    roll = qw.make_config(1, 40, 128, 128, 32, 16, 4, 120000, "bf16")
+    rows = 4 * 40 * 1560
+    o_bytes = (rows * 128 * 4 + 255) // 256 * 256
+    assert qw.quantwm_attend_workspace_bytes(roll, 120000, 1560) == o_bytes + rows * 8
+    # 40 heads x 19 Query blocks = 760 workgroups: no split
+    ling = qw.make_config(1, 40, 128, 128, 32, 16, 4, 32760, "bf16")
+    assert qw.quantwm_attend_workspace_bytes(ling, 32760, 4680) == 0
+    # too few key tiles to split (fewer than 8 per split)
+    assert qw.quantwm_attend_workspace_bytes(roll, 64 * 15, 1560) == 0
+    assert qw.quantwm_attend_workspace_bytes(roll, 120000, 0) == 0

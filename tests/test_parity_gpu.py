@@ -118,13 +118,19 @@ def check_append(case, gpu_cache, gpu_coef):
     return stats
 
 
-def gpu_attend(wl, cfg, calib, cache_np, q_full):
+def gpu_attend(wl, cfg, calib, cache_np, q_full, split=False):
+    """quantwm_attend without a workspace, or (split=True) with the workspace it
+    asks for, which splits the key range when the launch under-fills the GPU."""
     dt = cfg.torch_dtype
     cache = torch.from_numpy(cache_np).to(DEV)
     q = tdev(q_full, dt)
     out = torch.empty_like(q)
     lse = torch.empty((wl.batch, wl.heads, wl.n_q), dtype=torch.float32, device=DEV)
-    qw.quantwm_attend(cfg, calib, cache, wl.n_cache, q, wl.n_q, wl.q_start, wl.frame_tokens, out, lse)
+    ws = None
+    if split:
+        nb = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q)
+        ws = torch.empty(nb, dtype=torch.uint8, device=DEV)
+    qw.quantwm_attend(cfg, calib, cache, wl.n_cache, q, wl.n_q, wl.q_start, wl.frame_tokens, out, lse, ws)
     torch.cuda.synchronize()
     return out.float().cpu().numpy(), lse.cpu().numpy()
 
@@ -215,11 +221,16 @@ def run_case(wl, max_sources, n_heads_rows, row_step, logits_rows):
     _say(f"[ok] append {wl.name}: {st}")
     ora_full = harness.full_oracle_cache(case)
     q_full = harness.full_inputs(case, "q")
-    _say(f"[gpu] attend {wl.name}")
-    out, lse = gpu_attend(wl, cfg, calib, ora_full, q_full)
     rows = harness.sample_rows(wl, n_heads_rows, row_step)
-    mx, mean = check_attend(case, out, lse, rows)
-    _say(f"[ok] attend {wl.name}: max-abs {mx:.3g} mean-abs {mean:.3g} over {len(rows)} rows")
+    for split in (False, True):
+        nb = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q)
+        if split and nb == 0:
+            continue
+        _say(f"[gpu] attend {wl.name} (workspace {nb if split else 0} B)")
+        out, lse = gpu_attend(wl, cfg, calib, ora_full, q_full, split)
+        mx, mean = check_attend(case, out, lse, rows)
+        _say(f"[ok] attend{' split' if split else ''} {wl.name}: max-abs {mx:.3g} mean-abs {mean:.3g} "
+             f"over {len(rows)} rows")
     if logits_rows:
         worst = check_logits(case, cfg, calib, ora_full, q_full, logits_rows)
         _say(f"[ok] logits {wl.name}: worst relative error {worst:.3g}")
