@@ -202,25 +202,29 @@ def decode(cfg: OraCfg, tables, cache, b, h, n):
 
 
 def attend(cfg: OraCfg, tables, cache, n_cache, q, q_start, frame_tokens, rows=None,
-           coef_override=None, want_logits=False):
-    """rows: int array [n_rows, 3] of (b, h, i); default all rows.
+           coef_override=None, want_logits=False, k_act=None, v_act=None):
+    """rows: int array [n_rows, 3] of (b, h, i); default all rows. k_act / v_act
+    ([B, n_act, H, d]) append an exact active chunk after the packed keys.
 
-    Returns (out [n_rows, d] fp64, lse [n_rows], logits [n_rows, n_cache] or None).
+    Returns (out [n_rows, d] fp64, lse [n_rows], logits [n_rows, n_cache + n_act] or None).
     """
     mu_k, mu_v, _, u_t = (_f32(t) for t in tables[:4])
     q = _f32(q)
     B, n_q, H, d = q.shape
+    n_act = 0 if k_act is None else int(k_act.shape[1])
+    ka = _f32(k_act) if k_act is not None else None
+    va = _f32(v_act) if v_act is not None else None
     if rows is None:
         rows = np.array([(b, h, i) for b in range(B) for h in range(H) for i in range(n_q)], np.int32)
     rows = np.ascontiguousarray(rows, dtype=np.int32).reshape(-1, 3)
     nr = rows.shape[0]
     out = np.zeros((nr, d)); lse = np.zeros(nr)
-    logits = np.zeros((nr, n_cache)) if want_logits else None
+    logits = np.zeros((nr, n_cache + n_act)) if want_logits else None
     co = _f32(coef_override) if coef_override is not None else None
-    rc = lib().ora_attend(ctypes.byref(cfg), _p(mu_k), _p(mu_v), _p(u_t), _p(cache, ctypes.c_uint8),
-                          ctypes.c_longlong(n_cache), _p(q), ctypes.c_longlong(n_q),
-                          ctypes.c_longlong(q_start), int(frame_tokens), _p(co), nr,
-                          _p(rows, ctypes.c_int), _p(out, ctypes.c_double), _p(lse, ctypes.c_double),
-                          _p(logits, ctypes.c_double))
+    rc = lib().ora_attend_active(ctypes.byref(cfg), _p(mu_k), _p(mu_v), _p(u_t), _p(cache, ctypes.c_uint8),
+                                 ctypes.c_longlong(n_cache), _p(ka), _p(va), ctypes.c_longlong(n_act), _p(q),
+                                 ctypes.c_longlong(n_q), ctypes.c_longlong(q_start), int(frame_tokens), _p(co), nr,
+                                 _p(rows, ctypes.c_int), _p(out, ctypes.c_double), _p(lse, ctypes.c_double),
+                                 _p(logits, ctypes.c_double))
     _check(rc, "attend")
     return out, lse, logits

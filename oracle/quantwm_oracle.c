@@ -545,9 +545,22 @@ int ora_attend(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
                const uint8_t* cache, long long n_cache, const float* q, long long n_q,
                long long q_start, int frame_tokens, const float* coef_override,
                int n_rows, const int* rows, double* out, double* lse, double* logits) {
-  if (!valid_cfg(cfg) || n_cache < 0 || n_cache > cfg->capacity || n_q < 0 || q_start < 0 ||
-      q_start > n_cache || frame_tokens < 1 || n_rows < 0)
+  return ora_attend_active(cfg, mu_k, mu_v, u_t, cache, n_cache, NULL, NULL, 0, q, n_q, q_start, frame_tokens,
+                           coef_override, n_rows, rows, out, lse, logits);
+}
+
+/* Keys [0, n_cache) are decoded from the packed cache; keys [n_cache, n_cache +
+ * n_act) are the exact active-chunk tokens, rounded to the table type like every
+ * other operand, with no PSAC term (only completed chunks are packed). */
+int ora_attend_active(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const float* u_t,
+                      const uint8_t* cache, long long n_cache, const float* k_act, const float* v_act,
+                      long long n_act, const float* q, long long n_q, long long q_start, int frame_tokens,
+                      const float* coef_override, int n_rows, const int* rows, double* out, double* lse,
+                      double* logits) {
+  if (!valid_cfg(cfg) || n_cache < 0 || n_cache > cfg->capacity || n_act < 0 || (n_act > 0 && (!k_act || !v_act)) ||
+      n_q < 0 || q_start < 0 || q_start > n_cache + n_act || frame_tokens < 1 || n_rows < 0)
     return -1;
+  const long long n_all = n_cache + n_act;
   const int d = cfg->head_dim, H = cfg->heads, r = cfg->rank;
   /* rows sorted by head so that each head's cache is decoded once; idx[4] keeps
    * the caller's row number */
@@ -559,9 +572,9 @@ int ora_attend(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
         rows[3 * i + 2] < 0 || rows[3 * i + 2] >= n_q) { free(srt); return -1; }
   }
   qsort(srt, (size_t)n_rows, sizeof(int) * 4, cmp_rows);
-  double* K0 = (double*)malloc(sizeof(double) * (n_cache > 0 ? n_cache : 1) * d);
-  double* V = (double*)malloc(sizeof(double) * (n_cache > 0 ? n_cache : 1) * d);
-  double* Ch = (double*)malloc(sizeof(double) * (n_cache > 0 ? n_cache : 1) * (r > 0 ? r : 1));
+  double* K0 = (double*)malloc(sizeof(double) * (n_all > 0 ? n_all : 1) * d);
+  double* V = (double*)malloc(sizeof(double) * (n_all > 0 ? n_all : 1) * d);
+  double* Ch = (double*)malloc(sizeof(double) * (n_all > 0 ? n_all : 1) * (r > 0 ? r : 1));
   if (!K0 || !V || !Ch) { free(srt); free(K0); free(V); free(Ch); return -2; }
   const double inv_sqrt_d = 1.0 / sqrt((double)d);
   int i0 = 0, status = 0;
@@ -574,6 +587,14 @@ int ora_attend(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
     for (long long t = 0; t < n_cache * d; ++t) { K0[t] = round_table(cfg, K0[t]); V[t] = round_table(cfg, V[t]); }
     for (long long t = 0; t < n_cache * r; ++t)
       Ch[t] = coef_override ? (double)coef_override[bh * n_cache * r + t] : round_table(cfg, Ch[t]);
+    for (long long j = 0; j < n_act; ++j) {
+      const long long src = (((long long)b * n_act + j) * H + h) * d;
+      for (int c = 0; c < d; ++c) {
+        K0[(n_cache + j) * d + c] = round_table(cfg, (double)k_act[src + c]);
+        V[(n_cache + j) * d + c] = round_table(cfg, (double)v_act[src + c]);
+      }
+      for (int kk = 0; kk < r; ++kk) Ch[(n_cache + j) * r + kk] = 0.0;
+    }
 #pragma omp parallel for schedule(dynamic)
     for (int ri = i0; ri < i1; ++ri) {
       long long i = srt[4 * ri + 2];
@@ -585,9 +606,9 @@ int ora_attend(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
         for (int c = 0; c < d; ++c) acc += (double)qi[c] * (double)u_t[(bh * r + kk) * d + c];
         u[kk] = round_table(cfg, acc); /* qU_r enters the product in the table type */
       }
-      double* L = (double*)malloc(sizeof(double) * (n_cache > 0 ? n_cache : 1));
+      double* L = (double*)malloc(sizeof(double) * (n_all > 0 ? n_all : 1));
       double m = -INFINITY;
-      for (long long j = 0; j < n_cache; ++j) {
+      for (long long j = 0; j < n_all; ++j) {
         int visible = j < q_start || (j - q_start) / frame_tokens <= i / frame_tokens;
         if (!visible) { L[j] = -INFINITY; continue; }
         /* Eq. 5 with Eq. 17: (q khat_0 + (q U_r) c) / sqrt(d) */
@@ -601,7 +622,7 @@ int ora_attend(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
       double* o = out + (long long)dst * d;
       for (int c = 0; c < d; ++c) o[c] = 0.0;
       if (m > -INFINITY) {
-        for (long long j = 0; j < n_cache; ++j) {
+        for (long long j = 0; j < n_all; ++j) {
           if (L[j] == -INFINITY) continue;
           double p = exp(L[j] - m);
           l += p;
@@ -612,7 +633,7 @@ int ora_attend(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
       } else {
         lse[dst] = -INFINITY;
       }
-      if (logits) memcpy(logits + (long long)dst * n_cache, L, sizeof(double) * n_cache);
+      if (logits) memcpy(logits + (long long)dst * n_all, L, sizeof(double) * n_all);
       free(L);
     }
     i0 = i1;

@@ -94,6 +94,16 @@ int ora_attend(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
                long long q_start, int frame_tokens, const float* coef_override,
                int n_rows, const int* rows, double* out, double* lse, double* logits);
 
+/* The same over [packed history | active chunk]: keys [0, n_cache) decoded from
+ * the cache, keys [n_cache, n_cache + n_act) taken exactly from k_act / v_act
+ * ([B, n_act, H, d], rounded to the table type) with no PSAC term. Positions are
+ * concatenated, so the mask and q_start (<= n_cache + n_act) refer to them. */
+int ora_attend_active(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const float* u_t,
+                      const uint8_t* cache, long long n_cache, const float* k_act, const float* v_act,
+                      long long n_act, const float* q, long long n_q, long long q_start, int frame_tokens,
+                      const float* coef_override, int n_rows, const int* rows, double* out, double* lse,
+                      double* logits);
+
 int ora_max_threads(void);
 void ora_set_threads(int n);
 

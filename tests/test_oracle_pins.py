@@ -468,3 +468,45 @@ def test_token_bytes_and_paper_compression():
     for d, G, r, want in [(128, 32, 8, (52, 42)), (128, 32, 16, (60, 42)), (128, 64, 32, (72, 38)),
                           (64, 32, 4, (28, 22))]:
         assert oracle.token_bytes(oracle.cfg_of(1, 1, d, 16, G, r, 4, 64, True)) == want
+
+
+# ------------------------------------------------- BF16 active chunk (NEXT f2)
+
+def test_active_chunk_alone_is_plain_attention():
+    # Keys of the active chunk enter exactly, with no PSAC term: with an empty
+    # packed history the oracle is torch's SDPA in fp64 on those Keys and Values,
+    # under the block-causal mask over their positions.
+    wl = _small_workload(rank=4)
+    cfg, tables, cache, k, v, q, _ = _encoded(wl)
+    n_act = wl.n_cache
+    out, lse, _ = oracle.attend(cfg, tables, cache, 0, q, wl.q_start, wl.frame_tokens, k_act=k, v_act=v)
+    for h in range(wl.heads):
+        qh = q[0, :, h, :].astype(np.float64)
+        ref = _sdpa(qh, k[0, :, h, :].astype(np.float64), v[0, :, h, :].astype(np.float64), _mask(wl, n_act))
+        np.testing.assert_allclose(out[h * wl.n_q:(h + 1) * wl.n_q], ref, atol=1e-10)
+
+
+def test_active_chunk_merges_by_log_sum_exp():
+    # Softmax over disjoint key sets: attention over [packed | active] equals the
+    # log-sum-exp merge of attention over each part (all keys visible here).
+    wl = _small_workload(rank=4)
+    cfg, tables, cache, k, v, q, _ = _encoded(wl)
+    n_p, big = wl.n_cache - 100, 10 ** 6
+    ka, va = np.ascontiguousarray(k[:, n_p:]), np.ascontiguousarray(v[:, n_p:])
+    o_all, l_all, _ = oracle.attend(cfg, tables, cache, n_p, q, 0, big, k_act=ka, v_act=va)
+    o_p, l_p, _ = oracle.attend(cfg, tables, cache, n_p, q, 0, big)
+    o_a, l_a, _ = oracle.attend(cfg, tables, cache, 0, q, 0, big, k_act=ka, v_act=va)
+    lse = np.logaddexp(l_p, l_a)
+    ref = np.exp(l_p - lse)[:, None] * o_p + np.exp(l_a - lse)[:, None] * o_a
+    np.testing.assert_allclose(l_all, lse, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(o_all, ref, atol=1e-12)
+
+
+def test_active_chunk_empty_equals_packed_only():
+    wl = _small_workload(rank=4)
+    cfg, tables, cache, k, v, q, _ = _encoded(wl)
+    e = np.zeros((1, 0, wl.heads, wl.head_dim), np.float32)
+    a = oracle.attend(cfg, tables, cache, wl.n_cache, q, wl.q_start, wl.frame_tokens, k_act=e, v_act=e)
+    b = oracle.attend(cfg, tables, cache, wl.n_cache, q, wl.q_start, wl.frame_tokens)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
