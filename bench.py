@@ -232,6 +232,23 @@ def main():
     ms_step = wall * 1000.0 / args.steps
     assert torch.isfinite(outs[0].float()).all(), "non-finite attention output"
 
+    # the streaming variant: the last chunk stays exact (BF16) beside the packed
+    # history of the rest, timed separately on the same inputs
+    n_pk = wl.n_cache - n_new
+    ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ws_act = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q)
+    act_ws = torch.empty(ws_act, dtype=torch.uint8, device=dev) if ws_act else None
+    for i in range(2):
+        qw.quantwm_attend_active(cfg, calib, caches[0], n_pk, k_new[0], v_new[0], n_new, qs[0], wl.n_q,
+                                 wl.q_start, wl.frame_tokens, outs[0], lse, act_ws)
+    ea.record()
+    for i in range(5):
+        qw.quantwm_attend_active(cfg, calib, caches[0], n_pk, k_new[0], v_new[0], n_new, qs[0], wl.n_q,
+                                 wl.q_start, wl.frame_tokens, outs[0], lse, act_ws)
+    eb.record()
+    torch.cuda.synchronize()
+    act_ms = ea.elapsed_time(eb) / 5
+
     flops = attend_flops(wl)
     achieved = flops / (att_ms * 1e-3) / 1e12
     app_bytes = append_bytes(wl, n_new)
@@ -261,6 +278,8 @@ def main():
         "append_traffic": measured_traffic("append", wl.name),
         "copies": args.copies,
         "attend_workspace_bytes": ws_bytes,
+        "attend_active_ms": act_ms,
+        "attend_active_config": f"{n_pk} packed + {n_new} exact BF16 keys",
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)

@@ -164,6 +164,20 @@ quantwm_status quantwm_attend(const quantwm_config* cfg, const void* calib, cons
                               int32_t frame_tokens, void* out, float* lse_out, void* workspace,
                               size_t workspace_bytes, void* stream);
 
+/* quantwm_attend over [packed history | active chunk] (Sec. 5 streaming setting:
+ * the chunk being generated stays in BF16 until it is complete and appended).
+ * Keys [0, n_cache) come from the packed cache; keys [n_cache, n_cache + n_act)
+ * are k_act / v_act ([B, n_act, H, d] dtype, device, 16-byte aligned), used
+ * exactly, with no PSAC term. Positions are concatenated: the mask is that of
+ * quantwm_attend over n_cache + n_act keys, and q_start <= n_cache + n_act.
+ * n_act <= 2^26. With n_act == 0 this is quantwm_attend. The workspace size is
+ * quantwm_attend_workspace_bytes(cfg, n_cache + n_act, n_q). */
+quantwm_status quantwm_attend_active(const quantwm_config* cfg, const void* calib, const void* cache,
+                                     int64_t n_cache, const void* k_act, const void* v_act, int64_t n_act,
+                                     const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens,
+                                     void* out, float* lse_out, void* workspace, size_t workspace_bytes,
+                                     void* stream);
+
 /* Test hook: the scaled logits of quantwm_attend, [B,H,n_q,n_cache] f32,
  * -inf where masked. Same tile code as quantwm_attend. */
 quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, const void* cache,

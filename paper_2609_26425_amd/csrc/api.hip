@@ -284,18 +284,23 @@ size_t quantwm_attend_workspace_bytes(const quantwm_config* cfg, int64_t n_cache
 }
 
 static quantwm_status attend_common(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
-                                    const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
-                                    float* lse_out, float* logits_out, void* workspace, size_t workspace_bytes,
-                                    void* stream) {
+                                    const void* k_act, const void* v_act, int64_t n_act, const void* q, int64_t n_q,
+                                    int64_t q_start, int32_t frame_tokens, void* out, float* lse_out,
+                                    float* logits_out, void* workspace, size_t workspace_bytes, void* stream) {
   QWM_TRY(check_cfg(cfg));
-  if (n_cache < 0 || n_q < 0 || q_start < 0) return fail(QWM_ERR_INVALID_ARG, "sizes must be >= 0");
+  if (n_cache < 0 || n_act < 0 || n_q < 0 || q_start < 0) return fail(QWM_ERR_INVALID_ARG, "sizes must be >= 0");
   if (n_cache > cfg->capacity) return fail(QWM_ERR_CAPACITY, "n_cache exceeds capacity");
-  if (q_start > n_cache) return fail(QWM_ERR_INVALID_ARG, "q_start > n_cache");
+  if (n_act > (int64_t(1) << 26)) return fail(QWM_ERR_UNSUPPORTED, "n_act above 2^26");
+  if (q_start > n_cache + n_act) return fail(QWM_ERR_INVALID_ARG, "q_start > n_cache + n_act");
   if (frame_tokens < 1) return fail(QWM_ERR_INVALID_ARG, "frame_tokens must be >= 1");
   if (n_q == 0) return ok();
   QWM_TRY(check_dev(calib, "calib"));
   QWM_TRY(check_dev(cache, "cache"));
   QWM_TRY(check_dev(q, "q"));
+  if (n_act > 0) {
+    QWM_TRY(check_dev(k_act, "k_act"));
+    QWM_TRY(check_dev(v_act, "v_act"));
+  }
   if (logits_out) {
     if (reinterpret_cast<uintptr_t>(logits_out) & 3) return fail(QWM_ERR_INVALID_ARG, "logits_out misaligned");
   } else {
@@ -314,6 +319,9 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   a.L = qwm::cache_layout(*cfg);
   a.q = q; a.out = out; a.lse = lse_out; a.logits = logits_out;
   a.n_cache = n_cache; a.n_q = n_q; a.q_start = q_start;
+  a.k_act = n_act > 0 ? k_act : nullptr;
+  a.v_act = n_act > 0 ? v_act : nullptr;
+  a.n_act = n_act;
   a.frame_tokens = frame_tokens; a.heads = cfg->heads; a.n_centroids = cfg->n_centroids; a.rank = cfg->rank;
   a.tables_in_lds = tables ? 1 : 0;
   a.n_split = 1;
@@ -322,7 +330,7 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   if (!logits_out && workspace) {
     if (reinterpret_cast<uintptr_t>(workspace) & 255) return fail(QWM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
     int ns = 1;
-    const size_t need = attend_split_bytes(cfg, n_cache, n_q, &ns);
+    const size_t need = attend_split_bytes(cfg, n_cache + n_act, n_q, &ns);
     if (ns > 1 && workspace_bytes >= need) {
       const size_t rows = size_t(ns) * cfg->batch * cfg->heads * size_t(n_q);
       a.n_split = ns;
@@ -342,16 +350,24 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
 quantwm_status quantwm_attend(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
                               const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
                               float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
-  return attend_common(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, out, lse_out, nullptr, workspace,
-                       workspace_bytes, stream);
+  return attend_common(cfg, calib, cache, n_cache, nullptr, nullptr, 0, q, n_q, q_start, frame_tokens, out, lse_out,
+                       nullptr, workspace, workspace_bytes, stream);
+}
+
+quantwm_status quantwm_attend_active(const quantwm_config* cfg, const void* calib, const void* cache,
+                                     int64_t n_cache, const void* k_act, const void* v_act, int64_t n_act,
+                                     const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
+                                     float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
+  return attend_common(cfg, calib, cache, n_cache, k_act, v_act, n_act, q, n_q, q_start, frame_tokens, out, lse_out,
+                       nullptr, workspace, workspace_bytes, stream);
 }
 
 quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
                               const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, float* logits_out,
                               void* stream) {
   if (!logits_out && n_q > 0) return fail(QWM_ERR_INVALID_ARG, "logits_out is null");
-  return attend_common(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, nullptr, nullptr, logits_out,
-                       nullptr, 0, stream);
+  return attend_common(cfg, calib, cache, n_cache, nullptr, nullptr, 0, q, n_q, q_start, frame_tokens, nullptr,
+                       nullptr, logits_out, nullptr, 0, stream);
 }
 
 }  // extern "C"

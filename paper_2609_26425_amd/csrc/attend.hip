@@ -160,6 +160,21 @@ __device__ inline void dequant_codes(uint32_t cw, _Float16 s, uint32_t zz, const
   }
 }
 
+// N values of type T held as raw 32-bit words -> floats (exact).
+template <typename T, int N>
+__device__ inline void raw_to_float(const uint32_t* w, float (&x)[N]) {
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int i = 0; i < N / 2; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] = __uint_as_float(w[i]);
+  }
+}
+
 // Builds a bf16x8 MFMA operand from 8 floats with paired conversions.
 template <typename V>
 __device__ inline V pack_operand(const float* x) {
@@ -235,7 +250,8 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 
   // ---- key range of this workgroup: Query block blockIdx.x / n_split, and the
   // split-th of n_split equal runs of its key tiles
-  const int64_t F = a.frame_tokens, qs = a.q_start, nc = a.n_cache;
+  // keys [0, npk) are packed; keys [npk, nc) are the exact active chunk
+  const int64_t F = a.frame_tokens, qs = a.q_start, npk = a.n_cache, nc = a.n_cache + a.n_act;
   const int split = int(blockIdx.x) % a.n_split;
   const int64_t qa = int64_t(blockIdx.x / a.n_split) * BQ;
   const int64_t qb = qa + BQ < a.n_q ? qa + BQ : a.n_q;
@@ -247,7 +263,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   const int64_t per_split = (ntile_all + a.n_split - 1) / a.n_split;
   const int64_t t0 = split * per_split < ntile_all ? split * per_split : ntile_all;
   const int64_t ntile = t0 + per_split < ntile_all ? t0 + per_split : ntile_all;  // this split: tiles [t0, ntile)
-  const int64_t nfull = nc / KT;  // tiles [0, nfull) hold no key past n_cache
+  const int64_t nfull = npk / KT;  // tiles [0, nfull) hold packed keys only
 
   // ======================= producer state (waves NC .. NC+NP-1)
   const int ptid = producer ? tid - NC * 64 : 0;
@@ -271,11 +287,30 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   float c_s = 0.0f;
 #pragma unroll
   for (int u = 0; u < NSUB; ++u) { k_cw[u] = 0; k_z[u] = 0x64006400u; k_s[u] = 0; }
+  // keys of the active chunk are read in dequant itself (only the flags travel
+  // from one tile to the next), so they cost no registers across the loop
+  constexpr int KW = CHK * int(sizeof(T)) / 4, VW = CHV * int(sizeof(T)) / 4;
+  bool k_on_act = false, v_on_act[2] = {false, false};
+  const T* __restrict__ k_act = reinterpret_cast<const T*>(a.k_act);
+  const T* __restrict__ v_act = reinterpret_cast<const T*>(a.v_act);
+  const uint32_t npku = uint32_t(npk);
   // Packed fields are read with buffer loads: one resource per field of this
   // head (base = its first slot), this thread's byte offset inside a tile as the
   // vector offset (fixed for all tiles) and the tile's byte offset as the scalar
   // offset, so advancing a tile costs no vector instruction.
   const uint32_t zpb = L.zpb, sstride = 2 * L.ng, ncu = uint32_t(nc);
+  // active-chunk row of key `key` (>= npk) at channel c0: [B, n_act, H, d]
+  auto act_row = [&](const T* base, uint32_t key, int c0) {
+    return base + ((int64_t(b) * a.n_act + (key - npku)) * a.heads + h) * D + c0;
+  };
+  auto load_words = [&](const T* src, uint32_t* w, int nw) {
+    const uint4* p = reinterpret_cast<const uint4*>(src);
+#pragma unroll
+    for (int i = 0; i < nw / 4; ++i) {
+      const uint4 u = p[i];
+      w[4 * i] = u.x; w[4 * i + 1] = u.y; w[4 * i + 2] = u.z; w[4 * i + 3] = u.w;
+    }
+  };
   auto field = [&](int64_t off, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc((void*)(cache + off + slot0 * bytes), 0,
                                              int(uint32_t(L.slots) * bytes), 0x00020000);
@@ -294,7 +329,10 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   auto load_raw = [&](auto full_tag, uint32_t k0) {
     constexpr bool FULL = decltype(full_tag)::value;
     const int k0i = int(k0);
-    if (FULL || k0 + kkey < ncu) {
+    k_on_act = !FULL && k0 + kkey >= npku && k0 + kkey < ncu;
+    if (!FULL && k_on_act) {
+      k_id = 0;
+    } else if (FULL || k0 + kkey < npku) {
       const int id = __builtin_amdgcn_raw_buffer_load_b8(r_ki, kkey, k0i, 0);
       k_id = id < Kc ? id : Kc - 1;
 #pragma unroll
@@ -320,7 +358,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       c_s = 0.0f;
       c_w[0] = 0;
       c_w[1] = 0;
-      if (crole && (FULL || k0 + ckey < ncu)) {
+      if (crole && (FULL || k0 + ckey < npku)) {
         c_s = (float)__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_cs, o_cs, k0i * 2, 0));
         if (raligned) {
           if constexpr (RCH == 8) {
@@ -339,7 +377,11 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     }
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      if (FULL || k0 + 2 * vkp + e < ncu) {
+      const uint32_t key = k0 + 2 * vkp + e;
+      v_on_act[e] = !FULL && key >= npku && key < ncu;
+      if (!FULL && v_on_act[e]) {
+        v_id[e] = 0;
+      } else if (FULL || key < npku) {
         const int id = __builtin_amdgcn_raw_buffer_load_b8(r_vi, 2 * vkp + e, k0i, 0);
         v_id[e] = id < Kc ? id : Kc - 1;
         const uint32_t zb = __builtin_amdgcn_raw_buffer_load_b8(r_vz, o_vz + e * int(zpb), k0i * int(zpb), 0);
@@ -356,7 +398,9 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   // rebuild khat_0 = mu + s (q - z) (Eq. 4), chat = code * cscale and vhat into
   // tile buffer `buf`. s (q - z) is exact in fp32, so the fma rounds once,
   // exactly like mu + s (q - z).
-  auto dequant = [&](int buf) {
+  auto dequant = [&](int64_t t) {
+    const int buf = int(t & 1);
+    const uint32_t k0 = uint32_t(t * KT);
     T* kt = smem + tile0 + buf * LY::tile_elems;
     T* ct = kt + KT * LY::KS;
     T* vt = ct + KT * LY::CS;
@@ -365,7 +409,13 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       float mu[16], x[16];
       if constexpr (TAB) load_vals<T, 16>(tabK + k_id * LY::TS + kch0 + 16 * u, mu);
       else load_vals<T, 16>(gtabK + k_id * D + kch0 + 16 * u, mu);
-      dequant_codes<16>(k_cw[u], k_s[u], k_z[u], mu, x);
+      if (k_on_act) {
+        uint32_t w[16 * sizeof(T) / 4];
+        load_words(act_row(k_act, k0 + kkey, kch0 + 16 * u), w, 16 * int(sizeof(T)) / 4);
+        raw_to_float<T, 16>(w, x);
+      } else {
+        dequant_codes<16>(k_cw[u], k_s[u], k_z[u], mu, x);
+      }
       store_vals<T, 16>(kt + kkey * LY::KS + kch0 + 16 * u, x);
     }
     if constexpr (RP > 0) {
@@ -386,8 +436,24 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         load_vals<T, CHV>(gtabV + v_id[0] * D + vch0, mu0);
         load_vals<T, CHV>(gtabV + v_id[1] * D + vch0, mu1);
       }
-      dequant_codes<CHV>(v_cw[0], v_s[0], v_z[0], mu0, x0);
-      dequant_codes<CHV>(v_cw[1], v_s[1], v_z[1], mu1, x1);
+      if (v_on_act[0] || v_on_act[1]) {
+        uint32_t w[VW];
+        if (v_on_act[0]) {
+          load_words(act_row(v_act, k0 + 2 * vkp, vch0), w, VW);
+          raw_to_float<T, CHV>(w, x0);
+        } else {
+          dequant_codes<CHV>(v_cw[0], v_s[0], v_z[0], mu0, x0);
+        }
+        if (v_on_act[1]) {
+          load_words(act_row(v_act, k0 + 2 * vkp + 1, vch0), w, VW);
+          raw_to_float<T, CHV>(w, x1);
+        } else {
+          dequant_codes<CHV>(v_cw[1], v_s[1], v_z[1], mu1, x1);
+        }
+      } else {
+        dequant_codes<CHV>(v_cw[0], v_s[0], v_z[0], mu0, x0);
+        dequant_codes<CHV>(v_cw[1], v_s[1], v_z[1], mu1, x1);
+      }
 #pragma unroll
       for (int c = 0; c < CHV; ++c) store_pair<T>(vt + (vch0 + c) * LY::VS + 2 * vkp, x0[c], x1[c]);
     }
@@ -452,14 +518,14 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     __builtin_amdgcn_s_setprio(2);
     if (t0 < ntile) {
       prefetch(t0);
-      dequant(int(t0 & 1));
+      dequant(t0);
       if (t0 + 1 < ntile) prefetch(t0 + 1);
     }
     for (int64_t it = t0; it < ntile; ++it) {
       // buffer it&1 is complete and every consumer is done with buffer (it+1)&1
       __syncthreads();
       if (it + 1 < ntile) {
-        dequant(int((it + 1) & 1));
+        dequant(it + 1);
         if (it + 2 < ntile) prefetch(it + 2);
       }
     }

@@ -100,6 +100,9 @@ struct AttendArgs {
   float* lse;
   float* logits;
   int64_t n_cache, n_q, q_start;
+  const void* k_act;  // [B, n_act, H, d] exact active-chunk Keys (after the packed ones)
+  const void* v_act;
+  int64_t n_act;
   int frame_tokens, heads, n_centroids, rank;
   int tables_in_lds;
   int n_split;    // workgroups per Query block, each over its share of the key tiles

@@ -60,6 +60,7 @@ def _load():
         "quantwm_append": (I32, [C, P, P, I64, P, P, I64, P, P]),
         "quantwm_attend_workspace_bytes": (SZ, [C, I64, I64]),
         "quantwm_attend": (I32, [C, P, P, I64, P, I64, I64, I32, P, P, P, SZ, P]),
+        "quantwm_attend_active": (I32, [C, P, P, I64, P, P, I64, P, I64, I64, I32, P, P, P, SZ, P]),
         "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I32, P, P]),
         "quantwm_last_error": (ctypes.c_char_p, []),
     }
@@ -73,8 +74,8 @@ _lib = _load()
 
 EXPORTED = ("quantwm_cache_bytes", "quantwm_token_bytes", "quantwm_calib_bytes", "quantwm_calib_offsets",
             "quantwm_calibrate_workspace_bytes", "quantwm_calib_pack", "quantwm_calibrate",
-            "quantwm_append", "quantwm_attend_workspace_bytes", "quantwm_attend", "quantwm_logits",
-            "quantwm_last_error")
+            "quantwm_append", "quantwm_attend_workspace_bytes", "quantwm_attend", "quantwm_attend_active",
+            "quantwm_logits", "quantwm_last_error")
 
 
 def library():
@@ -167,6 +168,15 @@ def quantwm_attend(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, ou
                                frame_tokens, _ptr(out), _ptr(lse_out), _ptr(workspace),
                                0 if workspace is None else workspace.numel() * workspace.element_size(),
                                _stream(stream)))
+
+
+def quantwm_attend_active(cfg, calib, cache, n_cache, k_act, v_act, n_act, q, n_q, q_start, frame_tokens, out,
+                          lse_out=None, workspace=None, stream=None):
+    _check(_lib.quantwm_attend_active(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cache, _ptr(k_act),
+                                      _ptr(v_act), n_act, _ptr(q), n_q, q_start, frame_tokens, _ptr(out),
+                                      _ptr(lse_out), _ptr(workspace),
+                                      0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                      _stream(stream)))
 
 
 def quantwm_logits(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, logits_out, stream=None):

@@ -368,3 +368,61 @@ def test_capacity_and_argument_errors():
     with pytest.raises(qw.QuantwmError) as e:
         qw.quantwm_attend(cfg, calib, cache, 10, k, 10, 11, 1, k)
     assert e.value.status == qw.ERR_INVALID_ARG
+
+
+# ----------------------------------------- BF16 active chunk (packed history + exact chunk)
+
+def _active_case(wl, max_sources, n_heads_rows, row_step):
+    """Packed history = the first n_cache - n_act tokens; the last n_act tokens
+    (the chunk being generated) enter exactly. Runs with and without a split
+    workspace; both against the oracle."""
+    case = case_for(wl, max_sources)
+    cfg = gpu_config(wl)
+    calib = gpu_calib_from_tables(cfg, harness.full_tables(case))
+    n_act = min(wl.chunk, wl.n_cache // 3)
+    n_pk = wl.n_cache - n_act
+    dt = cfg.torch_dtype
+    cache = torch.from_numpy(harness.full_oracle_cache(case)).to(DEV)
+    k_full, v_full = harness.full_inputs(case, "k"), harness.full_inputs(case, "v")
+    k_act = tdev(np.ascontiguousarray(k_full[:, n_pk:]), dt)
+    v_act = tdev(np.ascontiguousarray(v_full[:, n_pk:]), dt)
+    q = tdev(harness.full_inputs(case, "q"), dt)
+    rows = harness.sample_rows(wl, n_heads_rows, row_step)
+    src_rows = np.array([(0, int(case.src_of[b * wl.heads + h]), i) for b, h, i in rows], np.int32)
+    uniq, inv = np.unique(src_rows, axis=0, return_inverse=True)
+    o_out, o_lse, _ = oracle.attend(case.cfg, case.tables, case.cache, n_pk, case.q, wl.q_start, wl.frame_tokens,
+                                    rows=uniq, k_act=np.ascontiguousarray(case.k[:, n_pk:]),
+                                    v_act=np.ascontiguousarray(case.v[:, n_pk:]))
+    o_out, o_lse = o_out[inv.ravel()], o_lse[inv.ravel()]
+    tol = 2e-2 if wl.dtype == "bf16" else 1e-4
+    for split in (False, True):
+        nb = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q) if split else 0
+        if split and nb == 0:
+            continue
+        ws = torch.empty(nb, dtype=torch.uint8, device=DEV) if nb else None
+        out = torch.empty_like(q)
+        lse = torch.empty((wl.batch, wl.heads, wl.n_q), dtype=torch.float32, device=DEV)
+        _say(f"[gpu] attend_active {wl.name}: {n_pk} packed + {n_act} exact keys, workspace {nb} B")
+        qw.quantwm_attend_active(cfg, calib, cache, n_pk, k_act, v_act, n_act, q, wl.n_q, wl.q_start,
+                                 wl.frame_tokens, out, lse, ws)
+        torch.cuda.synchronize()
+        g = out.float().cpu().numpy()[rows[:, 0], rows[:, 2], rows[:, 1], :]
+        gl = lse.cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]]
+        err = np.abs(g - o_out)
+        assert err.max() <= tol, f"active-chunk attention max-abs error {err.max():.3g} > {tol}"
+        fin = np.isfinite(o_lse)
+        assert np.array_equal(np.isfinite(gl), fin)
+        assert np.all(np.abs(gl[fin] - o_lse[fin]) <= harness.lse_tol(o_lse[fin]))
+        _say(f"[ok] attend_active{' split' if split else ''} {wl.name}: max-abs {err.max():.3g} "
+             f"mean-abs {err.mean():.3g} over {len(rows)} rows")
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=[w.name for w in SMALL])
+def test_active_chunk_small(wl):
+    _active_case(wl, 64, 64, 1)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["lingbot-40h", "rollout-30k"])
+def test_active_chunk_full(name):
+    _active_case(synth.WORKLOADS[name], 3, 6, 37)
