@@ -398,7 +398,9 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   // rebuild khat_0 = mu + s (q - z) (Eq. 4), chat = code * cscale and vhat into
   // tile buffer `buf`. s (q - z) is exact in fp32, so the fma rounds once,
   // exactly like mu + s (q - z).
-  auto dequant = [&](int64_t t) {
+  auto dequant_tile = [&](auto full_tag, int64_t t) {
+    // FULL: every key of the tile is packed, so no active-chunk branch
+    constexpr bool FULL = decltype(full_tag)::value;
     const int buf = int(t & 1);
     const uint32_t k0 = uint32_t(t * KT);
     T* kt = smem + tile0 + buf * LY::tile_elems;
@@ -409,7 +411,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       float mu[16], x[16];
       if constexpr (TAB) load_vals<T, 16>(tabK + k_id * LY::TS + kch0 + 16 * u, mu);
       else load_vals<T, 16>(gtabK + k_id * D + kch0 + 16 * u, mu);
-      if (k_on_act) {
+      if (!FULL && k_on_act) {
         uint32_t w[16 * sizeof(T) / 4];
         load_words(act_row(k_act, k0 + kkey, kch0 + 16 * u), w, 16 * int(sizeof(T)) / 4);
         raw_to_float<T, 16>(w, x);
@@ -436,7 +438,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         load_vals<T, CHV>(gtabV + v_id[0] * D + vch0, mu0);
         load_vals<T, CHV>(gtabV + v_id[1] * D + vch0, mu1);
       }
-      if (v_on_act[0] || v_on_act[1]) {
+      if (!FULL && (v_on_act[0] || v_on_act[1])) {
         uint32_t w[VW];
         if (v_on_act[0]) {
           load_words(act_row(v_act, k0 + 2 * vkp, vch0), w, VW);
@@ -461,6 +463,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 
   using Full = std::integral_constant<bool, true>;
   using Tail = std::integral_constant<bool, false>;
+
   auto prefetch = [&](int64_t t) {
     if (t < nfull) load_raw(Full{}, uint32_t(t * KT));
     else load_raw(Tail{}, uint32_t(t * KT));
@@ -518,14 +521,22 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     __builtin_amdgcn_s_setprio(2);
     if (t0 < ntile) {
       prefetch(t0);
-      dequant(t0);
+      dequant_tile(Tail{}, t0);  // the general form is right for any tile
       if (t0 + 1 < ntile) prefetch(t0 + 1);
     }
-    for (int64_t it = t0; it < ntile; ++it) {
+    // tiles whose successor is all packed, then the rest: one dequant form per loop
+    const int64_t nf = nfull - 1 < ntile ? nfull - 1 : ntile;
+    int64_t it = t0;
+    for (; it < nf; ++it) {
       // buffer it&1 is complete and every consumer is done with buffer (it+1)&1
       __syncthreads();
+      dequant_tile(Full{}, it + 1);
+      if (it + 2 < ntile) prefetch(it + 2);
+    }
+    for (; it < ntile; ++it) {
+      __syncthreads();
       if (it + 1 < ntile) {
-        dequant(it + 1);
+        dequant_tile(Tail{}, it + 1);
         if (it + 2 < ntile) prefetch(it + 2);
       }
     }
