@@ -206,7 +206,9 @@ struct Lds {
   static constexpr int tile_elems = KT * KS + KT * CS + D * VS;
 };
 
-template <typename T, int D, int RP, bool LOGITS, bool TAB>
+// ACT: the launch has an exact active chunk after the packed keys (a separate
+// instance, so packed-only launches carry none of its code).
+template <typename T, int D, int RP, bool LOGITS, bool TAB, bool ACT>
 __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   typedef Mfma<T> MF;
   typedef typename MF::V V;
@@ -329,8 +331,8 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   auto load_raw = [&](auto full_tag, uint32_t k0) {
     constexpr bool FULL = decltype(full_tag)::value;
     const int k0i = int(k0);
-    k_on_act = !FULL && k0 + kkey >= npku && k0 + kkey < ncu;
-    if (!FULL && k_on_act) {
+    k_on_act = ACT && !FULL && k0 + kkey >= npku && k0 + kkey < ncu;
+    if (ACT && !FULL && k_on_act) {
       k_id = 0;
     } else if (FULL || k0 + kkey < npku) {
       const int id = __builtin_amdgcn_raw_buffer_load_b8(r_ki, kkey, k0i, 0);
@@ -378,8 +380,8 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const uint32_t key = k0 + 2 * vkp + e;
-      v_on_act[e] = !FULL && key >= npku && key < ncu;
-      if (!FULL && v_on_act[e]) {
+      v_on_act[e] = ACT && !FULL && key >= npku && key < ncu;
+      if (ACT && !FULL && v_on_act[e]) {
         v_id[e] = 0;
       } else if (FULL || key < npku) {
         const int id = __builtin_amdgcn_raw_buffer_load_b8(r_vi, 2 * vkp + e, k0i, 0);
@@ -411,7 +413,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       float mu[16], x[16];
       if constexpr (TAB) load_vals<T, 16>(tabK + k_id * LY::TS + kch0 + 16 * u, mu);
       else load_vals<T, 16>(gtabK + k_id * D + kch0 + 16 * u, mu);
-      if (!FULL && k_on_act) {
+      if (ACT && !FULL && k_on_act) {
         uint32_t w[16 * sizeof(T) / 4];
         load_words(act_row(k_act, k0 + kkey, kch0 + 16 * u), w, 16 * int(sizeof(T)) / 4);
         raw_to_float<T, 16>(w, x);
@@ -438,7 +440,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         load_vals<T, CHV>(gtabV + v_id[0] * D + vch0, mu0);
         load_vals<T, CHV>(gtabV + v_id[1] * D + vch0, mu1);
       }
-      if (!FULL && (v_on_act[0] || v_on_act[1])) {
+      if (ACT && !FULL && (v_on_act[0] || v_on_act[1])) {
         uint32_t w[VW];
         if (v_on_act[0]) {
           load_words(act_row(v_act, k0 + 2 * vkp, vch0), w, VW);
@@ -760,12 +762,12 @@ size_t lds_bytes_t(int rank, int kc, bool tables) {
   return (2 * tile + (tables ? size_t(2) * kc * TS : 0)) * sizeof(T);  // two tile buffers
 }
 
-template <typename T, int D, int RP, bool LOGITS, bool TAB>
+template <typename T, int D, int RP, bool LOGITS, bool TAB, bool ACT = false>
 hipError_t launch_k(const AttendArgs& a, const dim3& grid, size_t lds, hipStream_t s) {
-  const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, LOGITS, TAB>,
+  const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, LOGITS, TAB, ACT>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attend_kernel<T, D, RP, LOGITS, TAB>), grid, dim3(NT), lds, s, a);
+  hipLaunchKernelGGL((attend_kernel<T, D, RP, LOGITS, TAB, ACT>), grid, dim3(NT), lds, s, a);
   return hipGetLastError();
 }
 
@@ -775,7 +777,11 @@ hipError_t launch_r(const AttendArgs& a, int batch, bool logits, hipStream_t s) 
   const bool tab = a.tables_in_lds != 0;
   const size_t lds = lds_bytes_t<T, D>(a.rank, a.n_centroids, tab);
   if (logits) return tab ? launch_k<T, D, RP, true, true>(a, grid, lds, s) : launch_k<T, D, RP, true, false>(a, grid, lds, s);
-  const hipError_t e = tab ? launch_k<T, D, RP, false, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false>(a, grid, lds, s);
+  hipError_t e;
+  if (a.n_act > 0)
+    e = tab ? launch_k<T, D, RP, false, true, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false, true>(a, grid, lds, s);
+  else
+    e = tab ? launch_k<T, D, RP, false, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false>(a, grid, lds, s);
   if (e != hipSuccess || a.n_split == 1) return e;
   hipLaunchKernelGGL((attend_combine<T, D>), dim3((unsigned)((a.n_q + 3) / 4), (unsigned)a.heads, (unsigned)batch),
                      dim3(256), 0, s, a);
