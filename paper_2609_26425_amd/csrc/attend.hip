@@ -517,12 +517,17 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 
   // Producers and consumers run separate loops with one barrier per tile each,
   // so neither keeps the other's registers live.
+  // Every thread staged part of the centroid tables: they must be complete
+  // before the first dequantisation. The producers' first packed loads are
+  // already in flight across this barrier.
+  if (producer && t0 < ntile) prefetch(t0);
+  if constexpr (TAB) __syncthreads();
+
   if (producer) {
     // Producers issue first: their vector work fills the matrix-core phases of
     // the consumers, and a late tile would stall all eight consumers.
     __builtin_amdgcn_s_setprio(2);
     if (t0 < ntile) {
-      prefetch(t0);
       dequant_tile(Tail{}, t0);  // the general form is right for any tile
       if (t0 + 1 < ntile) prefetch(t0 + 1);
     }
