@@ -202,13 +202,21 @@ def decode(cfg: OraCfg, tables, cache, b, h, n):
 
 
 def attend(cfg: OraCfg, tables, cache, n_cache, q, q_start, frame_tokens, rows=None,
-           coef_override=None, want_logits=False, k_act=None, v_act=None):
+           coef_override=None, want_logits=False, k_act=None, v_act=None, epochs=None):
     """rows: int array [n_rows, 3] of (b, h, i); default all rows. k_act / v_act
     ([B, n_act, H, d]) append an exact active chunk after the packed keys.
+    epochs: optional list of (first key, tables) in increasing order, the first
+    at key 0; packed keys then decode with their epoch's tables (`tables` unused).
 
     Returns (out [n_rows, d] fp64, lse [n_rows], logits [n_rows, n_cache + n_act] or None).
     """
-    mu_k, mu_v, _, u_t = (_f32(t) for t in tables[:4])
+    if epochs is None:
+        epochs = [(0, tables)]
+    starts = np.array([e[0] for e in epochs], np.int64)
+    mu_k = np.ascontiguousarray(np.stack([_f32(e[1][0]) for e in epochs]))
+    mu_v = np.ascontiguousarray(np.stack([_f32(e[1][1]) for e in epochs]))
+    u_t = (np.ascontiguousarray(np.stack([_f32(e[1][3]) for e in epochs]))
+           if cfg.rank > 0 and epochs[0][1][3] is not None else None)
     q = _f32(q)
     B, n_q, H, d = q.shape
     n_act = 0 if k_act is None else int(k_act.shape[1])
@@ -221,10 +229,10 @@ def attend(cfg: OraCfg, tables, cache, n_cache, q, q_start, frame_tokens, rows=N
     out = np.zeros((nr, d)); lse = np.zeros(nr)
     logits = np.zeros((nr, n_cache + n_act)) if want_logits else None
     co = _f32(coef_override) if coef_override is not None else None
-    rc = lib().ora_attend_active(ctypes.byref(cfg), _p(mu_k), _p(mu_v), _p(u_t), _p(cache, ctypes.c_uint8),
-                                 ctypes.c_longlong(n_cache), _p(ka), _p(va), ctypes.c_longlong(n_act), _p(q),
-                                 ctypes.c_longlong(n_q), ctypes.c_longlong(q_start), int(frame_tokens), _p(co), nr,
-                                 _p(rows, ctypes.c_int), _p(out, ctypes.c_double), _p(lse, ctypes.c_double),
-                                 _p(logits, ctypes.c_double))
+    rc = lib().ora_attend_epochs(ctypes.byref(cfg), len(epochs), _p(starts, ctypes.c_longlong), _p(mu_k), _p(mu_v),
+                                 _p(u_t), _p(cache, ctypes.c_uint8), ctypes.c_longlong(n_cache), _p(ka), _p(va),
+                                 ctypes.c_longlong(n_act), _p(q), ctypes.c_longlong(n_q), ctypes.c_longlong(q_start),
+                                 int(frame_tokens), _p(co), nr, _p(rows, ctypes.c_int), _p(out, ctypes.c_double),
+                                 _p(lse, ctypes.c_double), _p(logits, ctypes.c_double))
     _check(rc, "attend")
     return out, lse, logits

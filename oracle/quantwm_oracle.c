@@ -557,11 +557,31 @@ int ora_attend_active(const ora_cfg* cfg, const float* mu_k, const float* mu_v, 
                       long long n_act, const float* q, long long n_q, long long q_start, int frame_tokens,
                       const float* coef_override, int n_rows, const int* rows, double* out, double* lse,
                       double* logits) {
+  const long long start0 = 0;
+  return ora_attend_epochs(cfg, 1, &start0, mu_k, mu_v, u_t, cache, n_cache, k_act, v_act, n_act, q, n_q, q_start,
+                           frame_tokens, coef_override, n_rows, rows, out, lse, logits);
+}
+
+/* Keys [epoch_start[e], epoch_start[e+1]) of the packed cache were appended with
+ * the tables of epoch e (centroids and U_r of that epoch, Sec. 5 streaming):
+ * their Khat_0 and Vhat decode with epoch e's centroids, and their PSAC term is
+ * (q U_r^(e)) . chat (Eq. 17 with the epoch's own subspace). Tables are
+ * [n_epochs][B][H][...]; epoch_start[0] = 0 and increases. */
+int ora_attend_epochs(const ora_cfg* cfg, int n_epochs, const long long* epoch_start, const float* mu_k,
+                      const float* mu_v, const float* u_t, const uint8_t* cache, long long n_cache,
+                      const float* k_act, const float* v_act, long long n_act, const float* q, long long n_q,
+                      long long q_start, int frame_tokens, const float* coef_override, int n_rows, const int* rows,
+                      double* out, double* lse, double* logits) {
   if (!valid_cfg(cfg) || n_cache < 0 || n_cache > cfg->capacity || n_act < 0 || (n_act > 0 && (!k_act || !v_act)) ||
-      n_q < 0 || q_start < 0 || q_start > n_cache + n_act || frame_tokens < 1 || n_rows < 0)
+      n_q < 0 || q_start < 0 || q_start > n_cache + n_act || frame_tokens < 1 || n_rows < 0 || n_epochs < 1 ||
+      !epoch_start || epoch_start[0] != 0)
     return -1;
+  for (int e = 1; e < n_epochs; ++e)
+    if (epoch_start[e] <= epoch_start[e - 1]) return -1;
   const long long n_all = n_cache + n_act;
   const int d = cfg->head_dim, H = cfg->heads, r = cfg->rank;
+  const long long tab_mu = (long long)cfg->batch * H * cfg->n_centroids * d;  /* floats per epoch */
+  const long long tab_u = (long long)cfg->batch * H * (r > 0 ? r : 1) * d;
   /* rows sorted by head so that each head's cache is decoded once; idx[4] keeps
    * the caller's row number */
   int* srt = (int*)malloc(sizeof(int) * 4 * (n_rows > 0 ? n_rows : 1));
@@ -572,17 +592,40 @@ int ora_attend_active(const ora_cfg* cfg, const float* mu_k, const float* mu_v, 
         rows[3 * i + 2] < 0 || rows[3 * i + 2] >= n_q) { free(srt); return -1; }
   }
   qsort(srt, (size_t)n_rows, sizeof(int) * 4, cmp_rows);
-  double* K0 = (double*)malloc(sizeof(double) * (n_all > 0 ? n_all : 1) * d);
-  double* V = (double*)malloc(sizeof(double) * (n_all > 0 ? n_all : 1) * d);
-  double* Ch = (double*)malloc(sizeof(double) * (n_all > 0 ? n_all : 1) * (r > 0 ? r : 1));
-  if (!K0 || !V || !Ch) { free(srt); free(K0); free(V); free(Ch); return -2; }
+  const long long nd = n_all > 0 ? n_all : 1, nc1 = n_cache > 0 ? n_cache : 1;
+  double* K0 = (double*)malloc(sizeof(double) * nd * d);
+  double* V = (double*)malloc(sizeof(double) * nd * d);
+  double* Ch = (double*)malloc(sizeof(double) * nd * (r > 0 ? r : 1));
+  double* tk = (double*)malloc(sizeof(double) * nc1 * d);
+  double* tv = (double*)malloc(sizeof(double) * nc1 * d);
+  double* tc = (double*)malloc(sizeof(double) * nc1 * (r > 0 ? r : 1));
+  int* ep = (int*)malloc(sizeof(int) * nd);
+  if (!K0 || !V || !Ch || !tk || !tv || !tc || !ep) {
+    free(srt); free(K0); free(V); free(Ch); free(tk); free(tv); free(tc); free(ep);
+    return -2;
+  }
+  for (long long j = 0, e = 0; j < n_all; ++j) {
+    while (e + 1 < n_epochs && j >= epoch_start[e + 1]) ++e;
+    ep[j] = (int)e;
+  }
   const double inv_sqrt_d = 1.0 / sqrt((double)d);
   int i0 = 0, status = 0;
   while (i0 < n_rows) {
     int b = srt[4 * i0], h = srt[4 * i0 + 1], i1 = i0;
     while (i1 < n_rows && srt[4 * i1] == b && srt[4 * i1 + 1] == h) ++i1;
     long long bh = (long long)b * H + h;
-    if (ora_decode(cfg, mu_k, mu_v, cache, b, h, n_cache, K0, Ch, V)) { status = -4; break; }
+    /* each epoch's keys decode with that epoch's centroids */
+    for (int e = 0; e < n_epochs && status == 0; ++e) {
+      const long long s0 = epoch_start[e], s1 = e + 1 < n_epochs ? epoch_start[e + 1] : n_cache;
+      if (s0 >= n_cache) break;
+      if (ora_decode(cfg, mu_k + e * tab_mu, mu_v + e * tab_mu, cache, b, h, n_cache, tk, tc, tv)) { status = -4; break; }
+      for (long long j = s0; j < s1 && j < n_cache; ++j) {
+        memcpy(K0 + j * d, tk + j * d, sizeof(double) * d);
+        memcpy(V + j * d, tv + j * d, sizeof(double) * d);
+        if (r > 0) memcpy(Ch + j * r, tc + j * r, sizeof(double) * r);
+      }
+    }
+    if (status) break;
     /* operands of the attention product, in the table type (BF16 per App. D.1) */
     for (long long t = 0; t < n_cache * d; ++t) { K0[t] = round_table(cfg, K0[t]); V[t] = round_table(cfg, V[t]); }
     for (long long t = 0; t < n_cache * r; ++t)
@@ -600,21 +643,24 @@ int ora_attend_active(const ora_cfg* cfg, const float* mu_k, const float* mu_v, 
       long long i = srt[4 * ri + 2];
       int dst = srt[4 * ri + 3];
       const float* qi = q + (((long long)b * n_q + i) * H + h) * d;
-      double u[256];
-      for (int kk = 0; kk < r; ++kk) {
-        double acc = 0.0;
-        for (int c = 0; c < d; ++c) acc += (double)qi[c] * (double)u_t[(bh * r + kk) * d + c];
-        u[kk] = round_table(cfg, acc); /* qU_r enters the product in the table type */
-      }
-      double* L = (double*)malloc(sizeof(double) * (n_all > 0 ? n_all : 1));
+      /* q U_r^(e) of every epoch, in the table type */
+      double* u = (double*)malloc(sizeof(double) * n_epochs * (r > 0 ? r : 1));
+      for (int e = 0; e < n_epochs; ++e)
+        for (int kk = 0; kk < r; ++kk) {
+          double acc = 0.0;
+          const float* ur = u_t + e * tab_u + (bh * r + kk) * d;
+          for (int c = 0; c < d; ++c) acc += (double)qi[c] * (double)ur[c];
+          u[e * r + kk] = round_table(cfg, acc);
+        }
+      double* L = (double*)malloc(sizeof(double) * nd);
       double m = -INFINITY;
       for (long long j = 0; j < n_all; ++j) {
         int visible = j < q_start || (j - q_start) / frame_tokens <= i / frame_tokens;
         if (!visible) { L[j] = -INFINITY; continue; }
-        /* Eq. 5 with Eq. 17: (q khat_0 + (q U_r) c) / sqrt(d) */
+        /* Eq. 5 with Eq. 17: (q khat_0 + (q U_r) c) / sqrt(d), U_r of the key's epoch */
         double acc = 0.0;
         for (int c = 0; c < d; ++c) acc += (double)qi[c] * K0[j * d + c];
-        for (int kk = 0; kk < r; ++kk) acc += u[kk] * Ch[j * r + kk];
+        for (int kk = 0; kk < r; ++kk) acc += u[ep[j] * r + kk] * Ch[j * r + kk];
         L[j] = acc * inv_sqrt_d;
         if (L[j] > m) m = L[j];
       }
@@ -635,10 +681,11 @@ int ora_attend_active(const ora_cfg* cfg, const float* mu_k, const float* mu_v, 
       }
       if (logits) memcpy(logits + (long long)dst * n_all, L, sizeof(double) * n_all);
       free(L);
+      free(u);
     }
     i0 = i1;
   }
-  free(srt); free(K0); free(V); free(Ch);
+  free(srt); free(K0); free(V); free(Ch); free(tk); free(tv); free(tc); free(ep);
   return status;
 }
 

@@ -104,6 +104,15 @@ int ora_attend_active(const ora_cfg* cfg, const float* mu_k, const float* mu_v, 
                       const float* coef_override, int n_rows, const int* rows, double* out, double* lse,
                       double* logits);
 
+/* The same with the packed keys in epochs: keys [epoch_start[e], epoch_start[e+1])
+ * were appended with epoch e's tables ([n_epochs][B][H][...] for mu_k, mu_v,
+ * u_t) and decode with them; their PSAC term uses q U_r of epoch e. */
+int ora_attend_epochs(const ora_cfg* cfg, int n_epochs, const long long* epoch_start, const float* mu_k,
+                      const float* mu_v, const float* u_t, const uint8_t* cache, long long n_cache,
+                      const float* k_act, const float* v_act, long long n_act, const float* q, long long n_q,
+                      long long q_start, int frame_tokens, const float* coef_override, int n_rows, const int* rows,
+                      double* out, double* lse, double* logits);
+
 int ora_max_threads(void);
 void ora_set_threads(int n);
 

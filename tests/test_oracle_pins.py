@@ -510,3 +510,57 @@ def test_active_chunk_empty_equals_packed_only():
     b = oracle.attend(cfg, tables, cache, wl.n_cache, q, wl.q_start, wl.frame_tokens)
     np.testing.assert_array_equal(a[0], b[0])
     np.testing.assert_array_equal(a[1], b[1])
+
+
+# ------------------------------------------- per-chunk calibration epochs (NEXT f1)
+
+def _two_epoch_cache(wl):
+    """Chunk 1 appended with tables calibrated on it, chunk 2 with tables
+    recalibrated on chunk 2 (and a second, different Query history)."""
+    cfg = oracle.cfg_from_workload(wl)
+    k = synth.tensor(wl, "k", wl.n_cache)
+    v = synth.tensor(wl, "v", wl.n_cache)
+    qh = synth.tensor(wl, "qhist", 2 * wl.n_hist)
+    split = wl.n_cache // 2 + 7
+    t1 = oracle.calibrate(cfg, qh[:, :wl.n_hist], k[:, :split], v[:, :split], 5)
+    t2 = oracle.calibrate(cfg, qh, k[:, split:], v[:, split:], 5)
+    cache = oracle.new_cache(cfg)
+    oracle.append(cfg, t1, cache, 0, np.ascontiguousarray(k[:, :split]), np.ascontiguousarray(v[:, :split]))
+    oracle.append(cfg, t2, cache, split, np.ascontiguousarray(k[:, split:]), np.ascontiguousarray(v[:, split:]))
+    return cfg, k, v, split, t1, t2, cache
+
+
+def test_single_epoch_equals_plain_attention():
+    wl = _small_workload(rank=4)
+    cfg, tables, cache, k, v, q, _ = _encoded(wl)
+    a = oracle.attend(cfg, tables, cache, wl.n_cache, q, wl.q_start, wl.frame_tokens)
+    b = oracle.attend(cfg, None, cache, wl.n_cache, q, wl.q_start, wl.frame_tokens, epochs=[(0, tables)])
+    np.testing.assert_array_equal(a[0], b[0])
+    c = oracle.attend(cfg, None, cache, wl.n_cache, q, wl.q_start, wl.frame_tokens,
+                      epochs=[(0, tables), (77, tables), (150, tables)])
+    np.testing.assert_array_equal(a[0], c[0])
+    np.testing.assert_array_equal(a[1], c[1])
+
+
+def test_epochs_match_explicit_reconstruction_fp32():
+    # Each key decodes with its epoch's centroids, and its Eq. 17 term uses its
+    # epoch's U_r: attention equals torch's SDPA (fp64) over the explicitly
+    # reconstructed Khat = Khat_0 + chat U_r^(e)T, epoch by epoch.
+    wl = _small_workload(rank=4)
+    cfg, k, v, split, t1, t2, cache = _two_epoch_cache(wl)
+    q = synth.tensor(wl, "q", wl.n_q)
+    out, _, _ = oracle.attend(cfg, None, cache, wl.n_cache, q, wl.q_start, wl.frame_tokens,
+                              epochs=[(0, t1), (split, t2)])
+    plain, _, _ = oracle.attend(cfg, t1, cache, wl.n_cache, q, wl.q_start, wl.frame_tokens)
+    for h in range(wl.heads):
+        rows_k, rows_v = [], []
+        for (s0, s1, t) in ((0, split, t1), (split, wl.n_cache, t2)):
+            k0, ch, vh = oracle.decode(cfg, t, cache, 0, h, wl.n_cache)
+            rows_k.append(k0[s0:s1] + ch[s0:s1] @ t[3][0, h].astype(np.float64))
+            rows_v.append(vh[s0:s1])
+        Khat, Vhat = np.concatenate(rows_k), np.concatenate(rows_v)
+        ref = _sdpa(q[0, :, h, :].astype(np.float64), Khat, Vhat, _mask(wl, wl.n_cache))
+        got = out[h * wl.n_q:(h + 1) * wl.n_q]
+        assert np.abs(got - ref).max() < 1e-5
+        # and decoding the second chunk with the first epoch's tables is wrong
+        assert np.abs(plain[h * wl.n_q:(h + 1) * wl.n_q] - ref).max() > 1e-3
