@@ -123,6 +123,28 @@ quantwm_status quantwm_calibrate(const quantwm_config* cfg, const void* q_hist, 
                                  int32_t kmeans_iters, void* calib, void* workspace,
                                  size_t workspace_bytes, void* stream);
 
+/* Running Query statistics for calibration epochs (Eq. 6 computed online, the
+ * streaming setting of Sec. 5 and App. C.3). A stats buffer holds a 256-byte
+ * header (int64 token count) and the fp64 sums of q q^T, [B*H][d][d]. The caller
+ * zeroes it once; a zero count is the cold start. */
+size_t quantwm_stats_bytes(const quantwm_config* cfg);
+
+/* Adds q q^T of the n Query tokens q [B,n,H,d] (dtype, device) to the sums and n
+ * to the count. The sums continue from their stored values in token order, so
+ * any sequence of updates equals one pass over all tokens in order. Ordered on
+ * `stream` like every call; n == 0 is a no-op. */
+quantwm_status quantwm_stats_update(const quantwm_config* cfg, const void* q, int64_t n, void* stats,
+                                    void* stream);
+
+/* quantwm_calibrate with the statistics of a stats buffer in place of q_hist:
+ * M = sums / count (Eq. 6), w (Eq. 8), U_r (Eq. 15), and the centroids by
+ * K-means on k_calib / v_calib (Eq. 3), e.g. the chunk that opens the epoch.
+ * Workspace: quantwm_calibrate_workspace_bytes(cfg, 0, n_calib). Synchronises
+ * `stream` (it reads the sums back to the host). */
+quantwm_status quantwm_calibrate_epoch(const quantwm_config* cfg, const void* stats, const void* k_calib,
+                                       const void* v_calib, int64_t n_calib, int32_t kmeans_iters, void* calib,
+                                       void* workspace, size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------- hot path */
 
 /* Quantize-on-append (Sec. 4.1-4.2, App. D.1) of n_new new tokens per (b, h)
@@ -177,6 +199,21 @@ quantwm_status quantwm_attend_active(const quantwm_config* cfg, const void* cali
                                      const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens,
                                      void* out, float* lse_out, void* workspace, size_t workspace_bytes,
                                      void* stream);
+
+/* quantwm_attend_active over a cache appended in calibration epochs (the
+ * streaming setting of Sec. 5: statistics and centroids are refreshed at chunk
+ * boundaries, and every chunk keeps the tables it was quantised with). Packed
+ * keys [epoch_start[e], epoch_start[e+1]) were appended with calibration block e
+ * of `calibs` (n_epochs blocks of quantwm_calib_bytes(cfg), contiguous, device);
+ * they decode with that block's centroids, and their PSAC term is
+ * (q U_r^(e)) . c with that block's U_r (Eq. 17 per epoch). epoch_start is a
+ * host array: epoch_start[0] = 0, each epoch spans at least 64 keys, every start
+ * is < n_cache; n_epochs in [1, 64]. n_epochs == 1 is quantwm_attend_active. */
+quantwm_status quantwm_attend_epochs(const quantwm_config* cfg, const void* calibs, int32_t n_epochs,
+                                     const int64_t* epoch_start, const void* cache, int64_t n_cache,
+                                     const void* k_act, const void* v_act, int64_t n_act, const void* q,
+                                     int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
+                                     float* lse_out, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Test hook: the scaled logits of quantwm_attend, [B,H,n_q,n_cache] f32,
  * -inf where masked. Same tile code as quantwm_attend. */

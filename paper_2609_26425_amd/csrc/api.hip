@@ -127,38 +127,15 @@ quantwm_status quantwm_calib_pack(const quantwm_config* cfg, const void* mu_k, c
   return ok();
 }
 
-quantwm_status quantwm_calibrate(const quantwm_config* cfg, const void* q_hist, int64_t n_hist, const void* k_calib,
-                                 const void* v_calib, int64_t n_calib, int32_t kmeans_iters, void* calib,
-                                 void* workspace, size_t workspace_bytes, void* stream) {
-  QWM_TRY(check_cfg(cfg));
-  if (n_hist < 0 || n_calib < 1 || kmeans_iters < 0)
-    return fail(QWM_ERR_INVALID_ARG, "need n_hist >= 0, n_calib >= 1, kmeans_iters >= 0");
-  QWM_TRY(check_dev(q_hist, "q_hist", n_hist > 0));
-  QWM_TRY(check_dev(k_calib, "k_calib"));
-  QWM_TRY(check_dev(v_calib, "v_calib"));
-  QWM_TRY(check_dev(calib, "calib"));
-  QWM_TRY(check_dev(workspace, "workspace"));
-  if (workspace_bytes < quantwm_calibrate_workspace_bytes(cfg, n_hist, n_calib))
-    return fail(QWM_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes,
-                quantwm_calibrate_workspace_bytes(cfg, n_hist, n_calib));
-  const quantwm_config& c = *cfg;
-  hipStream_t s = static_cast<hipStream_t>(stream);
+// Eq. 8 and Eq. 15 on the host in fp64 from the second moment M ([B*H][d][d],
+// already divided by the token count), then Eq. 3 centroids on the device.
+// cold: no historical Query yet (w = 1, U_r = 0).
+static quantwm_status finish_calibration(const quantwm_config& c, const std::vector<double>& M, bool cold,
+                                         const void* k_calib, const void* v_calib, int64_t n_calib,
+                                         int32_t kmeans_iters, uint8_t* cal, int32_t* assign, hipStream_t s) {
   const quantwm_calib_layout C = qwm::calib_layout(c);
   const int bh = c.batch * c.heads, d = c.head_dim, r = c.rank, e = qwm::elem_bytes(c);
-  uint8_t* cal = static_cast<uint8_t*>(calib);
-  double* m_dev = static_cast<double*>(workspace);
-  int32_t* assign = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) +
-                                               qwm::align256(int64_t(size_t(bh) * d * d * sizeof(double))));
   hipError_t he;
-
-  // Eq. 6 on the device, then Eq. 8 and Eq. 15 on the host in fp64.
-  std::vector<double> M(size_t(bh) * d * d, 0.0);
-  if (n_hist > 0) {
-    if ((he = qwm::launch_second_moment(c, q_hist, n_hist, m_dev, s)) != hipSuccess) return hip_fail(he, "moment");
-    if ((he = hipMemcpyAsync(M.data(), m_dev, M.size() * sizeof(double), hipMemcpyDeviceToHost, s)) != hipSuccess)
-      return hip_fail(he, "moment readback");
-    if ((he = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(he, "moment sync");
-  }
   std::vector<float> w(size_t(bh) * d), lam(size_t(bh) * (r > 0 ? r : 1));
   std::vector<uint8_t> ut(size_t(bh) * (r > 0 ? r : 1) * d * e, 0);
   std::vector<double> ev(d), vt(size_t(d) * d);
@@ -167,7 +144,7 @@ quantwm_status quantwm_calibrate(const quantwm_config* cfg, const void* q_hist, 
     double tr = 0.0;
     for (int k = 0; k < d; ++k) tr += Mi[size_t(k) * d + k];
     float* wi = w.data() + size_t(i) * d;
-    if (n_hist == 0 || tr == 0.0) {  // cold start: uniform sensitivity, PSAC inactive
+    if (cold || tr == 0.0) {  // cold start: uniform sensitivity, PSAC inactive
       for (int k = 0; k < d; ++k) wi[k] = 1.0f;
       for (int k = 0; k < r; ++k) lam[size_t(i) * r + k] = 0.0f;
       continue;
@@ -216,6 +193,89 @@ quantwm_status quantwm_calibrate(const quantwm_config* cfg, const void* q_hist, 
   // the host staging buffers die with this call
   if ((he = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(he, "calibrate sync");
   return ok();
+}
+
+quantwm_status quantwm_calibrate(const quantwm_config* cfg, const void* q_hist, int64_t n_hist, const void* k_calib,
+                                 const void* v_calib, int64_t n_calib, int32_t kmeans_iters, void* calib,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  QWM_TRY(check_cfg(cfg));
+  if (n_hist < 0 || n_calib < 1 || kmeans_iters < 0)
+    return fail(QWM_ERR_INVALID_ARG, "need n_hist >= 0, n_calib >= 1, kmeans_iters >= 0");
+  QWM_TRY(check_dev(q_hist, "q_hist", n_hist > 0));
+  QWM_TRY(check_dev(k_calib, "k_calib"));
+  QWM_TRY(check_dev(v_calib, "v_calib"));
+  QWM_TRY(check_dev(calib, "calib"));
+  QWM_TRY(check_dev(workspace, "workspace"));
+  if (workspace_bytes < quantwm_calibrate_workspace_bytes(cfg, n_hist, n_calib))
+    return fail(QWM_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes,
+                quantwm_calibrate_workspace_bytes(cfg, n_hist, n_calib));
+  const quantwm_config& c = *cfg;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int bh = c.batch * c.heads, d = c.head_dim;
+  double* m_dev = static_cast<double*>(workspace);
+  int32_t* assign = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) +
+                                               qwm::align256(int64_t(size_t(bh) * d * d * sizeof(double))));
+  hipError_t he;
+  // Eq. 6 on the device
+  std::vector<double> M(size_t(bh) * d * d, 0.0);
+  if (n_hist > 0) {
+    if ((he = qwm::launch_second_moment(c, q_hist, n_hist, m_dev, s)) != hipSuccess) return hip_fail(he, "moment");
+    if ((he = hipMemcpyAsync(M.data(), m_dev, M.size() * sizeof(double), hipMemcpyDeviceToHost, s)) != hipSuccess)
+      return hip_fail(he, "moment readback");
+    if ((he = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(he, "moment sync");
+  }
+  return finish_calibration(c, M, n_hist == 0, k_calib, v_calib, n_calib, kmeans_iters, static_cast<uint8_t*>(calib),
+                            assign, s);
+}
+
+size_t quantwm_stats_bytes(const quantwm_config* cfg) {
+  if (check_cfg(cfg) != QWM_OK) return 0;
+  return 256 + size_t(cfg->batch) * cfg->heads * cfg->head_dim * cfg->head_dim * sizeof(double);
+}
+
+quantwm_status quantwm_stats_update(const quantwm_config* cfg, const void* q, int64_t n, void* stats, void* stream) {
+  QWM_TRY(check_cfg(cfg));
+  if (n < 0) return fail(QWM_ERR_INVALID_ARG, "n must be >= 0");
+  if (n == 0) return ok();
+  QWM_TRY(check_dev(q, "q"));
+  QWM_TRY(check_dev(stats, "stats"));
+  int64_t* count = static_cast<int64_t*>(stats);
+  double* sums = reinterpret_cast<double*>(static_cast<uint8_t*>(stats) + 256);
+  const hipError_t he = qwm::launch_moment_accumulate(*cfg, q, n, sums, count, static_cast<hipStream_t>(stream));
+  if (he != hipSuccess) return hip_fail(he, "stats update");
+  return ok();
+}
+
+quantwm_status quantwm_calibrate_epoch(const quantwm_config* cfg, const void* stats, const void* k_calib,
+                                       const void* v_calib, int64_t n_calib, int32_t kmeans_iters, void* calib,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+  QWM_TRY(check_cfg(cfg));
+  if (n_calib < 1 || kmeans_iters < 0) return fail(QWM_ERR_INVALID_ARG, "need n_calib >= 1, kmeans_iters >= 0");
+  QWM_TRY(check_dev(stats, "stats"));
+  QWM_TRY(check_dev(k_calib, "k_calib"));
+  QWM_TRY(check_dev(v_calib, "v_calib"));
+  QWM_TRY(check_dev(calib, "calib"));
+  QWM_TRY(check_dev(workspace, "workspace"));
+  if (workspace_bytes < quantwm_calibrate_workspace_bytes(cfg, 0, n_calib))
+    return fail(QWM_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes,
+                quantwm_calibrate_workspace_bytes(cfg, 0, n_calib));
+  const quantwm_config& c = *cfg;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t nm = size_t(c.batch) * c.heads * c.head_dim * c.head_dim;
+  std::vector<double> M(nm);
+  int64_t count = 0;
+  hipError_t he;
+  if ((he = hipMemcpyAsync(&count, stats, sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (he = hipMemcpyAsync(M.data(), static_cast<const uint8_t*>(stats) + 256, nm * sizeof(double),
+                           hipMemcpyDeviceToHost, s)) != hipSuccess)
+    return hip_fail(he, "stats readback");
+  if ((he = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(he, "stats sync");
+  if (count < 0) return fail(QWM_ERR_INVALID_ARG, "stats count is negative (buffer not initialised?)");
+  // Eq. 6: M = sum / count, the same fp64 division as the one-pass moment
+  if (count > 0)
+    for (double& x : M) x = x / (double)count;
+  return finish_calibration(c, M, count == 0, k_calib, v_calib, n_calib, kmeans_iters, static_cast<uint8_t*>(calib),
+                            static_cast<int32_t*>(workspace), s);
 }
 
 quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void* cache, int64_t n_cached,
@@ -283,11 +343,22 @@ size_t quantwm_attend_workspace_bytes(const quantwm_config* cfg, int64_t n_cache
   return attend_split_bytes(cfg, n_cache, n_q, nullptr);
 }
 
-static quantwm_status attend_common(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
+static quantwm_status attend_common(const quantwm_config* cfg, const void* calib, int32_t n_epochs,
+                                    const int64_t* epoch_start, const void* cache, int64_t n_cache,
                                     const void* k_act, const void* v_act, int64_t n_act, const void* q, int64_t n_q,
                                     int64_t q_start, int32_t frame_tokens, void* out, float* lse_out,
                                     float* logits_out, void* workspace, size_t workspace_bytes, void* stream) {
   QWM_TRY(check_cfg(cfg));
+  if (n_epochs < 1 || n_epochs > qwm::kMaxEpochs) return fail(QWM_ERR_UNSUPPORTED, "n_epochs must be in [1, 64]");
+  if (n_epochs > 1) {
+    if (!epoch_start) return fail(QWM_ERR_INVALID_ARG, "epoch_start is null");
+    if (epoch_start[0] != 0) return fail(QWM_ERR_INVALID_ARG, "epoch_start[0] must be 0");
+    for (int e = 1; e < n_epochs; ++e) {
+      if (epoch_start[e] - epoch_start[e - 1] < 64)
+        return fail(QWM_ERR_INVALID_ARG, "epoch %d spans fewer than 64 keys", e - 1);
+      if (epoch_start[e] >= n_cache) return fail(QWM_ERR_INVALID_ARG, "epoch %d starts at or past n_cache", e);
+    }
+  }
   if (n_cache < 0 || n_act < 0 || n_q < 0 || q_start < 0) return fail(QWM_ERR_INVALID_ARG, "sizes must be >= 0");
   if (n_cache > cfg->capacity) return fail(QWM_ERR_CAPACITY, "n_cache exceeds capacity");
   if (n_act > (int64_t(1) << 26)) return fail(QWM_ERR_UNSUPPORTED, "n_act above 2^26");
@@ -319,6 +390,9 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   a.L = qwm::cache_layout(*cfg);
   a.q = q; a.out = out; a.lse = lse_out; a.logits = logits_out;
   a.n_cache = n_cache; a.n_q = n_q; a.q_start = q_start;
+  a.n_epochs = n_epochs;
+  a.calib_stride = n_epochs > 1 ? int64_t(quantwm_calib_bytes(cfg)) : 0;
+  for (int e = 0; e < qwm::kMaxEpochs; ++e) a.epoch_start[e] = e < n_epochs && n_epochs > 1 ? epoch_start[e] : 0;
   a.k_act = n_act > 0 ? k_act : nullptr;
   a.v_act = n_act > 0 ? v_act : nullptr;
   a.n_act = n_act;
@@ -350,24 +424,33 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
 quantwm_status quantwm_attend(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
                               const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
                               float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
-  return attend_common(cfg, calib, cache, n_cache, nullptr, nullptr, 0, q, n_q, q_start, frame_tokens, out, lse_out,
-                       nullptr, workspace, workspace_bytes, stream);
+  return attend_common(cfg, calib, 1, nullptr, cache, n_cache, nullptr, nullptr, 0, q, n_q, q_start, frame_tokens, out,
+                       lse_out, nullptr, workspace, workspace_bytes, stream);
 }
 
 quantwm_status quantwm_attend_active(const quantwm_config* cfg, const void* calib, const void* cache,
                                      int64_t n_cache, const void* k_act, const void* v_act, int64_t n_act,
                                      const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
                                      float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
-  return attend_common(cfg, calib, cache, n_cache, k_act, v_act, n_act, q, n_q, q_start, frame_tokens, out, lse_out,
-                       nullptr, workspace, workspace_bytes, stream);
+  return attend_common(cfg, calib, 1, nullptr, cache, n_cache, k_act, v_act, n_act, q, n_q, q_start, frame_tokens, out,
+                       lse_out, nullptr, workspace, workspace_bytes, stream);
+}
+
+quantwm_status quantwm_attend_epochs(const quantwm_config* cfg, const void* calibs, int32_t n_epochs,
+                                     const int64_t* epoch_start, const void* cache, int64_t n_cache,
+                                     const void* k_act, const void* v_act, int64_t n_act, const void* q, int64_t n_q,
+                                     int64_t q_start, int32_t frame_tokens, void* out, float* lse_out,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  return attend_common(cfg, calibs, n_epochs, epoch_start, cache, n_cache, k_act, v_act, n_act, q, n_q, q_start,
+                       frame_tokens, out, lse_out, nullptr, workspace, workspace_bytes, stream);
 }
 
 quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
                               const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, float* logits_out,
                               void* stream) {
   if (!logits_out && n_q > 0) return fail(QWM_ERR_INVALID_ARG, "logits_out is null");
-  return attend_common(cfg, calib, cache, n_cache, nullptr, nullptr, 0, q, n_q, q_start, frame_tokens, nullptr,
-                       nullptr, logits_out, nullptr, 0, stream);
+  return attend_common(cfg, calib, 1, nullptr, cache, n_cache, nullptr, nullptr, 0, q, n_q, q_start, frame_tokens,
+                       nullptr, nullptr, logits_out, nullptr, 0, stream);
 }
 
 }  // extern "C"

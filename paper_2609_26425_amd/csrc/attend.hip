@@ -49,6 +49,12 @@ __device__ inline void vset(V& v, int j, T x) {
   else v[j] = x;
 }
 
+template <typename V>
+__device__ inline auto vget(const V& v, int j) {
+  if constexpr (std::is_same_v<V, float>) return v;
+  else return v[j];
+}
+
 // Row of the 32x32 accumulator held by accumulator slot i of a lane in half hf.
 __device__ inline constexpr int acc_row(int i, int hf) { return (i / 4) * 8 + hf * 4 + (i % 4); }
 
@@ -206,9 +212,10 @@ struct Lds {
   static constexpr int tile_elems = KT * KS + KT * CS + D * VS;
 };
 
-// ACT: the launch has an exact active chunk after the packed keys (a separate
-// instance, so packed-only launches carry none of its code).
-template <typename T, int D, int RP, bool LOGITS, bool TAB, bool ACT>
+// GEN: the launch has an exact active chunk after the packed keys and/or packed
+// keys in several calibration epochs (a separate instance, so plain launches
+// carry none of its code).
+template <typename T, int D, int RP, bool LOGITS, bool TAB, bool GEN>
 __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   typedef Mfma<T> MF;
   typedef typename MF::V V;
@@ -227,28 +234,25 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, l32 = lane % 32, hf = lane / 32;
   const int h = blockIdx.y, b = blockIdx.z;
   const int64_t bh = int64_t(b) * a.heads + h;
-  const uint8_t* slab = a.calib + bh * a.slab;
-  const T* gtabK = reinterpret_cast<const T*>(slab + a.o_mu_k);
-  const T* gtabV = reinterpret_cast<const T*>(slab + a.o_mu_v);
-  const T* gU = reinterpret_cast<const T*>(slab + a.o_u_t);
+  // calibration slab of this head in epoch e
+  auto epoch_slab = [&](int e) { return a.calib + int64_t(e) * a.calib_stride + bh * a.slab; };
+  // epoch of a (wave-uniform) key, and the first key past epoch e
+  auto epoch_at = [&](int64_t key) {
+    int e = 0;
+    if constexpr (GEN)
+      while (e + 1 < a.n_epochs && key >= a.epoch_start[e + 1]) ++e;
+    return e;
+  };
+  auto epoch_end = [&](int e) -> int64_t {
+    return GEN && e + 1 < a.n_epochs ? a.epoch_start[e + 1] : (int64_t(1) << 62);
+  };
+  auto tab_of = [&](int e, int64_t off) { return reinterpret_cast<const T*>(epoch_slab(e) + off); };
   const CacheLayout& L = a.L;
   const uint8_t* cache = a.cache;
   const int64_t slot0 = bh * L.slots;
   const int r = a.rank;
   const int G = D / L.ng;
   const bool producer = wave >= NC;
-
-  // ---- stage the centroid tables of this head (App. D.1: BF16 centroids)
-  if constexpr (TAB) {
-    constexpr int PER_ROW = D * int(sizeof(T)) / 16;  // 16-byte chunks per centroid row
-    const uint4* sk = reinterpret_cast<const uint4*>(gtabK);
-    const uint4* sv = reinterpret_cast<const uint4*>(gtabV);
-    for (int i = tid; i < Kc * PER_ROW; i += NT) {
-      const int row = i / PER_ROW, ch = i % PER_ROW;
-      *reinterpret_cast<uint4*>(tabK + row * LY::TS + ch * (16 / int(sizeof(T)))) = sk[i];
-      *reinterpret_cast<uint4*>(tabV + row * LY::TS + ch * (16 / int(sizeof(T)))) = sv[i];
-    }
-  }
 
   // ---- key range of this workgroup: Query block blockIdx.x / n_split, and the
   // split-th of n_split equal runs of its key tiles
@@ -266,6 +270,22 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   const int64_t t0 = split * per_split < ntile_all ? split * per_split : ntile_all;
   const int64_t ntile = t0 + per_split < ntile_all ? t0 + per_split : ntile_all;  // this split: tiles [t0, ntile)
   const int64_t nfull = npk / KT;  // tiles [0, nfull) hold packed keys only
+
+  // ---- stage the centroid tables of one epoch (App. D.1: BF16 centroids) with
+  // threads [first, first + count) of the workgroup
+  auto stage_tables = [&](int e, int first, int count) {
+    constexpr int PER_ROW = D * int(sizeof(T)) / 16;  // 16-byte chunks per centroid row
+    const uint4* sk = reinterpret_cast<const uint4*>(tab_of(e, a.o_mu_k));
+    const uint4* sv = reinterpret_cast<const uint4*>(tab_of(e, a.o_mu_v));
+    for (int i = tid - first; i < Kc * PER_ROW; i += count) {
+      const int row = i / PER_ROW, ch = i % PER_ROW;
+      *reinterpret_cast<uint4*>(tabK + row * LY::TS + ch * (16 / int(sizeof(T)))) = sk[i];
+      *reinterpret_cast<uint4*>(tabV + row * LY::TS + ch * (16 / int(sizeof(T)))) = sv[i];
+    }
+  };
+  // the staged epoch: that of the tile being dequantised (both roles track it)
+  int se = epoch_at(t0 * KT);
+  if constexpr (TAB) stage_tables(se, 0, NT);
 
   // ======================= producer state (waves NC .. NC+NP-1)
   const int ptid = producer ? tid - NC * 64 : 0;
@@ -331,8 +351,8 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   auto load_raw = [&](auto full_tag, uint32_t k0) {
     constexpr bool FULL = decltype(full_tag)::value;
     const int k0i = int(k0);
-    k_on_act = ACT && !FULL && k0 + kkey >= npku && k0 + kkey < ncu;
-    if (ACT && !FULL && k_on_act) {
+    k_on_act = GEN && !FULL && k0 + kkey >= npku && k0 + kkey < ncu;
+    if (GEN && !FULL && k_on_act) {
       k_id = 0;
     } else if (FULL || k0 + kkey < npku) {
       const int id = __builtin_amdgcn_raw_buffer_load_b8(r_ki, kkey, k0i, 0);
@@ -380,8 +400,8 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const uint32_t key = k0 + 2 * vkp + e;
-      v_on_act[e] = ACT && !FULL && key >= npku && key < ncu;
-      if (ACT && !FULL && v_on_act[e]) {
+      v_on_act[e] = GEN && !FULL && key >= npku && key < ncu;
+      if (GEN && !FULL && v_on_act[e]) {
         v_id[e] = 0;
       } else if (FULL || key < npku) {
         const int id = __builtin_amdgcn_raw_buffer_load_b8(r_vi, 2 * vkp + e, k0i, 0);
@@ -408,12 +428,24 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     T* kt = smem + tile0 + buf * LY::tile_elems;
     T* ct = kt + KT * LY::KS;
     T* vt = ct + KT * LY::CS;
+    // centroids: the staged epoch se (LDS tables when they fit); a tile may end in
+    // the next epoch, whose keys read that epoch's tables from global memory
+    const int64_t b1 = epoch_end(se);
+    const int se1 = se + 1 < a.n_epochs ? se + 1 : se;
+    const T* gK0 = tab_of(se, a.o_mu_k);
+    const T* gK1 = tab_of(se1, a.o_mu_k);
+    const T* gV0 = tab_of(se, a.o_mu_v);
+    const T* gV1 = tab_of(se1, a.o_mu_v);
+    const bool k_e1 = GEN && !FULL && int64_t(k0) + kkey >= b1;
+    bool v_e1[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) v_e1[e] = GEN && !FULL && int64_t(k0) + 2 * vkp + e >= b1;
 #pragma unroll
     for (int u = 0; u < NSUB; ++u) {
       float mu[16], x[16];
-      if constexpr (TAB) load_vals<T, 16>(tabK + k_id * LY::TS + kch0 + 16 * u, mu);
-      else load_vals<T, 16>(gtabK + k_id * D + kch0 + 16 * u, mu);
-      if (ACT && !FULL && k_on_act) {
+      if (TAB && !k_e1) load_vals<T, 16>(tabK + k_id * LY::TS + kch0 + 16 * u, mu);
+      else load_vals<T, 16>((k_e1 ? gK1 : gK0) + k_id * D + kch0 + 16 * u, mu);
+      if (GEN && !FULL && k_on_act) {
         uint32_t w[16 * sizeof(T) / 4];
         load_words(act_row(k_act, k0 + kkey, kch0 + 16 * u), w, 16 * int(sizeof(T)) / 4);
         raw_to_float<T, 16>(w, x);
@@ -433,14 +465,11 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     {
       float x0[CHV], x1[CHV];
       float mu0[CHV], mu1[CHV];
-      if constexpr (TAB) {
-        load_vals<T, CHV>(tabV + v_id[0] * LY::TS + vch0, mu0);
-        load_vals<T, CHV>(tabV + v_id[1] * LY::TS + vch0, mu1);
-      } else {
-        load_vals<T, CHV>(gtabV + v_id[0] * D + vch0, mu0);
-        load_vals<T, CHV>(gtabV + v_id[1] * D + vch0, mu1);
-      }
-      if (ACT && !FULL && (v_on_act[0] || v_on_act[1])) {
+      if (TAB && !v_e1[0]) load_vals<T, CHV>(tabV + v_id[0] * LY::TS + vch0, mu0);
+      else load_vals<T, CHV>((v_e1[0] ? gV1 : gV0) + v_id[0] * D + vch0, mu0);
+      if (TAB && !v_e1[1]) load_vals<T, CHV>(tabV + v_id[1] * LY::TS + vch0, mu1);
+      else load_vals<T, CHV>((v_e1[1] ? gV1 : gV0) + v_id[1] * D + vch0, mu1);
+      if (GEN && !FULL && (v_on_act[0] || v_on_act[1])) {
         uint32_t w[VW];
         if (v_on_act[0]) {
           load_words(act_row(v_act, k0 + 2 * vkp, vch0), w, VW);
@@ -475,7 +504,29 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   const int64_t qi = qa + (producer ? 0 : wave) * 32 + l32;
   const bool qvalid = !producer && qi < a.n_q;
   V qreg[D / KSTEP];
-  V ureg[RP > 0 ? RP / KSTEP : 1];
+  V ureg[RP > 0 ? RP / KSTEP : 1];   // q U_r of epoch ue
+  int ue = se;
+  // u = q U_r of epoch e on matrix cores (A operand: rows = ranks of U_r^T);
+  // every lane takes part, so callers stay wave-uniform
+  auto compute_u = [&](int e, V (&dst)[RP > 0 ? RP / KSTEP : 1]) {
+    const T* gU = tab_of(e, a.o_u_t);
+    f32x16 uacc;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) uacc[i] = 0.0f;
+#pragma unroll
+    for (int st = 0; st < D / KSTEP; ++st) {
+      V av;
+#pragma unroll
+      for (int j = 0; j < KPL; ++j)
+        vset(av, j, l32 < r ? gU[int64_t(l32) * D + st * KSTEP + hf * KPL + j] : T(0.0f));
+      uacc = MF::run(av, qreg[st], uacc);
+    }
+    // slot i holds rank acc_row(i, hf): round to the MFMA type (the operand of Eq. 17)
+#pragma unroll
+    for (int st = 0; st < (RP > 0 ? RP / KSTEP : 1); ++st)
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) vset(dst[st], j, T(uacc[st * KPL + j]));
+  };
   float m_run = -__builtin_inff(), l_run = 0.0f;
   f32x16 oacc[D / 32];
   int64_t lim = nc;
@@ -487,25 +538,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 #pragma unroll
       for (int j = 0; j < KPL; ++j) vset(qreg[st], j, qvalid ? qrow[st * KSTEP + hf * KPL + j] : T(0.0f));
     }
-    // u = q U_r on matrix cores (A operand: rows = ranks of U_r^T)
-    if constexpr (RP > 0) {
-      f32x16 uacc;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) uacc[i] = 0.0f;
-#pragma unroll
-      for (int st = 0; st < D / KSTEP; ++st) {
-        V av;
-#pragma unroll
-        for (int j = 0; j < KPL; ++j)
-          vset(av, j, l32 < r ? gU[int64_t(l32) * D + st * KSTEP + hf * KPL + j] : T(0.0f));
-        uacc = MF::run(av, qreg[st], uacc);
-      }
-      // slot i holds rank acc_row(i, hf): round to the MFMA type (the operand of Eq. 17)
-#pragma unroll
-      for (int st = 0; st < RP / KSTEP; ++st)
-#pragma unroll
-        for (int j = 0; j < KPL; ++j) vset(ureg[st], j, T(uacc[st * KPL + j]));
-    }
+    if constexpr (RP > 0) compute_u(se, ureg);
 #pragma unroll
     for (int cb = 0; cb < D / 32; ++cb)
 #pragma unroll
@@ -530,6 +563,30 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     if (t0 < ntile) {
       dequant_tile(Tail{}, t0);  // the general form is right for any tile
       if (t0 + 1 < ntile) prefetch(t0 + 1);
+    }
+    if constexpr (GEN) {
+      for (int64_t it = t0; it < ntile; ++it) {
+        __syncthreads();
+        if constexpr (TAB) {
+          // the next tile opens another epoch: restage its tables (every producer
+          // is done with the old ones after the barrier above), then sync
+          if (it + 1 < ntile) {
+            const int en = epoch_at((it + 1) * KT);
+            if (en != se) {
+              se = en;
+              stage_tables(se, NC * 64, PT);
+              __syncthreads();
+            }
+          }
+        } else {
+          if (it + 1 < ntile) se = epoch_at((it + 1) * KT);
+        }
+        if (it + 1 < ntile) {
+          dequant_tile(Tail{}, it + 1);
+          if (it + 2 < ntile) prefetch(it + 2);
+        }
+      }
+      return;
     }
     // tiles whose successor is all packed, then the rest: one dequant form per loop
     const int64_t nf = nfull - 1 < ntile ? nfull - 1 : ntile;
@@ -562,9 +619,34 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     constexpr bool MASKED = decltype(mask_tag)::value;
     const int64_t k0 = it * KT;
     __syncthreads();
+    if constexpr (GEN && TAB) {
+      // mirror of the producers' restage of the centroid tables (one more barrier)
+      if (it + 1 < ntile) {
+        const int en = epoch_at((it + 1) * KT);
+        if (en != se) {
+          se = en;
+          __syncthreads();
+        }
+      }
+    }
     const T* kt = smem + tile0 + int(it & 1) * LY::tile_elems;
     const T* ct = kt + KT * LY::KS;
     const T* vt = ct + KT * LY::CS;
+    // PSAC terms use q U_r of the key's epoch: the tile's first epoch e0 and,
+    // where the tile crosses into the next epoch at b1, that one too
+    V ureg2[RP > 0 ? RP / KSTEP : 1];
+    int64_t b1 = int64_t(1) << 62;
+    bool cross = false;
+    if constexpr (GEN && RP > 0) {
+      const int e0 = epoch_at(k0);
+      if (e0 != ue) {
+        compute_u(e0, ureg);
+        ue = e0;
+      }
+      b1 = epoch_end(e0);
+      cross = b1 < k0 + KT && b1 < npk;
+      if (cross) compute_u(e0 + 1, ureg2);
+    }
 
     // logits S^T of the 32 keys k0 + 32 kb + row (rows x Queries) on matrix cores
     auto logits_half = [&](int kb) {
@@ -586,7 +668,20 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
           V av;
 #pragma unroll
           for (int j = 0; j < KPL; ++j) vset(av, j, crow[acc_row(st * KPL + j, hf)]);
-          acc = MF::run(av, ureg[st], acc);
+          if (GEN && cross) {
+            // this lane's A row is key k0 + 32 kb + l32: its chat goes with its epoch's u
+            const bool first = k0 + kb * 32 + l32 < b1;
+            V a0, a1;
+#pragma unroll
+            for (int j = 0; j < KPL; ++j) {
+              vset(a0, j, first ? vget(av, j) : T(0.0f));
+              vset(a1, j, first ? T(0.0f) : vget(av, j));
+            }
+            acc = MF::run(a0, ureg[st], acc);
+            acc = MF::run(a1, ureg2[st], acc);
+          } else {
+            acc = MF::run(av, ureg[st], acc);
+          }
         }
       }
       return acc;
@@ -767,12 +862,12 @@ size_t lds_bytes_t(int rank, int kc, bool tables) {
   return (2 * tile + (tables ? size_t(2) * kc * TS : 0)) * sizeof(T);  // two tile buffers
 }
 
-template <typename T, int D, int RP, bool LOGITS, bool TAB, bool ACT = false>
+template <typename T, int D, int RP, bool LOGITS, bool TAB, bool GEN = false>
 hipError_t launch_k(const AttendArgs& a, const dim3& grid, size_t lds, hipStream_t s) {
-  const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, LOGITS, TAB, ACT>,
+  const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, LOGITS, TAB, GEN>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attend_kernel<T, D, RP, LOGITS, TAB, ACT>), grid, dim3(NT), lds, s, a);
+  hipLaunchKernelGGL((attend_kernel<T, D, RP, LOGITS, TAB, GEN>), grid, dim3(NT), lds, s, a);
   return hipGetLastError();
 }
 
@@ -783,7 +878,7 @@ hipError_t launch_r(const AttendArgs& a, int batch, bool logits, hipStream_t s) 
   const size_t lds = lds_bytes_t<T, D>(a.rank, a.n_centroids, tab);
   if (logits) return tab ? launch_k<T, D, RP, true, true>(a, grid, lds, s) : launch_k<T, D, RP, true, false>(a, grid, lds, s);
   hipError_t e;
-  if (a.n_act > 0)
+  if (a.n_act > 0 || a.n_epochs > 1)
     e = tab ? launch_k<T, D, RP, false, true, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false, true>(a, grid, lds, s);
   else
     e = tab ? launch_k<T, D, RP, false, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false>(a, grid, lds, s);

@@ -106,6 +106,26 @@ __global__ __launch_bounds__(256) void moment_kernel(const T* q, int64_t n, int 
   m[bh * d * d + p] = acc / (double)n;
 }
 
+// Eq. 6 online: continues the fp64 token-order sums of q q^T from their stored
+// values, so a sequence of updates equals one pass over all the tokens.
+template <typename T>
+__global__ __launch_bounds__(256) void moment_accumulate_kernel(const T* q, int64_t n, int heads, int d, double* sums,
+                                                                int64_t* count) {
+  const int64_t bh = blockIdx.y;
+  const int b = int(bh / heads), h = int(bh % heads);
+  const int p = blockIdx.x * 256 + threadIdx.x;
+  if (bh == 0 && p == 0) *count += n;
+  if (p >= d * d) return;
+  const int i = p / d, j = p % d;
+  const T* base = q + (int64_t(b) * n * heads + h) * d;
+  double acc = sums[bh * d * d + p];
+  for (int64_t t = 0; t < n; ++t) {
+    const T* row = base + t * heads * d;
+    acc = __builtin_fma((double)ldf(row + i), (double)ldf(row + j), acc);
+  }
+  sums[bh * d * d + p] = acc;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void km_init_kernel(const T* x, int64_t n, int heads, int d, int Kc,
                                                       uint8_t* calib, int64_t slab_bytes, int64_t o_mu) {
@@ -229,6 +249,19 @@ hipError_t launch_second_moment(const quantwm_config& c, const void* q, int64_t 
     hipLaunchKernelGGL(moment_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)q, n, c.heads, d, m);
   else
     hipLaunchKernelGGL(moment_kernel<float>, grid, dim3(256), 0, s, (const float*)q, n, c.heads, d, m);
+  return hipGetLastError();
+}
+
+hipError_t launch_moment_accumulate(const quantwm_config& c, const void* q, int64_t n, double* sums, int64_t* count,
+                                    hipStream_t s) {
+  const int d = c.head_dim;
+  const dim3 grid((unsigned)((d * d + 255) / 256), (unsigned)(c.batch * c.heads));
+  if (c.dtype == QWM_BF16)
+    hipLaunchKernelGGL(moment_accumulate_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)q, n, c.heads, d, sums,
+                       count);
+  else
+    hipLaunchKernelGGL(moment_accumulate_kernel<float>, grid, dim3(256), 0, s, (const float*)q, n, c.heads, d, sums,
+                       count);
   return hipGetLastError();
 }
 

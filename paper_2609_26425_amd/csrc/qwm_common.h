@@ -89,6 +89,8 @@ struct AppendArgs {
   float* coef_out;
 };
 
+constexpr int kMaxEpochs = 64;
+
 struct AttendArgs {
   const uint8_t* calib;
   int64_t slab;
@@ -106,6 +108,11 @@ struct AttendArgs {
   int frame_tokens, heads, n_centroids, rank;
   int tables_in_lds;
   int n_split;    // workgroups per Query block, each over its share of the key tiles
+  // calibration epochs: packed keys [epoch_start[e], epoch_start[e+1]) were
+  // appended with the calibration block at calib + e * calib_stride
+  int n_epochs;
+  int64_t calib_stride;
+  int64_t epoch_start[64];
   float* part_o;  // [n_split][B*H][n_q][d] unnormalised partial outputs (n_split > 1)
   float* part_ml; // [n_split][B*H][n_q][2] running max (raw logits) and sum per partial
 };
@@ -125,6 +132,8 @@ hipError_t launch_derive_constants(const quantwm_config& c, uint8_t* calib, hipS
 hipError_t launch_pack_tables(const quantwm_config& c, const void* mu_k, const void* mu_v,
                               const float* w, const void* u_t, const float* lam, uint8_t* calib,
                               hipStream_t s);
+hipError_t launch_moment_accumulate(const quantwm_config& c, const void* q, int64_t n, double* sums, int64_t* count,
+                                    hipStream_t s);
 hipError_t launch_second_moment(const quantwm_config& c, const void* q, int64_t n, double* m_out,
                                 hipStream_t s);
 hipError_t launch_kmeans(const quantwm_config& c, const void* x, int64_t n, int iters, uint8_t* calib,

@@ -57,10 +57,15 @@ def _load():
         "quantwm_calibrate_workspace_bytes": (SZ, [C, I64, I64]),
         "quantwm_calib_pack": (I32, [C, P, P, P, P, P, P, P]),
         "quantwm_calibrate": (I32, [C, P, I64, P, P, I64, I32, P, P, SZ, P]),
+        "quantwm_stats_bytes": (SZ, [C]),
+        "quantwm_stats_update": (I32, [C, P, I64, P, P]),
+        "quantwm_calibrate_epoch": (I32, [C, P, P, P, I64, I32, P, P, SZ, P]),
         "quantwm_append": (I32, [C, P, P, I64, P, P, I64, P, P]),
         "quantwm_attend_workspace_bytes": (SZ, [C, I64, I64]),
         "quantwm_attend": (I32, [C, P, P, I64, P, I64, I64, I32, P, P, P, SZ, P]),
         "quantwm_attend_active": (I32, [C, P, P, I64, P, P, I64, P, I64, I64, I32, P, P, P, SZ, P]),
+        "quantwm_attend_epochs": (I32, [C, P, I32, ctypes.POINTER(I64), P, I64, P, P, I64, P, I64, I64, I32, P, P,
+                                        P, SZ, P]),
         "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I32, P, P]),
         "quantwm_last_error": (ctypes.c_char_p, []),
     }
@@ -73,8 +78,10 @@ def _load():
 _lib = _load()
 
 EXPORTED = ("quantwm_cache_bytes", "quantwm_token_bytes", "quantwm_calib_bytes", "quantwm_calib_offsets",
-            "quantwm_calibrate_workspace_bytes", "quantwm_calib_pack", "quantwm_calibrate",
+            "quantwm_calibrate_workspace_bytes", "quantwm_calib_pack", "quantwm_calibrate", "quantwm_stats_bytes",
+            "quantwm_stats_update", "quantwm_calibrate_epoch",
             "quantwm_append", "quantwm_attend_workspace_bytes", "quantwm_attend", "quantwm_attend_active",
+            "quantwm_attend_epochs",
             "quantwm_logits", "quantwm_last_error")
 
 
@@ -153,6 +160,21 @@ def quantwm_calibrate(cfg, q_hist, n_hist, k_calib, v_calib, n_calib, kmeans_ite
                                   _stream(stream)))
 
 
+def quantwm_stats_bytes(cfg: Config) -> int:
+    return int(_lib.quantwm_stats_bytes(ctypes.byref(cfg)))
+
+
+def quantwm_stats_update(cfg, q, n, stats, stream=None):
+    _check(_lib.quantwm_stats_update(ctypes.byref(cfg), _ptr(q), n, _ptr(stats), _stream(stream)))
+
+
+def quantwm_calibrate_epoch(cfg, stats, k_calib, v_calib, n_calib, kmeans_iters, calib, workspace, stream=None):
+    _check(_lib.quantwm_calibrate_epoch(ctypes.byref(cfg), _ptr(stats), _ptr(k_calib), _ptr(v_calib), n_calib,
+                                        kmeans_iters, _ptr(calib), _ptr(workspace),
+                                        0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                        _stream(stream)))
+
+
 def quantwm_append(cfg, calib, cache, n_cached, k_new, v_new, n_new, coef_f32_out=None, stream=None):
     _check(_lib.quantwm_append(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cached, _ptr(k_new), _ptr(v_new),
                                n_new, _ptr(coef_f32_out), _stream(stream)))
@@ -175,6 +197,17 @@ def quantwm_attend_active(cfg, calib, cache, n_cache, k_act, v_act, n_act, q, n_
     _check(_lib.quantwm_attend_active(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cache, _ptr(k_act),
                                       _ptr(v_act), n_act, _ptr(q), n_q, q_start, frame_tokens, _ptr(out),
                                       _ptr(lse_out), _ptr(workspace),
+                                      0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                      _stream(stream)))
+
+
+def quantwm_attend_epochs(cfg, calibs, epoch_start, cache, n_cache, k_act, v_act, n_act, q, n_q, q_start,
+                          frame_tokens, out, lse_out=None, workspace=None, stream=None):
+    """calibs: one device buffer of len(epoch_start) calibration blocks; epoch_start: host ints."""
+    starts = (ctypes.c_int64 * len(epoch_start))(*[int(x) for x in epoch_start])
+    _check(_lib.quantwm_attend_epochs(ctypes.byref(cfg), _ptr(calibs), len(epoch_start), starts, _ptr(cache),
+                                      n_cache, _ptr(k_act), _ptr(v_act), n_act, _ptr(q), n_q, q_start, frame_tokens,
+                                      _ptr(out), _ptr(lse_out), _ptr(workspace),
                                       0 if workspace is None else workspace.numel() * workspace.element_size(),
                                       _stream(stream)))
 
