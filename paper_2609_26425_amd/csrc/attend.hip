@@ -582,7 +582,10 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
           if (it + 1 < ntile) se = epoch_at((it + 1) * KT);
         }
         if (it + 1 < ntile) {
-          dequant_tile(Tail{}, it + 1);
+          // a tile of packed keys inside one epoch takes the plain form
+          const int64_t kn = (it + 1) * KT;
+          if (kn + KT <= npk && kn + KT <= epoch_end(se)) dequant_tile(Full{}, it + 1);
+          else dequant_tile(Tail{}, it + 1);
           if (it + 2 < ntile) prefetch(it + 2);
         }
       }
