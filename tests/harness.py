@@ -52,7 +52,9 @@ def _gen_sources(wl, sources, what, n):
     return out
 
 
-def build_oracle_case(wl: synth.Workload, max_sources: int = 3, cold: bool = False) -> OracleCase:
+def build_oracle_case(wl: synth.Workload, max_sources: int = 3, cold: bool = False, transform=None) -> OracleCase:
+    """transform(k, v, q) -> (k, v, q) edits the generated source inputs (for edge
+    cases); its results are rounded to the workload's dtype."""
     sources = sources_for(wl, max_sources)
     S = len(sources)
     cfg = oracle.cfg_of(1, S, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank, wl.top_m,
@@ -60,6 +62,9 @@ def build_oracle_case(wl: synth.Workload, max_sources: int = 3, cold: bool = Fal
     k = _gen_sources(wl, sources, "k", wl.n_cache)
     v = _gen_sources(wl, sources, "v", wl.n_cache)
     q = _gen_sources(wl, sources, "q", wl.n_q)
+    if transform is not None:
+        k, v, q = (np.ascontiguousarray(synth.round_to(np.asarray(x, np.float32), wl.dtype))
+                   for x in transform(k, v, q))
     qh = None if cold else _gen_sources(wl, sources, "qhist", wl.n_hist)
     nc = min(wl.chunk, wl.n_cache)
     tables = oracle.calibrate(cfg, qh, np.ascontiguousarray(k[:, :nc]), np.ascontiguousarray(v[:, :nc]),
