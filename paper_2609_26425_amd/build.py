@@ -31,7 +31,11 @@ def _units():
         for d in (64, 128):
             units.append((f"append_{tn}_{d}.o", "append.hip",
                           [f"-DQWM_APPEND_T={t}", f"-DQWM_APPEND_TN={tn}", f"-DQWM_APPEND_D={d}"]))
-    for name in ("attend", "calib", "api"):
+    # attend: no NaN semantics, so maxima of matrix-core results are plain
+    # v_max3_f32 without a quieting v_max_f32 x, x per input (its logits and
+    # running maxima are finite or -inf)
+    units.append(("attend.o", "attend.hip", ["-fno-honor-nans"]))
+    for name in ("calib", "api"):
         units.append((f"{name}.o", f"{name}.hip", []))
     units.append(("eigh.o", "eigh.cpp", ["-x", "hip"]))
     return units

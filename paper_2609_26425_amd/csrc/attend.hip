@@ -49,6 +49,13 @@ __device__ inline void vset(V& v, int j, T x) {
   else v[j] = x;
 }
 
+// max(a, b, c): the compiler folds the pair into one v_max3_f32. This file is
+// built without NaN semantics (the logits and running maxima are finite or
+// -inf), so no input is first quieted with a v_max_f32 x, x. It is not inline
+// asm on purpose: its inputs come straight from matrix-core results, and only
+// the compiler inserts the wait states a VALU read of those needs.
+__device__ inline float max3f(float a, float b, float c) { return fmaxf(fmaxf(a, b), c); }
+
 template <typename V>
 __device__ inline auto vget(const V& v, int j) {
   if constexpr (std::is_same_v<V, float>) return v;
@@ -719,7 +726,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       auto raise_max = [&](const f32x16& sa, const f32x16& sb) {
         float mt = -__builtin_inff();
 #pragma unroll
-        for (int i = 0; i < 16; ++i) mt = fmaxf(mt, fmaxf(sa[i], sb[i]));
+        for (int i = 0; i < 16; ++i) mt = max3f(mt, sa[i], sb[i]);
         mt = max_halves(mt);
         if (__any(mt > m_run + tau)) {
           const float m_new = fmaxf(m_run, mt);
