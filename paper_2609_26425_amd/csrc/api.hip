@@ -11,6 +11,9 @@
 #include "qwm_common.h"
 
 namespace {
+// largest Query or key count per head the attention kernels take (positions
+// are 32-bit there, with room for a tile past the end)
+constexpr int64_t kMaxPositions = 0x7fff0000;
 
 thread_local std::string g_error;
 
@@ -413,6 +416,9 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
     }
   }
   if ((n_q + 255) / 256 * int64_t(a.n_split) > 0x7fffffff) return fail(QWM_ERR_UNSUPPORTED, "n_q too large");
+  // the kernel keeps Query and key positions in 32 bits
+  if (n_q > kMaxPositions || n_cache + n_act > kMaxPositions)
+    return fail(QWM_ERR_UNSUPPORTED, "more than %lld Queries or keys per head", (long long)kMaxPositions);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool lg = logits_out != nullptr;
   const hipError_t e = cfg->dtype == QWM_BF16 ? qwm::launch_attend_bf16(a, cfg->head_dim, cfg->batch, lg, s)

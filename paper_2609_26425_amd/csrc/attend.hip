@@ -62,6 +62,22 @@ __device__ inline auto vget(const V& v, int j) {
   else return v[j];
 }
 
+// Packed fields of one key tile held by one producer thread between their load
+// and their dequantisation, as loaded (codes, centroid ids, zero-point bytes,
+// binary16 scales), plus the active-chunk flags. Nothing is derived from a
+// loaded value until the tile is dequantised, so the loads stay in flight.
+// Marker: the coefficient-load form is chosen at run time.
+struct AnyAlign {};
+
+template <int NSUB>
+struct TileRegs {
+  uint32_t k_cw[NSUB], c_w[2], v_cw[2];
+  uint32_t k_idb, v_idb[2];
+  uint32_t k_zb[NSUB], v_zb[2];
+  _Float16 k_s[NSUB], v_s[2], c_s;  // loaded bits, reinterpreted (no arithmetic)
+  bool k_on_act, v_on_act[2];
+};
+
 // Row of the 32x32 accumulator held by accumulator slot i of a lane in half hf.
 __device__ inline constexpr int acc_row(int i, int hf) { return (i / 4) * 8 + hf * 4 + (i % 4); }
 
@@ -238,7 +254,11 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   T* tabV = smem + Kc * LY::TS;
   const int tile0 = TAB ? 2 * Kc * LY::TS : 0;
 
-  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, l32 = lane % 32, hf = lane / 32;
+  // the wave index is uniform across a wave: taken through readfirstlane, the
+  // producer/consumer split is a scalar branch, so neither role keeps the
+  // other's registers live
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / 64), lane = tid % 64, l32 = lane % 32,
+            hf = lane / 32;
   const int h = blockIdx.y, b = blockIdx.z;
   const int64_t bh = int64_t(b) * a.heads + h;
   // calibration slab of this head in epoch e
@@ -307,19 +327,26 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   const bool crole = RP > 0 && cr0 < r;
   const bool raligned = r % RCH == 0;
 
-  // packed tile fields of this thread, loaded one tile ahead of use
-  // zero-points are kept as (1024 + z) in both binary16 halves (dequant_codes)
-  uint32_t k_cw[NSUB], c_w[2] = {0, 0}, v_cw[2] = {0, 0};
-  int k_id = 0, v_id[2] = {0, 0};
-  uint32_t k_z[NSUB], v_z[2] = {0x64006400u, 0x64006400u};
-  _Float16 k_s[NSUB], v_s[2] = {0, 0};
-  float c_s = 0.0f;
+  // packed tile fields of this thread: tile t sits in register set (t - t0) & 1,
+  // so a tile's loads are issued two tiles ahead of its dequantisation
+  TileRegs<NSUB> P0, P1;
+  auto clear_regs = [&](TileRegs<NSUB>& p) __attribute__((always_inline)) {
 #pragma unroll
-  for (int u = 0; u < NSUB; ++u) { k_cw[u] = 0; k_z[u] = 0x64006400u; k_s[u] = 0; }
+    for (int u = 0; u < NSUB; ++u) { p.k_cw[u] = 0; p.k_zb[u] = 0; p.k_s[u] = 0; }
+    p.c_w[0] = p.c_w[1] = 0;
+    p.c_s = 0;
+    p.k_idb = 0;
+    p.k_on_act = false;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      p.v_cw[e] = 0; p.v_idb[e] = 0; p.v_zb[e] = 0; p.v_s[e] = 0; p.v_on_act[e] = false;
+    }
+  };
+  clear_regs(P0);
+  clear_regs(P1);
   // keys of the active chunk are read in dequant itself (only the flags travel
   // from one tile to the next), so they cost no registers across the loop
   constexpr int KW = CHK * int(sizeof(T)) / 4, VW = CHV * int(sizeof(T)) / 4;
-  bool k_on_act = false, v_on_act[2] = {false, false};
   const T* __restrict__ k_act = reinterpret_cast<const T*>(a.k_act);
   const T* __restrict__ v_act = reinterpret_cast<const T*>(a.v_act);
   const uint32_t npku = uint32_t(npk);
@@ -355,81 +382,114 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   // FULL: every key of the tile is < n_cache, so no per-thread guards. A key
   // past n_cache (tail tiles only) gets centroid 0, scale 0 and code 0: a finite
   // placeholder whose logit the mask turns into -inf, so it never contributes.
-  auto load_raw = [&](auto full_tag, uint32_t k0) {
+  // residual group, zero-point byte and 2-bit shift of each K piece and of the V run
+  int kgrp[NSUB];
+#pragma unroll
+  for (int u = 0; u < NSUB; ++u) kgrp[u] = (kch0 + 16 * u) / G;
+  const int vzsh = 2 * (vg % 4);
+  // Placeholder fields (all zero) decode to centroid 0 with scale 0.
+  // align_tag: std::true_type / std::false_type when the caller knows whether
+  // r is a multiple of RCH (one whole-word coefficient load), else AnyAlign
+  auto load_raw = [&](TileRegs<NSUB>& p, auto full_tag, uint32_t k0, auto align_tag) __attribute__((always_inline)) {
     constexpr bool FULL = decltype(full_tag)::value;
+    using AT = decltype(align_tag);
+    constexpr int AL = std::is_same_v<AT, std::true_type> ? 1 : std::is_same_v<AT, std::false_type> ? 0 : -1;
+    const bool aligned = AL == 1 || (AL == -1 && raligned);
     const int k0i = int(k0);
-    k_on_act = GEN && !FULL && k0 + kkey >= npku && k0 + kkey < ncu;
-    if (GEN && !FULL && k_on_act) {
-      k_id = 0;
-    } else if (FULL || k0 + kkey < npku) {
-      const int id = __builtin_amdgcn_raw_buffer_load_b8(r_ki, kkey, k0i, 0);
-      k_id = id < Kc ? id : Kc - 1;
+    // fields are gathered in locals and stored into the set once, at the end
+    uint32_t kid = 0, kzb[NSUB], kcw[NSUB], cw2[2] = {0, 0};
+    uint32_t vid[2] = {0, 0}, vzb[2] = {0, 0}, vcw[2] = {0, 0};
+    _Float16 ksb[NSUB], csb = 0, vsb[2] = {0, 0};
+#pragma unroll
+    for (int u = 0; u < NSUB; ++u) { kzb[u] = 0; ksb[u] = 0; kcw[u] = 0; }
+    const bool kact = GEN && !FULL && k0 + kkey >= npku && k0 + kkey < ncu;
+    if (!kact && (FULL || k0 + kkey < npku)) {
+      kid = __builtin_amdgcn_raw_buffer_load_b8(r_ki, kkey, k0i, 0);
 #pragma unroll
       for (int u = 0; u < NSUB; ++u) {
-        const int g = (kch0 + 16 * u) / G;
-        const uint32_t zb = __builtin_amdgcn_raw_buffer_load_b8(r_kz, o_kz + g / 4, k0i * int(zpb), 0);
-        k_z[u] = (0x6400u + ((zb >> (2 * (g % 4))) & 3)) * 0x00010001u;
-        k_s[u] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_ks, o_ks + 2 * g, k0i * int(sstride), 0));
+        const int g = kgrp[u];
+        kzb[u] = __builtin_amdgcn_raw_buffer_load_b8(r_kz, o_kz + g / 4, k0i * int(zpb), 0);
+        ksb[u] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_ks, o_ks + 2 * g, k0i * int(sstride), 0));
       }
       if constexpr (NSUB == 2) {
         const auto cw = __builtin_amdgcn_raw_buffer_load_b64(r_kc, o_kc, k0i * (D / 4), 0);
-        k_cw[0] = cw[0];
-        k_cw[NSUB - 1] = cw[1];
+        kcw[0] = cw[0];
+        kcw[1] = cw[1];
       } else {
-        k_cw[0] = __builtin_amdgcn_raw_buffer_load_b32(r_kc, o_kc, k0i * (D / 4), 0);
+        kcw[0] = __builtin_amdgcn_raw_buffer_load_b32(r_kc, o_kc, k0i * (D / 4), 0);
       }
-    } else {
-      k_id = 0;
-#pragma unroll
-      for (int u = 0; u < NSUB; ++u) { k_cw[u] = 0; k_z[u] = 0x64006400u; k_s[u] = 0; }
     }
     if constexpr (RP > 0) {
-      c_s = 0.0f;
-      c_w[0] = 0;
-      c_w[1] = 0;
       if (crole && (FULL || k0 + ckey < npku)) {
-        c_s = (float)__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_cs, o_cs, k0i * 2, 0));
-        if (raligned) {
+        csb = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_cs, o_cs, k0i * 2, 0));
+        if (aligned) {
           if constexpr (RCH == 8) {
             const auto u = __builtin_amdgcn_raw_buffer_load_b64(r_cc, o_cc, k0i * r, 0);
-            c_w[0] = u[0];
-            c_w[1] = u[1];
+            cw2[0] = u[0];
+            cw2[1] = u[1];
           } else {
-            c_w[0] = __builtin_amdgcn_raw_buffer_load_b32(r_cc, o_cc, k0i * r, 0);
+            cw2[0] = __builtin_amdgcn_raw_buffer_load_b32(r_cc, o_cc, k0i * r, 0);
           }
         } else {
 #pragma unroll
           for (int k = 0; k < RCH; ++k)
-            if (cr0 + k < r) c_w[k / 4] |= uint32_t(__builtin_amdgcn_raw_buffer_load_b8(r_cc, o_cc + k, k0i * r, 0)) << (8 * (k % 4));
+            if (cr0 + k < r) cw2[k / 4] |= uint32_t(__builtin_amdgcn_raw_buffer_load_b8(r_cc, o_cc + k, k0i * r, 0)) << (8 * (k % 4));
         }
       }
     }
+    bool vact[2];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const uint32_t key = k0 + 2 * vkp + e;
-      v_on_act[e] = GEN && !FULL && key >= npku && key < ncu;
-      if (GEN && !FULL && v_on_act[e]) {
-        v_id[e] = 0;
-      } else if (FULL || key < npku) {
-        const int id = __builtin_amdgcn_raw_buffer_load_b8(r_vi, 2 * vkp + e, k0i, 0);
-        v_id[e] = id < Kc ? id : Kc - 1;
-        const uint32_t zb = __builtin_amdgcn_raw_buffer_load_b8(r_vz, o_vz + e * int(zpb), k0i * int(zpb), 0);
-        v_z[e] = (0x6400u + ((zb >> (2 * (vg % 4))) & 3)) * 0x00010001u;
-        v_s[e] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_vs, o_vs + e * int(sstride), k0i * int(sstride), 0));
-        if constexpr (CHV == 16) v_cw[e] = __builtin_amdgcn_raw_buffer_load_b32(r_vc, o_vc + e * (D / 4), k0i * (D / 4), 0);
-        else v_cw[e] = __builtin_amdgcn_raw_buffer_load_b16(r_vc, o_vc + e * (D / 4), k0i * (D / 4), 0);
-      } else {
-        v_id[e] = 0; v_z[e] = 0x64006400u; v_s[e] = 0; v_cw[e] = 0;
+      vact[e] = GEN && !FULL && key >= npku && key < ncu;
+      if (!vact[e] && (FULL || key < npku)) {
+        vid[e] = __builtin_amdgcn_raw_buffer_load_b8(r_vi, 2 * vkp + e, k0i, 0);
+        vzb[e] = __builtin_amdgcn_raw_buffer_load_b8(r_vz, o_vz + e * int(zpb), k0i * int(zpb), 0);
+        vsb[e] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_vs, o_vs + e * int(sstride), k0i * int(sstride), 0));
+        if constexpr (CHV == 16) vcw[e] = __builtin_amdgcn_raw_buffer_load_b32(r_vc, o_vc + e * (D / 4), k0i * (D / 4), 0);
+        else vcw[e] = __builtin_amdgcn_raw_buffer_load_b16(r_vc, o_vc + e * (D / 4), k0i * (D / 4), 0);
       }
+    }
+    p.k_on_act = kact;
+    p.k_idb = kid;
+#pragma unroll
+    for (int u = 0; u < NSUB; ++u) { p.k_zb[u] = kzb[u]; p.k_s[u] = ksb[u]; p.k_cw[u] = kcw[u]; }
+    p.c_s = csb;
+    p.c_w[0] = cw2[0];
+    p.c_w[1] = cw2[1];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      p.v_on_act[e] = vact[e]; p.v_idb[e] = vid[e]; p.v_zb[e] = vzb[e]; p.v_s[e] = vsb[e]; p.v_cw[e] = vcw[e];
     }
   };
 
   // rebuild khat_0 = mu + s (q - z) (Eq. 4), chat = code * cscale and vhat into
   // tile buffer `buf`. s (q - z) is exact in fp32, so the fma rounds once,
   // exactly like mu + s (q - z).
-  auto dequant_tile = [&](auto full_tag, int64_t t) {
+  auto dequant_tile = [&](TileRegs<NSUB>& p, auto full_tag, int64_t t) __attribute__((always_inline)) {
     // FULL: every key of the tile is packed, so no active-chunk branch
     constexpr bool FULL = decltype(full_tag)::value;
+    const uint32_t (&k_cw)[NSUB] = p.k_cw;
+    const uint32_t (&c_w)[2] = p.c_w;
+    const uint32_t (&v_cw)[2] = p.v_cw;
+    const bool k_on_act = p.k_on_act, v_on_act[2] = {p.v_on_act[0], p.v_on_act[1]};
+    // fields as the decode takes them: clamped ids, (1024 + z) pairs, binary16 scales
+    const int k_id = int(p.k_idb) < Kc ? int(p.k_idb) : Kc - 1;
+    uint32_t k_z[NSUB], v_z[2];
+    _Float16 k_s[NSUB], v_s[2];
+    int v_id[2];
+#pragma unroll
+    for (int u = 0; u < NSUB; ++u) {
+      k_z[u] = (0x6400u + ((p.k_zb[u] >> (2 * (kgrp[u] % 4))) & 3)) * 0x00010001u;
+      k_s[u] = p.k_s[u];
+    }
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      v_id[e] = int(p.v_idb[e]) < Kc ? int(p.v_idb[e]) : Kc - 1;
+      v_z[e] = (0x6400u + ((p.v_zb[e] >> vzsh) & 3)) * 0x00010001u;
+      v_s[e] = p.v_s[e];
+    }
+    const float c_s = (float)p.c_s;
     const int buf = int(t & 1);
     const uint32_t k0 = uint32_t(t * KT);
     T* kt = smem + tile0 + buf * LY::tile_elems;
@@ -502,13 +562,14 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   using Full = std::integral_constant<bool, true>;
   using Tail = std::integral_constant<bool, false>;
 
-  auto prefetch = [&](int64_t t) {
-    if (t < nfull) load_raw(Full{}, uint32_t(t * KT));
-    else load_raw(Tail{}, uint32_t(t * KT));
+  auto prefetch = [&](TileRegs<NSUB>& p, int64_t t) __attribute__((always_inline)) {
+    if (t < nfull) load_raw(p, Full{}, uint32_t(t * KT), AnyAlign{});
+    else load_raw(p, Tail{}, uint32_t(t * KT), AnyAlign{});
   };
 
   // ======================= consumer state (waves 0 .. NC-1)
-  const int64_t qi = qa + (producer ? 0 : wave) * 32 + l32;
+  // Query and key positions fit in 32 bits (the host rejects larger calls)
+  const int qi = int(qa) + (producer ? 0 : wave) * 32 + l32;
   const bool qvalid = !producer && qi < a.n_q;
   V qreg[D / KSTEP];
   V ureg[RP > 0 ? RP / KSTEP : 1];   // q U_r of epoch ue
@@ -536,7 +597,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   };
   float m_run = -__builtin_inff(), l_run = 0.0f;
   f32x16 oacc[D / 32];
-  int64_t lim = nc;
+  int lim = int(nc);
   if (!producer) {
     // Query fragment (B operand: k = channel, column = Query)
     const T* qrow = reinterpret_cast<const T*>(a.q) + ((int64_t(b) * a.n_q + (qvalid ? qi : 0)) * a.heads + h) * D;
@@ -550,8 +611,10 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     for (int cb = 0; cb < D / 32; ++cb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) oacc[cb][i] = 0.0f;
-    if (qvalid) lim = qs + (qi / F + 1) * F;  // this lane's Query sees keys j < lim
-    if (lim > nc) lim = nc;
+    if (qvalid) {
+      const int64_t l = qs + (qi / F + 1) * F;  // this lane's Query sees keys j < lim
+      lim = int(l < nc ? l : nc);
+    }
   }
   const float mscale = 1.4426950408889634f / sqrtf((float)D);  // logits are exponentiated as 2^(S log2(e)/sqrt(d))
 
@@ -560,7 +623,10 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   // Every thread staged part of the centroid tables: they must be complete
   // before the first dequantisation. The producers' first packed loads are
   // already in flight across this barrier.
-  if (producer && t0 < ntile) prefetch(t0);
+  if (producer && t0 < ntile) {
+    prefetch(P0, t0);
+    if (t0 + 1 < ntile) prefetch(P1, t0 + 1);
+  }
   if constexpr (TAB) __syncthreads();
 
   if (producer) {
@@ -568,11 +634,21 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     // the consumers, and a late tile would stall all eight consumers.
     __builtin_amdgcn_s_setprio(2);
     if (t0 < ntile) {
-      dequant_tile(Tail{}, t0);  // the general form is right for any tile
-      if (t0 + 1 < ntile) prefetch(t0 + 1);
+      dequant_tile(P0, Tail{}, t0);  // the general form is right for any tile
+      if (t0 + 2 < ntile) prefetch(P0, t0 + 2);
     }
+    // One step per key tile `it`, after its barrier (buffer it&1 is complete and
+    // every consumer is done with buffer (it+1)&1): dequantise tile it + 1 from
+    // its register set, then refill that set with tile it + 3. Every call names
+    // its set statically (a set chosen at run time would be kept in memory).
+    auto refill = [&](TileRegs<NSUB>& p, int64_t it, auto full_tag) __attribute__((always_inline)) {
+      dequant_tile(p, full_tag, it + 1);
+      if (it + 3 < ntile) prefetch(p, it + 3);
+    };
+    // The steady loops take two tiles per trip with the sets in fixed places, so
+    // the wait before each dequantisation covers only the older set's loads.
     if constexpr (GEN) {
-      for (int64_t it = t0; it < ntile; ++it) {
+      auto gstep = [&](int64_t it, TileRegs<NSUB>& p) __attribute__((always_inline)) {
         __syncthreads();
         if constexpr (TAB) {
           // the next tile opens another epoch: restage its tables (every producer
@@ -591,27 +667,43 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         if (it + 1 < ntile) {
           // a tile of packed keys inside one epoch takes the plain form
           const int64_t kn = (it + 1) * KT;
-          if (kn + KT <= npk && kn + KT <= epoch_end(se)) dequant_tile(Full{}, it + 1);
-          else dequant_tile(Tail{}, it + 1);
-          if (it + 2 < ntile) prefetch(it + 2);
+          if (kn + KT <= npk && kn + KT <= epoch_end(se)) refill(p, it, Full{});
+          else refill(p, it, Tail{});
         }
+      };
+      int64_t it = t0;
+      for (; it + 1 < ntile; it += 2) {
+        gstep(it, P1);
+        gstep(it + 1, P0);
       }
+      if (it < ntile) gstep(it, P1);
       return;
     }
-    // tiles whose successor is all packed, then the rest: one dequant form per loop
-    const int64_t nf = nfull - 1 < ntile ? nfull - 1 : ntile;
+    // Steady state: the dequantised tile and the prefetched one (it + 3) are both
+    // all packed, so every load is issued unconditionally and the loads of one
+    // set stay in flight across the other set's dequantisation. The loop is
+    // compiled once per coefficient-load form.
+    const int64_t nsteady = (nfull < ntile ? nfull : ntile) - 3;  // it < nsteady: it + 3 < min(nfull, ntile)
     int64_t it = t0;
-    for (; it < nf; ++it) {
-      // buffer it&1 is complete and every consumer is done with buffer (it+1)&1
+    auto steady = [&](auto align_tag) __attribute__((always_inline)) {
+      for (; it + 1 < nsteady; it += 2) {
+        __syncthreads();
+        dequant_tile(P1, Full{}, it + 1);
+        load_raw(P1, Full{}, uint32_t((it + 3) * KT), align_tag);
+        __syncthreads();
+        dequant_tile(P0, Full{}, it + 2);
+        load_raw(P0, Full{}, uint32_t((it + 4) * KT), align_tag);
+      }
+    };
+    if (raligned) steady(std::true_type{});
+    else steady(std::false_type{});
+    // the last steps (it - t0 is even here) in the general form
+    for (; it < ntile; it += 2) {
       __syncthreads();
-      dequant_tile(Full{}, it + 1);
-      if (it + 2 < ntile) prefetch(it + 2);
-    }
-    for (; it < ntile; ++it) {
-      __syncthreads();
+      if (it + 1 < ntile) refill(P1, it, Tail{});
       if (it + 1 < ntile) {
-        dequant_tile(Tail{}, it + 1);
-        if (it + 2 < ntile) prefetch(it + 2);
+        __syncthreads();
+        if (it + 2 < ntile) refill(P0, it + 1, Tail{});
       }
     }
     return;
@@ -719,14 +811,14 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         if constexpr (MASKED) {
 #pragma unroll
           for (int i = 0; i < 16; ++i)
-            if (k0 + kb * 32 + acc_row(i, hf) >= lim) sv[i] = -__builtin_inff();
+            if (int(k0) + kb * 32 + acc_row(i, hf) >= lim) sv[i] = -__builtin_inff();
         }
       };
-      // raise m_run if the tile's max exceeds it by more than tau
-      auto raise_max = [&](const f32x16& sa, const f32x16& sb) {
+      // raise m_run if the max over these 32 keys exceeds it by more than tau
+      auto raise_max = [&](const f32x16& sv) {
         float mt = -__builtin_inff();
 #pragma unroll
-        for (int i = 0; i < 16; ++i) mt = max3f(mt, sa[i], sb[i]);
+        for (int i = 0; i < 8; ++i) mt = max3f(mt, sv[2 * i], sv[2 * i + 1]);
         mt = max_halves(mt);
         if (__any(mt > m_run + tau)) {
           const float m_new = fmaxf(m_run, mt);
@@ -778,15 +870,16 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         }
       };
 
-      f32x16 s0 = logits_half(0);
-      f32x16 s1 = logits_half(1);
-      mask_half(s0, 0);
-      mask_half(s1, 1);
-      raise_max(s0, s1);
-      probs(s0);
-      probs(s1);
-      pv_half(s0, 0);
-      pv_half(s1, 1);
+      // the tile's two halves of 32 keys in turn, so only one half's logits are
+      // live at a time
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        f32x16 sv = logits_half(kb);
+        mask_half(sv, kb);
+        raise_max(sv);
+        probs(sv);
+        pv_half(sv, kb);
+      }
     }
   };
   const int64_t nclean = kfull / KT < ntile ? kfull / KT : ntile;
