@@ -180,7 +180,9 @@ size_t quantwm_attend_workspace_bytes(const quantwm_config* cfg, int64_t n_cache
  * is only ever read in packed form. workspace: optional device scratch of
  * workspace_bytes, 256-byte aligned, owned by the caller and not read back (NULL,
  * or fewer bytes than quantwm_attend_workspace_bytes(), means no split). Calls
- * that share a workspace must be ordered on one stream. */
+ * that share a workspace must be ordered on one stream. QWM_ERR_UNSUPPORTED
+ * when n_q or the key count (n_cache, plus n_act for the active-chunk forms)
+ * exceeds 0x7fff0000 per head. */
 quantwm_status quantwm_attend(const quantwm_config* cfg, const void* calib, const void* cache,
                               int64_t n_cache, const void* q, int64_t n_q, int64_t q_start,
                               int32_t frame_tokens, void* out, float* lse_out, void* workspace,
