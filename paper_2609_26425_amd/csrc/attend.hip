@@ -264,15 +264,18 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   // calibration slab of this head in epoch e
   auto epoch_slab = [&](int e) { return a.calib + int64_t(e) * a.calib_stride + bh * a.slab; };
   // epoch of a (wave-uniform) key, and the first key past epoch e
-  auto epoch_at = [&](int64_t key) {
-    int e = 0;
+  // epoch of a key at or after the start of epoch e (epochs only advance with
+  // the key, so the search starts from the last one found)
+  auto epoch_from = [&](int e, int64_t key) {
     if constexpr (GEN)
       while (e + 1 < a.n_epochs && key >= a.epoch_start[e + 1]) ++e;
     return e;
   };
+  auto epoch_at = [&](int64_t key) { return epoch_from(0, key); };
   auto epoch_end = [&](int e) -> int64_t {
     return GEN && e + 1 < a.n_epochs ? a.epoch_start[e + 1] : (int64_t(1) << 62);
   };
+  auto epoch_begin = [&](int e) -> int64_t { return GEN ? a.epoch_start[e] : 0; };
   auto tab_of = [&](int e, int64_t off) { return reinterpret_cast<const T*>(epoch_slab(e) + off); };
   const CacheLayout& L = a.L;
   const uint8_t* cache = a.cache;
@@ -654,7 +657,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
           // the next tile opens another epoch: restage its tables (every producer
           // is done with the old ones after the barrier above), then sync
           if (it + 1 < ntile) {
-            const int en = epoch_at((it + 1) * KT);
+            const int en = epoch_from(se, (it + 1) * KT);
             if (en != se) {
               se = en;
               stage_tables(se, NC * 64, PT);
@@ -662,7 +665,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
             }
           }
         } else {
-          if (it + 1 < ntile) se = epoch_at((it + 1) * KT);
+          if (it + 1 < ntile) se = epoch_from(se, (it + 1) * KT);
         }
         if (it + 1 < ntile) {
           // a tile of packed keys inside one epoch takes the plain form
@@ -724,7 +727,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     if constexpr (GEN && TAB) {
       // mirror of the producers' restage of the centroid tables (one more barrier)
       if (it + 1 < ntile) {
-        const int en = epoch_at((it + 1) * KT);
+        const int en = epoch_from(se, (it + 1) * KT);
         if (en != se) {
           se = en;
           __syncthreads();
@@ -734,27 +737,21 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     const T* kt = smem + tile0 + int(it & 1) * LY::tile_elems;
     const T* ct = kt + KT * LY::KS;
     const T* vt = ct + KT * LY::CS;
-    // PSAC terms use q U_r of the key's epoch: the tile's first epoch e0 and,
-    // where the tile crosses into the next epoch at b1, that one too
-    V ureg2[RP > 0 ? RP / KSTEP : 1];
+    // PSAC terms use q U_r of the key's epoch (ureg holds that of epoch ue): the
+    // tile's first epoch here, and where a half crosses into the next epoch at
+    // b1, u is recomputed for it in the middle of that half's product
     int64_t b1 = int64_t(1) << 62;
-    bool cross = false;
     if constexpr (GEN && RP > 0) {
-      const int e0 = epoch_at(k0);
+      const int e0 = epoch_from(ue, k0);
       if (e0 != ue) {
         compute_u(e0, ureg);
         ue = e0;
       }
-      b1 = epoch_end(e0);
-      cross = b1 < k0 + KT && b1 < npk;
-      if (cross) compute_u(e0 + 1, ureg2);
+      b1 = epoch_end(e0) < npk ? epoch_end(e0) : (int64_t(1) << 62);
     }
 
     // logits S^T of the 32 keys k0 + 32 kb + row (rows x Queries) on matrix cores
-    auto logits_half = [&](int kb) {
-      f32x16 acc;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+    auto k_part = [&](f32x16 acc, int kb) __attribute__((always_inline)) {
       const T* krow = kt + (kb * 32 + l32) * LY::KS;
 #pragma unroll
       for (int st = 0; st < D / KSTEP; ++st) {
@@ -763,30 +760,50 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         else av = krow[st * KSTEP + hf];
         acc = MF::run(av, qreg[st], acc);
       }
+      return acc;
+    };
+    auto logits_half = [&](int kb) {
+      f32x16 acc;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
       if constexpr (RP > 0) {
         const T* crow = ct + (kb * 32 + l32) * LY::CS;
+        V av[RP / KSTEP];
 #pragma unroll
-        for (int st = 0; st < RP / KSTEP; ++st) {
-          V av;
+        for (int st = 0; st < RP / KSTEP; ++st)
 #pragma unroll
-          for (int j = 0; j < KPL; ++j) vset(av, j, crow[acc_row(st * KPL + j, hf)]);
-          if (GEN && cross) {
-            // this lane's A row is key k0 + 32 kb + l32: its chat goes with its epoch's u
-            const bool first = k0 + kb * 32 + l32 < b1;
+          for (int j = 0; j < KPL; ++j) vset(av[st], j, crow[acc_row(st * KPL + j, hf)]);
+        const int64_t h0 = k0 + kb * 32;
+        if (GEN && b1 >= h0 && b1 < h0 + 32) {
+          // the half crosses into the next epoch: this lane's A row is key
+          // h0 + l32, whose chat goes with its own epoch's u. u of the next
+          // epoch is computed first, while no accumulator is live, and the PSAC
+          // term goes in before q . khat_0
+          V un[RP > 0 ? RP / KSTEP : 1];
+          compute_u(ue + 1, un);
+          const bool first = h0 + l32 < b1;
+#pragma unroll
+          for (int st = 0; st < RP / KSTEP; ++st) {
             V a0, a1;
 #pragma unroll
             for (int j = 0; j < KPL; ++j) {
-              vset(a0, j, first ? vget(av, j) : T(0.0f));
-              vset(a1, j, first ? T(0.0f) : vget(av, j));
+              vset(a0, j, first ? vget(av[st], j) : T(0.0f));
+              vset(a1, j, first ? T(0.0f) : vget(av[st], j));
             }
             acc = MF::run(a0, ureg[st], acc);
-            acc = MF::run(a1, ureg2[st], acc);
-          } else {
-            acc = MF::run(av, ureg[st], acc);
+            acc = MF::run(a1, un[st], acc);
           }
+#pragma unroll
+          for (int st = 0; st < RP / KSTEP; ++st) ureg[st] = un[st];
+          ue = ue + 1;
+          return k_part(acc, kb);
         }
+        acc = k_part(acc, kb);
+#pragma unroll
+        for (int st = 0; st < RP / KSTEP; ++st) acc = MF::run(av[st], ureg[st], acc);
+        return acc;
       }
-      return acc;
+      return k_part(acc, kb);
     };
 
     if constexpr (LOGITS) {
