@@ -32,7 +32,12 @@ class OraCfg(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int), ("heads", ctypes.c_int), ("head_dim", ctypes.c_int),
                 ("n_centroids", ctypes.c_int), ("group_size", ctypes.c_int),
                 ("rank", ctypes.c_int), ("top_m", ctypes.c_int),
-                ("capacity", ctypes.c_longlong), ("table_bf16", ctypes.c_int)]
+                ("capacity", ctypes.c_longlong), ("table_bf16", ctypes.c_int), ("storage", ctypes.c_int)]
+
+
+# App. D.1 storage options (ORA_STORE_* in quantwm_oracle.h)
+STORE_SCALE_I8 = 1
+STORE_GATE = 2
 
 
 _lib = None
@@ -56,13 +61,14 @@ def lib():
     return _lib
 
 
-def cfg_of(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, bf16) -> OraCfg:
-    return OraCfg(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, int(bf16))
+def cfg_of(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, bf16, storage=0) -> OraCfg:
+    return OraCfg(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, int(bf16), int(storage))
 
 
 def cfg_from_workload(wl, capacity=None) -> OraCfg:
     return cfg_of(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank,
-                  wl.top_m, wl.capacity if capacity is None else capacity, wl.dtype == "bf16")
+                  wl.top_m, wl.capacity if capacity is None else capacity, wl.dtype == "bf16",
+                  getattr(wl, "storage", 0))
 
 
 def _p(a, ct=ctypes.c_float):
@@ -113,6 +119,36 @@ def f16_bits(x: float) -> int:
 
 def f16_value(bits: int) -> float:
     return lib().ora_f16_value(int(bits))
+
+
+def scales_i8(t):
+    """App. D.1 8-bit group scales of one token-head: (sigma FP16 bits, codes, steps)."""
+    t = _f32(t)
+    ng = t.shape[0]
+    codes = np.zeros(ng, np.uint8)
+    steps = np.zeros(ng, np.float32)
+    sig = ctypes.c_uint16(0)
+    lib().ora_scales_i8(_p(t), ng, ctypes.byref(sig), _p(codes, ctypes.c_uint8), _p(steps))
+    return int(sig.value), codes, steps
+
+
+def int2_quantise(x, mu, step):
+    """Eq. 1-2 and Eq. 4 of one group with a given (stored) step size."""
+    x, mu = _f32(x), _f32(mu)
+    n = x.shape[0]
+    codes = np.zeros(n, np.uint8)
+    xhat = np.zeros(n, np.float32)
+    zp = ctypes.c_uint8(0)
+    lib().ora_int2_quantise(_p(x), _p(mu), n, ctypes.c_float(step), _p(codes, ctypes.c_uint8),
+                            ctypes.byref(zp), _p(xhat))
+    return codes, int(zp.value), xhat
+
+
+def keep_row(C, codes, scale, lam):
+    """App. D.1 retention gate for one INT8 coefficient row."""
+    C, lam = _f32(C), _f32(lam)
+    codes = np.ascontiguousarray(codes, dtype=np.int8)
+    return bool(lib().ora_keep_row(_p(C), _p(codes, ctypes.c_int8), ctypes.c_float(scale), _p(lam), C.shape[0]))
 
 
 def int2_group(x, mu):
@@ -173,6 +209,7 @@ def new_cache(cfg: OraCfg) -> np.ndarray:
 def append(cfg: OraCfg, tables, cache, n_cached, k_new, v_new, diagnostics=False):
     """Writes slots [n_cached, n_cached + n) in place; returns diagnostics if asked."""
     mu_k, mu_v, w, u_t = (_f32(t) for t in tables[:4])
+    lam = _f32(tables[4]) if len(tables) > 4 and tables[4] is not None else None
     k_new, v_new = _f32(k_new), _f32(v_new)
     B, n, H = k_new.shape[0], k_new.shape[1], k_new.shape[2]
     M = min(cfg.top_m, cfg.n_centroids)
@@ -180,7 +217,7 @@ def append(cfg: OraCfg, tables, cache, n_cached, k_new, v_new, diagnostics=False
     kid = np.zeros((B, H, n), np.int32) if diagnostics else None
     vid = np.zeros((B, H, n), np.int32) if diagnostics else None
     cand = np.zeros((B, H, n, M), np.int32) if diagnostics else None
-    rc = lib().ora_append(ctypes.byref(cfg), _p(mu_k), _p(mu_v), _p(w), _p(u_t),
+    rc = lib().ora_append(ctypes.byref(cfg), _p(mu_k), _p(mu_v), _p(w), _p(u_t), _p(lam),
                           _p(cache, ctypes.c_uint8), ctypes.c_longlong(n_cached),
                           _p(k_new), _p(v_new), ctypes.c_longlong(n), _p(coef),
                           _p(kid, ctypes.c_int), _p(vid, ctypes.c_int), _p(cand, ctypes.c_int))

@@ -84,8 +84,11 @@ typedef struct {
   int d, ng, zpb, r;
   int k_bytes, v_bytes;
   long long slots; /* capacity rounded up to 64 */
+  int i8;            /* ORA_STORE_SCALE_I8 */
+  int sb;            /* group-scale bytes per token: 2 ng (FP16) or ng (8-bit codes) */
   long long k_codes, k_ids, k_zp, k_scale, k_coef, k_cscale;
   long long v_codes, v_ids, v_zp, v_scale;
+  long long k_sigma, v_sigma; /* SCALE_I8: the FP16 secondary scale per token */
   long long total;
 } layout;
 
@@ -97,6 +100,7 @@ static int valid_cfg(const ora_cfg* c) {
   if (c->n_centroids < 1 || c->n_centroids > 256) return 0;
   if (c->rank < 0 || c->rank > c->head_dim) return 0;
   if (c->top_m < 1 || c->capacity < 0) return 0;
+  if (c->storage & ~(ORA_STORE_SCALE_I8 | ORA_STORE_GATE)) return 0;
   return 1;
 }
 
@@ -107,22 +111,26 @@ static layout make_layout(const ora_cfg* c) {
   L.zpb = (L.ng + 3) / 4;
   L.r = c->rank;
   L.slots = (c->capacity + 63) / 64 * 64;
+  L.i8 = (c->storage & ORA_STORE_SCALE_I8) != 0;
+  L.sb = L.i8 ? L.ng : 2 * L.ng;
   long long bh = (long long)c->batch * c->heads, n = bh * L.slots, off = 0;
 #define SECTION(field, per_token) \
   do { L.field = off; off = up256(off + n * (long long)(per_token)); } while (0)
   SECTION(k_codes, L.d / 4);
   SECTION(k_ids, 1);
   SECTION(k_zp, L.zpb);
-  SECTION(k_scale, 2 * L.ng);
+  SECTION(k_scale, L.sb);
   SECTION(k_coef, L.r);
   SECTION(k_cscale, L.r > 0 ? 2 : 0);
   SECTION(v_codes, L.d / 4);
   SECTION(v_ids, 1);
   SECTION(v_zp, L.zpb);
-  SECTION(v_scale, 2 * L.ng);
+  SECTION(v_scale, L.sb);
+  SECTION(k_sigma, L.i8 ? 2 : 0);
+  SECTION(v_sigma, L.i8 ? 2 : 0);
 #undef SECTION
   L.total = off;
-  L.v_bytes = L.d / 4 + 1 + L.zpb + 2 * L.ng;
+  L.v_bytes = L.d / 4 + 1 + L.zpb + L.sb + (L.i8 ? 2 : 0);
   L.k_bytes = L.v_bytes + (L.r > 0 ? L.r + 2 : 0);
   return L;
 }
@@ -147,31 +155,73 @@ static uint16_t get16(const uint8_t* p) { return (uint16_t)(p[0] | (p[1] << 8));
 
 static float clampf(float x, float lo, float hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
+/* Eq. 2 step size of one group: the residual range extended to contain 0, over
+ * the 2^2 - 1 = 3 steps of q_min = 0 .. q_max = 3 (fp32). */
+static float group_step(const float* x, const float* mu, int n, float* lo_out) {
+  float lo = 0.0f, hi = 0.0f;
+  for (int c = 0; c < n; ++c) {
+    float r = x[c] - mu[c];
+    if (r < lo) lo = r;
+    if (r > hi) hi = r;
+  }
+  *lo_out = lo;
+  return (hi - lo) / 3.0f;
+}
+
+void ora_int2_quantise(const float* x, const float* mu, int n, float step, uint8_t* codes,
+                       uint8_t* zero_point, float* xhat) {
+  /* Eq. 3 residual; Eq. 1-2 with the stored step; Eq. 4 reconstruction */
+  float lo = 0.0f;
+  (void)group_step(x, mu, n, &lo);
+  int z = 0;
+  if (step != 0.0f) z = (int)clampf(rintf(0.0f - lo / step), 0.0f, 3.0f);
+  *zero_point = (uint8_t)z;
+  for (int c = 0; c < n; ++c) {
+    float r = x[c] - mu[c];
+    int q = 0;
+    if (step != 0.0f) q = (int)clampf(rintf(r / step) + (float)z, 0.0f, 3.0f); /* Eq. 1 */
+    codes[c] = (uint8_t)q;
+    xhat[c] = mu[c] + step * (float)(q - z); /* Eq. 4: centroid + dequantised residual */
+  }
+}
+
 void ora_int2_group(const float* x, const float* mu, int n, uint8_t* codes,
                     uint8_t* zero_point, uint16_t* scale_f16, float* xhat) {
-  /* Eq. 3: residual against the assigned centroid. */
-  float r[256];
-  float lo = 0.0f, hi = 0.0f; /* range extended to contain 0 */
-  for (int c = 0; c < n; ++c) {
-    r[c] = x[c] - mu[c];
-    if (r[c] < lo) lo = r[c];
-    if (r[c] > hi) hi = r[c];
-  }
-  /* Eq. 2 with q_min = 0, q_max = 2^2 - 1 = 3; the scale is stored as FP16. */
-  float s = (hi - lo) / 3.0f;
+  /* the step size stored as FP16 (saturating), then the quantiser with it */
+  float lo;
+  float s = group_step(x, mu, n, &lo);
   if (s > 65504.0f) s = 65504.0f;
   double sh = ora_round_f16((double)s);
   *scale_f16 = ora_f16_bits(sh);
-  float shf = (float)sh;
-  int z = 0;
-  if (shf != 0.0f) z = (int)clampf(rintf(0.0f - lo / shf), 0.0f, 3.0f);
-  *zero_point = (uint8_t)z;
-  for (int c = 0; c < n; ++c) {
-    int q = 0;
-    if (shf != 0.0f) q = (int)clampf(rintf(r[c] / shf) + (float)z, 0.0f, 3.0f); /* Eq. 1 */
-    codes[c] = (uint8_t)q;
-    xhat[c] = mu[c] + shf * (float)(q - z); /* Eq. 4: centroid + dequantised residual */
+  ora_int2_quantise(x, mu, n, (float)sh, codes, zero_point, xhat);
+}
+
+void ora_scales_i8(const float* t, int ng, uint16_t* sigma_f16, uint8_t* codes, float* step_out) {
+  /* App. D.1: 8-bit codes with one FP16 secondary scale; the largest step sets
+   * the secondary scale, sigma = FP16(max_g t_g / 255), and c_g = RN(t_g / sigma) */
+  float mx = 0.0f;
+  for (int g = 0; g < ng; ++g)
+    if (t[g] > mx) mx = t[g];
+  float sg = mx / 255.0f;
+  if (sg > 65504.0f) sg = 65504.0f;
+  double sh = ora_round_f16((double)sg);
+  *sigma_f16 = ora_f16_bits(sh);
+  float sf = (float)sh;
+  for (int g = 0; g < ng; ++g) {
+    int c = sf != 0.0f ? (int)clampf(rintf(t[g] / sf), 0.0f, 255.0f) : 0;
+    codes[g] = (uint8_t)c;
+    step_out[g] = sf * (float)c; /* exact: 11-bit times 8-bit significands */
   }
+}
+
+int ora_keep_row(const float* C, const int8_t* codes, float scale, const float* lam, int r) {
+  float before = 0.0f, after = 0.0f;
+  for (int k = 0; k < r; ++k) {
+    float e = C[k] - (float)codes[k] * scale;
+    before = before + lam[k] * (C[k] * C[k]);
+    after = after + lam[k] * (e * e);
+  }
+  return after < before;
 }
 
 /* ------------------------------------------------------------ QSAC (O2) */
@@ -411,29 +461,46 @@ static void put_codes(uint8_t* dst, const uint8_t* q, int d) {
     dst[i] = (uint8_t)(q[4 * i] | (q[4 * i + 1] << 2) | (q[4 * i + 2] << 4) | (q[4 * i + 3] << 6));
 }
 
-/* One token: centroid + per-group INT2 residual, written at slot pointers. */
+/* One token: centroid + per-group INT2 residual, written at slot pointers. With
+ * SCALE_I8 all group steps are found first: they share the secondary scale. */
 static void store_residual(const layout* L, int G, const float* x, const float* mu_z,
-                           uint8_t* codes_dst, uint8_t* zp_dst, uint8_t* scale_dst, float* xhat) {
+                           uint8_t* codes_dst, uint8_t* zp_dst, uint8_t* scale_dst, uint8_t* sigma_dst,
+                           float* xhat) {
   uint8_t q[256];
   memset(zp_dst, 0, (size_t)L->zpb);
-  for (int g = 0; g < L->ng; ++g) {
-    uint8_t zg;
-    uint16_t sg;
-    ora_int2_group(x + g * G, mu_z + g * G, G, q + g * G, &zg, &sg, xhat + g * G);
-    zp_dst[g / 4] |= (uint8_t)(zg << (2 * (g % 4)));
-    put16(scale_dst + 2 * g, sg);
+  if (L->i8) {
+    float t[256], step[256], lo;
+    uint16_t sigma;
+    for (int g = 0; g < L->ng; ++g) t[g] = group_step(x + g * G, mu_z + g * G, G, &lo);
+    ora_scales_i8(t, L->ng, &sigma, scale_dst, step);
+    put16(sigma_dst, sigma);
+    for (int g = 0; g < L->ng; ++g) {
+      uint8_t zg;
+      ora_int2_quantise(x + g * G, mu_z + g * G, G, step[g], q + g * G, &zg, xhat + g * G);
+      zp_dst[g / 4] |= (uint8_t)(zg << (2 * (g % 4)));
+    }
+  } else {
+    for (int g = 0; g < L->ng; ++g) {
+      uint8_t zg;
+      uint16_t sg;
+      ora_int2_group(x + g * G, mu_z + g * G, G, q + g * G, &zg, &sg, xhat + g * G);
+      zp_dst[g / 4] |= (uint8_t)(zg << (2 * (g % 4)));
+      put16(scale_dst + 2 * g, sg);
+    }
   }
   put_codes(codes_dst, q, L->d);
 }
 
 int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const float* w,
-               const float* u_t, uint8_t* cache, long long n_cached,
+               const float* u_t, const float* lam, uint8_t* cache, long long n_cached,
                const float* k_new, const float* v_new, long long n_new,
                float* coef_f32, int* k_ids, int* v_ids, int* cand) {
   if (!valid_cfg(cfg) || n_cached < 0 || n_new < 0) return -1;
   if (n_cached + n_new > cfg->capacity) return -3;
   if (n_new == 0) return 0;
   if (!mu_k || !mu_v || !w || !cache || !k_new || !v_new || (cfg->rank > 0 && !u_t)) return -1;
+  const int gate = (cfg->storage & ORA_STORE_GATE) && cfg->rank > 0;
+  if (gate && !lam) return -1;
   const layout L = make_layout(cfg);
   const int d = cfg->head_dim, H = cfg->heads, K = cfg->n_centroids, r = cfg->rank, G = cfg->group_size;
   const int M = cfg->top_m < K ? cfg->top_m : K;
@@ -457,7 +524,8 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
       int z = ora_qsac_assign(k, muk, wh, K, d, G, M, cands);
       cache[L.k_ids + slot] = (uint8_t)z;
       store_residual(&L, G, k, muk + (long long)z * d, cache + L.k_codes + slot * (d / 4),
-                     cache + L.k_zp + slot * L.zpb, cache + L.k_scale + slot * 2 * L.ng, xhat);
+                     cache + L.k_zp + slot * L.zpb, cache + L.k_scale + slot * L.sb, cache + L.k_sigma + slot * 2,
+                     xhat);
       if (k_ids) k_ids[diag] = z;
       if (cand) for (int m = 0; m < M; ++m) cand[diag * M + m] = cands[m];
       if (r > 0) {
@@ -478,13 +546,19 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
         int8_t* code = (int8_t*)(cache + L.k_coef + slot * r);
         for (int kk = 0; kk < r; ++kk)
           code[kk] = (int8_t)(shf != 0.0f ? (int)clampf(rintf(Cf[kk] / shf), -127.0f, 127.0f) : 0);
+        /* App. D.1 retention: a row that does not lower the error is zeroed */
+        if (gate && !ora_keep_row(Cf, code, shf, lam + (long long)bh * r, r)) {
+          memset(code, 0, (size_t)r);
+          sh = 0.0;
+        }
         put16(cache + L.k_cscale + slot * 2, ora_f16_bits(sh));
       }
       /* Values: nearest centroid, same residual path, no PSAC */
       int zv = ora_nearest(v, muv, K, d);
       cache[L.v_ids + slot] = (uint8_t)zv;
       store_residual(&L, G, v, muv + (long long)zv * d, cache + L.v_codes + slot * (d / 4),
-                     cache + L.v_zp + slot * L.zpb, cache + L.v_scale + slot * 2 * L.ng, xhat);
+                     cache + L.v_zp + slot * L.zpb, cache + L.v_scale + slot * L.sb, cache + L.v_sigma + slot * 2,
+                     xhat);
       if (v_ids) v_ids[diag] = zv;
     }
   }
@@ -494,12 +568,13 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
 /* ------------------------------------------------------------- decode */
 
 static void load_residual(const layout* L, int G, const uint8_t* codes, const uint8_t* zp,
-                          const uint8_t* scale, const float* mu_z, double* out) {
+                          const uint8_t* scale, const uint8_t* sigma, const float* mu_z, double* out) {
   for (int c = 0; c < L->d; ++c) {
     int g = c / G;
     int q = (codes[c / 4] >> (2 * (c % 4))) & 3;
     int z = (zp[g / 4] >> (2 * (g % 4))) & 3;
-    float s = (float)ora_f16_value(get16(scale + 2 * g));
+    float s = L->i8 ? (float)ora_f16_value(get16(sigma)) * (float)scale[g]
+                    : (float)ora_f16_value(get16(scale + 2 * g));
     out[c] = (double)(mu_z[c] + s * (float)(q - z)); /* Eq. 4, fp32 as when encoding */
   }
 }
@@ -518,10 +593,12 @@ int ora_decode(const ora_cfg* cfg, const float* mu_k, const float* mu_v,
     if (zk >= K || zv >= K) return -4;
     if (k0)
       load_residual(&L, G, cache + L.k_codes + slot * (d / 4), cache + L.k_zp + slot * L.zpb,
-                    cache + L.k_scale + slot * 2 * L.ng, mu_k + (bh * K + zk) * d, k0 + t * d);
+                    cache + L.k_scale + slot * L.sb, cache + L.k_sigma + slot * 2, mu_k + (bh * K + zk) * d,
+                    k0 + t * d);
     if (v)
       load_residual(&L, G, cache + L.v_codes + slot * (d / 4), cache + L.v_zp + slot * L.zpb,
-                    cache + L.v_scale + slot * 2 * L.ng, mu_v + (bh * K + zv) * d, v + t * d);
+                    cache + L.v_scale + slot * L.sb, cache + L.v_sigma + slot * 2, mu_v + (bh * K + zv) * d,
+                    v + t * d);
     if (chat && r > 0) {
       float s = (float)ora_f16_value(get16(cache + L.k_cscale + slot * 2));
       const int8_t* code = (const int8_t*)(cache + L.k_coef + slot * r);

@@ -38,7 +38,17 @@ typedef struct {
   int top_m;                   /* M: QSAC candidate count (Sec. 4.1) */
   long long capacity;          /* cache slots per (b, h) */
   int table_bf16;              /* 1: centroids, U_r and attention operands are BF16 */
+  int storage;                 /* ORA_STORE_* flags (App. D.1 packed-storage options) */
 } ora_cfg;
+
+/* App. D.1 storage options. SCALE_I8: the group step sizes of a token-head are
+ * stored as 8-bit codes c_g in [0, 255] with one FP16 secondary scale sigma shared
+ * by the token-head's groups; the step is sigma * c_g. GATE: a PSAC row is kept
+ * only when it lowers the Query-weighted error approximated on the principal
+ * subspace (sum_k lam_k C_k^2 before, sum_k lam_k (C_k - chat_k)^2 after);
+ * otherwise its codes and scale are zero. */
+#define ORA_STORE_SCALE_I8 1
+#define ORA_STORE_GATE 2
 
 /* Packed cache size in bytes and the per-token-head byte counts (K and V). */
 long long ora_cache_bytes(const ora_cfg* cfg);
@@ -53,6 +63,19 @@ double ora_f16_value(uint16_t bits);
 /* Eq. 1-2 with b = 2 on one residual group, plus Eq. 4 reconstruction. */
 void ora_int2_group(const float* x, const float* mu, int n, uint8_t* codes,
                     uint8_t* zero_point, uint16_t* scale_f16, float* xhat);
+
+/* The same with the step size given (the stored scale): Eq. 1-2 codes and
+ * zero-point for the group's residual range, Eq. 4 reconstruction. */
+void ora_int2_quantise(const float* x, const float* mu, int n, float step, uint8_t* codes,
+                       uint8_t* zero_point, float* xhat);
+
+/* SCALE_I8: the fp32 step sizes t[0..ng) of one token-head -> FP16 secondary
+ * scale (bits) and 8-bit codes; step_out[g] = sigma * c_g. */
+void ora_scales_i8(const float* t, int ng, uint16_t* sigma_f16, uint8_t* codes, float* step_out);
+
+/* GATE: 1 when the INT8 row chat (codes * scale) lowers the lam-weighted error
+ * of the coefficients C, else 0. fp32, ranks in order. */
+int ora_keep_row(const float* C, const int8_t* codes, float scale, const float* lam, int r);
 
 /* Eq. 9-12 on one Key token. cand receives the top-M ids in (d_Q, id) order. */
 int ora_qsac_assign(const float* k, const float* mu, const float* w, int n_centroids,
@@ -73,9 +96,10 @@ int ora_eigh(const double* a, int n, double* lam, double* vecs_t);
 /* QSAC + INT2 residual + PSAC for Keys, nearest centroid + INT2 for Values,
  * written into cache slots [n_cached, n_cached + n_new) of every (b, h).
  * coef_f32 [B,H,n_new,r], k_ids/v_ids [B,H,n_new] and cand [B,H,n_new,M] are
- * optional diagnostics (NULL to skip). */
+ * optional diagnostics (NULL to skip). lam [B,H,r] (the stored eigenvalues) is
+ * read only with ORA_STORE_GATE. */
 int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const float* w,
-               const float* u_t, uint8_t* cache, long long n_cached,
+               const float* u_t, const float* lam, uint8_t* cache, long long n_cached,
                const float* k_new, const float* v_new, long long n_new,
                float* coef_f32, int* k_ids, int* v_ids, int* cand);
 

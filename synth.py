@@ -55,6 +55,7 @@ class Workload:
     chunk: int            # tokens per append call
     seed: int
     kmeans_iters: int = 10
+    storage: int = 0      # App. D.1 storage options: 1 = 8-bit group scales, 2 = retention gate
 
     @property
     def capacity(self) -> int:

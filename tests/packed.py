@@ -9,20 +9,24 @@ def _up256(x):
     return (x + 255) // 256 * 256
 
 
-def layout(batch, heads, d, G, r, capacity):
+def layout(batch, heads, d, G, r, capacity, storage=0):
+    """storage bit 0: group scales as 8-bit codes plus an FP16 secondary scale
+    per token (sections k_sigma / v_sigma at the end)."""
     ng = d // G
     zpb = (ng + 3) // 4
     slots = (capacity + 63) // 64 * 64
     rows = batch * heads * slots
-    per = [("k_codes", d // 4), ("k_ids", 1), ("k_zp", zpb), ("k_scale", 2 * ng), ("k_coef", r),
+    i8 = bool(storage & 1)
+    sb = ng if i8 else 2 * ng
+    per = [("k_codes", d // 4), ("k_ids", 1), ("k_zp", zpb), ("k_scale", sb), ("k_coef", r),
            ("k_cscale", 2 if r > 0 else 0), ("v_codes", d // 4), ("v_ids", 1), ("v_zp", zpb),
-           ("v_scale", 2 * ng)]
+           ("v_scale", sb), ("k_sigma", 2 if i8 else 0), ("v_sigma", 2 if i8 else 0)]
     off, at = {}, 0
     for name, nbytes in per:
         off[name] = (at, nbytes)
         at = _up256(at + rows * nbytes)
     return {"off": off, "slots": slots, "total": at, "ng": ng, "zpb": zpb, "d": d, "r": r,
-            "bh": batch * heads}
+            "bh": batch * heads, "i8": i8}
 
 
 def fields(buf: np.ndarray, lay, bh: int, t0: int, t1: int):
@@ -44,7 +48,11 @@ def fields(buf: np.ndarray, lay, bh: int, t0: int, t1: int):
         zp = out[f"{p}_zp"].astype(np.uint32)
         zw = sum(zp[:, i] << (8 * i) for i in range(zp.shape[1]))
         res[f"{p}_zp"] = np.stack([(zw >> (2 * g)) & 3 for g in range(ng)], -1)
-        res[f"{p}_scale"] = np.ascontiguousarray(out[f"{p}_scale"]).view(np.uint16).reshape(t1 - t0, ng)
+        if lay.get("i8"):
+            res[f"{p}_scale"] = np.ascontiguousarray(out[f"{p}_scale"]).reshape(t1 - t0, ng)
+            res[f"{p}_sigma"] = np.ascontiguousarray(out[f"{p}_sigma"]).view(np.uint16)[:, 0]
+        else:
+            res[f"{p}_scale"] = np.ascontiguousarray(out[f"{p}_scale"]).view(np.uint16).reshape(t1 - t0, ng)
     if r > 0:
         res["k_coef"] = np.ascontiguousarray(out["k_coef"]).view(np.int8)
         res["k_cscale"] = np.ascontiguousarray(out["k_cscale"]).view(np.uint16)[:, 0]

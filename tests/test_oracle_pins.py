@@ -470,6 +470,162 @@ def test_token_bytes_and_paper_compression():
         assert oracle.token_bytes(oracle.cfg_of(1, 1, d, 16, G, r, 4, 64, True)) == want
 
 
+def test_token_bytes_with_8bit_group_scales():
+    # App. D.1: group scales as 8-bit codes plus one FP16 secondary scale per
+    # token-head, so ng group scales take ng + 2 bytes instead of 2 ng.
+    for d, G, r in [(128, 32, 16), (128, 64, 8), (128, 16, 0), (64, 32, 4)]:
+        ng = d // G
+        cfg = oracle.cfg_of(1, 1, d, 16, G, r, 4, 64, True, oracle.STORE_SCALE_I8)
+        v = d // 4 + 1 + (ng + 3) // 4 + ng + 2
+        assert oracle.token_bytes(cfg) == (v + (r + 2 if r else 0), v)
+
+
+# ------------------------------------- App. D.1 storage refinements (NEXT f3)
+
+def test_scales_i8_hand_example():
+    # t = (0.3, 0.15, 0, 1.2): sigma = FP16(1.2 / 255) = FP16(0.0047059) =
+    # 1234 * 2^-18 (binary16 0x1CD2; 1233.6 units of 2^-18 round up), and
+    # c = RN(t / sigma) = RN(63.73, 31.87, 0, 254.92) = (64, 32, 0, 255).
+    t = np.array([0.3, 0.15, 0.0, 1.2], np.float32)
+    sig, codes, steps = oracle.scales_i8(t)
+    assert sig == 0x1CD2
+    assert list(codes) == [64, 32, 0, 255]
+    sigma = 1234.0 * 2.0 ** -18
+    np.testing.assert_array_equal(steps.astype(np.float64), sigma * np.array([64, 32, 0, 255]))
+
+
+def test_scales_i8_invariants():
+    # For any steps: the largest gets code 255 (sigma is max / 255 within FP16
+    # rounding), every decoded step lies within sigma / 2 of its step, zero steps
+    # get code 0, and scaling all steps by 2^k scales sigma by 2^k and leaves the
+    # codes unchanged (binary rounding commutes with powers of two while sigma
+    # stays a normal binary16 number, as it does for these ranges).
+    r = rng(21)
+    for _ in range(500):
+        ng = int(r.choice([1, 2, 4, 8]))
+        t = (10.0 ** r.uniform(-1, 1.5, ng)).astype(np.float32)
+        t[r.random(ng) < 0.2] = 0.0
+        sig, codes, steps = oracle.scales_i8(t)
+        if not t.any():
+            assert sig == 0 and not codes.any()
+            continue
+        sigma = float(np.uint16(sig).view(np.float16))
+        assert codes[np.argmax(t)] == 255
+        assert np.all(np.abs(steps.astype(np.float64) - t) <= sigma / 2 * (1 + 1e-6))
+        assert np.all(codes[t == 0] == 0)
+        k = int(r.integers(-2, 4))
+        sig2, codes2, _ = oracle.scales_i8((t * np.float32(2.0 ** k)).astype(np.float32))
+        assert float(np.uint16(sig2).view(np.float16)) == sigma * 2.0 ** k
+        np.testing.assert_array_equal(codes2, codes)
+    sig, codes, steps = oracle.scales_i8(np.zeros(4, np.float32))
+    assert sig == 0 and not codes.any() and not steps.any()
+
+
+def test_int2_quantise_with_the_fp16_step_is_the_group_quantiser():
+    # Eq. 1-2 with the stored step: given the FP16 step, the quantiser with a
+    # given step reproduces the pinned FP16 group quantiser bit for bit.
+    r = rng(22)
+    for _ in range(200):
+        n = int(r.choice([16, 32, 64]))
+        mu = synth.round_to(r.standard_normal(n), "bf16")
+        x = synth.round_to(mu + r.standard_normal(n) * 10.0 ** r.uniform(-3, 1), "bf16")
+        codes, zp, sc, xhat = oracle.int2_group(x, mu)
+        step = float(np.uint16(sc).view(np.float16))
+        c2, z2, x2 = oracle.int2_quantise(x, mu, step)
+        assert z2 == zp
+        np.testing.assert_array_equal(c2, codes)
+        np.testing.assert_array_equal(x2, xhat)
+
+
+def test_keep_row_cases():
+    # App. D.1 retention: keep a row only when sum lam (C - chat)^2 < sum lam C^2.
+    lam = np.array([2.0, 1.0], np.float32)
+    # exact codes: no error left
+    assert oracle.keep_row(np.array([1.0, -0.5], np.float32), np.array([2, -1]), 0.5, lam)
+    # hand example: codes (1, -1) at scale 1 leave 1 * (0.5)^2 = 0.25 < 2 + 0.25
+    assert oracle.keep_row(np.array([1.0, -0.5], np.float32), np.array([1, -1]), 1.0, lam)
+    # a zero row, or zero eigenvalues, never lowers the error
+    assert not oracle.keep_row(np.zeros(2, np.float32), np.zeros(2), 1.0, lam)
+    assert not oracle.keep_row(np.array([1.0, -0.5], np.float32), np.array([2, -1]), 0.5, np.zeros(2, np.float32))
+    # the wrong sign doubles the error: 2 * (1 + 1)^2 + (0.5 + 0.5)^2 > 2.25
+    assert not oracle.keep_row(np.array([1.0, -0.5], np.float32), np.array([-1, 1]), 1.0, lam)
+    # the eigenvalues weight the ranks: moving error from a heavy rank to a light
+    # one helps (10 -> 1), the other way round it hurts (1 -> 10)
+    C = np.array([1.0, 0.0], np.float32)
+    assert oracle.keep_row(C, np.array([1, 1]), 1.0, np.array([10.0, 1.0], np.float32))
+    assert not oracle.keep_row(C, np.array([1, 1]), 1.0, np.array([1.0, 10.0], np.float32))
+
+
+def test_append_8bit_scales_decode_within_half_a_step():
+    # Eq. 1-4 with the App. D.1 8-bit scales: the packed fields decode to steps
+    # sigma * c_g, every code picks the nearest level of its group's grid, and the
+    # decoded Key is within half a step of the input (plus fp32 rounding).
+    import packed
+    wl = _small_workload(rank=4, storage=oracle.STORE_SCALE_I8)
+    cfg, tables, cache, k, v, q, _ = _encoded(wl)
+    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.capacity, wl.storage)
+    assert lay["total"] == oracle.cache_bytes(cfg)
+    G, ng = wl.group_size, wl.head_dim // wl.group_size
+    for h in range(wl.heads):
+        f = packed.fields(cache, lay, h, 0, wl.n_cache)
+        k0, _, vh = oracle.decode(cfg, tables, cache, 0, h, wl.n_cache)
+        for name, x, xhat, mu_t in (("k", k[0, :, h], k0, tables[0][0, h]), ("v", v[0, :, h], vh, tables[1][0, h])):
+            sigma = f[f"{name}_sigma"].view(np.float16).astype(np.float64)
+            steps = sigma[:, None] * f[f"{name}_scale"].astype(np.float64)
+            mu = mu_t[f[f"{name}_ids"]].astype(np.float64)
+            res = x.astype(np.float64) - mu
+            for g in range(ng):
+                sl = slice(g * G, (g + 1) * G)
+                levels = steps[:, g, None, None] * (np.arange(4)[None, None, :] - f[f"{name}_zp"][:, g, None, None])
+                dist = np.abs(res[:, sl, None] - levels)
+                chosen = np.take_along_axis(dist, f[f"{name}_codes"][:, sl, None], axis=2)[..., 0]
+                assert np.all(chosen <= dist.min(axis=2) + 1e-5 * steps[:, g, None] + 1e-30)
+            # Eq. 2 step of each group (range extended to contain 0); a decoded step
+            # below it can clip the group's ends by up to 3 |t - step|
+            rg = res.reshape(len(res), ng, G)
+            t = (np.maximum(rg.max(axis=2), 0) - np.minimum(rg.min(axis=2), 0)) / 3
+            err = np.abs(xhat - x.astype(np.float64))
+            bound = np.repeat(steps / 2 + 3 * np.abs(t - steps), G, axis=1) + 1e-6 * np.abs(x) + 1e-30
+            assert np.all(err <= bound)
+
+
+def test_append_gate_follows_the_keep_rule():
+    # App. D.1 retention with the stored eigenvalues: a row is stored as written
+    # without the gate exactly when the rule keeps it, else as zeros; with all
+    # eigenvalues 0 every row is zeroed.
+    import packed
+    base = _small_workload(rank=4)
+    gated = synth.scaled(base, storage=oracle.STORE_GATE)
+    cfg0, tables, cache0, k, v, q, diag = _encoded(base)
+    cfg1 = oracle.cfg_from_workload(gated)
+    cache1 = oracle.new_cache(cfg1)
+    oracle.append(cfg1, tables, cache1, 0, k, v)
+    lay = packed.layout(base.batch, base.heads, base.head_dim, base.group_size, base.rank, base.capacity)
+    kept = total = 0
+    for h in range(base.heads):
+        f0 = packed.fields(cache0, lay, h, 0, base.n_cache)
+        f1 = packed.fields(cache1, lay, h, 0, base.n_cache)
+        for t in range(base.n_cache):
+            s0 = float(np.uint16(f0["k_cscale"][t]).view(np.float16))
+            keep = oracle.keep_row(diag["coef"][0, h, t], f0["k_coef"][t], s0, tables[4][0, h])
+            total += 1
+            if keep:
+                kept += 1
+                np.testing.assert_array_equal(f1["k_coef"][t], f0["k_coef"][t])
+                assert f1["k_cscale"][t] == f0["k_cscale"][t]
+            else:
+                assert not f1["k_coef"][t].any() and f1["k_cscale"][t] == 0
+        for name in ("k_codes", "k_ids", "k_zp", "k_scale", "v_codes", "v_ids", "v_zp", "v_scale"):
+            np.testing.assert_array_equal(f1[name], f0[name])
+    assert kept > 0.9 * total
+    zero_lam = tables[:4] + (np.zeros_like(tables[4]),)
+    cache2 = oracle.new_cache(cfg1)
+    oracle.append(cfg1, zero_lam, cache2, 0, k, v)
+    for h in range(base.heads):
+        f2 = packed.fields(cache2, lay, h, 0, base.n_cache)
+        assert not f2["k_coef"].any() and not f2["k_cscale"].any()
+
+
 # ------------------------------------------------- BF16 active chunk (NEXT f2)
 
 def test_active_chunk_alone_is_plain_attention():
