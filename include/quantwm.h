@@ -53,7 +53,22 @@ typedef struct {
   int32_t top_m;       /* M: QSAC candidates in [1, 8] (Sec. 4.1; the paper uses 4) */
   int32_t dtype;       /* quantwm_dtype of Q/K/V/O, centroids and U_r */
   int64_t capacity;    /* cache slots per (b, h), at most 2^26 */
+  int32_t storage;     /* QWM_STORE_* flags, 0 for the plain format (App. D.1 options) */
 } quantwm_config;
+
+/* Packed-storage options of App. D.1 (flags of quantwm_config.storage).
+ * QWM_STORE_SCALE_I8: the Eq. 2 step sizes t_g of a token-head's groups are kept
+ *   as 8-bit codes c_g = RN(t_g / sigma) in [0, 255] with one binary16 secondary
+ *   scale sigma = RN16(max_g t_g / 255) per token-head; the step is sigma * c_g
+ *   (exact in fp32), and the residual is quantised with it.
+ * QWM_STORE_GATE: a PSAC row is kept only when its INT8 codes lower the
+ *   Query-weighted error approximated on the principal subspace,
+ *   sum_k lam_k (C_k - code_k * cscale)^2 < sum_k lam_k C_k^2 (fp32, ranks in
+ *   order, lam from the calibration block); otherwise the row and its scale are
+ *   stored as zeros. The attention calls do not take SCALE_I8 together with an
+ *   active chunk or calibration epochs (QWM_ERR_UNSUPPORTED). */
+#define QWM_STORE_SCALE_I8 1
+#define QWM_STORE_GATE 2
 
 /* ------------------------------------------------------------------ sizes */
 
@@ -64,11 +79,15 @@ typedef struct {
  *   K ids      1 byte: centroid id (uint8)
  *   K zp       ceil(d/G/4) bytes: group g in bits 2(g%4) of byte g/4 (INT2 zero-points)
  *   K scale    2*d/G bytes: IEEE binary16 group scales, little-endian
+ *              (with QWM_STORE_SCALE_I8: d/G bytes, the 8-bit codes c_g)
  *   K coef     r bytes: INT8 PSAC coefficients
  *   K cscale   2 bytes (0 if r = 0): binary16 row scale of the coefficients
  *   V codes, V ids, V zp, V scale: as for K (Values carry no PSAC row).
- * A token's reconstruction is centroid + scale * (code - zero_point) (Eq. 4)
- * and its coefficients are code * cscale (Eq. 16, App. D.1). */
+ *   K sigma, V sigma  2 bytes each, only with QWM_STORE_SCALE_I8: the binary16
+ *              secondary scale of the token-head's group scales.
+ * A token's reconstruction is centroid + scale * (code - zero_point) (Eq. 4),
+ * with scale = sigma * c_g under QWM_STORE_SCALE_I8, and its coefficients are
+ * code * cscale (Eq. 16, App. D.1). */
 size_t quantwm_cache_bytes(const quantwm_config* cfg);
 
 /* Packed bytes per token-head for Keys and Values. Returns a status. */

@@ -59,6 +59,8 @@ quantwm_status check_cfg(const quantwm_config* c) {
   if (c->top_m > 8) return fail(QWM_ERR_UNSUPPORTED, "top_m must be <= 8");
   if (c->capacity > (int64_t(1) << 26))  // kernels address a head's slots with 32-bit offsets
     return fail(QWM_ERR_UNSUPPORTED, "capacity must be <= 2^26 slots per (b, h)");
+  if (c->storage & ~(QWM_STORE_SCALE_I8 | QWM_STORE_GATE))
+    return fail(QWM_ERR_INVALID_ARG, "storage has unknown flags 0x%x", unsigned(c->storage));
   return QWM_OK;
 }
 
@@ -303,6 +305,8 @@ quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void
   a.slab = C.slab_bytes;
   a.o_mu_k = C.mu_k; a.o_mu_v = C.mu_v; a.o_a_k = C.a_k; a.o_b_k = C.b_k;
   a.o_a_v = C.a_v; a.o_b_v = C.b_v; a.o_wg = C.wg; a.o_u_t = C.u_t; a.o_u_dr = C.u_dr;
+  a.o_lam = C.lam;
+  a.gate = (cfg->storage & QWM_STORE_GATE) && cfg->rank > 0 ? 1 : 0;
   a.cache = static_cast<uint8_t*>(cache);
   a.L = qwm::cache_layout(*cfg);
   a.k = k_new; a.v = v_new;
@@ -353,6 +357,8 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
                                     float* logits_out, void* workspace, size_t workspace_bytes, void* stream) {
   QWM_TRY(check_cfg(cfg));
   if (n_epochs < 1 || n_epochs > qwm::kMaxEpochs) return fail(QWM_ERR_UNSUPPORTED, "n_epochs must be in [1, 64]");
+  if ((cfg->storage & QWM_STORE_SCALE_I8) && (n_act > 0 || n_epochs > 1))
+    return fail(QWM_ERR_UNSUPPORTED, "8-bit group scales are not taken with an active chunk or calibration epochs");
   if (n_epochs > 1) {
     if (!epoch_start) return fail(QWM_ERR_INVALID_ARG, "epoch_start is null");
     if (epoch_start[0] != 0) return fail(QWM_ERR_INVALID_ARG, "epoch_start[0] must be 0");

@@ -101,22 +101,25 @@ __device__ inline void round_quotients(const float (&xv)[N], const float (&mu)[N
 
 // Residual of one token against centroid row mu_row, group by group (Eq. 1-2
 // with q_min = 0, q_max = 3, the range extended to contain 0, the residual
-// quantised with the stored FP16 scale). Token and centroid values stream from
+// quantised with the stored scale). Token and centroid values stream from
 // memory 16 channels at a time in two passes (range, then codes). Codes are
 // stored as they are made; `each(c, e)` receives e = x_c - (mu_c + s (q_c - z))
 // for every channel c in order (Eq. 4, Eq. 13), and `chunk(c0)` follows the
 // last channel of every chunk of CH channels starting at c0.
-template <typename T, int D, int G, typename F, typename FC>
+// SI8 (App. D.1 8-bit group scales): the range passes of all groups come first,
+// since the groups share the secondary scale sig = RN16(max_g t_g / 255); a
+// group's step is then sig * c_g with c_g = RN(t_g / sig) in [0, 255].
+template <typename T, int D, int G, bool SI8, typename F, typename FC>
 __device__ inline void quant_stream(const T* __restrict__ xrow, const T* __restrict__ mrow,
                                     uint8_t* __restrict__ codes, bool active, int (&zg)[D / G],
-                                    float (&sg)[D / G], F each, FC chunk) {
+                                    float (&sg)[D / G], int (&cg)[D / G], float& sig, F each, FC chunk) {
   constexpr int CH = G < 16 ? G : 16;
-  static_for<0, D / G>([&](auto gi) {
+  constexpr int NG = D / G;
+  // 0-extended residual range of group g
+  auto range = [&](auto gi, float& lo, float& hi) {
     constexpr int g = decltype(gi)::value;
-    // keep each group's loads inside the group: hoisting them all ahead would
-    // hold every chunk in registers at once
-    __builtin_amdgcn_sched_barrier(0);
-    float lo = 0.0f, hi = 0.0f;
+    lo = 0.0f;
+    hi = 0.0f;
     static_for<0, G, CH>([&](auto ci) {
       constexpr int c0 = g * G + decltype(ci)::value;
       float xv[CH], mu[CH];
@@ -129,12 +132,45 @@ __device__ inline void quant_stream(const T* __restrict__ xrow, const T* __restr
         hi = r > hi ? r : hi;
       }
     });
-    const float s = f16_round((hi - lo) / 3.0f);
+  };
+  float glo[SI8 ? NG : 1];
+  if constexpr (SI8) {
+    float tg[NG], mx = 0.0f;
+    static_for<0, NG>([&](auto gi) {
+      constexpr int g = decltype(gi)::value;
+      __builtin_amdgcn_sched_barrier(0);
+      float lo, hi;
+      range(gi, lo, hi);
+      glo[g] = lo;
+      tg[g] = (hi - lo) / 3.0f;
+      mx = tg[g] > mx ? tg[g] : mx;
+    });
+    sig = f16_round(mx / 255.0f);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const int c = sig != 0.0f ? (int)fminf(fmaxf(rintf(tg[g] / sig), 0.0f), 255.0f) : 0;
+      cg[g] = c;
+      sg[g] = sig * (float)c;  // exact: 11-bit times 8-bit significands
+    }
+  }
+  static_for<0, NG>([&](auto gi) {
+    constexpr int g = decltype(gi)::value;
+    // keep each group's loads inside the group: hoisting them all ahead would
+    // hold every chunk in registers at once
+    __builtin_amdgcn_sched_barrier(0);
+    float lo;
+    if constexpr (SI8) {
+      lo = glo[g];
+    } else {
+      float hi;
+      range(gi, lo, hi);
+      sg[g] = f16_round((hi - lo) / 3.0f);
+    }
+    const float s = sg[g];
     const float sd = s != 0.0f ? s : 1.0f;
     const int z = s != 0.0f ? (int)fminf(fmaxf(rintf(0.0f - lo / sd), 0.0f), 3.0f) : 0;
     const float inv = s != 0.0f ? 1.0f / s : 0.0f;
     zg[g] = z;
-    sg[g] = s;
     static_for<0, G, CH>([&](auto ci) {
       constexpr int c0 = g * G + decltype(ci)::value;
       float xv[CH], mu[CH];
@@ -158,18 +194,27 @@ __device__ inline void quant_stream(const T* __restrict__ xrow, const T* __restr
   });
 }
 
-template <int D, int G>
+// zero-points (INT2, four per byte) and the group scales: binary16 steps, or
+// (SI8) the 8-bit codes c_g and the binary16 secondary scale
+template <int D, int G, bool SI8>
 __device__ inline void store_meta(uint8_t* __restrict__ zp_dst, uint8_t* __restrict__ scale_dst,
-                                  const int (&zg)[D / G], const float (&sg)[D / G]) {
+                                  uint8_t* __restrict__ sigma_dst, const int (&zg)[D / G],
+                                  const float (&sg)[D / G], const int (&cg)[D / G], float sig) {
   constexpr int NG = D / G;
   uint32_t z = 0;
 #pragma unroll
   for (int g = 0; g < NG; ++g) z |= uint32_t(zg[g]) << (2 * g);
   zp_dst[0] = uint8_t(z & 255);
   if constexpr (NG > 4) zp_dst[1] = uint8_t(z >> 8);
-  uint16_t* sp = reinterpret_cast<uint16_t*>(scale_dst);
+  if constexpr (SI8) {
 #pragma unroll
-  for (int g = 0; g < NG; ++g) sp[g] = f16_bits(sg[g]);
+    for (int g = 0; g < NG; ++g) scale_dst[g] = uint8_t(cg[g]);
+    *reinterpret_cast<uint16_t*>(sigma_dst) = f16_bits(sig);
+  } else {
+    uint16_t* sp = reinterpret_cast<uint16_t*>(scale_dst);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) sp[g] = f16_bits(sg[g]);
+  }
 }
 
 // Bubble (dist, id) into a list kept sorted by (dist, id); ids arrive in
@@ -188,7 +233,7 @@ __device__ inline void topm_insert(float (&bd)[MM], int (&bi)[MM], float dv, int
   }
 }
 
-template <typename T, int D, int G, int RP, int MM>
+template <typename T, int D, int G, int RP, int MM, bool SI8>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void append_kernel(const AppendArgs a) {
   constexpr int NG = D / G;
   const int t = blockIdx.x * 256 + threadIdx.x;
@@ -300,8 +345,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     float C[RP > 0 ? RP : 1];
 #pragma unroll
     for (int k = 0; k < (RP > 0 ? RP : 1); ++k) C[k] = 0.0f;
-    int zg[NG];
-    float sg[NG];
+    int zg[NG], cg[NG];
+    float sg[NG], sig = 0.0f;
     // The errors of one chunk go to this thread's LDS row, and a rolled loop over
     // the chunk's channels adds e_c U_r[c, :] to C. Written as straight-line code,
     // the compiler hoisted the wave-uniform loads of all d x RP entries of U_r
@@ -309,8 +354,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     constexpr int CHK = G < 16 ? G : 16, ES = CHK + 1;
     __shared__ float s_err[RP > 0 ? 256 * ES : 1];
     float* my_err = s_err + threadIdx.x * ES;
-    quant_stream<T, D, G>(
-        krow, mrow, a.cache + a.L.k_codes + slot * (D / 4), active, zg, sg,
+    quant_stream<T, D, G, SI8>(
+        krow, mrow, a.cache + a.L.k_codes + slot * (D / 4), active, zg, sg, cg, sig,
         [&](int c, float e) {
           if constexpr (RP > 0) my_err[c % CHK] = e;
         },
@@ -326,7 +371,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
           }
         });
     if (active) {
-      store_meta<D, G>(a.cache + a.L.k_zp + slot * a.L.zpb, a.cache + a.L.k_scale + slot * 2 * NG, zg, sg);
+      store_meta<D, G, SI8>(a.cache + a.L.k_zp + slot * a.L.zpb, a.cache + a.L.k_scale + slot * a.L.sb,
+                            a.cache + a.L.k_sigma + slot * 2, zg, sg, cg, sig);
       a.cache[a.L.k_ids + slot] = uint8_t(z);
     }
     if constexpr (RP > 0) {
@@ -337,50 +383,77 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
         if (k < r) amax = fmaxf(amax, fabsf(C[k]));
       const float s = f16_round(amax / 127.0f);
       const float sd = s != 0.0f ? s : 1.0f;
+      int qc[RP];
+#pragma unroll
+      for (int k = 0; k < RP; ++k)
+        qc[k] = k < r && s != 0.0f ? (int)fminf(fmaxf(rintf(C[k] / sd), -127.0f), 127.0f) : 0;
+      // App. D.1 retention: keep the row only if it lowers the lam-weighted
+      // error on the principal subspace (ranks in order, fp32)
+      bool keep = true;
+      if (a.gate) {
+        const float* __restrict__ lam = reinterpret_cast<const float*>(slab + a.o_lam);
+        float before = 0.0f, after = 0.0f;
+#pragma unroll
+        for (int k = 0; k < RP; ++k) {
+          if (k < r) {
+            const float e = C[k] - (float)qc[k] * s;
+            before = before + lam[k] * (C[k] * C[k]);
+            after = after + lam[k] * (e * e);
+          }
+        }
+        keep = after < before;
+      }
       if (active) {
         int8_t* code = reinterpret_cast<int8_t*>(a.cache + a.L.k_coef + slot * r);
         float* co = a.coef_out ? a.coef_out + (bh * a.n_new + tt) * r : nullptr;
 #pragma unroll
         for (int k = 0; k < RP; ++k) {
           if (k < r) {
-            code[k] = int8_t(s != 0.0f ? (int)fminf(fmaxf(rintf(C[k] / sd), -127.0f), 127.0f) : 0);
+            code[k] = int8_t(keep ? qc[k] : 0);
             if (co) co[k] = C[k];
           }
         }
-        *reinterpret_cast<uint16_t*>(a.cache + a.L.k_cscale + slot * 2) = f16_bits(s);
+        *reinterpret_cast<uint16_t*>(a.cache + a.L.k_cscale + slot * 2) = f16_bits(keep ? s : 0.0f);
       }
     }
   }
 
   // ---- Values: the same residual path as Keys, no PSAC
   {
-    int zg[NG];
-    float sg[NG];
-    quant_stream<T, D, G>(reinterpret_cast<const T*>(a.v) + src, muv + int64_t(zv) * D,
-                          a.cache + a.L.v_codes + slot * (D / 4), active, zg, sg, [](int, float) {}, [](int) {});
+    int zg[NG], cg[NG];
+    float sg[NG], sig = 0.0f;
+    quant_stream<T, D, G, SI8>(reinterpret_cast<const T*>(a.v) + src, muv + int64_t(zv) * D,
+                               a.cache + a.L.v_codes + slot * (D / 4), active, zg, sg, cg, sig, [](int, float) {},
+                               [](int) {});
     if (active) {
-      store_meta<D, G>(a.cache + a.L.v_zp + slot * a.L.zpb, a.cache + a.L.v_scale + slot * 2 * NG, zg, sg);
+      store_meta<D, G, SI8>(a.cache + a.L.v_zp + slot * a.L.zpb, a.cache + a.L.v_scale + slot * a.L.sb,
+                            a.cache + a.L.v_sigma + slot * 2, zg, sg, cg, sig);
       a.cache[a.L.v_ids + slot] = uint8_t(zv);
     }
   }
 }
 
-template <typename T, int D, int G>
-hipError_t launch_dg(const AppendArgs& a, int batch, hipStream_t s) {
+template <typename T, int D, int G, bool SI8>
+hipError_t launch_dgs(const AppendArgs& a, int batch, hipStream_t s) {
   const dim3 grid((unsigned)((a.n_new + 255) / 256), (unsigned)a.heads, (unsigned)batch);
   const int rp = a.rank == 0 ? 0 : (a.rank <= 16 ? 16 : 32);  // the [d][rs] stride of U_r
   const bool wide = a.top_m > 4;
   if (rp == 32) {
-    if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 32, 8>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((append_kernel<T, D, G, 32, 4>), grid, dim3(256), 0, s, a);
+    if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 32, 8, SI8>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((append_kernel<T, D, G, 32, 4, SI8>), grid, dim3(256), 0, s, a);
   } else if (rp == 16) {
-    if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 16, 8>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((append_kernel<T, D, G, 16, 4>), grid, dim3(256), 0, s, a);
+    if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 16, 8, SI8>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((append_kernel<T, D, G, 16, 4, SI8>), grid, dim3(256), 0, s, a);
   } else {
-    if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 0, 8>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((append_kernel<T, D, G, 0, 4>), grid, dim3(256), 0, s, a);
+    if (wide) hipLaunchKernelGGL((append_kernel<T, D, G, 0, 8, SI8>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((append_kernel<T, D, G, 0, 4, SI8>), grid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
+}
+
+template <typename T, int D, int G>
+hipError_t launch_dg(const AppendArgs& a, int batch, hipStream_t s) {
+  return a.L.i8 ? launch_dgs<T, D, G, true>(a, batch, s) : launch_dgs<T, D, G, false>(a, batch, s);
 }
 
 }  // namespace

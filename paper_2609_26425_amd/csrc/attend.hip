@@ -75,6 +75,7 @@ struct TileRegs {
   uint32_t k_idb, v_idb[2];
   uint32_t k_zb[NSUB], v_zb[2];
   _Float16 k_s[NSUB], v_s[2], c_s;  // loaded bits, reinterpreted (no arithmetic)
+  uint32_t k_cb[NSUB], v_cb[2];     // 8-bit group-scale codes (App. D.1 SI8 form only)
   bool k_on_act, v_on_act[2];
 };
 
@@ -175,15 +176,20 @@ __device__ inline uint32_t and_or(uint32_t x, uint32_t m, uint32_t o) {
 // (exponent 10: one unit per ulp), so one packed f16 subtraction of 1024 + z
 // yields two exact (code - z), and v_fma_mix_f32 takes them and the binary16
 // scale as fp32 operands: one rounding, the same value as fma(s, code - z, mu).
-template <int N>
-__device__ inline void dequant_codes(uint32_t cw, _Float16 s, uint32_t zz, const float (&mu)[N], float (&x)[N]) {
+// SI8 (App. D.1 8-bit group scales): the step is sigma * c with s = sigma and cm
+// = (c, c); c (code - z) is an integer of magnitude <= 765, exact in binary16,
+// so the fma still rounds once.
+template <int N, bool SI8 = false>
+__device__ inline void dequant_codes(uint32_t cw, _Float16 s, uint32_t zz, const float (&mu)[N], float (&x)[N],
+                                     f16x2 cm = {}) {
   static_assert(N == 16 || N == 8, "16 or 8 channels per code word");
   const f16x2 zh = __builtin_bit_cast(f16x2, zz);
   // N == 8: channels 4..7 move to bits 16..23, so half k pairs channels k and k + N/2
   const uint32_t w = N == 16 ? cw : ((cw & 0xffu) | ((cw & 0xff00u) << 8));
 #pragma unroll
   for (int k = 0; k < N / 2; ++k) {
-    const f16x2 d = __builtin_bit_cast(f16x2, and_or(w >> (2 * k), 0x00030003u, 0x64006400u)) - zh;
+    f16x2 d = __builtin_bit_cast(f16x2, and_or(w >> (2 * k), 0x00030003u, 0x64006400u)) - zh;
+    if constexpr (SI8) d = d * cm;
     x[k] = __builtin_fmaf((float)s, (float)d.x, mu[k]);
     x[k + N / 2] = __builtin_fmaf((float)s, (float)d.y, mu[k + N / 2]);
   }
@@ -238,7 +244,7 @@ struct Lds {
 // GEN: the launch has an exact active chunk after the packed keys and/or packed
 // keys in several calibration epochs (a separate instance, so plain launches
 // carry none of its code).
-template <typename T, int D, int RP, bool LOGITS, bool TAB, bool GEN>
+template <typename T, int D, int RP, bool LOGITS, bool TAB, bool GEN, bool SI8>
 __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   typedef Mfma<T> MF;
   typedef typename MF::V V;
@@ -335,14 +341,14 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   TileRegs<NSUB> P0, P1;
   auto clear_regs = [&](TileRegs<NSUB>& p) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < NSUB; ++u) { p.k_cw[u] = 0; p.k_zb[u] = 0; p.k_s[u] = 0; }
+    for (int u = 0; u < NSUB; ++u) { p.k_cw[u] = 0; p.k_zb[u] = 0; p.k_s[u] = 0; p.k_cb[u] = 0; }
     p.c_w[0] = p.c_w[1] = 0;
     p.c_s = 0;
     p.k_idb = 0;
     p.k_on_act = false;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      p.v_cw[e] = 0; p.v_idb[e] = 0; p.v_zb[e] = 0; p.v_s[e] = 0; p.v_on_act[e] = false;
+      p.v_cw[e] = 0; p.v_idb[e] = 0; p.v_zb[e] = 0; p.v_s[e] = 0; p.v_cb[e] = 0; p.v_on_act[e] = false;
     }
   };
   clear_regs(P0);
@@ -357,7 +363,8 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   // head (base = its first slot), this thread's byte offset inside a tile as the
   // vector offset (fixed for all tiles) and the tile's byte offset as the scalar
   // offset, so advancing a tile costs no vector instruction.
-  const uint32_t zpb = L.zpb, sstride = 2 * L.ng, ncu = uint32_t(nc);
+  // group-scale bytes per token: binary16 steps, or 8-bit codes (SI8)
+  const uint32_t zpb = L.zpb, sstride = SI8 ? L.ng : 2 * L.ng, ncu = uint32_t(nc);
   // active-chunk row of key `key` (>= npk) at channel c0: [B, n_act, H, d]
   auto act_row = [&](const T* base, uint32_t key, int c0) {
     return base + ((int64_t(b) * a.n_act + (key - npku)) * a.heads + h) * D + c0;
@@ -378,9 +385,11 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
              r_ks = field(L.k_scale, sstride), r_vc = field(L.v_codes, D / 4), r_vi = field(L.v_ids, 1),
              r_vz = field(L.v_zp, zpb), r_vs = field(L.v_scale, sstride);
   const auto r_cc = field(L.k_coef, uint32_t(r)), r_cs = field(L.k_cscale, 2);
+  const auto r_ksg = field(L.k_sigma, 2), r_vsg = field(L.v_sigma, 2);  // SI8 secondary scales
   const int o_kc = kkey * (D / 4) + kch0 / 4, o_kz = kkey * zpb, o_ks = kkey * sstride;
   const int o_cc = ckey * r + cr0, o_cs = ckey * 2;
-  const int o_vc = 2 * vkp * (D / 4) + vch0 / 4, o_vz = 2 * vkp * zpb + vg / 4, o_vs = 2 * vkp * sstride + 2 * vg;
+  const int o_vc = 2 * vkp * (D / 4) + vch0 / 4, o_vz = 2 * vkp * zpb + vg / 4,
+            o_vs = 2 * vkp * sstride + (SI8 ? vg : 2 * vg);
 
   // FULL: every key of the tile is < n_cache, so no per-thread guards. A key
   // past n_cache (tail tiles only) gets centroid 0, scale 0 and code 0: a finite
@@ -400,11 +409,11 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     const bool aligned = AL == 1 || (AL == -1 && raligned);
     const int k0i = int(k0);
     // fields are gathered in locals and stored into the set once, at the end
-    uint32_t kid = 0, kzb[NSUB], kcw[NSUB], cw2[2] = {0, 0};
-    uint32_t vid[2] = {0, 0}, vzb[2] = {0, 0}, vcw[2] = {0, 0};
+    uint32_t kid = 0, kzb[NSUB], kcw[NSUB], kcb[NSUB], cw2[2] = {0, 0};
+    uint32_t vid[2] = {0, 0}, vzb[2] = {0, 0}, vcw[2] = {0, 0}, vcb[2] = {0, 0};
     _Float16 ksb[NSUB], csb = 0, vsb[2] = {0, 0};
 #pragma unroll
-    for (int u = 0; u < NSUB; ++u) { kzb[u] = 0; ksb[u] = 0; kcw[u] = 0; }
+    for (int u = 0; u < NSUB; ++u) { kzb[u] = 0; ksb[u] = 0; kcw[u] = 0; kcb[u] = 0; }
     const bool kact = GEN && !FULL && k0 + kkey >= npku && k0 + kkey < ncu;
     if (!kact && (FULL || k0 + kkey < npku)) {
       kid = __builtin_amdgcn_raw_buffer_load_b8(r_ki, kkey, k0i, 0);
@@ -412,7 +421,13 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       for (int u = 0; u < NSUB; ++u) {
         const int g = kgrp[u];
         kzb[u] = __builtin_amdgcn_raw_buffer_load_b8(r_kz, o_kz + g / 4, k0i * int(zpb), 0);
-        ksb[u] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_ks, o_ks + 2 * g, k0i * int(sstride), 0));
+        if constexpr (SI8) kcb[u] = __builtin_amdgcn_raw_buffer_load_b8(r_ks, o_ks + g, k0i * int(sstride), 0);
+        else ksb[u] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_ks, o_ks + 2 * g, k0i * int(sstride), 0));
+      }
+      if constexpr (SI8) {
+        const _Float16 sg = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_ksg, 2 * kkey, k0i * 2, 0));
+#pragma unroll
+        for (int u = 0; u < NSUB; ++u) ksb[u] = sg;
       }
       if constexpr (NSUB == 2) {
         const auto cw = __builtin_amdgcn_raw_buffer_load_b64(r_kc, o_kc, k0i * (D / 4), 0);
@@ -448,7 +463,12 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       if (!vact[e] && (FULL || key < npku)) {
         vid[e] = __builtin_amdgcn_raw_buffer_load_b8(r_vi, 2 * vkp + e, k0i, 0);
         vzb[e] = __builtin_amdgcn_raw_buffer_load_b8(r_vz, o_vz + e * int(zpb), k0i * int(zpb), 0);
-        vsb[e] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_vs, o_vs + e * int(sstride), k0i * int(sstride), 0));
+        if constexpr (SI8) {
+          vcb[e] = __builtin_amdgcn_raw_buffer_load_b8(r_vs, o_vs + e * int(sstride), k0i * int(sstride), 0);
+          vsb[e] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_vsg, 2 * (2 * vkp + e), k0i * 2, 0));
+        } else {
+          vsb[e] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_vs, o_vs + e * int(sstride), k0i * int(sstride), 0));
+        }
         if constexpr (CHV == 16) vcw[e] = __builtin_amdgcn_raw_buffer_load_b32(r_vc, o_vc + e * (D / 4), k0i * (D / 4), 0);
         else vcw[e] = __builtin_amdgcn_raw_buffer_load_b16(r_vc, o_vc + e * (D / 4), k0i * (D / 4), 0);
       }
@@ -456,13 +476,14 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     p.k_on_act = kact;
     p.k_idb = kid;
 #pragma unroll
-    for (int u = 0; u < NSUB; ++u) { p.k_zb[u] = kzb[u]; p.k_s[u] = ksb[u]; p.k_cw[u] = kcw[u]; }
+    for (int u = 0; u < NSUB; ++u) { p.k_zb[u] = kzb[u]; p.k_s[u] = ksb[u]; p.k_cw[u] = kcw[u]; p.k_cb[u] = kcb[u]; }
     p.c_s = csb;
     p.c_w[0] = cw2[0];
     p.c_w[1] = cw2[1];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       p.v_on_act[e] = vact[e]; p.v_idb[e] = vid[e]; p.v_zb[e] = vzb[e]; p.v_s[e] = vsb[e]; p.v_cw[e] = vcw[e];
+      p.v_cb[e] = vcb[e];
     }
   };
 
@@ -520,7 +541,8 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         load_words(act_row(k_act, k0 + kkey, kch0 + 16 * u), w, 16 * int(sizeof(T)) / 4);
         raw_to_float<T, 16>(w, x);
       } else {
-        dequant_codes<16>(k_cw[u], k_s[u], k_z[u], mu, x);
+        const _Float16 cb = (_Float16)p.k_cb[u];
+        dequant_codes<16, SI8>(k_cw[u], k_s[u], k_z[u], mu, x, f16x2{cb, cb});
       }
       store_vals<T, 16>(kt + kkey * LY::KS + kch0 + 16 * u, x);
     }
@@ -535,6 +557,8 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     {
       float x0[CHV], x1[CHV];
       float mu0[CHV], mu1[CHV];
+      const _Float16 vc0 = (_Float16)p.v_cb[0], vc1 = (_Float16)p.v_cb[1];
+      const f16x2 vcm0 = {vc0, vc0}, vcm1 = {vc1, vc1};
       if (TAB && !v_e1[0]) load_vals<T, CHV>(tabV + v_id[0] * LY::TS + vch0, mu0);
       else load_vals<T, CHV>((v_e1[0] ? gV1 : gV0) + v_id[0] * D + vch0, mu0);
       if (TAB && !v_e1[1]) load_vals<T, CHV>(tabV + v_id[1] * LY::TS + vch0, mu1);
@@ -545,17 +569,17 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
           load_words(act_row(v_act, k0 + 2 * vkp, vch0), w, VW);
           raw_to_float<T, CHV>(w, x0);
         } else {
-          dequant_codes<CHV>(v_cw[0], v_s[0], v_z[0], mu0, x0);
+          dequant_codes<CHV, SI8>(v_cw[0], v_s[0], v_z[0], mu0, x0, vcm0);
         }
         if (v_on_act[1]) {
           load_words(act_row(v_act, k0 + 2 * vkp + 1, vch0), w, VW);
           raw_to_float<T, CHV>(w, x1);
         } else {
-          dequant_codes<CHV>(v_cw[1], v_s[1], v_z[1], mu1, x1);
+          dequant_codes<CHV, SI8>(v_cw[1], v_s[1], v_z[1], mu1, x1, vcm1);
         }
       } else {
-        dequant_codes<CHV>(v_cw[0], v_s[0], v_z[0], mu0, x0);
-        dequant_codes<CHV>(v_cw[1], v_s[1], v_z[1], mu1, x1);
+        dequant_codes<CHV, SI8>(v_cw[0], v_s[0], v_z[0], mu0, x0, vcm0);
+        dequant_codes<CHV, SI8>(v_cw[1], v_s[1], v_z[1], mu1, x1, vcm1);
       }
 #pragma unroll
       for (int c = 0; c < CHV; ++c) store_pair<T>(vt + (vch0 + c) * LY::VS + 2 * vkp, x0[c], x1[c]);
@@ -982,12 +1006,12 @@ size_t lds_bytes_t(int rank, int kc, bool tables) {
   return (2 * tile + (tables ? size_t(2) * kc * TS : 0)) * sizeof(T);  // two tile buffers
 }
 
-template <typename T, int D, int RP, bool LOGITS, bool TAB, bool GEN = false>
+template <typename T, int D, int RP, bool LOGITS, bool TAB, bool GEN = false, bool SI8 = false>
 hipError_t launch_k(const AttendArgs& a, const dim3& grid, size_t lds, hipStream_t s) {
-  const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, LOGITS, TAB, GEN>,
+  const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, LOGITS, TAB, GEN, SI8>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attend_kernel<T, D, RP, LOGITS, TAB, GEN>), grid, dim3(NT), lds, s, a);
+  hipLaunchKernelGGL((attend_kernel<T, D, RP, LOGITS, TAB, GEN, SI8>), grid, dim3(NT), lds, s, a);
   return hipGetLastError();
 }
 
@@ -996,10 +1020,20 @@ hipError_t launch_r(const AttendArgs& a, int batch, bool logits, hipStream_t s) 
   const dim3 grid((unsigned)((a.n_q + BQ - 1) / BQ * a.n_split), (unsigned)a.heads, (unsigned)batch);
   const bool tab = a.tables_in_lds != 0;
   const size_t lds = lds_bytes_t<T, D>(a.rank, a.n_centroids, tab);
-  if (logits) return tab ? launch_k<T, D, RP, true, true>(a, grid, lds, s) : launch_k<T, D, RP, true, false>(a, grid, lds, s);
+  const bool si8 = a.L.i8 != 0;
+  if (si8 && (a.n_act > 0 || a.n_epochs > 1)) return hipErrorNotSupported;
+  if (logits) {
+    if (si8)
+      return tab ? launch_k<T, D, RP, true, true, false, true>(a, grid, lds, s)
+                 : launch_k<T, D, RP, true, false, false, true>(a, grid, lds, s);
+    return tab ? launch_k<T, D, RP, true, true>(a, grid, lds, s) : launch_k<T, D, RP, true, false>(a, grid, lds, s);
+  }
   hipError_t e;
   if (a.n_act > 0 || a.n_epochs > 1)
     e = tab ? launch_k<T, D, RP, false, true, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false, true>(a, grid, lds, s);
+  else if (si8)
+    e = tab ? launch_k<T, D, RP, false, true, false, true>(a, grid, lds, s)
+            : launch_k<T, D, RP, false, false, false, true>(a, grid, lds, s);
   else
     e = tab ? launch_k<T, D, RP, false, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false>(a, grid, lds, s);
   if (e != hipSuccess || a.n_split == 1) return e;

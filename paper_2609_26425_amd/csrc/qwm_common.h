@@ -14,10 +14,13 @@ typedef __bf16 bf16;
 // Packed cache layout (App. D.1 storage, section order fixed by quantwm.h).
 struct CacheLayout {
   int d, ng, zpb, r;
+  int i8;  // group scales as 8-bit codes + a binary16 secondary scale per token
+  int sb;  // group-scale bytes per token: 2 ng (binary16) or ng (8-bit codes)
   int k_bytes, v_bytes;
   int64_t slots;  // per (b, h): capacity rounded up to 64
   int64_t k_codes, k_ids, k_zp, k_scale, k_coef, k_cscale;
   int64_t v_codes, v_ids, v_zp, v_scale;
+  int64_t k_sigma, v_sigma;  // i8 only: the secondary scale per token
   int64_t total;
 };
 
@@ -30,21 +33,25 @@ inline CacheLayout cache_layout(const quantwm_config& c) {
   L.zpb = (L.ng + 3) / 4;
   L.r = c.rank;
   L.slots = (c.capacity + 63) / 64 * 64;
+  L.i8 = (c.storage & QWM_STORE_SCALE_I8) != 0;
+  L.sb = L.i8 ? L.ng : 2 * L.ng;
   const int64_t rows = int64_t(c.batch) * c.heads * L.slots;
   int64_t at = 0;
   auto take = [&](int64_t per_token) { int64_t o = at; at = align256(at + rows * per_token); return o; };
   L.k_codes = take(L.d / 4);
   L.k_ids = take(1);
   L.k_zp = take(L.zpb);
-  L.k_scale = take(2 * L.ng);
+  L.k_scale = take(L.sb);
   L.k_coef = take(L.r);
   L.k_cscale = take(L.r > 0 ? 2 : 0);
   L.v_codes = take(L.d / 4);
   L.v_ids = take(1);
   L.v_zp = take(L.zpb);
-  L.v_scale = take(2 * L.ng);
+  L.v_scale = take(L.sb);
+  L.k_sigma = take(L.i8 ? 2 : 0);
+  L.v_sigma = take(L.i8 ? 2 : 0);
   L.total = at;
-  L.v_bytes = L.d / 4 + 1 + L.zpb + 2 * L.ng;
+  L.v_bytes = L.d / 4 + 1 + L.zpb + L.sb + (L.i8 ? 2 : 0);
   L.k_bytes = L.v_bytes + (L.r > 0 ? L.r + 2 : 0);
   return L;
 }
@@ -87,6 +94,8 @@ struct AppendArgs {
   int64_t n_new, n_cached;
   int heads, n_centroids, rank, top_m;
   float* coef_out;
+  int gate;        // QWM_STORE_GATE with r > 0
+  int64_t o_lam;   // eigenvalues in the slab (read with the gate)
 };
 
 constexpr int kMaxEpochs = 64;

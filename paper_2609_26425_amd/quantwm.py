@@ -29,7 +29,7 @@ class Config(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("n_centroids", ctypes.c_int32), ("group_size", ctypes.c_int32),
                 ("rank", ctypes.c_int32), ("top_m", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("capacity", ctypes.c_int64)]
+                ("capacity", ctypes.c_int64), ("storage", ctypes.c_int32)]
 
     @property
     def torch_dtype(self):
@@ -89,9 +89,15 @@ def library():
     return _lib
 
 
-def make_config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, dtype) -> Config:
+# App. D.1 storage options (QWM_STORE_* in include/quantwm.h)
+STORE_SCALE_I8 = 1
+STORE_GATE = 2
+
+
+def make_config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, dtype,
+                storage=0) -> Config:
     dt = {"bf16": BF16, "f32": F32, BF16: BF16, F32: F32}[dtype]
-    return Config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, dt, capacity)
+    return Config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, dt, capacity, storage)
 
 
 def _ptr(t):

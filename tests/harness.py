@@ -58,7 +58,7 @@ def build_oracle_case(wl: synth.Workload, max_sources: int = 3, cold: bool = Fal
     sources = sources_for(wl, max_sources)
     S = len(sources)
     cfg = oracle.cfg_of(1, S, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank, wl.top_m,
-                        wl.n_cache, wl.dtype == "bf16")
+                        wl.n_cache, wl.dtype == "bf16", wl.storage)
     k = _gen_sources(wl, sources, "k", wl.n_cache)
     v = _gen_sources(wl, sources, "v", wl.n_cache)
     q = _gen_sources(wl, sources, "q", wl.n_q)
@@ -71,7 +71,7 @@ def build_oracle_case(wl: synth.Workload, max_sources: int = 3, cold: bool = Fal
                               wl.kmeans_iters)
     cache = oracle.new_cache(cfg)
     diag = oracle.append(cfg, tables, cache, 0, k, v, diagnostics=True)
-    lay = packed.layout(1, S, wl.head_dim, wl.group_size, wl.rank, wl.n_cache)
+    lay = packed.layout(1, S, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage)
     bh = wl.batch * wl.heads
     src_of = np.arange(bh) % S
     if S == bh:
@@ -102,7 +102,7 @@ def full_tables(case: OracleCase):
 
 def full_oracle_cache(case: OracleCase) -> np.ndarray:
     wl = case.wl
-    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.n_cache)
+    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage)
     out = np.zeros(lay["total"], np.uint8)
     for bh in range(wl.batch * wl.heads):
         packed.copy_head(out, lay, bh, case.cache, case.lay, int(case.src_of[bh]), wl.n_cache)

@@ -31,10 +31,11 @@ def test_header_symbols_are_exported():
                                    (1, 40, 128, 128, 32, 16, 4, 32760, "bf16"),
                                    (4, 30, 128, 256, 64, 32, 4, 24960, "bf16"), (2, 3, 128, 37, 32, 12, 3, 1000, "bf16"),
                                    (1, 2, 64, 24, 16, 20, 8, 700, "bf16"), (1, 2, 128, 5, 64, 0, 1, 513, "bf16")])
-def test_sizes_agree_with_the_oracle_format(shape):
+@pytest.mark.parametrize("storage", [0, 1, 2, 3])
+def test_sizes_agree_with_the_oracle_format(shape, storage):
     B, H, d, K, G, r, M, cap, dt = shape
-    cfg = qw.make_config(B, H, d, K, G, r, M, cap, dt)
-    ocfg = oracle.cfg_of(B, H, d, K, G, r, M, cap, dt == "bf16")
+    cfg = qw.make_config(B, H, d, K, G, r, M, cap, dt, storage)
+    ocfg = oracle.cfg_of(B, H, d, K, G, r, M, cap, dt == "bf16", storage)
     assert qw.quantwm_cache_bytes(cfg) == oracle.cache_bytes(ocfg)
     assert qw.quantwm_token_bytes(cfg) == oracle.token_bytes(ocfg)
     L = qw.quantwm_calib_offsets(cfg)
@@ -55,6 +56,15 @@ def test_validation_without_a_gpu():
             qw.quantwm_token_bytes(bad)
         assert e.value.status == status
         assert qw.quantwm_cache_bytes(bad) == 0
+    # unknown storage flags
+    with pytest.raises(qw.QuantwmError) as e:
+        qw.quantwm_token_bytes(qw.make_config(1, 2, 128, 16, 32, 8, 4, 100, "bf16", 4))
+    assert e.value.status == qw.ERR_INVALID_ARG
+    # 8-bit group scales are not taken by the streaming attention forms
+    i8 = qw.make_config(1, 2, 128, 16, 32, 8, 4, 100, "bf16", qw.STORE_SCALE_I8)
+    with pytest.raises(qw.QuantwmError) as e:
+        qw.quantwm_attend_active(i8, None, None, 50, None, None, 10, None, 4, 55, 1, None)
+    assert e.value.status == qw.ERR_UNSUPPORTED
     # checks that fire before any device work
     with pytest.raises(qw.QuantwmError) as e:
         qw._check(qw.library().quantwm_append(ctypes.byref(good), None, None, 90, None, None, 20, None, None))

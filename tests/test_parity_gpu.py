@@ -34,7 +34,7 @@ def tdev(x, dtype):
 
 def gpu_config(wl, capacity=None):
     return qw.make_config(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank,
-                          wl.top_m, wl.n_cache if capacity is None else capacity, wl.dtype)
+                          wl.top_m, wl.n_cache if capacity is None else capacity, wl.dtype, wl.storage)
 
 
 def gpu_calib_from_tables(cfg, tables):
@@ -66,10 +66,13 @@ def gpu_append_all(wl, cfg, calib, k_full, v_full):
 
 def check_append(case, gpu_cache, gpu_coef):
     wl = case.wl
-    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.n_cache)
+    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage)
     mu_k, mu_v, w = case.tables[0][0], case.tables[1][0], case.tables[2][0]
+    lam = case.tables[4][0] if wl.rank > 0 else None
     M = min(wl.top_m, wl.n_centroids)
-    stats = {"tokens": 0, "k_ties": 0, "v_ties": 0, "coef_half": 0, "cscale_f16": 0}
+    stats = {"tokens": 0, "k_ties": 0, "v_ties": 0, "coef_half": 0, "cscale_f16": 0, "gate_ties": 0}
+    i8 = bool(wl.storage & oracle.STORE_SCALE_I8)
+    gate = bool(wl.storage & oracle.STORE_GATE) and wl.rank > 0
     for bh in range(wl.batch * wl.heads):
         s = int(case.src_of[bh])
         g = packed.fields(gpu_cache, lay, bh, 0, wl.n_cache)
@@ -87,10 +90,10 @@ def check_append(case, gpu_cache, gpu_coef):
         stats["v_ties"] += len(vmis)
         kok = np.ones(wl.n_cache, bool); kok[kmis] = False
         vok = np.ones(wl.n_cache, bool); vok[vmis] = False
-        for f in ("k_codes", "k_zp", "k_scale"):
+        for f in ("k_codes", "k_zp", "k_scale") + (("k_sigma",) if i8 else ()):
             bad = np.nonzero((g[f][kok] != o[f][kok]).reshape(kok.sum(), -1).any(1))[0]
             assert len(bad) == 0, f"head {bh}: {f} differs at tokens {np.nonzero(kok)[0][bad][:8]}"
-        for f in ("v_codes", "v_zp", "v_scale"):
+        for f in ("v_codes", "v_zp", "v_scale") + (("v_sigma",) if i8 else ()):
             bad = np.nonzero((g[f][vok] != o[f][vok]).reshape(vok.sum(), -1).any(1))[0]
             assert len(bad) == 0, f"head {bh}: {f} differs at tokens {np.nonzero(vok)[0][bad][:8]}"
         if wl.rank > 0:
@@ -102,6 +105,25 @@ def check_append(case, gpu_cache, gpu_coef):
             assert np.all(err <= tol), f"head {bh}: PSAC coefficient error {err.max()} > 1e-4 relative"
             sc_g, sc_o = g["k_cscale"][kok], o["k_cscale"][kok]
             amax = np.abs(Co).max(1).astype(np.float32) / np.float32(127.0)
+            if gate:
+                # a row kept on one side and zeroed on the other: the keep rule
+                # must be at a tie (errors before and after within rounding)
+                flip = (sc_g == 0) != (sc_o == 0)
+                for t in np.nonzero(flip)[0]:
+                    src = g if sc_o[t] == 0 else o
+                    sv = float(np.uint16(src["k_cscale"][kok][t]).view(np.float16))
+                    e = Co[t] - src["k_coef"][kok][t].astype(np.float64) * sv
+                    before = float(np.sum(lam[s].astype(np.float64) * Co[t] ** 2))
+                    after = float(np.sum(lam[s].astype(np.float64) * e ** 2))
+                    assert abs(after - before) <= 1e-4 * before + 1e-30, f"head {bh}: gate differs off a tie"
+                stats["gate_ties"] += int(flip.sum())
+                both = ~flip
+                Co, sc_g, sc_o, amax = Co[both], sc_g[both], sc_o[both], amax[both]
+                kok_rows = np.nonzero(kok)[0][both]
+                kok = np.zeros_like(kok)
+                kok[kok_rows] = True
+                zero = sc_o == 0  # dropped on both sides: all codes 0
+                assert not g["k_coef"][kok][zero].any() and not o["k_coef"][kok][zero].any()
             sbad = sc_g != sc_o
             assert np.all(harness.f16_boundary(amax[sbad])), f"head {bh}: coefficient scale differs off a tie"
             stats["cscale_f16"] += int(sbad.sum())
@@ -198,6 +220,16 @@ NOPSAC = synth.Workload(name="g64-r0-m1", dtype="bf16", batch=1, heads=2, head_d
 SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC]
 FULL = ["mg2-12h", "lingbot-40h", "batched-4x30h", "rollout-30k", "rollout-120k"]
 
+# App. D.1 storage options: 8-bit group scales (I8), the retention gate, both.
+# D64 has r = 20 over a 32-rank stride (the unaligned coefficient load), RAGGED
+# uneven tiles and batch 2, NOPSAC r = 0 (the gate has nothing to do).
+_I8, _GATE = oracle.STORE_SCALE_I8, oracle.STORE_GATE
+STORAGE = [synth.scaled(synth.WORKLOADS["tiny-f32"], name="tiny-f32-i8", storage=_I8),
+           synth.scaled(RAGGED, name="ragged-i8-gate", storage=_I8 | _GATE),
+           synth.scaled(D64, name="d64-i8", storage=_I8),
+           synth.scaled(D64, name="d64-gate", storage=_GATE),
+           synth.scaled(NOPSAC, name="g64-r0-i8-gate", storage=_I8 | _GATE)]
+
 _cases = {}
 
 
@@ -251,6 +283,18 @@ def test_small_parity(wl):
 def test_full_size_parity(name):
     wl = synth.WORKLOADS[name]
     run_case(wl, max_sources=3, n_heads_rows=6, row_step=37, logits_rows=16)
+
+
+@pytest.mark.parametrize("wl", STORAGE, ids=[w.name for w in STORAGE])
+def test_storage_parity(wl):
+    run_case(wl, max_sources=64, n_heads_rows=64, row_step=1, logits_rows=wl.n_q)
+
+
+@pytest.mark.timeout(900)
+def test_storage_full_size_parity():
+    wl = synth.scaled(synth.WORKLOADS["mg2-12h"], name="mg2-12h-i8-gate", storage=_I8 | _GATE)
+    run_case(wl, max_sources=3, n_heads_rows=6, row_step=37, logits_rows=16)
+
 
 
 # ------------------------------------------------------------ calibration
