@@ -107,14 +107,15 @@ def mode_tables(tables, wl, mode):
     return (top_m or wl.top_m, rank), (mu_k, mu_v, w_m, u_t if rank else None, lam if rank else None)
 
 
-def gpu_logits(wl, tables, top_m: int, rank: int, n_eval: int) -> np.ndarray:
+def gpu_logits(wl, tables, top_m: int, rank: int, n_eval: int, storage: int = 0) -> np.ndarray:
     """Quantise the whole cache with these tables and return the masked logits
-    [B, H, n_eval, n_cache] of the first n_eval Queries (scaled by 1/sqrt(d))."""
+    [B, H, n_eval, n_cache] of the first n_eval Queries (scaled by 1/sqrt(d)).
+    storage: App. D.1 options (1 = 8-bit group scales, 2 = retention gate)."""
     torch, qw = _torch()
     dev = "cuda:0"
     dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     cfg = qw.make_config(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, rank, top_m, wl.n_cache,
-                         wl.dtype)
+                         wl.dtype, storage)
     mu_k, mu_v, w, u_t, lam = tables
     T = lambda x, t=dt: torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(dev).to(t)  # noqa: E731
     calib = torch.zeros(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=dev)
@@ -144,10 +145,17 @@ def exact_logits(wl, n_eval: int) -> np.ndarray:
     return out
 
 
-def evaluate(wl, tables, n_eval: int, modes=tuple(MODES), m_sweep=(1, 2, 4, 8)) -> dict:
+# App. D.1 storage options, applied to the "both" mode
+STORAGE = {"i8_scales": 1, "gate": 2, "i8_scales+gate": 3}
+
+
+def evaluate(wl, tables, n_eval: int, modes=tuple(MODES), m_sweep=(1, 2, 4, 8), storage=tuple(STORAGE)) -> dict:
     exact = exact_logits(wl, n_eval)
     vis = visible_mask(wl, n_eval, wl.n_cache)
-    res = {"modes": {}, "m_sweep": {}}
+    res = {"modes": {}, "m_sweep": {}, "storage": {}}
+    for name in storage:
+        (top_m, rank), t = mode_tables(tables, wl, "both")
+        res["storage"][name] = metrics(exact, gpu_logits(wl, t, top_m, rank, n_eval, STORAGE[name]), vis)
     for mode in modes:
         (top_m, rank), t = mode_tables(tables, wl, mode)
         res["modes"][mode] = metrics(exact, gpu_logits(wl, t, top_m, rank, n_eval), vis)

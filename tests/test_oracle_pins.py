@@ -470,6 +470,16 @@ def test_token_bytes_and_paper_compression():
         assert oracle.token_bytes(oracle.cfg_of(1, 1, d, 16, G, r, 4, 64, True)) == want
 
 
+def test_psac_rank_bits_match_the_rank_sweep():
+    # T9 context: dense INT8 rows cost 8 bits per rank per Key token-head, so
+    # going from r = 8 to r = 16 adds 64 bits over the 2d = 256 K and V elements:
+    # 0.25 bits per element, within 3% of the 0.2569 reported on Causal-Forcing.
+    kb8, vb8 = oracle.token_bytes(oracle.cfg_of(1, 1, 128, 128, 32, 8, 4, 64, True))
+    kb16, vb16 = oracle.token_bytes(oracle.cfg_of(1, 1, 128, 128, 32, 16, 4, 64, True))
+    dbits = 8 * ((kb16 + vb16) - (kb8 + vb8)) / 256
+    assert dbits == 0.25 and abs(dbits / 0.2569 - 1) < 0.03
+
+
 def test_token_bytes_with_8bit_group_scales():
     # App. D.1: group scales as 8-bit codes plus one FP16 secondary scale per
     # token-head, so ng group scales take ng + 2 bytes instead of 2 ng.

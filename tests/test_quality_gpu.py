@@ -24,9 +24,9 @@ def _oracle_tables(wl):
     return oracle.calibrate(cfg, qh, k, v, wl.kmeans_iters)
 
 
-def _oracle_logits(wl, tables, top_m, rank, n_eval):
+def _oracle_logits(wl, tables, top_m, rank, n_eval, storage=0):
     cfg = oracle.cfg_of(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, rank, top_m, wl.n_cache,
-                        wl.dtype == "bf16")
+                        wl.dtype == "bf16", storage)
     cache = oracle.new_cache(cfg)
     k = synth.round_to(synth.tensor(wl, "k", wl.n_cache), wl.dtype)
     v = synth.round_to(synth.tensor(wl, "v", wl.n_cache), wl.dtype)
@@ -53,6 +53,13 @@ def test_quality_metrics_match_oracle():
         g = quality.metrics(exact, quality.gpu_logits(wl, t, top_m, rank, n_eval), vis)
         o = quality.metrics(exact, _oracle_logits(wl, t, top_m, rank, n_eval), vis)
         _say(f"[ok] quality {mode}: gpu {g} oracle {o}")
+        assert abs(g["logit_mse"] - o["logit_mse"]) <= 1e-3 * o["logit_mse"]
+        assert abs(g["top1_shift"] - o["top1_shift"]) <= 2.0 / (wl.batch * wl.heads * n_eval)
+    for name, storage in quality.STORAGE.items():
+        (top_m, rank), t = quality.mode_tables(tables, wl, "both")
+        g = quality.metrics(exact, quality.gpu_logits(wl, t, top_m, rank, n_eval, storage), vis)
+        o = quality.metrics(exact, _oracle_logits(wl, t, top_m, rank, n_eval, storage), vis)
+        _say(f"[ok] quality both + {name}: gpu {g} oracle {o}")
         assert abs(g["logit_mse"] - o["logit_mse"]) <= 1e-3 * o["logit_mse"]
         assert abs(g["top1_shift"] - o["top1_shift"]) <= 2.0 / (wl.batch * wl.heads * n_eval)
 
