@@ -43,6 +43,12 @@ CASES = [
     (_wl("token-causal", frame_tokens=1), None),
     (_wl("zero-query"), "zero_q"),
     (_wl("large-logits", out_scale=10.0), "big_q"),
+    # App. D.1 storage options on the degenerate cases: all-zero group steps give
+    # sigma = 0 (every step code 0), a single centroid, and a lone partial tile
+    (_wl("zero-residual-i8-gate", kmeans_iters=0, storage=3), "zero_residual"),
+    (_wl("kc1-i8", n_centroids=1, head_dim=64, group_size=16, rank=4, q_rank=4, storage=1), None),
+    (_wl("one-partial-tile-i8-gate", n_cache=40, n_q=1, q_start=39, frame_tokens=1, chunk=40, n_hist=100,
+         storage=3), None),
 ]
 
 
@@ -68,6 +74,8 @@ def test_edge_case(wl, kind):
         import packed
         f = packed.fields(case.cache, case.lay, 0, 0, wl.n_cache)
         assert int((f["k_scale"] == 0).sum()) > 0, "the case should contain zero-scale groups"
+        if wl.storage & 1:
+            assert int((f["k_sigma"] == 0).sum()) > 0, "the case should contain zero secondary scales"
         if wl.rank:
             assert int((f["k_cscale"] == 0).sum()) > 0, "the case should contain zero coefficient rows"
     tp.run_case(wl, max_sources=64, n_heads_rows=64, row_step=1, logits_rows=wl.n_q)
