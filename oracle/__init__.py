@@ -32,12 +32,16 @@ class OraCfg(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int), ("heads", ctypes.c_int), ("head_dim", ctypes.c_int),
                 ("n_centroids", ctypes.c_int), ("group_size", ctypes.c_int),
                 ("rank", ctypes.c_int), ("top_m", ctypes.c_int),
-                ("capacity", ctypes.c_longlong), ("table_bf16", ctypes.c_int), ("storage", ctypes.c_int)]
+                ("capacity", ctypes.c_longlong), ("table_bf16", ctypes.c_int), ("storage", ctypes.c_int),
+                ("metric", ctypes.c_int)]
 
 
 # App. D.1 storage options (ORA_STORE_* in quantwm_oracle.h)
 STORE_SCALE_I8 = 1
 STORE_GATE = 2
+# QSAC candidate metric (ORA_METRIC_*): Eq. 9 or the full quadratic form
+METRIC_DIAG = 0
+METRIC_FULL = 1
 
 
 _lib = None
@@ -61,14 +65,16 @@ def lib():
     return _lib
 
 
-def cfg_of(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, bf16, storage=0) -> OraCfg:
-    return OraCfg(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, int(bf16), int(storage))
+def cfg_of(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, bf16, storage=0,
+           metric=0) -> OraCfg:
+    return OraCfg(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, int(bf16), int(storage),
+                  int(metric))
 
 
 def cfg_from_workload(wl, capacity=None) -> OraCfg:
     return cfg_of(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank,
                   wl.top_m, wl.capacity if capacity is None else capacity, wl.dtype == "bf16",
-                  getattr(wl, "storage", 0))
+                  getattr(wl, "storage", 0), getattr(wl, "metric", 0))
 
 
 def _p(a, ct=ctypes.c_float):
@@ -170,6 +176,17 @@ def qsac_assign(k, mu, w, group_size, top_m):
     return int(z), cand[: min(top_m, kc)].copy()
 
 
+def qsac_assign_full(k, mu, m, w, group_size, top_m):
+    """QSAC with the candidates ranked by (k - mu)^T m (k - mu); m is [d, d]."""
+    k, mu, m, w = _f32(k), _f32(mu), _f32(m), _f32(w)
+    kc, d = mu.shape
+    assert m.shape == (d, d)
+    cand = np.zeros(max(kc, 1), np.int32)
+    z = lib().ora_qsac_assign_full(_p(k), _p(mu), _p(m), _p(w), kc, d, group_size, top_m,
+                                   _p(cand, ctypes.c_int))
+    return int(z), cand[: min(top_m, kc)].copy()
+
+
 def nearest(x, mu):
     x, mu = _f32(x), _f32(mu)
     return int(lib().ora_nearest(_p(x), _p(mu), mu.shape[0], mu.shape[1]))
@@ -186,7 +203,9 @@ def eigh(a):
 
 
 def calibrate(cfg: OraCfg, q_hist, k_cal, v_cal, kmeans_iters):
-    """Returns (mu_k, mu_v, w, u_t, lam) as float32 arrays."""
+    """Returns (mu_k, mu_v, w, u_t, lam) as float32 arrays, and with the full
+    metric (cfg.metric == METRIC_FULL) a sixth table: m [B, H, d, d], the Query
+    second moment over the mean of its diagonal."""
     B, H, d, K, r = cfg.batch, cfg.heads, cfg.head_dim, cfg.n_centroids, cfg.rank
     q_hist = _f32(q_hist) if q_hist is not None else np.zeros((B, 0, H, d), np.float32)
     k_cal, v_cal = _f32(k_cal), _f32(v_cal)
@@ -195,11 +214,13 @@ def calibrate(cfg: OraCfg, q_hist, k_cal, v_cal, kmeans_iters):
     w = np.zeros((B, H, d), np.float32)
     u_t = np.zeros((B, H, max(r, 0), d), np.float32)
     lam = np.zeros((B, H, max(r, 0)), np.float32)
+    full = cfg.metric == METRIC_FULL
+    m = np.zeros((B, H, d, d), np.float32) if full else None
     rc = lib().ora_calibrate(ctypes.byref(cfg), _p(q_hist), ctypes.c_longlong(q_hist.shape[1]),
                              _p(k_cal), _p(v_cal), ctypes.c_longlong(k_cal.shape[1]), kmeans_iters,
-                             _p(mu_k), _p(mu_v), _p(w), _p(u_t), _p(lam))
+                             _p(mu_k), _p(mu_v), _p(w), _p(u_t), _p(lam), _p(m))
     _check(rc, "calibrate")
-    return mu_k, mu_v, w, u_t, lam
+    return (mu_k, mu_v, w, u_t, lam, m) if full else (mu_k, mu_v, w, u_t, lam)
 
 
 def new_cache(cfg: OraCfg) -> np.ndarray:
@@ -207,9 +228,11 @@ def new_cache(cfg: OraCfg) -> np.ndarray:
 
 
 def append(cfg: OraCfg, tables, cache, n_cached, k_new, v_new, diagnostics=False):
-    """Writes slots [n_cached, n_cached + n) in place; returns diagnostics if asked."""
+    """Writes slots [n_cached, n_cached + n) in place; returns diagnostics if asked.
+    tables: (mu_k, mu_v, w, u_t[, lam[, m]]); m is read with the full metric only."""
     mu_k, mu_v, w, u_t = (_f32(t) for t in tables[:4])
     lam = _f32(tables[4]) if len(tables) > 4 and tables[4] is not None else None
+    m = _f32(tables[5]) if len(tables) > 5 and tables[5] is not None else None
     k_new, v_new = _f32(k_new), _f32(v_new)
     B, n, H = k_new.shape[0], k_new.shape[1], k_new.shape[2]
     M = min(cfg.top_m, cfg.n_centroids)
@@ -217,7 +240,7 @@ def append(cfg: OraCfg, tables, cache, n_cached, k_new, v_new, diagnostics=False
     kid = np.zeros((B, H, n), np.int32) if diagnostics else None
     vid = np.zeros((B, H, n), np.int32) if diagnostics else None
     cand = np.zeros((B, H, n, M), np.int32) if diagnostics else None
-    rc = lib().ora_append(ctypes.byref(cfg), _p(mu_k), _p(mu_v), _p(w), _p(u_t), _p(lam),
+    rc = lib().ora_append(ctypes.byref(cfg), _p(mu_k), _p(mu_v), _p(w), _p(u_t), _p(lam), _p(m),
                           _p(cache, ctypes.c_uint8), ctypes.c_longlong(n_cached),
                           _p(k_new), _p(v_new), ctypes.c_longlong(n), _p(coef),
                           _p(kid, ctypes.c_int), _p(vid, ctypes.c_int), _p(cand, ctypes.c_int))

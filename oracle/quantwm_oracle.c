@@ -101,6 +101,7 @@ static int valid_cfg(const ora_cfg* c) {
   if (c->rank < 0 || c->rank > c->head_dim) return 0;
   if (c->top_m < 1 || c->capacity < 0) return 0;
   if (c->storage & ~(ORA_STORE_SCALE_I8 | ORA_STORE_GATE)) return 0;
+  if (c->metric != ORA_METRIC_DIAG && c->metric != ORA_METRIC_FULL) return 0;
   return 1;
 }
 
@@ -262,13 +263,13 @@ static void group_weights(const float* w, int d, int G, float* Wg) {
 
 static int less_pair(float a, int ia, float b, int ib) { return a < b || (a == b && ia < ib); }
 
-int ora_qsac_assign(const float* k, const float* mu, const float* w, int n_centroids,
-                    int d, int group_size, int top_m, int* cand) {
-  float dist[256], Wg[256];
+/* Top-M candidate set C_i by (distance, id), then the argmin of the Eq. 12
+ * score over it (ties to the lower id). */
+static int qsac_select(const float* k, const float* mu, const float* dist, const float* w, int n_centroids,
+                       int d, int group_size, int top_m, int* cand) {
+  float Wg[256];
   int taken[256] = {0};
   int M = top_m < n_centroids ? top_m : n_centroids;
-  for (int j = 0; j < n_centroids; ++j) dist[j] = dq_distance(k, mu + (long long)j * d, w, d);
-  /* top-M candidate set C_i by (d_Q, id) */
   for (int m = 0; m < M; ++m) {
     int best = -1;
     for (int j = 0; j < n_centroids; ++j)
@@ -285,6 +286,34 @@ int ora_qsac_assign(const float* k, const float* mu, const float* w, int n_centr
     if (z < 0 || less_pair(S, j, Sz, z)) { z = j; Sz = S; }
   }
   return z;
+}
+
+int ora_qsac_assign(const float* k, const float* mu, const float* w, int n_centroids,
+                    int d, int group_size, int top_m, int* cand) {
+  float dist[256];
+  for (int j = 0; j < n_centroids; ++j) dist[j] = dq_distance(k, mu + (long long)j * d, w, d);
+  return qsac_select(k, mu, dist, w, n_centroids, d, group_size, top_m, cand);
+}
+
+/* The full quadratic form (k - mu_j)^T m (k - mu_j) of the diagonal-approximation
+ * ablation (App. C), fp32: the matrix-vector product first, rows in order. */
+static float full_distance(const float* k, const float* mu_j, const float* m, int d) {
+  float e[256];
+  for (int c = 0; c < d; ++c) e[c] = k[c] - mu_j[c];
+  float acc = 0.0f;
+  for (int c = 0; c < d; ++c) {
+    float t = 0.0f;
+    for (int c2 = 0; c2 < d; ++c2) t = t + m[(long long)c * d + c2] * e[c2];
+    acc = acc + e[c] * t;
+  }
+  return acc;
+}
+
+int ora_qsac_assign_full(const float* k, const float* mu, const float* m, const float* w, int n_centroids,
+                         int d, int group_size, int top_m, int* cand) {
+  float dist[256];
+  for (int j = 0; j < n_centroids; ++j) dist[j] = full_distance(k, mu + (long long)j * d, m, d);
+  return qsac_select(k, mu, dist, w, n_centroids, d, group_size, top_m, cand);
 }
 
 int ora_nearest(const float* x, const float* mu, int n_centroids, int d) {
@@ -399,7 +428,7 @@ static void kmeans(const ora_cfg* c, const float* x, long long xs, long long n, 
 
 int ora_calibrate(const ora_cfg* cfg, const float* q_hist, long long n_hist,
                   const float* k_cal, const float* v_cal, long long n_cal, int kmeans_iters,
-                  float* mu_k, float* mu_v, float* w, float* u_t, float* lam) {
+                  float* mu_k, float* mu_v, float* w, float* u_t, float* lam, float* m_out) {
   if (!valid_cfg(cfg) || n_hist < 0 || n_cal < 0 || kmeans_iters < 0) return -1;
   if ((n_hist > 0 && !q_hist) || (n_cal > 0 && (!k_cal || !v_cal))) return -1;
   if (!mu_k || !mu_v || !w || (cfg->rank > 0 && (!u_t || !lam))) return -1;
@@ -429,12 +458,18 @@ int ora_calibrate(const ora_cfg* cfg, const float* q_hist, long long n_hist,
       for (int i = 0; i < d * d; ++i) M[i] /= (double)n_hist;
       for (int i = 0; i < d; ++i) tr += M[i * d + i];
     }
+    float* mo = m_out ? m_out + (long long)bh * d * d : NULL;
     if (n_hist == 0 || tr == 0.0) {
       /* cold start: uniform sensitivity, PSAC inactive */
       for (int c = 0; c < d; ++c) wo[c] = 1.0f;
       for (long long i = 0; i < (long long)r * d; ++i) uo[i] = 0.0f;
       for (int k = 0; k < r; ++k) lo[k] = 0.0f;
+      if (mo)
+        for (int i = 0; i < d * d; ++i) mo[i] = (i / d == i % d) ? 1.0f : 0.0f;
     } else {
+      /* the full metric: M over the mean of its diagonal, so its diagonal is w */
+      if (mo)
+        for (int i = 0; i < d * d; ++i) mo[i] = (float)(M[i] / (tr / (double)d));
       /* Eq. 8: w_c = M_cc / ((1/d) sum_c' M_c'c') */
       for (int c = 0; c < d; ++c) wo[c] = (float)(M[c * d + c] / (tr / (double)d));
       /* Eq. 15-16: top-r eigenvectors of M */
@@ -492,7 +527,7 @@ static void store_residual(const layout* L, int G, const float* x, const float* 
 }
 
 int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const float* w,
-               const float* u_t, const float* lam, uint8_t* cache, long long n_cached,
+               const float* u_t, const float* lam, const float* m_full, uint8_t* cache, long long n_cached,
                const float* k_new, const float* v_new, long long n_new,
                float* coef_f32, int* k_ids, int* v_ids, int* cand) {
   if (!valid_cfg(cfg) || n_cached < 0 || n_new < 0) return -1;
@@ -501,6 +536,8 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
   if (!mu_k || !mu_v || !w || !cache || !k_new || !v_new || (cfg->rank > 0 && !u_t)) return -1;
   const int gate = (cfg->storage & ORA_STORE_GATE) && cfg->rank > 0;
   if (gate && !lam) return -1;
+  const int full = cfg->metric == ORA_METRIC_FULL;
+  if (full && !m_full) return -1;
   const layout L = make_layout(cfg);
   const int d = cfg->head_dim, H = cfg->heads, K = cfg->n_centroids, r = cfg->rank, G = cfg->group_size;
   const int M = cfg->top_m < K ? cfg->top_m : K;
@@ -520,8 +557,9 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
       const float* k = k_new + src;
       const float* v = v_new + src;
       long long diag = ((long long)bh * n_new + t);
-      /* QSAC: top-M by Eq. 9, then argmin of Eq. 12 */
-      int z = ora_qsac_assign(k, muk, wh, K, d, G, M, cands);
+      /* QSAC: top-M by Eq. 9 (or the full form), then argmin of Eq. 12 */
+      int z = full ? ora_qsac_assign_full(k, muk, m_full + (long long)bh * d * d, wh, K, d, G, M, cands)
+                   : ora_qsac_assign(k, muk, wh, K, d, G, M, cands);
       cache[L.k_ids + slot] = (uint8_t)z;
       store_residual(&L, G, k, muk + (long long)z * d, cache + L.k_codes + slot * (d / 4),
                      cache + L.k_zp + slot * L.zpb, cache + L.k_scale + slot * L.sb, cache + L.k_sigma + slot * 2,

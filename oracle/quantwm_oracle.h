@@ -39,6 +39,7 @@ typedef struct {
   long long capacity;          /* cache slots per (b, h) */
   int table_bf16;              /* 1: centroids, U_r and attention operands are BF16 */
   int storage;                 /* ORA_STORE_* flags (App. D.1 packed-storage options) */
+  int metric;                  /* ORA_METRIC_*: the distance of the QSAC candidate search */
 } ora_cfg;
 
 /* App. D.1 storage options. SCALE_I8: the group step sizes of a token-head are
@@ -49,6 +50,15 @@ typedef struct {
  * otherwise its codes and scale are zero. */
 #define ORA_STORE_SCALE_I8 1
 #define ORA_STORE_GATE 2
+
+/* QSAC candidate metric. DIAG: Eq. 9, the channel-weighted distance with w, the
+ * diagonal of the normalised Query second moment. FULL: the full quadratic form
+ * of App. C (the diagonal-approximation ablation), (k - mu)^T Mn (k - mu) with
+ * Mn = M / ((1/d) tr M), whose diagonal is w; the ranking is the same for any
+ * positive multiple of M. At cold start Mn is the identity. The candidate score
+ * (Eq. 10-12) and everything after it are unchanged. */
+#define ORA_METRIC_DIAG 0
+#define ORA_METRIC_FULL 1
 
 /* Packed cache size in bytes and the per-token-head byte counts (K and V). */
 long long ora_cache_bytes(const ora_cfg* cfg);
@@ -81,13 +91,21 @@ int ora_keep_row(const float* C, const int8_t* codes, float scale, const float* 
 int ora_qsac_assign(const float* k, const float* mu, const float* w, int n_centroids,
                     int d, int group_size, int top_m, int* cand);
 
+/* The same with the candidates ranked by the full quadratic form (ORA_METRIC_FULL):
+ * e = k - mu_j (fp32), t_c = sum_c' m[c][c'] e_c' (c' in order), d_j = sum_c e_c t_c.
+ * m is [d][d] fp32; the Eq. 12 score still uses w. */
+int ora_qsac_assign_full(const float* k, const float* mu, const float* m, const float* w, int n_centroids,
+                         int d, int group_size, int top_m, int* cand);
+
 /* Plain nearest centroid (Euclidean), ties to the lower id. */
 int ora_nearest(const float* x, const float* mu, int n_centroids, int d);
 
-/* Eq. 6, Eq. 8 and Eq. 15, plus Lloyd K-means centroids (Eq. 3). */
+/* Eq. 6, Eq. 8 and Eq. 15, plus Lloyd K-means centroids (Eq. 3). m_out
+ * [B,H,d,d] (optional) receives Mn = M / ((1/d) tr M) rounded to fp32 (the
+ * identity at cold start), the matrix of ORA_METRIC_FULL. */
 int ora_calibrate(const ora_cfg* cfg, const float* q_hist, long long n_hist,
                   const float* k_cal, const float* v_cal, long long n_cal, int kmeans_iters,
-                  float* mu_k, float* mu_v, float* w, float* u_t, float* lam);
+                  float* mu_k, float* mu_v, float* w, float* u_t, float* lam, float* m_out);
 
 /* Cyclic Jacobi eigendecomposition of a symmetric n x n matrix (fp64).
  * Returns eigenvalues descending in lam and eigenvectors as rows of vecs_t. */
@@ -97,9 +115,9 @@ int ora_eigh(const double* a, int n, double* lam, double* vecs_t);
  * written into cache slots [n_cached, n_cached + n_new) of every (b, h).
  * coef_f32 [B,H,n_new,r], k_ids/v_ids [B,H,n_new] and cand [B,H,n_new,M] are
  * optional diagnostics (NULL to skip). lam [B,H,r] (the stored eigenvalues) is
- * read only with ORA_STORE_GATE. */
+ * read only with ORA_STORE_GATE, m_full [B,H,d,d] only with ORA_METRIC_FULL. */
 int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const float* w,
-               const float* u_t, const float* lam, uint8_t* cache, long long n_cached,
+               const float* u_t, const float* lam, const float* m_full, uint8_t* cache, long long n_cached,
                const float* k_new, const float* v_new, long long n_new,
                float* coef_f32, int* k_ids, int* v_ids, int* cand);
 

@@ -224,6 +224,108 @@ def test_qsac_candidates_are_top_m_and_exhaustive_limit():
         assert S[z4] == S[list(cand)].min() or abs(S[z4] - S[list(cand)].min()) <= 1e-5 * S[z4]
 
 
+def _spd(r, d, cond=20.0):
+    """A random symmetric positive-definite matrix with mean diagonal 1 (fp32)."""
+    q, _ = np.linalg.qr(r.standard_normal((d, d)))
+    ev = np.exp(np.linspace(0.0, math.log(cond), d))
+    m = (q * ev[None, :]) @ q.T
+    return (m / np.trace(m) * d).astype(np.float32)
+
+
+def _clear_gap(dist, m, rel=1e-4):
+    srt = np.sort(dist)
+    return m >= len(dist) or srt[m] - srt[m - 1] > rel * abs(srt[m - 1]) + 1e-12
+
+
+def test_full_metric_candidates_are_mahalanobis_top_m():
+    # App. C ablation: the full quadratic form (k - mu)^T M (k - mu) is the squared
+    # Mahalanobis distance with inverse covariance M (scipy's cdist).
+    from scipy.spatial.distance import cdist
+    r = rng(21)
+    d, kc, G = 64, 16, 16
+    m = _spd(r, d)
+    w = np.diag(m).astype(np.float32)
+    mu = synth.round_to(r.standard_normal((kc, d)), "bf16")
+    checked = 0
+    for _ in range(100):
+        k = synth.round_to(mu[r.integers(kc)] + 0.7 * r.standard_normal(d), "bf16")
+        dist = cdist(k[None].astype(np.float64), mu.astype(np.float64), "mahalanobis",
+                     VI=m.astype(np.float64))[0] ** 2
+        _, cand = oracle.qsac_assign_full(k, mu, m, w, G, 4)
+        if _clear_gap(dist, 4):
+            assert set(cand) == set(np.argsort(dist)[:4])
+            checked += 1
+    assert checked > 90
+
+
+def test_full_metric_with_a_diagonal_matrix_is_eq9():
+    # With M diagonal the full form is the Eq. 9 distance with w = diag(M): the
+    # candidate lists and the choice equal those of plain QSAC.
+    r = rng(22)
+    d, kc, G = 64, 32, 32
+    w = r.uniform(0.1, 3.0, d).astype(np.float32)
+    m = np.diag(w).astype(np.float32)
+    mu = synth.round_to(r.standard_normal((kc, d)) * 2, "bf16")
+    for _ in range(100):
+        k = synth.round_to(mu[r.integers(kc)] + r.standard_normal(d), "bf16")
+        dist = ((k.astype(np.float64) - mu) ** 2 * w).sum(1)
+        zf, cf = oracle.qsac_assign_full(k, mu, m, w, G, 4)
+        zd, cd = oracle.qsac_assign(k, mu, w, G, 4)
+        if _clear_gap(dist, 4) and all(_clear_gap(np.sort(dist)[:4], i) for i in range(1, 4)):
+            assert list(cf) == list(cd) and zf == zd
+
+
+def test_full_metric_rank_one_is_nearest_along_the_direction():
+    # M = u u^T gives (u.(k - mu))^2: the candidates are the centroids whose
+    # projections on u are nearest to k's (a one-dimensional nearest neighbour).
+    r = rng(23)
+    d, kc, G = 32, 16, 16
+    u = r.standard_normal(d)
+    u /= np.linalg.norm(u)
+    m = np.outer(u, u).astype(np.float32)
+    w = np.diag(m).astype(np.float32)
+    mu = synth.round_to(r.standard_normal((kc, d)), "bf16")
+    checked = 0
+    for _ in range(100):
+        k = synth.round_to(r.standard_normal(d), "bf16")
+        gap = np.abs(mu.astype(np.float64) @ u - k.astype(np.float64) @ u)
+        _, cand = oracle.qsac_assign_full(k, mu, m, w, G, 3)
+        if _clear_gap(gap ** 2, 3, 1e-3):
+            assert set(cand) == set(np.argsort(gap)[:3])
+            checked += 1
+    assert checked > 80
+
+
+def test_full_metric_is_rotation_invariant():
+    # Rotating Keys, centroids and the metric together (k -> Qk, mu -> Q mu,
+    # M -> Q M Q^T) keeps every full-form distance, so the candidate list is the
+    # same; the diagonal form has no such invariance.
+    r = rng(24)
+    d, kc, G = 32, 16, 16
+    m = _spd(r, d, cond=50.0)
+    q, _ = np.linalg.qr(r.standard_normal((d, d)))
+    mu = r.standard_normal((kc, d)).astype(np.float32)
+    mu_r = (mu.astype(np.float64) @ q.T).astype(np.float32)
+    m_r = (q @ m.astype(np.float64) @ q.T).astype(np.float32)
+    w, w_r = np.diag(m).copy(), np.diag(m_r).copy()
+    same = differ_diag = 0
+    for _ in range(100):
+        k = (mu[r.integers(kc)] + 0.8 * r.standard_normal(d)).astype(np.float32)
+        k_r = (k.astype(np.float64) @ q.T).astype(np.float32)
+        e = k.astype(np.float64) - mu
+        dist = np.einsum("jc,cd,jd->j", e, m.astype(np.float64), e)
+        if not all(_clear_gap(np.sort(dist)[:5], i, 1e-3) for i in range(1, 5)):
+            continue
+        _, c0 = oracle.qsac_assign_full(k, mu, m, w, G, 4)
+        _, c1 = oracle.qsac_assign_full(k_r, mu_r, m_r, w_r, G, 4)
+        assert list(c0) == list(c1)
+        same += 1
+        _, d0 = oracle.qsac_assign(k, mu, w, G, 4)
+        _, d1 = oracle.qsac_assign(k_r, mu_r, w_r, G, 4)
+        differ_diag += list(d0) != list(d1)
+    assert same > 50 and differ_diag > 0
+
+
 # ------------------------------------------------------------- calibration
 
 def _small_workload(**kw):
@@ -295,6 +397,55 @@ def test_calibrate_cold_start():
     k = synth.tensor(wl, "k", 64)
     _, _, w, u_t, lam = oracle.calibrate(cfg, None, k, k, 2)
     assert np.all(w == 1.0) and not u_t.any() and not lam.any()
+
+
+def test_calibrate_full_metric_matrix():
+    # The full metric's matrix is Eq. 6's M over the mean of its diagonal: its
+    # diagonal is exactly w (Eq. 8), it is symmetric, it matches numpy's M up to
+    # that scale, and at cold start it is the identity.
+    wl = _small_workload()
+    cfg = oracle.cfg_from_workload(wl)
+    cfg.metric = oracle.METRIC_FULL
+    qh = synth.tensor(wl, "qhist", wl.n_hist)
+    k = synth.tensor(wl, "k", 256)
+    mu_k, _, w, _, _, m = oracle.calibrate(cfg, qh, k, k, 2)
+    for h in range(wl.heads):
+        assert np.array_equal(np.diag(m[0, h]), w[0, h])
+        assert np.array_equal(m[0, h], m[0, h].T)
+        q = qh[0, :, h, :].astype(np.float64)
+        M = q.T @ q / q.shape[0]
+        np.testing.assert_allclose(m[0, h], M / np.trace(M) * wl.head_dim, rtol=1e-5, atol=1e-6)
+    *_, m0 = oracle.calibrate(cfg, None, k, k, 2)
+    assert np.array_equal(m0[0, 0], np.eye(wl.head_dim, dtype=np.float32))
+
+
+def test_append_full_metric_uses_each_heads_matrix():
+    # The append path ranks each head's Keys with that head's matrix: its ids and
+    # candidates equal QSAC with the full form per token, and the candidate
+    # lists differ from the Eq. 9 ones.
+    wl = _small_workload(heads=2, n_centroids=16)
+    cfg = oracle.cfg_from_workload(wl, capacity=128)
+    cfg.metric = oracle.METRIC_FULL
+    r = rng(25)
+    tables = list(oracle.calibrate(cfg, synth.tensor(wl, "qhist", 500), synth.tensor(wl, "k", 128),
+                                   synth.tensor(wl, "v", 128), 3))
+    tables[5] = np.stack([np.stack([_spd(r, wl.head_dim, 200.0) for _ in range(2)])])
+    tables[2] = np.ascontiguousarray(np.diagonal(tables[5], axis1=2, axis2=3))
+    k = synth.tensor(wl, "k", 128)
+    v = synth.tensor(wl, "v", 128)
+    cache = oracle.new_cache(cfg)
+    got = oracle.append(cfg, tables, cache, 0, k, v, diagnostics=True)
+    diff = 0
+    for h in range(2):
+        for t in range(128):
+            z, cand = oracle.qsac_assign_full(k[0, t, h], tables[0][0, h], tables[5][0, h], tables[2][0, h],
+                                              wl.group_size, wl.top_m)
+            assert got["k_ids"][0, h, t] == z and list(got["cand"][0, h, t]) == list(cand)
+            _, cd = oracle.qsac_assign(k[0, t, h], tables[0][0, h], tables[2][0, h], wl.group_size, wl.top_m)
+            diff += list(cd) != list(cand)
+    assert diff > 0
+    with pytest.raises(RuntimeError):
+        oracle.append(cfg, tables[:5], oracle.new_cache(cfg), 0, k, v)
 
 
 def test_kmeans_matches_sklearn_lloyd():
