@@ -54,7 +54,19 @@ typedef struct {
   int32_t dtype;       /* quantwm_dtype of Q/K/V/O, centroids and U_r */
   int64_t capacity;    /* cache slots per (b, h), at most 2^26 */
   int32_t storage;     /* QWM_STORE_* flags, 0 for the plain format (App. D.1 options) */
+  int32_t metric;      /* QWM_METRIC_*: distance of the QSAC candidate search */
 } quantwm_config;
+
+/* QSAC candidate metric (quantwm_config.metric).
+ * QWM_METRIC_DIAG (0): Eq. 9, sum_c w_c (k_c - mu_c)^2 with w from Eq. 8.
+ * QWM_METRIC_FULL (1): the full quadratic form (k - mu)^T Mn (k - mu) of the
+ *   diagonal-approximation ablation (App. C), with Mn = M / ((1/d) tr M) the
+ *   Eq. 6 second moment over the mean of its diagonal (so diag(Mn) = w; the
+ *   identity at cold start). Only the top-M candidate ranking changes: the
+ *   Eq. 12 score, the quantisers and the cache format are those of
+ *   QWM_METRIC_DIAG. The calibration block then carries Mn (field m). */
+#define QWM_METRIC_DIAG 0
+#define QWM_METRIC_FULL 1
 
 /* Packed-storage options of App. D.1 (flags of quantwm_config.storage).
  * QWM_STORE_SCALE_I8: the Eq. 2 step sizes t_g of a token-head's groups are kept
@@ -98,18 +110,20 @@ size_t quantwm_calib_bytes(const quantwm_config* cfg);
 
 /* Byte offsets of the fields inside one (b, h) slab of the calibration block:
  *   mu_k, mu_v  [Kc][d] dtype   Key / Value centroids (Eq. 3)
- *   a_k         [Kc][d] f32     -2 * w_c * mu_k[j][c]   (search constants of Eq. 9)
- *   b_k         [Kc]    f32     sum_c w_c * mu_k[j][c]^2
+ *   a_k         [Kc][d] f32     -2 * w_c * mu_k[j][c]   (search constants of Eq. 9;
+ *                               with QWM_METRIC_FULL: -2 * p_jc, p_j = Mn mu_k[j])
+ *   b_k         [Kc]    f32     sum_c w_c * mu_k[j][c]^2 (QWM_METRIC_FULL: sum_c p_jc mu_k[j][c])
  *   a_v, b_v                    the same for Values with w = 1
  *   w           [d]     f32     channel sensitivities (Eq. 8)
  *   wg          [d/G]   f32     per-group sums of w (Eq. 12)
  *   u_t         [r][d]  dtype   U_r transposed: row k is the k-th eigenvector (Eq. 15)
  *   lam         [r]     f32     the matching eigenvalues (0 at cold start)
  *   u_dr        [d][rs] f32     U_r itself (the transpose of u_t), ranks zero-padded to
- *                               rs = 16 (r <= 16) or 32 (r <= 32), for per-channel use */
+ *                               rs = 16 (r <= 16) or 32 (r <= 32), for per-channel use
+ *   m           [d][d]  f32     Mn, only with QWM_METRIC_FULL (no bytes otherwise) */
 typedef struct {
   int64_t slab_bytes;
-  int64_t mu_k, mu_v, a_k, b_k, a_v, b_v, w, wg, u_t, lam, u_dr;
+  int64_t mu_k, mu_v, a_k, b_k, a_v, b_v, w, wg, u_t, lam, u_dr, m;
 } quantwm_calib_layout;
 quantwm_status quantwm_calib_offsets(const quantwm_config* cfg, quantwm_calib_layout* out);
 
@@ -120,10 +134,12 @@ size_t quantwm_calibrate_workspace_bytes(const quantwm_config* cfg, int64_t n_hi
 
 /* Builds the calibration block from method-level tables (all device):
  * mu_k, mu_v [B,H,Kc,d] dtype; w [B,H,d] f32; u_t [B,H,r,d] dtype (NULL allowed
- * when r = 0); lam [B,H,r] f32 or NULL (then stored as 0). It derives the
- * search constants and group sums (Eq. 9, Eq. 12) on the device. */
+ * when r = 0); lam [B,H,r] f32 or NULL (then stored as 0); m [B,H,d,d] f32, the
+ * matrix of QWM_METRIC_FULL (required with it, ignored otherwise). It derives
+ * the search constants and group sums (Eq. 9 or the full form, Eq. 12) on the
+ * device. */
 quantwm_status quantwm_calib_pack(const quantwm_config* cfg, const void* mu_k, const void* mu_v,
-                                  const float* w, const void* u_t, const float* lam,
+                                  const float* w, const void* u_t, const float* lam, const float* m,
                                   void* calib, void* stream);
 
 /* QSAC/PSAC statistics and centroids for every (b, h):

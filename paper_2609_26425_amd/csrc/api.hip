@@ -61,6 +61,8 @@ quantwm_status check_cfg(const quantwm_config* c) {
     return fail(QWM_ERR_UNSUPPORTED, "capacity must be <= 2^26 slots per (b, h)");
   if (c->storage & ~(QWM_STORE_SCALE_I8 | QWM_STORE_GATE))
     return fail(QWM_ERR_INVALID_ARG, "storage has unknown flags 0x%x", unsigned(c->storage));
+  if (c->metric != QWM_METRIC_DIAG && c->metric != QWM_METRIC_FULL)
+    return fail(QWM_ERR_INVALID_ARG, "metric must be QWM_METRIC_DIAG or QWM_METRIC_FULL");
   return QWM_OK;
 }
 
@@ -117,17 +119,19 @@ size_t quantwm_calibrate_workspace_bytes(const quantwm_config* cfg, int64_t n_hi
 }
 
 quantwm_status quantwm_calib_pack(const quantwm_config* cfg, const void* mu_k, const void* mu_v, const float* w,
-                                  const void* u_t, const float* lam, void* calib, void* stream) {
+                                  const void* u_t, const float* lam, const float* m, void* calib, void* stream) {
   QWM_TRY(check_cfg(cfg));
   QWM_TRY(check_dev(mu_k, "mu_k"));
   QWM_TRY(check_dev(mu_v, "mu_v"));
   QWM_TRY(check_dev(w, "w"));
   QWM_TRY(check_dev(u_t, "u_t", false));
   QWM_TRY(check_dev(lam, "lam", false));
+  const bool full = cfg->metric == QWM_METRIC_FULL;
+  QWM_TRY(check_dev(m, "m", full));
   QWM_TRY(check_dev(calib, "calib"));
   if (cfg->rank > 0 && !u_t) return fail(QWM_ERR_INVALID_ARG, "u_t is null with rank > 0");
-  const hipError_t e = qwm::launch_pack_tables(*cfg, mu_k, mu_v, w, u_t, lam, static_cast<uint8_t*>(calib),
-                                               static_cast<hipStream_t>(stream));
+  const hipError_t e = qwm::launch_pack_tables(*cfg, mu_k, mu_v, w, u_t, lam, full ? m : nullptr,
+                                               static_cast<uint8_t*>(calib), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "calib_pack launch");
   return ok();
 }
@@ -144,17 +148,25 @@ static quantwm_status finish_calibration(const quantwm_config& c, const std::vec
   std::vector<float> w(size_t(bh) * d), lam(size_t(bh) * (r > 0 ? r : 1));
   std::vector<uint8_t> ut(size_t(bh) * (r > 0 ? r : 1) * d * e, 0);
   std::vector<double> ev(d), vt(size_t(d) * d);
+  const bool full = c.metric == QWM_METRIC_FULL;
+  std::vector<float> mn(full ? size_t(bh) * d * d : 0);
   for (int i = 0; i < bh; ++i) {
     const double* Mi = M.data() + size_t(i) * d * d;
     double tr = 0.0;
     for (int k = 0; k < d; ++k) tr += Mi[size_t(k) * d + k];
     float* wi = w.data() + size_t(i) * d;
+    float* mi = full ? mn.data() + size_t(i) * d * d : nullptr;
     if (cold || tr == 0.0) {  // cold start: uniform sensitivity, PSAC inactive
       for (int k = 0; k < d; ++k) wi[k] = 1.0f;
       for (int k = 0; k < r; ++k) lam[size_t(i) * r + k] = 0.0f;
+      if (mi)
+        for (int k = 0; k < d * d; ++k) mi[k] = (k / d == k % d) ? 1.0f : 0.0f;
       continue;
     }
     for (int k = 0; k < d; ++k) wi[k] = (float)(Mi[size_t(k) * d + k] / (tr / (double)d));
+    // the full metric: M over the mean of its diagonal (its diagonal is w)
+    if (mi)
+      for (int k = 0; k < d * d; ++k) mi[k] = (float)(Mi[k] / (tr / (double)d));
     qwm::host_eigh(Mi, d, ev.data(), vt.data());
     for (int k = 0; k < r; ++k) {
       lam[size_t(i) * r + k] = (float)ev[k];
@@ -185,6 +197,7 @@ static quantwm_status finish_calibration(const quantwm_config& c, const std::vec
     return hipMemcpy2DAsync(cal + off, size_t(C.slab_bytes), src, row, row, size_t(bh), hipMemcpyHostToDevice, s);
   };
   if ((he = put(C.w, w.data(), size_t(d) * 4)) != hipSuccess) return hip_fail(he, "w upload");
+  if (full && (he = put(C.m, mn.data(), size_t(d) * d * 4)) != hipSuccess) return hip_fail(he, "m upload");
   if (r > 0) {
     if ((he = put(C.u_t, ut.data(), size_t(r) * d * e)) != hipSuccess) return hip_fail(he, "u_t upload");
     if ((he = put(C.lam, lam.data(), size_t(r) * 4)) != hipSuccess) return hip_fail(he, "lam upload");

@@ -24,9 +24,12 @@ __device__ inline void store_rn(bf16* p, double x) { *p = to_bf16_rn(x); }
 // Eq. 12 group sums W_g, the expanded-distance constants of Eq. 9
 // (a_jc = -2 (w_c mu_jc), b_j = sum_c (w_c mu_jc) mu_jc; Values use w = 1) and
 // U_r in [d][r] order for the append kernel's per-channel PSAC accumulation.
+// With the full metric the Key constants expand (k - mu_j)^T Mn (k - mu_j)
+// instead: p_j = Mn mu_j (fp32, columns in order), a_jc = -2 p_jc and
+// b_j = sum_c p_jc mu_jc; the k^T Mn k term is the same for every centroid.
 template <typename T>
 __global__ __launch_bounds__(256) void derive_kernel(uint8_t* calib, quantwm_calib_layout C, int d, int G,
-                                                     int Kc, int r) {
+                                                     int Kc, int r, int full) {
   uint8_t* slab = calib + int64_t(blockIdx.x) * C.slab_bytes;
   const float* w = reinterpret_cast<const float*>(slab + C.w);
   float* wg = reinterpret_cast<float*>(slab + C.wg);
@@ -41,12 +44,21 @@ __global__ __launch_bounds__(256) void derive_kernel(uint8_t* calib, quantwm_cal
     for (int c = g * G; c < (g + 1) * G; ++c) s = s + w[c];
     wg[g] = s;
   }
+  const float* mm = reinterpret_cast<const float*>(slab + C.m);
   for (int i = threadIdx.x; i < Kc * d; i += 256) {
     const int c = i % d;
     const float mkv = ldf(mk + i), mvv = ldf(mv + i);
-    ak[i] = -2.0f * (w[c] * mkv);
+    if (full) {
+      const T* mj = mk + (i / d) * d;
+      float p = 0.0f;
+      for (int c2 = 0; c2 < d; ++c2) p = __builtin_fmaf(mm[c * d + c2], ldf(mj + c2), p);
+      ak[i] = -2.0f * p;
+    } else {
+      ak[i] = -2.0f * (w[c] * mkv);
+    }
     av[i] = -2.0f * mvv;
   }
+  __syncthreads();  // b_k reads the a_k rows written by other threads
   const T* ut = reinterpret_cast<const T*>(slab + C.u_t);
   float* udr = reinterpret_cast<float*>(slab + C.u_dr);
   const int rs = r == 0 ? 0 : (r <= 16 ? 16 : 32);
@@ -58,7 +70,8 @@ __global__ __launch_bounds__(256) void derive_kernel(uint8_t* calib, quantwm_cal
     float sk = 0.0f, sv = 0.0f;
     for (int c = 0; c < d; ++c) {
       const float mkv = ldf(mk + j * d + c), mvv = ldf(mv + j * d + c);
-      sk = __builtin_fmaf(w[c] * mkv, mkv, sk);
+      // full metric: -0.5 a_jc is p_jc exactly
+      sk = __builtin_fmaf(full ? -0.5f * ak[j * d + c] : w[c] * mkv, mkv, sk);
       sv = __builtin_fmaf(mvv, mvv, sv);
     }
     bk[j] = sk;
@@ -67,11 +80,12 @@ __global__ __launch_bounds__(256) void derive_kernel(uint8_t* calib, quantwm_cal
 }
 
 // Copy method-level tables into the slabs: mu [BH][Kc][d], w [BH][d],
-// u_t [BH][r][d] (zeros if null), lam [BH][r] (zeros if null).
+// u_t [BH][r][d] (zeros if null), lam [BH][r] (zeros if null), and the full
+// metric's matrix m [BH][d][d] when given.
 template <typename T>
 __global__ __launch_bounds__(256) void pack_kernel(uint8_t* calib, quantwm_calib_layout C, int d, int Kc, int r,
                                                    const T* mu_k, const T* mu_v, const float* w, const T* u_t,
-                                                   const float* lam) {
+                                                   const float* lam, const float* m) {
   const int64_t bh = blockIdx.x;
   uint8_t* slab = calib + bh * C.slab_bytes;
   T* mk = reinterpret_cast<T*>(slab + C.mu_k);
@@ -86,6 +100,10 @@ __global__ __launch_bounds__(256) void pack_kernel(uint8_t* calib, quantwm_calib
   for (int i = threadIdx.x; i < d; i += 256) wo[i] = w[bh * d + i];
   for (int i = threadIdx.x; i < r * d; i += 256) ut[i] = u_t ? u_t[bh * r * d + i] : T(0.0f);
   for (int i = threadIdx.x; i < r; i += 256) lo[i] = lam ? lam[bh * r + i] : 0.0f;
+  if (m) {
+    float* mo = reinterpret_cast<float*>(slab + C.m);
+    for (int i = threadIdx.x; i < d * d; i += 256) mo[i] = m[bh * d * d + i];
+  }
 }
 
 // Eq. 6 without the 1/N: thread (i, j) sums q_i q_j over the tokens in order,
@@ -218,25 +236,26 @@ hipError_t kmeans_t(const quantwm_config& c, const T* x, int64_t n, int iters, u
 hipError_t launch_derive_constants(const quantwm_config& c, uint8_t* calib, hipStream_t s) {
   const quantwm_calib_layout C = calib_layout(c);
   const dim3 grid((unsigned)(c.batch * c.heads));
+  const int full = c.metric == QWM_METRIC_FULL;
   if (c.dtype == QWM_BF16)
     hipLaunchKernelGGL(derive_kernel<bf16>, grid, dim3(256), 0, s, calib, C, c.head_dim, c.group_size, c.n_centroids,
-                       c.rank);
+                       c.rank, full);
   else
     hipLaunchKernelGGL(derive_kernel<float>, grid, dim3(256), 0, s, calib, C, c.head_dim, c.group_size, c.n_centroids,
-                       c.rank);
+                       c.rank, full);
   return hipGetLastError();
 }
 
 hipError_t launch_pack_tables(const quantwm_config& c, const void* mu_k, const void* mu_v, const float* w,
-                              const void* u_t, const float* lam, uint8_t* calib, hipStream_t s) {
+                              const void* u_t, const float* lam, const float* m, uint8_t* calib, hipStream_t s) {
   const quantwm_calib_layout C = calib_layout(c);
   const dim3 grid((unsigned)(c.batch * c.heads));
   if (c.dtype == QWM_BF16)
     hipLaunchKernelGGL(pack_kernel<bf16>, grid, dim3(256), 0, s, calib, C, c.head_dim, c.n_centroids, c.rank,
-                       (const bf16*)mu_k, (const bf16*)mu_v, w, (const bf16*)u_t, lam);
+                       (const bf16*)mu_k, (const bf16*)mu_v, w, (const bf16*)u_t, lam, m);
   else
     hipLaunchKernelGGL(pack_kernel<float>, grid, dim3(256), 0, s, calib, C, c.head_dim, c.n_centroids, c.rank,
-                       (const float*)mu_k, (const float*)mu_v, w, (const float*)u_t, lam);
+                       (const float*)mu_k, (const float*)mu_v, w, (const float*)u_t, lam, m);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_derive_constants(c, calib, s);

@@ -77,6 +77,7 @@ inline quantwm_calib_layout calib_layout(const quantwm_config& c) {
   L.u_t = take(r * d * e);
   L.lam = take(r * 4);
   L.u_dr = take(int64_t(rank_stride(c)) * d * 4);
+  L.m = take(c.metric == QWM_METRIC_FULL ? d * d * 4 : 0);
   L.slab_bytes = at;
   return L;
 }
@@ -139,8 +140,8 @@ bool attend_tables_fit(int d, int elem, int rank, int n_centroids);
 
 hipError_t launch_derive_constants(const quantwm_config& c, uint8_t* calib, hipStream_t s);
 hipError_t launch_pack_tables(const quantwm_config& c, const void* mu_k, const void* mu_v,
-                              const float* w, const void* u_t, const float* lam, uint8_t* calib,
-                              hipStream_t s);
+                              const float* w, const void* u_t, const float* lam, const float* m,
+                              uint8_t* calib, hipStream_t s);
 hipError_t launch_moment_accumulate(const quantwm_config& c, const void* q, int64_t n, double* sums, int64_t* count,
                                     hipStream_t s);
 hipError_t launch_second_moment(const quantwm_config& c, const void* q, int64_t n, double* m_out,

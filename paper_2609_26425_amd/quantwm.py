@@ -29,7 +29,7 @@ class Config(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("n_centroids", ctypes.c_int32), ("group_size", ctypes.c_int32),
                 ("rank", ctypes.c_int32), ("top_m", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("capacity", ctypes.c_int64), ("storage", ctypes.c_int32)]
+                ("capacity", ctypes.c_int64), ("storage", ctypes.c_int32), ("metric", ctypes.c_int32)]
 
     @property
     def torch_dtype(self):
@@ -39,7 +39,7 @@ class Config(ctypes.Structure):
 class CalibLayout(ctypes.Structure):
     """Mirror of quantwm_calib_layout (byte offsets inside one (b, h) slab)."""
     _fields_ = [(n, ctypes.c_int64) for n in
-                ("slab_bytes", "mu_k", "mu_v", "a_k", "b_k", "a_v", "b_v", "w", "wg", "u_t", "lam", "u_dr")]
+                ("slab_bytes", "mu_k", "mu_v", "a_k", "b_k", "a_v", "b_v", "w", "wg", "u_t", "lam", "u_dr", "m")]
 
 
 def _load():
@@ -55,7 +55,7 @@ def _load():
         "quantwm_calib_bytes": (SZ, [C]),
         "quantwm_calib_offsets": (I32, [C, ctypes.POINTER(CalibLayout)]),
         "quantwm_calibrate_workspace_bytes": (SZ, [C, I64, I64]),
-        "quantwm_calib_pack": (I32, [C, P, P, P, P, P, P, P]),
+        "quantwm_calib_pack": (I32, [C, P, P, P, P, P, P, P, P]),
         "quantwm_calibrate": (I32, [C, P, I64, P, P, I64, I32, P, P, SZ, P]),
         "quantwm_stats_bytes": (SZ, [C]),
         "quantwm_stats_update": (I32, [C, P, I64, P, P]),
@@ -92,12 +92,15 @@ def library():
 # App. D.1 storage options (QWM_STORE_* in include/quantwm.h)
 STORE_SCALE_I8 = 1
 STORE_GATE = 2
+# QSAC candidate metric (QWM_METRIC_*): Eq. 9 or the full quadratic form
+METRIC_DIAG = 0
+METRIC_FULL = 1
 
 
 def make_config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, dtype,
-                storage=0) -> Config:
+                storage=0, metric=0) -> Config:
     dt = {"bf16": BF16, "f32": F32, BF16: BF16, F32: F32}[dtype]
-    return Config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, dt, capacity, storage)
+    return Config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, dt, capacity, storage, metric)
 
 
 def _ptr(t):
@@ -153,9 +156,10 @@ def quantwm_calibrate_workspace_bytes(cfg: Config, n_hist: int, n_calib: int) ->
     return int(_lib.quantwm_calibrate_workspace_bytes(ctypes.byref(cfg), n_hist, n_calib))
 
 
-def quantwm_calib_pack(cfg, mu_k, mu_v, w, u_t, lam, calib, stream=None):
+def quantwm_calib_pack(cfg, mu_k, mu_v, w, u_t, lam, calib, stream=None, m=None):
+    """m: [B, H, d, d] float32, the matrix of the full metric (METRIC_FULL only)."""
     _check(_lib.quantwm_calib_pack(ctypes.byref(cfg), _ptr(mu_k), _ptr(mu_v), _ptr(w), _ptr(u_t), _ptr(lam),
-                                   _ptr(calib), _stream(stream)))
+                                   _ptr(m), _ptr(calib), _stream(stream)))
 
 
 def quantwm_calibrate(cfg, q_hist, n_hist, k_calib, v_calib, n_calib, kmeans_iters, calib, workspace,

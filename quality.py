@@ -4,7 +4,9 @@ For a seeded synthetic workload this measures how far the attention logits over
 the packed cache move from the exact ones, for the four settings the paper
 ablates (Sec. 5, the component ablation): plain nearest-centroid quantisation
 (M = 1, w = 1, r = 0, the QVG setting), QSAC alone (r = 0), PSAC alone (M = 1,
-w = 1) and both; plus a sweep over the candidate count M. The metrics are
+w = 1) and both; a sweep over the candidate count M; both with the App. D.1
+storage options; and both with the candidates ranked by the full quadratic form
+of the Query second moment instead of its diagonal (App. C). The metrics are
 taken over the visible (Query, key) pairs of the first `n_eval` Queries of the
 chunk:
 
@@ -68,12 +70,13 @@ def _torch():
 
 def gpu_tables(wl):
     """Calibrate on the GPU at the workload's (M, r) and read the tables back:
-    (mu_k, mu_v, w, u_t, lam) as numpy arrays [B, H, ...]."""
+    (mu_k, mu_v, w, u_t, lam, m) as numpy arrays [B, H, ...]; m [B, H, d, d] is
+    the full metric's matrix."""
     torch, qw = _torch()
     dev = "cuda:0"
     dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     cfg = qw.make_config(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank, wl.top_m,
-                         wl.n_cache, wl.dtype)
+                         wl.n_cache, wl.dtype, metric=qw.METRIC_FULL)
     nc = min(wl.chunk, wl.n_cache)
     k = torch.from_numpy(synth.tensor(wl, "k", nc)).to(dev, dt)
     v = torch.from_numpy(synth.tensor(wl, "v", nc)).to(dev, dt)
@@ -95,32 +98,37 @@ def gpu_tables(wl):
     w = field(L.w, d, torch.float32).reshape(wl.batch, wl.heads, d)
     u_t = field(L.u_t, r * d, dt).reshape(wl.batch, wl.heads, r, d) if r else None
     lam = field(L.lam, r, torch.float32).reshape(wl.batch, wl.heads, r) if r else None
-    return mu_k, mu_v, w, u_t, lam
+    m = field(L.m, d * d, torch.float32).reshape(wl.batch, wl.heads, d, d)
+    return mu_k, mu_v, w, u_t, lam, m
 
 
 def mode_tables(tables, wl, mode):
-    """(config overrides, tables) of one mode from the calibrated tables."""
+    """(config overrides, tables) of one mode from the calibrated tables; a sixth
+    table (the full metric's matrix) is passed through."""
     top_m, w_one, psac = MODES[mode] if isinstance(mode, str) else mode
-    mu_k, mu_v, w, u_t, lam = tables
+    mu_k, mu_v, w, u_t, lam = tables[:5]
     rank = wl.rank if psac else 0
     w_m = np.ones_like(w) if w_one else w
-    return (top_m or wl.top_m, rank), (mu_k, mu_v, w_m, u_t if rank else None, lam if rank else None)
+    return (top_m or wl.top_m, rank), (mu_k, mu_v, w_m, u_t if rank else None, lam if rank else None) + \
+        tuple(tables[5:])
 
 
-def gpu_logits(wl, tables, top_m: int, rank: int, n_eval: int, storage: int = 0) -> np.ndarray:
+def gpu_logits(wl, tables, top_m: int, rank: int, n_eval: int, storage: int = 0, metric: int = 0) -> np.ndarray:
     """Quantise the whole cache with these tables and return the masked logits
     [B, H, n_eval, n_cache] of the first n_eval Queries (scaled by 1/sqrt(d)).
-    storage: App. D.1 options (1 = 8-bit group scales, 2 = retention gate)."""
+    storage: App. D.1 options (1 = 8-bit group scales, 2 = retention gate);
+    metric: 1 ranks the QSAC candidates by the full form (tables[5] is its matrix)."""
     torch, qw = _torch()
     dev = "cuda:0"
     dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     cfg = qw.make_config(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, rank, top_m, wl.n_cache,
-                         wl.dtype, storage)
-    mu_k, mu_v, w, u_t, lam = tables
+                         wl.dtype, storage, metric)
+    mu_k, mu_v, w, u_t, lam = tables[:5]
     T = lambda x, t=dt: torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(dev).to(t)  # noqa: E731
     calib = torch.zeros(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=dev)
     qw.quantwm_calib_pack(cfg, T(mu_k), T(mu_v), T(w, torch.float32), T(u_t) if rank else None,
-                          T(lam, torch.float32) if rank else None, calib)
+                          T(lam, torch.float32) if rank else None, calib,
+                          m=T(tables[5], torch.float32) if metric else None)
     cache = torch.zeros(qw.quantwm_cache_bytes(cfg), dtype=torch.uint8, device=dev)
     for s0, n in wl.chunks():
         k = T(synth.tensor(wl, "k", n, start=s0))
@@ -147,15 +155,21 @@ def exact_logits(wl, n_eval: int) -> np.ndarray:
 
 # App. D.1 storage options, applied to the "both" mode
 STORAGE = {"i8_scales": 1, "gate": 2, "i8_scales+gate": 3}
+# QSAC candidate metric of the "both" mode: Eq. 9 (diagonal) or the full form
+METRIC = {"diagonal": 0, "full": 1}
 
 
-def evaluate(wl, tables, n_eval: int, modes=tuple(MODES), m_sweep=(1, 2, 4, 8), storage=tuple(STORAGE)) -> dict:
+def evaluate(wl, tables, n_eval: int, modes=tuple(MODES), m_sweep=(1, 2, 4, 8), storage=tuple(STORAGE),
+             metric=tuple(METRIC)) -> dict:
     exact = exact_logits(wl, n_eval)
     vis = visible_mask(wl, n_eval, wl.n_cache)
-    res = {"modes": {}, "m_sweep": {}, "storage": {}}
+    res = {"modes": {}, "m_sweep": {}, "storage": {}, "metric": {}}
     for name in storage:
         (top_m, rank), t = mode_tables(tables, wl, "both")
         res["storage"][name] = metrics(exact, gpu_logits(wl, t, top_m, rank, n_eval, STORAGE[name]), vis)
+    for name in metric:
+        (top_m, rank), t = mode_tables(tables, wl, "both")
+        res["metric"][name] = metrics(exact, gpu_logits(wl, t, top_m, rank, n_eval, metric=METRIC[name]), vis)
     for mode in modes:
         (top_m, rank), t = mode_tables(tables, wl, mode)
         res["modes"][mode] = metrics(exact, gpu_logits(wl, t, top_m, rank, n_eval), vis)

@@ -56,6 +56,7 @@ class Workload:
     seed: int
     kmeans_iters: int = 10
     storage: int = 0      # App. D.1 storage options: 1 = 8-bit group scales, 2 = retention gate
+    metric: int = 0       # QSAC candidate metric: 0 = Eq. 9 (diagonal), 1 = the full quadratic form
 
     @property
     def capacity(self) -> int:

@@ -58,7 +58,7 @@ def build_oracle_case(wl: synth.Workload, max_sources: int = 3, cold: bool = Fal
     sources = sources_for(wl, max_sources)
     S = len(sources)
     cfg = oracle.cfg_of(1, S, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank, wl.top_m,
-                        wl.n_cache, wl.dtype == "bf16", wl.storage)
+                        wl.n_cache, wl.dtype == "bf16", wl.storage, wl.metric)
     k = _gen_sources(wl, sources, "k", wl.n_cache)
     v = _gen_sources(wl, sources, "v", wl.n_cache)
     q = _gen_sources(wl, sources, "q", wl.n_q)
@@ -133,6 +133,22 @@ def qsac_near_tie(k, mu, w, M, rel=2.0 ** -16):
         return False
     a, b = o[M - 1], o[M]
     return abs(dq[b] - dq[a]) <= rel * (mag[a] + mag[b])
+
+
+def qsac_near_tie_full(k, mu, m, M, rel=2.0 ** -16):
+    """The same for the full quadratic form (k - mu)^T m (k - mu): the GPU ranks
+    with the expanded constants m mu_j, the oracle with the literal form; both
+    round within rel times (|k| + |mu|)^T |m| (|k| + |mu|)."""
+    k = k.astype(np.float64); mu = mu.astype(np.float64); m = m.astype(np.float64)
+    e = k[None, :] - mu
+    dq = np.einsum("jc,cd,jd->j", e, m, e)
+    a = np.abs(k)[None, :] + np.abs(mu)
+    mag = np.einsum("jc,cd,jd->j", a, np.abs(m), a)
+    o = np.argsort(dq, kind="stable")
+    if M >= len(dq):
+        return False
+    i, j = o[M - 1], o[M]
+    return abs(dq[j] - dq[i]) <= rel * (mag[i] + mag[j])
 
 
 def nearest_near_tie(x, mu, rel=2.0 ** -16):

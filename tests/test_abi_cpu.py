@@ -44,6 +44,27 @@ def test_sizes_agree_with_the_oracle_format(shape, storage):
     assert all(o % 256 == 0 for o in offs) and offs == sorted(offs) and L.slab_bytes % 256 == 0
 
 
+@pytest.mark.parametrize("d", [64, 128])
+def test_full_metric_adds_the_matrix_to_the_calibration_block(d):
+    # QWM_METRIC_FULL keeps the cache format and appends Mn ([d][d] fp32) to the slab.
+    diag = qw.make_config(1, 3, d, 32, 32, 8, 4, 500, "bf16")
+    full = qw.make_config(1, 3, d, 32, 32, 8, 4, 500, "bf16", metric=qw.METRIC_FULL)
+    assert qw.quantwm_cache_bytes(full) == qw.quantwm_cache_bytes(diag)
+    Ld, Lf = qw.quantwm_calib_offsets(diag), qw.quantwm_calib_offsets(full)
+    assert Lf.m == Ld.slab_bytes and Lf.slab_bytes == Ld.slab_bytes + d * d * 4
+    assert all(getattr(Lf, n) == getattr(Ld, n) for n in ("mu_k", "a_k", "b_k", "w", "u_t", "lam", "u_dr"))
+    assert Ld.m == Ld.slab_bytes  # no bytes without the full metric
+    with pytest.raises(qw.QuantwmError) as e:
+        qw.quantwm_token_bytes(qw.make_config(1, 3, d, 32, 32, 8, 4, 500, "bf16", metric=2))
+    assert e.value.status == qw.ERR_INVALID_ARG and "metric" in qw.quantwm_last_error()
+    # the full metric needs its matrix
+    P = ctypes.c_void_p
+    with pytest.raises(qw.QuantwmError) as e:
+        qw._check(qw.library().quantwm_calib_pack(ctypes.byref(full), P(0x1000), P(0x2000), P(0x3000), P(0x4000), None,
+                                                  None, P(0x5000), None))
+    assert e.value.status == qw.ERR_INVALID_ARG and "m is null" in qw.quantwm_last_error()
+
+
 def test_validation_without_a_gpu():
     good = qw.make_config(1, 2, 128, 16, 32, 8, 4, 100, "bf16")
     for bad, status in [(qw.make_config(1, 2, 96, 16, 32, 8, 4, 100, "bf16"), qw.ERR_UNSUPPORTED),

@@ -34,16 +34,18 @@ def tdev(x, dtype):
 
 def gpu_config(wl, capacity=None):
     return qw.make_config(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank,
-                          wl.top_m, wl.n_cache if capacity is None else capacity, wl.dtype, wl.storage)
+                          wl.top_m, wl.n_cache if capacity is None else capacity, wl.dtype, wl.storage, wl.metric)
 
 
 def gpu_calib_from_tables(cfg, tables):
-    mu_k, mu_v, w, u_t, lam = tables
+    """tables: (mu_k, mu_v, w, u_t, lam[, m]); m is the full metric's matrix."""
+    mu_k, mu_v, w, u_t, lam = tables[:5]
+    m = tables[5] if len(tables) > 5 else None
     dt = cfg.torch_dtype
     calib = torch.empty(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=DEV)
     qw.quantwm_calib_pack(cfg, tdev(mu_k, dt), tdev(mu_v, dt), tdev(w, torch.float32),
                           tdev(u_t, dt) if cfg.rank > 0 else None, tdev(lam, torch.float32) if cfg.rank > 0 else None,
-                          calib)
+                          calib, m=tdev(m, torch.float32) if m is not None else None)
     return calib
 
 
@@ -69,6 +71,7 @@ def check_append(case, gpu_cache, gpu_coef):
     lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage)
     mu_k, mu_v, w = case.tables[0][0], case.tables[1][0], case.tables[2][0]
     lam = case.tables[4][0] if wl.rank > 0 else None
+    mfull = case.tables[5][0] if wl.metric == oracle.METRIC_FULL else None
     M = min(wl.top_m, wl.n_centroids)
     stats = {"tokens": 0, "k_ties": 0, "v_ties": 0, "coef_half": 0, "cscale_f16": 0, "gate_ties": 0}
     i8 = bool(wl.storage & oracle.STORE_SCALE_I8)
@@ -80,8 +83,9 @@ def check_append(case, gpu_cache, gpu_coef):
         stats["tokens"] += wl.n_cache
         kmis = np.nonzero(g["k_ids"] != o["k_ids"])[0]
         for t in kmis:
-            assert harness.qsac_near_tie(case.k[0, t, s], mu_k[s], w[s], M), \
-                f"head {bh} token {t}: K centroid {g['k_ids'][t]} vs oracle {o['k_ids'][t]} is not a near-tie"
+            tie = harness.qsac_near_tie(case.k[0, t, s], mu_k[s], w[s], M) if mfull is None else \
+                harness.qsac_near_tie_full(case.k[0, t, s], mu_k[s], mfull[s], M)
+            assert tie, f"head {bh} token {t}: K centroid {g['k_ids'][t]} vs oracle {o['k_ids'][t]} is not a near-tie"
         vmis = np.nonzero(g["v_ids"] != o["v_ids"])[0]
         for t in vmis:
             assert harness.nearest_near_tie(case.v[0, t, s], mu_v[s]), \
@@ -230,6 +234,16 @@ STORAGE = [synth.scaled(synth.WORKLOADS["tiny-f32"], name="tiny-f32-i8", storage
            synth.scaled(D64, name="d64-gate", storage=_GATE),
            synth.scaled(NOPSAC, name="g64-r0-i8-gate", storage=_I8 | _GATE)]
 
+# The full quadratic QSAC metric (the diagonal-approximation ablation of App. C):
+# fp32 d = 64, bf16 with batch 2 and ragged tiles, M = 8 over a small Kc, and
+# one LingBot-shaped head pair (Kc = 128, d = 128, G = 32, r = 16) over one frame.
+_FULL = oracle.METRIC_FULL
+METRIC = [synth.scaled(synth.WORKLOADS["tiny-f32"], name="tiny-f32-fullm", metric=_FULL),
+          synth.scaled(RAGGED, name="ragged-fullm", metric=_FULL),
+          synth.scaled(D64, name="d64-fullm", metric=_FULL),
+          synth.scaled(synth.WORKLOADS["lingbot-40h"], name="lingbot-2h-fullm", heads=2, n_cache=1560, n_q=520,
+                       q_start=1040, frame_tokens=260, chunk=780, n_hist=1560, metric=_FULL)]
+
 _cases = {}
 
 
@@ -288,6 +302,11 @@ def test_full_size_parity(name):
 @pytest.mark.parametrize("wl", STORAGE, ids=[w.name for w in STORAGE])
 def test_storage_parity(wl):
     run_case(wl, max_sources=64, n_heads_rows=64, row_step=1, logits_rows=wl.n_q)
+
+
+@pytest.mark.parametrize("wl", METRIC, ids=[w.name for w in METRIC])
+def test_full_metric_parity(wl):
+    run_case(wl, max_sources=64, n_heads_rows=64, row_step=3, logits_rows=64)
 
 
 @pytest.mark.timeout(900)
@@ -359,6 +378,30 @@ def test_calibrate_parity(name):
             tol = 2.0 ** -8 if bf else 1e-5
             assert np.all(np.abs(u - uo) <= tol * np.abs(uo) + 1e-6), f"U_r head {bh}"
     _say(f"[ok] calibrate {name}")
+
+
+def test_calibrate_full_metric_parity():
+    # the block carries the oracle's Mn exactly (same fp64 sums and division),
+    # and the identity at cold start
+    wl = METRIC[1]
+    case = case_for(wl, 64)
+    cfg, buf = _gpu_calibrate(case)
+    d = wl.head_dim
+    for bh in range(wl.batch * wl.heads):
+        s = int(case.src_of[bh])
+        m = _slab_field(cfg, buf, bh, "m", d * d, np.float32).reshape(d, d)
+        np.testing.assert_array_equal(m, case.tables[5][0, s], err_msg=f"m head {bh}")
+        np.testing.assert_array_equal(np.diag(m), _slab_field(cfg, buf, bh, "w", d, np.float32))
+    k = tdev(synth.tensor(wl, "k", 64), cfg.torch_dtype)
+    calib = torch.zeros(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=DEV)
+    ws = torch.empty(qw.quantwm_calibrate_workspace_bytes(cfg, 0, 64), dtype=torch.uint8, device=DEV)
+    qw.quantwm_calibrate(cfg, None, 0, k, k, 64, 2, calib, ws)
+    torch.cuda.synchronize()
+    cold = calib.cpu().numpy()
+    for bh in range(wl.batch * wl.heads):
+        assert np.array_equal(_slab_field(cfg, cold, bh, "m", d * d, np.float32).reshape(d, d),
+                              np.eye(d, dtype=np.float32))
+    _say("[ok] calibrate full metric")
 
 
 def test_calibrate_cold_start():

@@ -16,7 +16,9 @@ def _say(msg):
 
 
 def _oracle_tables(wl):
+    # with the full metric's matrix as a sixth table
     cfg = oracle.cfg_from_workload(wl)
+    cfg.metric = oracle.METRIC_FULL
     nc = min(wl.chunk, wl.n_cache)
     k = synth.round_to(synth.tensor(wl, "k", nc), wl.dtype)
     v = synth.round_to(synth.tensor(wl, "v", nc), wl.dtype)
@@ -24,9 +26,9 @@ def _oracle_tables(wl):
     return oracle.calibrate(cfg, qh, k, v, wl.kmeans_iters)
 
 
-def _oracle_logits(wl, tables, top_m, rank, n_eval, storage=0):
+def _oracle_logits(wl, tables, top_m, rank, n_eval, storage=0, metric=0):
     cfg = oracle.cfg_of(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, rank, top_m, wl.n_cache,
-                        wl.dtype == "bf16", storage)
+                        wl.dtype == "bf16", storage, metric)
     cache = oracle.new_cache(cfg)
     k = synth.round_to(synth.tensor(wl, "k", wl.n_cache), wl.dtype)
     v = synth.round_to(synth.tensor(wl, "v", wl.n_cache), wl.dtype)
@@ -62,6 +64,12 @@ def test_quality_metrics_match_oracle():
         _say(f"[ok] quality both + {name}: gpu {g} oracle {o}")
         assert abs(g["logit_mse"] - o["logit_mse"]) <= 1e-3 * o["logit_mse"]
         assert abs(g["top1_shift"] - o["top1_shift"]) <= 2.0 / (wl.batch * wl.heads * n_eval)
+    (top_m, rank), t = quality.mode_tables(tables, wl, "both")
+    g = quality.metrics(exact, quality.gpu_logits(wl, t, top_m, rank, n_eval, metric=1), vis)
+    o = quality.metrics(exact, _oracle_logits(wl, t, top_m, rank, n_eval, metric=1), vis)
+    _say(f"[ok] quality both, full metric: gpu {g} oracle {o}")
+    assert abs(g["logit_mse"] - o["logit_mse"]) <= 1e-3 * o["logit_mse"]
+    assert abs(g["top1_shift"] - o["top1_shift"]) <= 2.0 / (wl.batch * wl.heads * n_eval)
 
 
 def test_quality_orderings_on_matrix_game_shape():
@@ -72,7 +80,7 @@ def test_quality_orderings_on_matrix_game_shape():
                       chunk=880, n_hist=1760)
     res = quality.evaluate(wl, quality.gpu_tables(wl), 256, m_sweep=(1, 4))
     m = res["modes"]
-    _say(f"[ok] quality mg2-4h: {m}")
+    _say(f"[ok] quality mg2-4h: {m} storage {res['storage']} metric {res['metric']}")
     assert m["psac"]["logit_mse"] < m["qvg"]["logit_mse"]
     assert m["both"]["logit_mse"] < m["qsac"]["logit_mse"]
     assert m["both"]["logit_mse"] < m["qvg"]["logit_mse"]
