@@ -911,15 +911,33 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         }
       };
 
-      // the tile's two halves of 32 keys in turn, so only one half's logits are
-      // live at a time
+      if constexpr (!GEN) {
+        // the tile's two halves of 32 keys: the second half's logits products
+        // are issued before the first half's exponentials, which need none of
+        // them, so the matrix cores run while the vector unit computes
+        // probabilities. The running max of the second half is raised only
+        // after the first half's P V is in O (a rescale must cover it).
+        f32x16 s0 = logits_half(0);
+        mask_half(s0, 0);
+        raise_max(s0);
+        f32x16 s1 = logits_half(1);
+        probs(s0);
+        pv_half(s0, 0);
+        mask_half(s1, 1);
+        raise_max(s1);
+        probs(s1);
+        pv_half(s1, 1);
+      } else {
+        // streaming forms: one half at a time (the epoch-crossing path of the
+        // logits leaves no room for a second live half)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        f32x16 sv = logits_half(kb);
-        mask_half(sv, kb);
-        raise_max(sv);
-        probs(sv);
-        pv_half(sv, kb);
+        for (int kb = 0; kb < 2; ++kb) {
+          f32x16 sv = logits_half(kb);
+          mask_half(sv, kb);
+          raise_max(sv);
+          probs(sv);
+          pv_half(sv, kb);
+        }
       }
     }
   };
