@@ -54,6 +54,7 @@ def lib():
             raise RuntimeError(f"oracle library missing: {LIB} (run __graft_entry__.build())")
         _lib = ctypes.CDLL(LIB)
         _lib.ora_cache_bytes.restype = ctypes.c_longlong
+        _lib.ora_coef_record_bytes.restype = ctypes.c_longlong
         _lib.ora_round_bf16.restype = ctypes.c_double
         _lib.ora_round_bf16.argtypes = [ctypes.c_double]
         _lib.ora_round_f16.restype = ctypes.c_double
@@ -248,6 +249,39 @@ def append(cfg: OraCfg, tables, cache, n_cached, k_new, v_new, diagnostics=False
     if diagnostics:
         return {"coef": coef[..., : cfg.rank], "k_ids": kid, "v_ids": vid, "cand": cand}
     return None
+
+
+COEF_DENSE = 0
+COEF_SPARSE = 1
+
+
+def coef_record_bytes(cfg: OraCfg, cache, start, n):
+    """(bytes, layout) of the chunk's coefficient record (App. D.1 layout choice)."""
+    lay = ctypes.c_int()
+    b = lib().ora_coef_record_bytes(ctypes.byref(cfg), _p(cache, ctypes.c_uint8), ctypes.c_longlong(start),
+                                    ctypes.c_longlong(n), ctypes.byref(lay))
+    if b < 0:
+        raise RuntimeError("oracle coef_record_bytes failed")
+    return int(b), int(lay.value)
+
+
+def coef_pack(cfg: OraCfg, cache, start, n) -> np.ndarray:
+    size, _ = coef_record_bytes(cfg, cache, start, n)
+    out = np.zeros(size, np.uint8)
+    wr = ctypes.c_longlong()
+    _check(lib().ora_coef_pack(ctypes.byref(cfg), _p(cache, ctypes.c_uint8), ctypes.c_longlong(start),
+                               ctypes.c_longlong(n), _p(out, ctypes.c_uint8), ctypes.c_longlong(size),
+                               ctypes.byref(wr)), "coef_pack")
+    assert wr.value == size
+    return out
+
+
+def coef_unpack(cfg: OraCfg, rec, cache, start, n):
+    """Writes the record's rows into slots [start, start + n) of the cache in place."""
+    rec = np.ascontiguousarray(rec, dtype=np.uint8)
+    _check(lib().ora_coef_unpack(ctypes.byref(cfg), _p(rec, ctypes.c_uint8), ctypes.c_longlong(rec.size),
+                                 _p(cache, ctypes.c_uint8), ctypes.c_longlong(start), ctypes.c_longlong(n)),
+           "coef_unpack")
 
 
 def decode(cfg: OraCfg, tables, cache, b, h, n):

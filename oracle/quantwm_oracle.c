@@ -617,6 +617,130 @@ static void load_residual(const layout* L, int G, const uint8_t* codes, const ui
   }
 }
 
+/* ------------------------------------------- per-chunk coefficient layout */
+
+static void put32(uint8_t* p, uint32_t v) {
+  for (int i = 0; i < 4; ++i) p[i] = (uint8_t)(v >> (8 * i));
+}
+static uint32_t get32(const uint8_t* p) {
+  return (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16) | ((uint32_t)p[3] << 24);
+}
+
+static int coef_args_ok(const ora_cfg* cfg, long long start, long long n) {
+  return valid_cfg(cfg) && cfg->rank > 0 && start >= 0 && n >= 0 && n <= 65536 && start + n <= cfg->capacity;
+}
+
+/* kept rows (non-zero FP16 scale) of head bh in the chunk */
+static long long coef_kept(const layout* L, const uint8_t* cache, long long bh, long long start, long long n) {
+  long long k = 0;
+  for (long long t = start; t < start + n; ++t) k += get16(cache + L->k_cscale + (bh * L->slots + t) * 2) != 0;
+  return k;
+}
+
+long long ora_coef_record_bytes(const ora_cfg* cfg, const uint8_t* cache, long long start, long long n, int* layout_out) {
+  if (!coef_args_ok(cfg, start, n) || !cache) return -1;
+  const layout L = make_layout(cfg);
+  const long long nbh = (long long)cfg->batch * cfg->heads, r = cfg->rank;
+  long long kept = 0;
+  for (long long bh = 0; bh < nbh; ++bh) kept += coef_kept(&L, cache, bh, start, n);
+  const long long dense = 16 + nbh * n * (r + 2), sparse = 16 + 4 * nbh + kept * (r + 4);
+  const int lay = sparse < dense ? ORA_COEF_SPARSE : ORA_COEF_DENSE;
+  if (layout_out) *layout_out = lay;
+  return lay == ORA_COEF_SPARSE ? sparse : dense;
+}
+
+int ora_coef_pack(const ora_cfg* cfg, const uint8_t* cache, long long start, long long n, uint8_t* out,
+                  long long out_bytes, long long* written) {
+  int lay;
+  const long long need = ora_coef_record_bytes(cfg, cache, start, n, &lay);
+  if (need < 0 || !out) return -1;
+  if (out_bytes < need) return -3;
+  const layout L = make_layout(cfg);
+  const long long nbh = (long long)cfg->batch * cfg->heads, r = cfg->rank;
+  put32(out, (uint32_t)lay);
+  put32(out + 4, (uint32_t)n);
+  put32(out + 8, (uint32_t)r);
+  put32(out + 12, (uint32_t)nbh);
+  if (lay == ORA_COEF_DENSE) {
+    uint8_t* codes = out + 16;
+    uint8_t* scales = codes + nbh * n * r;
+    for (long long bh = 0; bh < nbh; ++bh)
+      for (long long t = 0; t < n; ++t) {
+        const long long slot = bh * L.slots + start + t, row = bh * n + t;
+        memcpy(codes + row * r, cache + L.k_coef + slot * r, (size_t)r);
+        memcpy(scales + row * 2, cache + L.k_cscale + slot * 2, 2);
+      }
+  } else {
+    uint8_t* p = out + 16 + 4 * nbh;
+    for (long long bh = 0; bh < nbh; ++bh) {
+      const long long cnt = coef_kept(&L, cache, bh, start, n);
+      put32(out + 16 + 4 * bh, (uint32_t)cnt);
+      uint8_t* idx = p;
+      uint8_t* codes = idx + 2 * cnt;
+      uint8_t* scales = codes + r * cnt;
+      long long m = 0;
+      for (long long t = 0; t < n; ++t) {
+        const long long slot = bh * L.slots + start + t;
+        if (get16(cache + L.k_cscale + slot * 2) == 0) continue;
+        put16(idx + 2 * m, (uint16_t)t);
+        memcpy(codes + m * r, cache + L.k_coef + slot * r, (size_t)r);
+        memcpy(scales + 2 * m, cache + L.k_cscale + slot * 2, 2);
+        ++m;
+      }
+      p = scales + 2 * cnt;
+    }
+  }
+  if (written) *written = need;
+  return 0;
+}
+
+int ora_coef_unpack(const ora_cfg* cfg, const uint8_t* rec, long long rec_bytes, uint8_t* cache, long long start,
+                    long long n) {
+  if (!coef_args_ok(cfg, start, n) || !rec || !cache || rec_bytes < 16) return -1;
+  const layout L = make_layout(cfg);
+  const long long nbh = (long long)cfg->batch * cfg->heads, r = cfg->rank;
+  const uint32_t lay = get32(rec);
+  if (get32(rec + 4) != (uint32_t)n || get32(rec + 8) != (uint32_t)r || get32(rec + 12) != (uint32_t)nbh) return -1;
+  if (lay == ORA_COEF_DENSE) {
+    if (rec_bytes < 16 + nbh * n * (r + 2)) return -1;
+    const uint8_t* codes = rec + 16;
+    const uint8_t* scales = codes + nbh * n * r;
+    for (long long bh = 0; bh < nbh; ++bh)
+      for (long long t = 0; t < n; ++t) {
+        const long long slot = bh * L.slots + start + t, row = bh * n + t;
+        memcpy(cache + L.k_coef + slot * r, codes + row * r, (size_t)r);
+        memcpy(cache + L.k_cscale + slot * 2, scales + row * 2, 2);
+      }
+    return 0;
+  }
+  if (lay != ORA_COEF_SPARSE || rec_bytes < 16 + 4 * nbh) return -1;
+  long long total = 16 + 4 * nbh;
+  for (long long bh = 0; bh < nbh; ++bh) total += (long long)get32(rec + 16 + 4 * bh) * (r + 4);
+  if (rec_bytes < total) return -1;
+  const uint8_t* p = rec + 16 + 4 * nbh;
+  for (long long bh = 0; bh < nbh; ++bh) {
+    const long long cnt = get32(rec + 16 + 4 * bh);
+    if (cnt > n) return -1;
+    for (long long t = 0; t < n; ++t) {
+      const long long slot = bh * L.slots + start + t;
+      memset(cache + L.k_coef + slot * r, 0, (size_t)r);
+      memset(cache + L.k_cscale + slot * 2, 0, 2);
+    }
+    const uint8_t* idx = p;
+    const uint8_t* codes = idx + 2 * cnt;
+    const uint8_t* scales = codes + r * cnt;
+    for (long long m = 0; m < cnt; ++m) {
+      const long long t = get16(idx + 2 * m);
+      if (t >= n) return -1;
+      const long long slot = bh * L.slots + start + t;
+      memcpy(cache + L.k_coef + slot * r, codes + m * r, (size_t)r);
+      memcpy(cache + L.k_cscale + slot * 2, scales + 2 * m, 2);
+    }
+    p = scales + 2 * cnt;
+  }
+  return 0;
+}
+
 int ora_decode(const ora_cfg* cfg, const float* mu_k, const float* mu_v,
                const uint8_t* cache, int b, int h, long long n,
                double* k0, double* chat, double* v) {

@@ -121,6 +121,26 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
                const float* k_new, const float* v_new, long long n_new,
                float* coef_f32, int* k_ids, int* v_ids, int* cand);
 
+/* App. D.1 per-chunk coefficient layout: the PSAC rows of slots [start, start + n)
+ * of every (b, h) as one record, dense or sparse, whichever is smaller counting
+ * the sparse indices. A row is kept when its FP16 scale is non-zero (a zero
+ * scale means zero codes: the gate dropped it, or C was zero). Little-endian:
+ *   header   16 B: u32 layout (0 dense, 1 sparse), u32 n, u32 r, u32 B*H
+ *   dense    codes [BH][n][r] int8, then scales [BH][n] binary16
+ *   sparse   counts [BH] u32, then for each (b, h) in order: indices [count] u16
+ *            (slot - start, increasing), codes [count][r] int8, scales [count] binary16
+ * Dense is 16 + BH n (r + 2) bytes, sparse 16 + 4 BH + (r + 4) x (kept rows);
+ * sparse is taken only when strictly smaller. n <= 65536, r >= 1. */
+#define ORA_COEF_DENSE 0
+#define ORA_COEF_SPARSE 1
+long long ora_coef_record_bytes(const ora_cfg* cfg, const uint8_t* cache, long long start, long long n, int* layout);
+int ora_coef_pack(const ora_cfg* cfg, const uint8_t* cache, long long start, long long n, uint8_t* out,
+                  long long out_bytes, long long* written);
+/* Writes the record's rows back into slots [start, start + n) of every (b, h):
+ * codes and scales, zeros for the rows a sparse record leaves out. */
+int ora_coef_unpack(const ora_cfg* cfg, const uint8_t* rec, long long rec_bytes, uint8_t* cache, long long start,
+                    long long n);
+
 /* Decode slots [0, n) of head (b, h): Khat_0 (Eq. 4), INT8-decoded C, Vhat. */
 int ora_decode(const ora_cfg* cfg, const float* mu_k, const float* mu_v,
                const uint8_t* cache, int b, int h, long long n,

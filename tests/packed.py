@@ -68,3 +68,24 @@ def copy_head(dst: np.ndarray, dst_lay, dst_bh: int, src: np.ndarray, src_lay, s
         sd, ss = dst_lay["slots"], src_lay["slots"]
         dst[o_d + dst_bh * sd * nb: o_d + (dst_bh * sd + n) * nb] = \
             src[o_s + src_bh * ss * nb: o_s + (src_bh * ss + n) * nb]
+
+
+def zero_coef_rows(buf: np.ndarray, lay, bh: int, slots):
+    """Zero the PSAC codes and scale of the given slots of head bh (a dropped row)."""
+    s = lay["slots"]
+    (oc, nc), (os_, ns) = lay["off"]["k_coef"], lay["off"]["k_cscale"]
+    for t in slots:
+        buf[oc + (bh * s + t) * nc: oc + (bh * s + t + 1) * nc] = 0
+        buf[os_ + (bh * s + t) * ns: os_ + (bh * s + t + 1) * ns] = 0
+
+
+def coef_byte_mask(lay, nbh: int, start: int, n: int) -> np.ndarray:
+    """Mask of the cache bytes holding the PSAC codes and scales of slots
+    [start, start + n) of every head."""
+    m = np.zeros(lay["total"], bool)
+    s = lay["slots"]
+    for name in ("k_coef", "k_cscale"):
+        o, nb = lay["off"][name]
+        for bh in range(nbh):
+            m[o + (bh * s + start) * nb: o + (bh * s + start + n) * nb] = True
+    return m

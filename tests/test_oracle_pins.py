@@ -787,6 +787,110 @@ def test_append_gate_follows_the_keep_rule():
         assert not f2["k_coef"].any() and not f2["k_cscale"].any()
 
 
+# -------------------------------------- per-chunk coefficient layout (App. D.1)
+
+def _read_coef_record(rec, n, r, nbh):
+    """Reader of the chunk record format written from its definition: (layout,
+    {(bh, t): (codes, scale bits)} of the stored rows, size)."""
+    hdr = rec[:16].view("<u4")
+    assert (int(hdr[1]), int(hdr[2]), int(hdr[3])) == (n, r, nbh)
+    lay, rows = int(hdr[0]), {}
+    if lay == oracle.COEF_DENSE:
+        codes = rec[16:16 + nbh * n * r].reshape(nbh, n, r)
+        scales = rec[16 + nbh * n * r:16 + nbh * n * (r + 2)].view("<u2").reshape(nbh, n)
+        for bh in range(nbh):
+            for t in range(n):
+                rows[(bh, t)] = (codes[bh, t], int(scales[bh, t]))
+        return lay, rows, 16 + nbh * n * (r + 2)
+    assert lay == oracle.COEF_SPARSE
+    counts = rec[16:16 + 4 * nbh].view("<u4")
+    pos = 16 + 4 * nbh
+    for bh in range(nbh):
+        c = int(counts[bh])
+        idx = rec[pos:pos + 2 * c].view("<u2")
+        codes = rec[pos + 2 * c:pos + 2 * c + r * c].reshape(c, r)
+        scales = rec[pos + 2 * c + r * c:pos + 4 * c + r * c].view("<u2")
+        assert np.all(np.diff(idx.astype(np.int64)) > 0)
+        for m in range(c):
+            rows[(bh, int(idx[m]))] = (codes[m], int(scales[m]))
+        pos += c * (r + 4)
+    return lay, rows, pos
+
+
+def _coef_cache(keep_frac, seed=31, rank=4):
+    """An encoded cache whose coefficient rows outside a random keep set are
+    zeroed, as the retention gate leaves them."""
+    import packed
+    wl = _small_workload(rank=rank)
+    cfg, tables, cache, *_ = _encoded(wl)
+    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.capacity)
+    r = rng(seed)
+    for bh in range(wl.batch * wl.heads):
+        drop = np.nonzero(r.random(wl.n_cache) >= keep_frac)[0]
+        packed.zero_coef_rows(cache, lay, bh, drop)
+    return wl, cfg, cache, lay
+
+
+@pytest.mark.parametrize("keep", [0.0, 0.1, 0.35, 0.7, 1.0])
+def test_coef_record_round_trip(keep):
+    # The record holds exactly the chunk's rows (all of them dense, the
+    # non-zero-scale ones sparse, indices increasing); unpacking it into a
+    # cache whose chunk rows hold garbage restores them and touches nothing else.
+    import packed
+    wl, cfg, cache, lay = _coef_cache(keep)
+    start, n, nbh, r = 64, 130, wl.batch * wl.heads, wl.rank
+    rec = oracle.coef_pack(cfg, cache, start, n)
+    layout, rows, size = _read_coef_record(rec, n, r, nbh)
+    assert size == rec.size
+    for bh in range(nbh):
+        f = packed.fields(cache, lay, bh, start, start + n)
+        for t in range(n):
+            kept = f["k_cscale"][t] != 0
+            if layout == oracle.COEF_SPARSE and not kept:
+                assert (bh, t) not in rows and not f["k_coef"][t].any()
+                continue
+            codes, sc = rows[(bh, t)]
+            assert sc == f["k_cscale"][t] and np.array_equal(codes.view(np.int8), f["k_coef"][t])
+    target = rng(5).integers(0, 256, cache.size, dtype=np.uint8)
+    before = target.copy()
+    oracle.coef_unpack(cfg, rec, target, start, n)
+    chunk = packed.coef_byte_mask(lay, nbh, start, n)
+    assert np.array_equal(target[chunk], cache[chunk])
+    assert np.array_equal(target[~chunk], before[~chunk])
+
+
+def test_coef_layout_choice_is_the_smaller_with_ties_dense():
+    # Two heads, r = 4, a 4-token chunk: dense takes 16 + 2*4*6 = 64 bytes and
+    # sparse 16 + 8 + 8k for k kept rows, so 5 kept rows tie (dense is kept) and
+    # 4 go sparse; no kept row leaves only the counts.
+    import packed
+    wl, cfg, cache, lay = _coef_cache(1.0)
+    start, n = 10, 4
+    for k, want, size in [(8, oracle.COEF_DENSE, 64), (5, oracle.COEF_DENSE, 64), (4, oracle.COEF_SPARSE, 56),
+                          (0, oracle.COEF_SPARSE, 24)]:
+        c = cache.copy()
+        drop = [(bh, t) for bh in range(2) for t in range(n)][k:]
+        for bh, t in drop:
+            packed.zero_coef_rows(c, lay, bh, [start + t])
+        assert oracle.coef_record_bytes(cfg, c, start, n) == (size, want)
+        assert oracle.coef_pack(cfg, c, start, n).size == size
+
+
+def test_coef_record_of_a_fully_gated_chunk():
+    # With all eigenvalues 0 the gate drops every row, and the record is the
+    # header plus one zero count per head.
+    wl = _small_workload(rank=4)
+    gated = synth.scaled(wl, storage=oracle.STORE_GATE)
+    cfg, tables, _, k, v, _, _ = _encoded(wl)
+    cfg1 = oracle.cfg_from_workload(gated)
+    cache = oracle.new_cache(cfg1)
+    oracle.append(cfg1, tables[:4] + (np.zeros_like(tables[4]),), cache, 0, k, v)
+    rec = oracle.coef_pack(cfg1, cache, 0, wl.n_cache)
+    nbh = wl.batch * wl.heads
+    assert rec.size == 16 + 4 * nbh and int(rec[:4].view("<u4")[0]) == oracle.COEF_SPARSE
+    assert not rec[16:].any()
+
+
 # ------------------------------------------------- BF16 active chunk (NEXT f2)
 
 def test_active_chunk_alone_is_plain_attention():
