@@ -258,6 +258,49 @@ quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, cons
                               int64_t n_cache, const void* q, int64_t n_q, int64_t q_start,
                               int32_t frame_tokens, float* logits_out, void* stream);
 
+/* ------------------------------------------- per-chunk coefficient records */
+
+/* App. D.1 per-chunk choice between dense and sparse PSAC coefficient layouts,
+ * for a chunk of the cache moved out of it (offloaded to the host, written to
+ * disk, sent elsewhere): the INT8 rows and FP16 scales of slots
+ * [start, start + n) of every (b, h) as one record, dense or sparse, whichever
+ * is smaller counting the sparse indices. A row is kept when its scale is
+ * non-zero; a zero scale means zero codes (the QWM_STORE_GATE rule dropped the
+ * row, or its coefficients were zero), so the sparse form loses nothing. The
+ * attention calls read the dense rows in the cache. Record (little-endian):
+ *   header   16 B: u32 layout (QWM_COEF_DENSE or QWM_COEF_SPARSE), u32 n,
+ *            u32 r, u32 B*H
+ *   dense    codes [B*H][n][r] int8, then scales [B*H][n] binary16:
+ *            16 + B*H*n*(r + 2) bytes
+ *   sparse   counts [B*H] u32, then per (b, h) in order: indices [count] u16
+ *            (slot - start, increasing), codes [count][r] int8, scales
+ *            [count] binary16: 16 + 4*B*H + (r + 4) * (kept rows) bytes
+ * Sparse is taken only when strictly smaller. Needs rank >= 1, 0 <= n <= 65536
+ * and start + n <= capacity (QWM_ERR_INVALID_ARG otherwise). */
+#define QWM_COEF_DENSE 0
+#define QWM_COEF_SPARSE 1
+
+/* Bytes a record buffer for n tokens must hold (the dense size, and at least
+ * the header and counts); 0 if the arguments are invalid. */
+size_t quantwm_coef_record_max_bytes(const quantwm_config* cfg, int64_t n);
+
+/* Writes the record of the chunk into `record` (device, record_bytes >=
+ * quantwm_coef_record_max_bytes(cfg, n)); *written (host) receives its size and
+ * *layout (host, may be NULL) the layout chosen. The cache is only read. The
+ * call synchronises `stream` once, to read the kept-row counts; the record is
+ * complete when the stream reaches the call's last kernel. */
+quantwm_status quantwm_coef_pack(const quantwm_config* cfg, const void* cache, int64_t start, int64_t n,
+                                 void* record, size_t record_bytes, int64_t* written, int32_t* layout,
+                                 void* stream);
+
+/* Writes a record made by quantwm_coef_pack back into slots [start, start + n)
+ * of every (b, h): the codes and scales of its rows, and zeros for the rows a
+ * sparse record leaves out. Nothing else in the cache changes. The header and
+ * counts are read back and checked first (n, r and B*H must match the call,
+ * and record_bytes must cover the record), which synchronises `stream`. */
+quantwm_status quantwm_coef_unpack(const quantwm_config* cfg, const void* record, size_t record_bytes,
+                                   void* cache, int64_t start, int64_t n, void* stream);
+
 /* Message for the last non-OK status on the calling thread ("" if none). */
 const char* quantwm_last_error(void);
 

@@ -35,7 +35,7 @@ def _units():
     # v_max3_f32 without a quieting v_max_f32 x, x per input (its logits and
     # running maxima are finite or -inf)
     units.append(("attend.o", "attend.hip", ["-fno-honor-nans"]))
-    for name in ("calib", "api"):
+    for name in ("calib", "coef", "api"):
         units.append((f"{name}.o", f"{name}.hip", []))
     units.append(("eigh.o", "eigh.cpp", ["-x", "hip"]))
     return units

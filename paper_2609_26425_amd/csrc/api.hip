@@ -84,6 +84,100 @@ extern "C" {
 
 const char* quantwm_last_error(void) { return g_error.c_str(); }
 
+}  // extern "C"
+
+namespace {
+// shape checks shared by the coefficient-record calls
+quantwm_status check_coef(const quantwm_config* cfg, int64_t start, int64_t n) {
+  QWM_TRY(check_cfg(cfg));
+  if (cfg->rank < 1) return fail(QWM_ERR_INVALID_ARG, "the config has no PSAC rows (rank 0)");
+  if (start < 0 || n < 0 || n > 65536 || start + n > cfg->capacity)
+    return fail(QWM_ERR_INVALID_ARG, "need start >= 0, 0 <= n <= 65536 and start + n <= capacity");
+  return QWM_OK;
+}
+int64_t coef_dense_bytes(const quantwm_config* c, int64_t n) {
+  return 16 + int64_t(c->batch) * c->heads * n * (c->rank + 2);
+}
+}  // namespace
+
+extern "C" {
+
+size_t quantwm_coef_record_max_bytes(const quantwm_config* cfg, int64_t n) {
+  if (check_cfg(cfg) != QWM_OK || cfg->rank < 1 || n < 0 || n > 65536) return 0;
+  const int64_t floor = 16 + 4 * int64_t(cfg->batch) * cfg->heads, dense = coef_dense_bytes(cfg, n);
+  return size_t(dense > floor ? dense : floor);
+}
+
+quantwm_status quantwm_coef_pack(const quantwm_config* cfg, const void* cache, int64_t start, int64_t n,
+                                 void* record, size_t record_bytes, int64_t* written, int32_t* layout,
+                                 void* stream) {
+  QWM_TRY(check_coef(cfg, start, n));
+  QWM_TRY(check_dev(cache, "cache"));
+  QWM_TRY(check_dev(record, "record"));
+  if (!written) return fail(QWM_ERR_INVALID_ARG, "written is null");
+  const size_t need = quantwm_coef_record_max_bytes(cfg, n);
+  if (record_bytes < need) return fail(QWM_ERR_INVALID_ARG, "record buffer too small: %zu < %zu bytes", record_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t nbh = int64_t(cfg->batch) * cfg->heads;
+  hipError_t he;
+  // kept-row counts go where a sparse record keeps them
+  uint8_t* rec = static_cast<uint8_t*>(record);
+  if ((he = qwm::launch_coef_count(*cfg, cache, start, int(n), rec + 16, s)) != hipSuccess)
+    return hip_fail(he, "coef count launch");
+  std::vector<uint32_t> counts(static_cast<size_t>(nbh));
+  if ((he = hipMemcpyAsync(counts.data(), rec + 16, counts.size() * 4, hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (he = hipStreamSynchronize(s)) != hipSuccess)
+    return hip_fail(he, "coef count readback");
+  int64_t kept = 0;
+  for (uint32_t k : counts) kept += k;
+  const int64_t dense = coef_dense_bytes(cfg, n), sparse = 16 + 4 * nbh + kept * (cfg->rank + 4);
+  const int lay = sparse < dense ? QWM_COEF_SPARSE : QWM_COEF_DENSE;
+  if ((he = qwm::launch_coef_pack(*cfg, cache, start, int(n), record, lay, s)) != hipSuccess)
+    return hip_fail(he, "coef pack launch");
+  *written = lay == QWM_COEF_SPARSE ? sparse : dense;
+  if (layout) *layout = lay;
+  return ok();
+}
+
+quantwm_status quantwm_coef_unpack(const quantwm_config* cfg, const void* record, size_t record_bytes,
+                                   void* cache, int64_t start, int64_t n, void* stream) {
+  QWM_TRY(check_coef(cfg, start, n));
+  QWM_TRY(check_dev(record, "record"));
+  QWM_TRY(check_dev(cache, "cache"));
+  if (record_bytes < 16) return fail(QWM_ERR_INVALID_ARG, "record shorter than its header");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t nbh = int64_t(cfg->batch) * cfg->heads;
+  hipError_t he;
+  uint32_t hdr[4];
+  if ((he = hipMemcpyAsync(hdr, record, 16, hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (he = hipStreamSynchronize(s)) != hipSuccess)
+    return hip_fail(he, "coef header readback");
+  if (hdr[1] != uint32_t(n) || hdr[2] != uint32_t(cfg->rank) || int64_t(hdr[3]) != nbh)
+    return fail(QWM_ERR_INVALID_ARG, "record header (n %u, r %u, heads %u) does not match the call", hdr[1], hdr[2],
+                hdr[3]);
+  if (hdr[0] == QWM_COEF_DENSE) {
+    if (int64_t(record_bytes) < coef_dense_bytes(cfg, n)) return fail(QWM_ERR_INVALID_ARG, "dense record is truncated");
+  } else if (hdr[0] == QWM_COEF_SPARSE) {
+    if (int64_t(record_bytes) < 16 + 4 * nbh) return fail(QWM_ERR_INVALID_ARG, "sparse record is truncated");
+    std::vector<uint32_t> counts(static_cast<size_t>(nbh));
+    if ((he = hipMemcpyAsync(counts.data(), static_cast<const uint8_t*>(record) + 16, counts.size() * 4,
+                             hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (he = hipStreamSynchronize(s)) != hipSuccess)
+      return hip_fail(he, "coef counts readback");
+    int64_t total = 16 + 4 * nbh;
+    for (uint32_t k : counts) {
+      if (int64_t(k) > n) return fail(QWM_ERR_INVALID_ARG, "sparse record counts more rows than the chunk holds");
+      total += int64_t(k) * (cfg->rank + 4);
+    }
+    if (int64_t(record_bytes) < total) return fail(QWM_ERR_INVALID_ARG, "sparse record is truncated");
+  } else {
+    return fail(QWM_ERR_INVALID_ARG, "record layout %u is neither dense nor sparse", hdr[0]);
+  }
+  if ((he = qwm::launch_coef_unpack(*cfg, record, int(hdr[0]), cache, start, int(n), s)) != hipSuccess)
+    return hip_fail(he, "coef unpack launch");
+  return ok();
+}
+
 size_t quantwm_cache_bytes(const quantwm_config* cfg) {
   if (check_cfg(cfg) != QWM_OK) return 0;
   return size_t(qwm::cache_layout(*cfg).total);

@@ -146,6 +146,12 @@ hipError_t launch_moment_accumulate(const quantwm_config& c, const void* q, int6
                                     hipStream_t s);
 hipError_t launch_second_moment(const quantwm_config& c, const void* q, int64_t n, double* m_out,
                                 hipStream_t s);
+hipError_t launch_coef_count(const quantwm_config& c, const void* cache, int64_t start, int n, void* counts,
+                             hipStream_t s);
+hipError_t launch_coef_pack(const quantwm_config& c, const void* cache, int64_t start, int n, void* record,
+                            int layout, hipStream_t s);
+hipError_t launch_coef_unpack(const quantwm_config& c, const void* record, int layout, void* cache, int64_t start,
+                              int n, hipStream_t s);
 hipError_t launch_kmeans(const quantwm_config& c, const void* x, int64_t n, int iters, uint8_t* calib,
                          int64_t o_mu, int32_t* assign_ws, hipStream_t s);
 

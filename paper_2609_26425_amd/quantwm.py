@@ -67,6 +67,9 @@ def _load():
         "quantwm_attend_epochs": (I32, [C, P, I32, ctypes.POINTER(I64), P, I64, P, P, I64, P, I64, I64, I32, P, P,
                                         P, SZ, P]),
         "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I32, P, P]),
+        "quantwm_coef_record_max_bytes": (SZ, [C, I64]),
+        "quantwm_coef_pack": (I32, [C, P, I64, I64, P, SZ, ctypes.POINTER(I64), ctypes.POINTER(I32), P]),
+        "quantwm_coef_unpack": (I32, [C, P, SZ, P, I64, I64, P]),
         "quantwm_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -82,7 +85,8 @@ EXPORTED = ("quantwm_cache_bytes", "quantwm_token_bytes", "quantwm_calib_bytes",
             "quantwm_stats_update", "quantwm_calibrate_epoch",
             "quantwm_append", "quantwm_attend_workspace_bytes", "quantwm_attend", "quantwm_attend_active",
             "quantwm_attend_epochs",
-            "quantwm_logits", "quantwm_last_error")
+            "quantwm_logits", "quantwm_coef_record_max_bytes", "quantwm_coef_pack", "quantwm_coef_unpack",
+            "quantwm_last_error")
 
 
 def library():
@@ -225,3 +229,26 @@ def quantwm_attend_epochs(cfg, calibs, epoch_start, cache, n_cache, k_act, v_act
 def quantwm_logits(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, logits_out, stream=None):
     _check(_lib.quantwm_logits(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cache, _ptr(q), n_q, q_start,
                                frame_tokens, _ptr(logits_out), _stream(stream)))
+
+
+# App. D.1 per-chunk coefficient records (QWM_COEF_* in include/quantwm.h)
+COEF_DENSE = 0
+COEF_SPARSE = 1
+
+
+def quantwm_coef_record_max_bytes(cfg, n) -> int:
+    return int(_lib.quantwm_coef_record_max_bytes(ctypes.byref(cfg), n))
+
+
+def quantwm_coef_pack(cfg, cache, start, n, record, stream=None):
+    """Writes the chunk's coefficient record into the uint8 device tensor
+    `record`; returns (bytes written, layout)."""
+    written, layout = ctypes.c_int64(), ctypes.c_int32()
+    _check(_lib.quantwm_coef_pack(ctypes.byref(cfg), _ptr(cache), start, n, _ptr(record), record.numel(),
+                                  ctypes.byref(written), ctypes.byref(layout), _stream(stream)))
+    return int(written.value), int(layout.value)
+
+
+def quantwm_coef_unpack(cfg, record, cache, start, n, record_bytes=None, stream=None):
+    nb = record.numel() if record_bytes is None else record_bytes
+    _check(_lib.quantwm_coef_unpack(ctypes.byref(cfg), _ptr(record), nb, _ptr(cache), start, n, _stream(stream)))

@@ -65,6 +65,30 @@ def test_full_metric_adds_the_matrix_to_the_calibration_block(d):
     assert e.value.status == qw.ERR_INVALID_ARG and "m is null" in qw.quantwm_last_error()
 
 
+def test_coef_record_sizes_and_validation():
+    # App. D.1 chunk records: the buffer bound is the dense size (at least the
+    # header and counts); bad shapes and short buffers fail before device work.
+    cfg = qw.make_config(2, 3, 128, 37, 32, 12, 3, 1000, "bf16")
+    assert qw.quantwm_coef_record_max_bytes(cfg, 700) == 16 + 6 * 700 * 14
+    assert qw.quantwm_coef_record_max_bytes(cfg, 0) == 16 + 4 * 6
+    assert qw.quantwm_coef_record_max_bytes(cfg, 65537) == 0
+    assert qw.quantwm_coef_record_max_bytes(qw.make_config(2, 3, 128, 37, 32, 0, 3, 1000, "bf16"), 10) == 0
+    P = ctypes.c_void_p
+    lib = qw.library()
+    wr, lay = ctypes.c_int64(), ctypes.c_int32()
+    cases = [(qw.make_config(2, 3, 128, 37, 32, 0, 3, 1000, "bf16"), 0, 10, 10 ** 6, "rank 0"),
+             (cfg, 900, 200, 10 ** 6, "capacity"),
+             (cfg, 0, 700, 100, "too small")]
+    for c, start, n, nbytes, msg in cases:
+        st = lib.quantwm_coef_pack(ctypes.byref(c), P(0x1000), start, n, P(0x2000), nbytes, ctypes.byref(wr),
+                                   ctypes.byref(lay), None)
+        assert st == qw.ERR_INVALID_ARG and msg in qw.quantwm_last_error(), qw.quantwm_last_error()
+    assert lib.quantwm_coef_pack(ctypes.byref(cfg), P(0x1000), 0, 5, P(0x2000), 10 ** 6, None, None,
+                                 None) == qw.ERR_INVALID_ARG
+    assert lib.quantwm_coef_unpack(ctypes.byref(cfg), P(0x2000), 8, P(0x1000), 0, 5, None) == qw.ERR_INVALID_ARG
+    assert "header" in qw.quantwm_last_error()
+
+
 def test_validation_without_a_gpu():
     good = qw.make_config(1, 2, 128, 16, 32, 8, 4, 100, "bf16")
     for bad, status in [(qw.make_config(1, 2, 96, 16, 32, 8, 4, 100, "bf16"), qw.ERR_UNSUPPORTED),
