@@ -236,7 +236,9 @@ def main():
     # history of the rest, timed separately on the same inputs
     n_pk = wl.n_cache - n_new
     ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ws_act = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q)
+    # with the two-part workspace: packed whole tiles through the plain kernel,
+    # the rest through the general one, merged by log-sum-exp
+    ws_act = qw.quantwm_attend_active_workspace_bytes(cfg, n_pk, n_new, wl.n_q)
     act_ws = torch.empty(ws_act, dtype=torch.uint8, device=dev) if ws_act else None
     for i in range(2):
         qw.quantwm_attend_active(cfg, calib, caches[0], n_pk, k_new[0], v_new[0], n_new, qs[0], wl.n_q,
@@ -296,7 +298,7 @@ def main():
         "copies": args.copies,
         "attend_workspace_bytes": ws_bytes,
         "attend_active_ms": act_ms,
-        "attend_active_config": f"{n_pk} packed + {n_new} exact BF16 keys",
+        "attend_active_config": f"{n_pk} packed + {n_new} exact BF16 keys, two-part workspace {ws_act} B",
         "attend_epochs_ms": ep_ms,
         "attend_epochs_config": f"{len(starts)} calibration epochs, one per {wl.chunk}-token chunk",
     }

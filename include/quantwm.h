@@ -229,8 +229,17 @@ quantwm_status quantwm_attend(const quantwm_config* cfg, const void* calib, cons
  * are k_act / v_act ([B, n_act, H, d] dtype, device, 16-byte aligned), used
  * exactly, with no PSAC term. Positions are concatenated: the mask is that of
  * quantwm_attend over n_cache + n_act keys, and q_start <= n_cache + n_act.
- * n_act <= 2^26. With n_act == 0 this is quantwm_attend. The workspace size is
- * quantwm_attend_workspace_bytes(cfg, n_cache + n_act, n_q). */
+ * n_act <= 2^26. With n_act == 0 this is quantwm_attend. With a workspace of
+ * quantwm_attend_active_workspace_bytes(cfg, n_cache, n_act, n_q) bytes or more
+ * (256-byte aligned) the call runs in two parts merged by log-sum-exp (the LSE
+ * merge of the streaming setting): the packed keys of whole 64-key tiles
+ * through the plain attention kernel, the remaining keys (the last packed tile
+ * and the active chunk) through the general one. With a smaller workspace it
+ * takes quantwm_attend_workspace_bytes(cfg, n_cache + n_act, n_q) as for
+ * quantwm_attend, and NULL runs one launch. All forms give the same result up
+ * to fp32 rounding order. */
+size_t quantwm_attend_active_workspace_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_act,
+                                             int64_t n_q);
 quantwm_status quantwm_attend_active(const quantwm_config* cfg, const void* calib, const void* cache,
                                      int64_t n_cache, const void* k_act, const void* v_act, int64_t n_act,
                                      const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens,

@@ -1,7 +1,7 @@
 """Builds libquantwm.so (the gfx950 HIP kernels plus the C ABI) in-tree.
 
 Translation units compile in parallel: append.hip once per (element type,
-head_dim), attend.hip, calib.hip, api.hip and the host eigensolver; the objects
+head_dim), attend.hip, calib.hip, coef.hip, api.hip and the host eigensolver; the objects
 link into ``paper_2609_26425_amd/libquantwm.so``.
 """
 from __future__ import annotations

@@ -457,6 +457,28 @@ size_t quantwm_attend_workspace_bytes(const quantwm_config* cfg, int64_t n_cache
   return attend_split_bytes(cfg, n_cache, n_q, nullptr);
 }
 
+// Two-part form of the active-chunk call: the plain kernel over the packed keys
+// of whole tiles [0, 64 floor(n_cache / 64)) as ns_a partial planes (its own key
+// split), then the general kernel over the rest (one plane), then the merge.
+static size_t active_two_part_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_act, int64_t n_q,
+                                    int* ns_a) {
+  const int64_t nfl = n_cache / qwm::kAttendTileKeys * qwm::kAttendTileKeys;
+  if (nfl == 0 || n_act == 0 || n_q <= 0) return 0;
+  const int ns = qwm::attend_splits(n_q, cfg->heads, cfg->batch, nfl, device_cus());
+  if (ns_a) *ns_a = ns;
+  const size_t rows = size_t(ns + 1) * cfg->batch * cfg->heads * size_t(n_q);
+  return (rows * cfg->head_dim * 4 + 255) / 256 * 256 + rows * 2 * 4;
+}
+
+size_t quantwm_attend_active_workspace_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_act,
+                                             int64_t n_q) {
+  if (check_cfg(cfg) != QWM_OK || n_cache < 0 || n_act < 0 || n_q <= 0) return 0;
+  if (cfg->storage & QWM_STORE_SCALE_I8) return 0;
+  const size_t two = active_two_part_bytes(cfg, n_cache, n_act, n_q, nullptr);
+  const size_t split = attend_split_bytes(cfg, n_cache + n_act, n_q, nullptr);
+  return two > split ? two : split;
+}
+
 static quantwm_status attend_common(const quantwm_config* cfg, const void* calib, int32_t n_epochs,
                                     const int64_t* epoch_start, const void* cache, int64_t n_cache,
                                     const void* k_act, const void* v_act, int64_t n_act, const void* q, int64_t n_q,
@@ -528,12 +550,55 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
       a.part_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + (rows * cfg->head_dim * 4 + 255) / 256 * 256);
     }
   }
+  a.tile_lo = 0;
+  a.split_base = 0;
+  a.partial = 0;
+  // the active chunk in two parts when the workspace holds their partials: the
+  // packed keys of whole tiles through the plain kernel, the rest through the
+  // general one, merged by log-sum-exp
+  int ns_a = 1;
+  const size_t two = (!logits_out && workspace && n_act > 0 && n_epochs == 1)
+                         ? active_two_part_bytes(cfg, n_cache, n_act, n_q, &ns_a) : 0;
+  const bool two_part = two > 0 && workspace_bytes >= two;
+  if (two_part) {
+    const size_t rows = size_t(ns_a + 1) * cfg->batch * cfg->heads * size_t(n_q);
+    a.n_split = 1;
+    a.part_o = static_cast<float*>(workspace);
+    a.part_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + (rows * cfg->head_dim * 4 + 255) / 256 * 256);
+    if ((n_q + 255) / 256 * int64_t(ns_a) > 0x7fffffff) return fail(QWM_ERR_UNSUPPORTED, "n_q too large");
+  }
   if ((n_q + 255) / 256 * int64_t(a.n_split) > 0x7fffffff) return fail(QWM_ERR_UNSUPPORTED, "n_q too large");
   // the kernel keeps Query and key positions in 32 bits
   if (n_q > kMaxPositions || n_cache + n_act > kMaxPositions)
     return fail(QWM_ERR_UNSUPPORTED, "more than %lld Queries or keys per head", (long long)kMaxPositions);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool lg = logits_out != nullptr;
+  if (two_part) {
+    const bool bf = cfg->dtype == QWM_BF16;
+    const int64_t nfl = n_cache / qwm::kAttendTileKeys * qwm::kAttendTileKeys;
+    qwm::AttendArgs pa = a;  // packed part: keys [0, nfl) only, planes [0, ns_a)
+    pa.n_cache = nfl;
+    pa.k_act = pa.v_act = nullptr;
+    pa.n_act = 0;
+    pa.n_split = ns_a;
+    pa.partial = 1;
+    qwm::AttendArgs ga = a;  // the rest: tiles from nfl / 64 on, plane ns_a
+    ga.tile_lo = nfl / qwm::kAttendTileKeys;
+    ga.split_base = ns_a;
+    ga.partial = 1;
+    hipError_t e = bf ? qwm::launch_attend_bf16(pa, cfg->head_dim, cfg->batch, false, s)
+                      : qwm::launch_attend_f32(pa, cfg->head_dim, cfg->batch, false, s);
+    if (e == hipSuccess)
+      e = bf ? qwm::launch_attend_bf16(ga, cfg->head_dim, cfg->batch, false, s)
+             : qwm::launch_attend_f32(ga, cfg->head_dim, cfg->batch, false, s);
+    if (e == hipSuccess) {
+      qwm::AttendArgs ca = a;
+      ca.n_split = ns_a + 1;
+      e = qwm::launch_attend_combine(ca, cfg->head_dim, cfg->batch, bf, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "attend launch (two parts)");
+    return ok();
+  }
   const hipError_t e = cfg->dtype == QWM_BF16 ? qwm::launch_attend_bf16(a, cfg->head_dim, cfg->batch, lg, s)
                                               : qwm::launch_attend_f32(a, cfg->head_dim, cfg->batch, lg, s);
   if (e != hipSuccess) return hip_fail(e, "attend launch");

@@ -225,7 +225,7 @@ __device__ inline V pack_operand(const float* x) {
 // matrix cores) and NP producer waves (read and dequantise the packed tiles).
 // Waves w and w + 4 share a SIMD, so every SIMD runs one producer beside two
 // consumers: the producer's vector work overlaps the consumers' matrix work.
-constexpr int NC = 8, NP = 4, BQ = 32 * NC, KT = 64, NT = 64 * (NC + NP), PT = 64 * NP;
+constexpr int NC = 8, NP = 4, BQ = 32 * NC, KT = kAttendTileKeys, NT = 64 * (NC + NP), PT = 64 * NP;
 
 // LDS row strides (elements), chosen so that the matrix-core operand reads are
 // free of bank conflicts: K tile rows of 272 B (16-byte reads), V^T rows of
@@ -302,8 +302,11 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   int64_t kfull = qs + (qa / F + 1) * F;  // keys below are visible to every Query of the workgroup
   if (kfull > nc) kfull = nc;
   const int64_t ntile_all = (kend + KT - 1) / KT;
-  const int64_t per_split = (ntile_all + a.n_split - 1) / a.n_split;
-  const int64_t t0 = split * per_split < ntile_all ? split * per_split : ntile_all;
+  // this launch covers tiles [tile_lo, ntile_all) (tile_lo is 0 unless the
+  // caller splits the key range over launches)
+  const int64_t tlo = a.tile_lo < ntile_all ? a.tile_lo : ntile_all;
+  const int64_t per_split = (ntile_all - tlo + a.n_split - 1) / a.n_split;
+  const int64_t t0 = tlo + split * per_split < ntile_all ? tlo + split * per_split : ntile_all;
   const int64_t ntile = t0 + per_split < ntile_all ? t0 + per_split : ntile_all;  // this split: tiles [t0, ntile)
   const int64_t nfull = npk / KT;  // tiles [0, nfull) hold packed keys only
 
@@ -948,11 +951,11 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 
   if constexpr (!LOGITS) {
     const float l_tot = l_run + __shfl_xor(l_run, 32);
-    if (a.n_split > 1) {
+    if (a.n_split > 1 || a.partial) {
       // partial result of this split: unnormalised O, the running max (raw logit
       // units) and the sum; attend_combine merges the splits
       if (qvalid) {
-        const int64_t row = (int64_t(split) * a.heads * gridDim.z + bh) * a.n_q + qi;
+        const int64_t row = (int64_t(a.split_base + split) * a.heads * gridDim.z + bh) * a.n_q + qi;
         float* po = a.part_o + row * D;
 #pragma unroll
         for (int cb = 0; cb < D / 32; ++cb)
@@ -1054,7 +1057,7 @@ hipError_t launch_r(const AttendArgs& a, int batch, bool logits, hipStream_t s) 
             : launch_k<T, D, RP, false, false, false, true>(a, grid, lds, s);
   else
     e = tab ? launch_k<T, D, RP, false, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false>(a, grid, lds, s);
-  if (e != hipSuccess || a.n_split == 1) return e;
+  if (e != hipSuccess || a.n_split == 1 || a.partial) return e;
   hipLaunchKernelGGL((attend_combine<T, D>), dim3((unsigned)((a.n_q + 3) / 4), (unsigned)a.heads, (unsigned)batch),
                      dim3(256), 0, s, a);
   return hipGetLastError();
@@ -1098,6 +1101,21 @@ hipError_t launch_attend_f32(const AttendArgs& a, int d, int batch, bool logits,
   if (d == 64) return launch_d<float, 64>(a, batch, logits, s);
   if (d == 128) return launch_d<float, 128>(a, batch, logits, s);
   return hipErrorInvalidValue;
+}
+
+// merges the a.n_split partial planes of a.part_o / a.part_ml into a.out and a.lse
+hipError_t launch_attend_combine(const AttendArgs& a, int d, int batch, bool is_bf16, hipStream_t s) {
+  const dim3 grid((unsigned)((a.n_q + 3) / 4), (unsigned)a.heads, (unsigned)batch);
+  if (is_bf16) {
+    if (d == 64) hipLaunchKernelGGL((attend_combine<bf16, 64>), grid, dim3(256), 0, s, a);
+    else if (d == 128) hipLaunchKernelGGL((attend_combine<bf16, 128>), grid, dim3(256), 0, s, a);
+    else return hipErrorInvalidValue;
+  } else {
+    if (d == 64) hipLaunchKernelGGL((attend_combine<float, 64>), grid, dim3(256), 0, s, a);
+    else if (d == 128) hipLaunchKernelGGL((attend_combine<float, 128>), grid, dim3(256), 0, s, a);
+    else return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_attend_bf16(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s) {

@@ -125,7 +125,15 @@ struct AttendArgs {
   int64_t epoch_start[64];
   float* part_o;  // [n_split][B*H][n_q][d] unnormalised partial outputs (n_split > 1)
   float* part_ml; // [n_split][B*H][n_q][2] running max (raw logits) and sum per partial
+  // a launch that covers key tiles [tile_lo, ...) only and writes its partial
+  // results at planes split_base + split; the caller merges them (partial = 1)
+  int64_t tile_lo;
+  int split_base;
+  int partial;
 };
+
+// keys per attention tile
+constexpr int kAttendTileKeys = 64;
 
 // Launchers (one translation unit per element type).
 hipError_t launch_append_f32_64(const AppendArgs& a, int g, int batch, hipStream_t s);
@@ -146,6 +154,7 @@ hipError_t launch_moment_accumulate(const quantwm_config& c, const void* q, int6
                                     hipStream_t s);
 hipError_t launch_second_moment(const quantwm_config& c, const void* q, int64_t n, double* m_out,
                                 hipStream_t s);
+hipError_t launch_attend_combine(const AttendArgs& a, int d, int batch, bool is_bf16, hipStream_t s);
 hipError_t launch_coef_count(const quantwm_config& c, const void* cache, int64_t start, int n, void* counts,
                              hipStream_t s);
 hipError_t launch_coef_pack(const quantwm_config& c, const void* cache, int64_t start, int n, void* record,

@@ -67,6 +67,7 @@ def _load():
         "quantwm_attend_epochs": (I32, [C, P, I32, ctypes.POINTER(I64), P, I64, P, P, I64, P, I64, I64, I32, P, P,
                                         P, SZ, P]),
         "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I32, P, P]),
+        "quantwm_attend_active_workspace_bytes": (SZ, [C, I64, I64, I64]),
         "quantwm_coef_record_max_bytes": (SZ, [C, I64]),
         "quantwm_coef_pack": (I32, [C, P, I64, I64, P, SZ, ctypes.POINTER(I64), ctypes.POINTER(I32), P]),
         "quantwm_coef_unpack": (I32, [C, P, SZ, P, I64, I64, P]),
@@ -85,7 +86,7 @@ EXPORTED = ("quantwm_cache_bytes", "quantwm_token_bytes", "quantwm_calib_bytes",
             "quantwm_stats_update", "quantwm_calibrate_epoch",
             "quantwm_append", "quantwm_attend_workspace_bytes", "quantwm_attend", "quantwm_attend_active",
             "quantwm_attend_epochs",
-            "quantwm_logits", "quantwm_coef_record_max_bytes", "quantwm_coef_pack", "quantwm_coef_unpack",
+            "quantwm_logits", "quantwm_attend_active_workspace_bytes", "quantwm_coef_record_max_bytes", "quantwm_coef_pack", "quantwm_coef_unpack",
             "quantwm_last_error")
 
 
@@ -196,6 +197,10 @@ def quantwm_append(cfg, calib, cache, n_cached, k_new, v_new, n_new, coef_f32_ou
 
 def quantwm_attend_workspace_bytes(cfg: Config, n_cache: int, n_q: int) -> int:
     return int(_lib.quantwm_attend_workspace_bytes(ctypes.byref(cfg), n_cache, n_q))
+
+
+def quantwm_attend_active_workspace_bytes(cfg: Config, n_cache: int, n_act: int, n_q: int) -> int:
+    return int(_lib.quantwm_attend_active_workspace_bytes(ctypes.byref(cfg), n_cache, n_act, n_q))
 
 
 def quantwm_attend(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, out, lse_out=None, workspace=None,

@@ -466,8 +466,10 @@ def test_capacity_and_argument_errors():
 
 def _active_case(wl, max_sources, n_heads_rows, row_step):
     """Packed history = the first n_cache - n_act tokens; the last n_act tokens
-    (the chunk being generated) enter exactly. Runs with and without a split
-    workspace; both against the oracle."""
+    (the chunk being generated) enter exactly. Runs with no workspace (one
+    launch), with a split workspace, and with the two-part workspace (packed
+    whole tiles through the plain kernel, the rest through the general one,
+    merged by log-sum-exp); each against the oracle."""
     case = case_for(wl, max_sources)
     cfg = gpu_config(wl)
     calib = gpu_calib_from_tables(cfg, harness.full_tables(case))
@@ -487,10 +489,12 @@ def _active_case(wl, max_sources, n_heads_rows, row_step):
                                     v_act=np.ascontiguousarray(case.v[:, n_pk:]))
     o_out, o_lse = o_out[inv.ravel()], o_lse[inv.ravel()]
     tol = 2e-2 if wl.dtype == "bf16" else 1e-4
-    for split in (False, True):
-        nb = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q) if split else 0
-        if split and nb == 0:
+    for mode in ("none", "split", "two-part"):
+        nb = {"none": 0, "split": qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q),
+              "two-part": qw.quantwm_attend_active_workspace_bytes(cfg, n_pk, n_act, wl.n_q)}[mode]
+        if mode != "none" and nb == 0:
             continue
+        split = mode != "none"
         ws = torch.empty(nb, dtype=torch.uint8, device=DEV) if nb else None
         out = torch.empty_like(q)
         lse = torch.empty((wl.batch, wl.heads, wl.n_q), dtype=torch.float32, device=DEV)
@@ -505,7 +509,7 @@ def _active_case(wl, max_sources, n_heads_rows, row_step):
         fin = np.isfinite(o_lse)
         assert np.array_equal(np.isfinite(gl), fin)
         assert np.all(np.abs(gl[fin] - o_lse[fin]) <= harness.lse_tol(o_lse[fin]))
-        _say(f"[ok] attend_active{' split' if split else ''} {wl.name}: max-abs {err.max():.3g} "
+        _say(f"[ok] attend_active ({mode}) {wl.name}: max-abs {err.max():.3g} "
              f"mean-abs {err.mean():.3g} over {len(rows)} rows")
 
 
