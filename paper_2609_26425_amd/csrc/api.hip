@@ -470,6 +470,54 @@ static size_t active_two_part_bytes(const quantwm_config* cfg, int64_t n_cache, 
   return (rows * cfg->head_dim * 4 + 255) / 256 * 256 + rows * 2 * 4;
 }
 
+// Per-epoch form of the epochs call: the keys of each calibration epoch through
+// the plain kernel with that epoch's block (its own key split), then, with an
+// active chunk, the general kernel from the last whole packed tile on; the
+// partial planes merge by log-sum-exp. Ranges and plane counts per epoch.
+struct EpochPlan {
+  int n = 0, planes = 0;
+  int64_t lo[qwm::kMaxEpochs], hi[qwm::kMaxEpochs];
+  int ns[qwm::kMaxEpochs];
+  int64_t tail_tile = -1;  // first tile of the general launch (active chunk), -1 if none
+};
+
+static EpochPlan plan_epochs(const quantwm_config* cfg, int n_epochs, const int64_t* es, int64_t n_cache,
+                             int64_t n_act, int64_t n_q) {
+  EpochPlan p;
+  const int64_t kt = qwm::kAttendTileKeys;
+  const int64_t end = n_act > 0 ? n_cache / kt * kt : n_cache;
+  const int cus = device_cus();
+  for (int e = 0; e < n_epochs; ++e) {
+    const int64_t lo = es[e], hi0 = e + 1 < n_epochs ? es[e + 1] : n_cache, hi = hi0 < end ? hi0 : end;
+    if (hi <= lo) continue;
+    p.lo[p.n] = lo;
+    p.hi[p.n] = hi;
+    p.ns[p.n] = qwm::attend_splits(n_q, cfg->heads, cfg->batch, hi - lo, cus);
+    p.planes += p.ns[p.n];
+    ++p.n;
+  }
+  if (n_act > 0) {
+    p.tail_tile = end / kt;
+    p.planes += 1;
+  }
+  return p;
+}
+
+static size_t planes_bytes(const quantwm_config* cfg, int planes, int64_t n_q) {
+  const size_t rows = size_t(planes) * cfg->batch * cfg->heads * size_t(n_q);
+  return (rows * cfg->head_dim * 4 + 255) / 256 * 256 + rows * 2 * 4;
+}
+
+size_t quantwm_attend_epochs_workspace_bytes(const quantwm_config* cfg, int32_t n_epochs, const int64_t* epoch_start,
+                                             int64_t n_cache, int64_t n_act, int64_t n_q) {
+  if (check_cfg(cfg) != QWM_OK || n_cache < 0 || n_act < 0 || n_q <= 0) return 0;
+  if (n_epochs < 2 || n_epochs > qwm::kMaxEpochs || !epoch_start || (cfg->storage & QWM_STORE_SCALE_I8)) return 0;
+  const EpochPlan p = plan_epochs(cfg, n_epochs, epoch_start, n_cache, n_act, n_q);
+  const size_t per = planes_bytes(cfg, p.planes, n_q);
+  const size_t split = attend_split_bytes(cfg, n_cache + n_act, n_q, nullptr);
+  return per > split ? per : split;
+}
+
 size_t quantwm_attend_active_workspace_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_act,
                                              int64_t n_q) {
   if (check_cfg(cfg) != QWM_OK || n_cache < 0 || n_act < 0 || n_q <= 0) return 0;
@@ -553,6 +601,65 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   a.tile_lo = 0;
   a.split_base = 0;
   a.partial = 0;
+  a.key_lo = 0;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // calibration epochs one by one through the plain kernel when the workspace
+  // holds a partial plane per launch
+  if (!logits_out && workspace && n_epochs > 1 && !(cfg->storage & QWM_STORE_SCALE_I8)) {
+    const EpochPlan p = plan_epochs(cfg, n_epochs, epoch_start, n_cache, n_act, n_q);
+    const size_t need = planes_bytes(cfg, p.planes, n_q);
+    if (workspace_bytes >= need && p.planes > 0) {
+      if (n_q > kMaxPositions || n_cache + n_act > kMaxPositions)
+        return fail(QWM_ERR_UNSUPPORTED, "more than %lld Queries or keys per head", (long long)kMaxPositions);
+      const size_t rows = size_t(p.planes) * cfg->batch * cfg->heads * size_t(n_q);
+      a.part_o = static_cast<float*>(workspace);
+      a.part_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + (rows * cfg->head_dim * 4 + 255) / 256 * 256);
+      const bool bf = cfg->dtype == QWM_BF16;
+      auto run = [&](const qwm::AttendArgs& x) {
+        return bf ? qwm::launch_attend_bf16(x, cfg->head_dim, cfg->batch, false, s)
+                  : qwm::launch_attend_f32(x, cfg->head_dim, cfg->batch, false, s);
+      };
+      hipError_t e = hipSuccess;
+      int base = 0;
+      for (int i = 0; i < p.n && e == hipSuccess; ++i) {
+        qwm::AttendArgs ea = a;  // one epoch's keys [lo, hi) with its own block
+        const int ep = [&] {
+          int k = 0;
+          while (k + 1 < n_epochs && epoch_start[k + 1] <= p.lo[i]) ++k;
+          return k;
+        }();
+        ea.calib = a.calib + int64_t(ep) * a.calib_stride;
+        ea.n_epochs = 1;
+        for (int k = 0; k < qwm::kMaxEpochs; ++k) ea.epoch_start[k] = 0;
+        ea.n_cache = p.hi[i];
+        ea.k_act = ea.v_act = nullptr;
+        ea.n_act = 0;
+        ea.tile_lo = p.lo[i] / qwm::kAttendTileKeys;
+        ea.key_lo = p.lo[i];
+        ea.n_split = p.ns[i];
+        ea.split_base = base;
+        ea.partial = 1;
+        if ((n_q + 255) / 256 * int64_t(ea.n_split) > 0x7fffffff) return fail(QWM_ERR_UNSUPPORTED, "n_q too large");
+        e = run(ea);
+        base += p.ns[i];
+      }
+      if (e == hipSuccess && p.tail_tile >= 0) {
+        qwm::AttendArgs ga = a;  // the last packed tile and the active chunk, all epochs
+        ga.tile_lo = p.tail_tile;
+        ga.n_split = 1;
+        ga.split_base = base;
+        ga.partial = 1;
+        e = run(ga);
+      }
+      if (e == hipSuccess) {
+        qwm::AttendArgs ca = a;
+        ca.n_split = p.planes;
+        e = qwm::launch_attend_combine(ca, cfg->head_dim, cfg->batch, bf, s);
+      }
+      if (e != hipSuccess) return hip_fail(e, "attend launch (per epoch)");
+      return ok();
+    }
+  }
   // the active chunk in two parts when the workspace holds their partials: the
   // packed keys of whole tiles through the plain kernel, the rest through the
   // general one, merged by log-sum-exp
@@ -571,7 +678,6 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   // the kernel keeps Query and key positions in 32 bits
   if (n_q > kMaxPositions || n_cache + n_act > kMaxPositions)
     return fail(QWM_ERR_UNSUPPORTED, "more than %lld Queries or keys per head", (long long)kMaxPositions);
-  hipStream_t s = static_cast<hipStream_t>(stream);
   const bool lg = logits_out != nullptr;
   if (two_part) {
     const bool bf = cfg->dtype == QWM_BF16;

@@ -850,12 +850,16 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         }
       }
     } else {
-      // masked keys (only in tiles past kfull) -> -inf
+      // masked keys (only in tiles past kfull, and a first tile that starts
+      // below key_lo) -> -inf
       auto mask_half = [&](f32x16& sv, int kb) {
         if constexpr (MASKED) {
+          const int klo = int(a.key_lo);
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            if (int(k0) + kb * 32 + acc_row(i, hf) >= lim) sv[i] = -__builtin_inff();
+          for (int i = 0; i < 16; ++i) {
+            const int key = int(k0) + kb * 32 + acc_row(i, hf);
+            if (key >= lim || key < klo) sv[i] = -__builtin_inff();
+          }
         }
       };
       // raise m_run if the max over these 32 keys exceeds it by more than tau
@@ -946,6 +950,10 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   };
   const int64_t nclean = kfull / KT < ntile ? kfull / KT : ntile;
   int64_t it = t0;
+  if (it < ntile && a.key_lo > it * KT) {  // the first tile holds keys below key_lo
+    tile(it, std::integral_constant<bool, true>{});
+    ++it;
+  }
   for (; it < nclean; ++it) tile(it, std::integral_constant<bool, false>{});
   for (; it < ntile; ++it) tile(it, std::integral_constant<bool, true>{});
 

@@ -130,6 +130,7 @@ struct AttendArgs {
   int64_t tile_lo;
   int split_base;
   int partial;
+  int64_t key_lo;  // keys below are masked (a launch over one calibration epoch's keys)
 };
 
 // keys per attention tile

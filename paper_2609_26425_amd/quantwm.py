@@ -68,6 +68,7 @@ def _load():
                                         P, SZ, P]),
         "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I32, P, P]),
         "quantwm_attend_active_workspace_bytes": (SZ, [C, I64, I64, I64]),
+        "quantwm_attend_epochs_workspace_bytes": (SZ, [C, I32, ctypes.POINTER(I64), I64, I64, I64]),
         "quantwm_coef_record_max_bytes": (SZ, [C, I64]),
         "quantwm_coef_pack": (I32, [C, P, I64, I64, P, SZ, ctypes.POINTER(I64), ctypes.POINTER(I32), P]),
         "quantwm_coef_unpack": (I32, [C, P, SZ, P, I64, I64, P]),
@@ -86,7 +87,7 @@ EXPORTED = ("quantwm_cache_bytes", "quantwm_token_bytes", "quantwm_calib_bytes",
             "quantwm_stats_update", "quantwm_calibrate_epoch",
             "quantwm_append", "quantwm_attend_workspace_bytes", "quantwm_attend", "quantwm_attend_active",
             "quantwm_attend_epochs",
-            "quantwm_logits", "quantwm_attend_active_workspace_bytes", "quantwm_coef_record_max_bytes", "quantwm_coef_pack", "quantwm_coef_unpack",
+            "quantwm_logits", "quantwm_attend_active_workspace_bytes", "quantwm_attend_epochs_workspace_bytes", "quantwm_coef_record_max_bytes", "quantwm_coef_pack", "quantwm_coef_unpack",
             "quantwm_last_error")
 
 
@@ -229,6 +230,12 @@ def quantwm_attend_epochs(cfg, calibs, epoch_start, cache, n_cache, k_act, v_act
                                       _ptr(out), _ptr(lse_out), _ptr(workspace),
                                       0 if workspace is None else workspace.numel() * workspace.element_size(),
                                       _stream(stream)))
+
+
+def quantwm_attend_epochs_workspace_bytes(cfg, epoch_start, n_cache, n_act, n_q) -> int:
+    starts = (ctypes.c_int64 * len(epoch_start))(*[int(x) for x in epoch_start])
+    return int(_lib.quantwm_attend_epochs_workspace_bytes(ctypes.byref(cfg), len(epoch_start), starts, n_cache,
+                                                          n_act, n_q))
 
 
 def quantwm_logits(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, logits_out, stream=None):

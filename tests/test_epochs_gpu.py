@@ -104,14 +104,16 @@ def _run_epochs(wl, starts, n_act, rows, seed_hist=300):
                                     v_act=np.ascontiguousarray(v[:, n_pk:]) if n_act else None,
                                     epochs=list(zip(starts, tables)))
     tol = 2e-2 if wl.dtype == "bf16" else 1e-4
-    for split in (False, True):
-        nb = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q) if split else 0
-        if split and nb == 0:
+    for mode in ("none", "split", "per-epoch"):
+        nb = {"none": 0, "split": qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q),
+              "per-epoch": qw.quantwm_attend_epochs_workspace_bytes(cfg, list(starts), n_pk, n_act, wl.n_q)}[mode]
+        if mode != "none" and nb == 0:
             continue
         ws = torch.empty(nb, dtype=torch.uint8, device=DEV) if nb else None
         out = torch.empty_like(qd)
         lse = torch.empty((wl.batch, wl.heads, wl.n_q), dtype=torch.float32, device=DEV)
-        _say(f"[gpu] attend_epochs {wl.name}: epochs {list(starts)}, {n_pk} packed + {n_act} exact, ws {nb} B")
+        _say(f"[gpu] attend_epochs ({mode}) {wl.name}: epochs {list(starts)}, {n_pk} packed + {n_act} exact, "
+             f"ws {nb} B")
         qw.quantwm_attend_epochs(cfg, calibs, list(starts), cache, n_pk, ka, va, n_act, qd, wl.n_q, wl.q_start,
                                  wl.frame_tokens, out, lse, ws)
         torch.cuda.synchronize()
@@ -122,7 +124,7 @@ def _run_epochs(wl, starts, n_act, rows, seed_hist=300):
         fin = np.isfinite(o_lse)
         assert np.array_equal(np.isfinite(gl), fin)
         assert np.all(np.abs(gl[fin] - o_lse[fin]) <= harness.lse_tol(o_lse[fin]))
-        _say(f"[ok] attend_epochs{' split' if split else ''} {wl.name}: max-abs {err.max():.3g} "
+        _say(f"[ok] attend_epochs ({mode}) {wl.name}: max-abs {err.max():.3g} "
              f"mean-abs {err.mean():.3g} over {len(rows)} rows")
     # the same cache read as a single epoch is further from the oracle's epochs
     return tables
