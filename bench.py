@@ -128,13 +128,35 @@ def cpu_baseline(wl):
     lim = np.minimum(wl.n_cache, wl.q_start + (i // wl.frame_tokens + 1) * wl.frame_tokens)
     t_att = t_sample * (visible_pairs(wl) / float(lim.sum())) * wl.batch * wl.heads
     t_step = t_app + t_att
+    # the same legs on one thread: one head's append, every 64th Query row
+    oracle.set_threads(1)
+    try:
+        c1 = oracle.cfg_of(1, 1, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank, wl.top_m, wl.n_cache,
+                           wl.dtype == "bf16")
+        cache_s = oracle.new_cache(c1)
+        t0 = time.perf_counter()
+        oracle.append(c1, t1, cache_s, wl.n_cache - wl.chunk, np.ascontiguousarray(k[:, :, :1]),
+                      np.ascontiguousarray(v[:, :, :1]))
+        t_app1 = (time.perf_counter() - t0) * wl.batch * wl.heads
+        rows1 = rows[::4]
+        t0 = time.perf_counter()
+        oracle.attend(cfg1, t1, cache1, wl.n_cache, q, wl.q_start, wl.frame_tokens, rows=rows1)
+        t_s1 = time.perf_counter() - t0
+        i1 = rows1[:, 2]
+        lim1 = np.minimum(wl.n_cache, wl.q_start + (i1 // wl.frame_tokens + 1) * wl.frame_tokens)
+        t_att1 = t_s1 * (visible_pairs(wl) / float(lim1.sum())) * wl.batch * wl.heads
+    finally:
+        oracle.set_threads(threads)
+    single = {"value": wl.batch * wl.heads * wl.n_cache / (t_app1 + t_att1), "cores": 1,
+              "sample": f"append of one head's {wl.chunk}-token chunk; attend of {len(rows1)} Query rows of one head",
+              "append_s_est": t_app1, "attend_s_est": t_att1}
     return {"value": wl.batch * wl.heads * wl.n_cache / t_step, "unit": "cache tokens/s", "cores": threads,
             "kind": "oracle",
             "sample": (f"append of one {wl.chunk}-token chunk on {nh} heads (one OpenMP thread per head), "
                        f"scaled to {wl.batch * wl.heads} heads; attend of {len(rows)} of {wl.n_q} Query rows of "
                        f"one head over {wl.n_cache} keys ({threads} threads over rows), scaled by visible pairs "
                        f"to all rows and heads"),
-            "append_s_est": t_app, "attend_s_est": t_att}
+            "append_s_est": t_app, "attend_s_est": t_att, "single_thread": single}
 
 
 def main():
