@@ -167,6 +167,8 @@ def main():
     ap.add_argument("--workload", default="lingbot-40h", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--copies", type=int, default=3, help="rotated input/cache copies (defeats the 256 MiB MALL)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-streaming", action="store_true",
+                    help="skip the active-chunk and calibration-epoch timings (for kernel traces)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one plain 1 GiB device copy kernel (read 1 GiB, write 1 GiB) outside the timed "
                          "region, as the scale for FETCH_SIZE / WRITE_SIZE counter runs")
@@ -254,45 +256,52 @@ def main():
     ms_step = wall * 1000.0 / args.steps
     assert torch.isfinite(outs[0].float()).all(), "non-finite attention output"
 
-    # the streaming variant: the last chunk stays exact (BF16) beside the packed
-    # history of the rest, timed separately on the same inputs
-    n_pk = wl.n_cache - n_new
-    ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    # with the two-part workspace: packed whole tiles through the plain kernel,
-    # the rest through the general one, merged by log-sum-exp
-    ws_act = qw.quantwm_attend_active_workspace_bytes(cfg, n_pk, n_new, wl.n_q)
-    act_ws = torch.empty(ws_act, dtype=torch.uint8, device=dev) if ws_act else None
-    for i in range(2):
-        qw.quantwm_attend_active(cfg, calib, caches[0], n_pk, k_new[0], v_new[0], n_new, qs[0], wl.n_q,
-                                 wl.q_start, wl.frame_tokens, outs[0], lse, act_ws)
-    ea.record()
-    for i in range(5):
-        qw.quantwm_attend_active(cfg, calib, caches[0], n_pk, k_new[0], v_new[0], n_new, qs[0], wl.n_q,
-                                 wl.q_start, wl.frame_tokens, outs[0], lse, act_ws)
-    eb.record()
-    torch.cuda.synchronize()
-    act_ms = ea.elapsed_time(eb) / 5
+    # the streaming forms, timed separately on the same inputs (skipped with
+    # --no-streaming, so that a kernel trace holds the step's launches only: the
+    # per-epoch and two-part forms launch the same plain attention kernel)
+    act_ms = ep_ms = act_cfg = ep_cfg = None
+    if not args.no_streaming:
+        # the streaming variant: the last chunk stays exact (BF16) beside the packed
+        # history of the rest, timed separately on the same inputs
+        n_pk = wl.n_cache - n_new
+        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        # with the two-part workspace: packed whole tiles through the plain kernel,
+        # the rest through the general one, merged by log-sum-exp
+        ws_act = qw.quantwm_attend_active_workspace_bytes(cfg, n_pk, n_new, wl.n_q)
+        act_ws = torch.empty(ws_act, dtype=torch.uint8, device=dev) if ws_act else None
+        for i in range(2):
+            qw.quantwm_attend_active(cfg, calib, caches[0], n_pk, k_new[0], v_new[0], n_new, qs[0], wl.n_q,
+                                     wl.q_start, wl.frame_tokens, outs[0], lse, act_ws)
+        ea.record()
+        for i in range(5):
+            qw.quantwm_attend_active(cfg, calib, caches[0], n_pk, k_new[0], v_new[0], n_new, qs[0], wl.n_q,
+                                     wl.q_start, wl.frame_tokens, outs[0], lse, act_ws)
+        eb.record()
+        torch.cuda.synchronize()
+        act_ms = ea.elapsed_time(eb) / 5
 
-    # calibration epochs: one per appended chunk (the timing does not depend on
-    # the tables' values, so every epoch reuses this calibration block)
-    starts = [s0 for s0, _ in wl.chunks()]
-    cb = qw.quantwm_calib_bytes(cfg)
-    calibs = calib.repeat(len(starts))
-    # with the per-epoch workspace: each epoch's keys through the plain kernel,
-    # merged by log-sum-exp
-    ws_ep = qw.quantwm_attend_epochs_workspace_bytes(cfg, starts, wl.n_cache, 0, wl.n_q)
-    ep_ws = torch.empty(ws_ep, dtype=torch.uint8, device=dev) if ws_ep else attend_ws
-    for i in range(2):
-        qw.quantwm_attend_epochs(cfg, calibs, starts, caches[0], wl.n_cache, None, None, 0, qs[0], wl.n_q,
-                                 wl.q_start, wl.frame_tokens, outs[0], lse, ep_ws)
-    ea.record()
-    for i in range(5):
-        qw.quantwm_attend_epochs(cfg, calibs, starts, caches[0], wl.n_cache, None, None, 0, qs[0], wl.n_q,
-                                 wl.q_start, wl.frame_tokens, outs[0], lse, ep_ws)
-    eb.record()
-    torch.cuda.synchronize()
-    ep_ms = ea.elapsed_time(eb) / 5
-    del calibs, cb, ep_ws
+        # calibration epochs: one per appended chunk (the timing does not depend on
+        # the tables' values, so every epoch reuses this calibration block)
+        starts = [s0 for s0, _ in wl.chunks()]
+        cb = qw.quantwm_calib_bytes(cfg)
+        calibs = calib.repeat(len(starts))
+        # with the per-epoch workspace: each epoch's keys through the plain kernel,
+        # merged by log-sum-exp
+        ws_ep = qw.quantwm_attend_epochs_workspace_bytes(cfg, starts, wl.n_cache, 0, wl.n_q)
+        ep_ws = torch.empty(ws_ep, dtype=torch.uint8, device=dev) if ws_ep else attend_ws
+        for i in range(2):
+            qw.quantwm_attend_epochs(cfg, calibs, starts, caches[0], wl.n_cache, None, None, 0, qs[0], wl.n_q,
+                                     wl.q_start, wl.frame_tokens, outs[0], lse, ep_ws)
+        ea.record()
+        for i in range(5):
+            qw.quantwm_attend_epochs(cfg, calibs, starts, caches[0], wl.n_cache, None, None, 0, qs[0], wl.n_q,
+                                     wl.q_start, wl.frame_tokens, outs[0], lse, ep_ws)
+        eb.record()
+        torch.cuda.synchronize()
+        ep_ms = ea.elapsed_time(eb) / 5
+        del calibs, cb, ep_ws
+        act_cfg = f"{n_pk} packed + {n_new} exact BF16 keys, two-part workspace {ws_act} B"
+        ep_cfg = f"{len(starts)} calibration epochs, one per {wl.chunk}-token chunk, per-epoch workspace {ws_ep} B"
 
     flops = attend_flops(wl)
     achieved = flops / (att_ms * 1e-3) / 1e12
@@ -324,10 +333,9 @@ def main():
         "copies": args.copies,
         "attend_workspace_bytes": ws_bytes,
         "attend_active_ms": act_ms,
-        "attend_active_config": f"{n_pk} packed + {n_new} exact BF16 keys, two-part workspace {ws_act} B",
+        "attend_active_config": act_cfg,
         "attend_epochs_ms": ep_ms,
-        "attend_epochs_config": f"{len(starts)} calibration epochs, one per {wl.chunk}-token chunk, per-epoch "
-                                f"workspace {ws_ep} B",
+        "attend_epochs_config": ep_cfg,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
