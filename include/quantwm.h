@@ -238,26 +238,19 @@ quantwm_status quantwm_attend(const quantwm_config* cfg, const void* calib, cons
  * takes quantwm_attend_workspace_bytes(cfg, n_cache + n_act, n_q) as for
  * quantwm_attend, and NULL runs one launch. All forms give the same result up
  * to fp32 rounding order. */
-size_t quantwm_attend_active_workspace_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_act,
-                                             int64_t n_q);
-
-/* Workspace bytes for the per-epoch form of quantwm_attend_epochs (n_epochs >=
- * 2; 0 otherwise, and 0 with QWM_STORE_SCALE_I8): each epoch's packed keys run
- * through the plain attention kernel with that epoch's calibration block as
- * partial results of their own; with an active chunk, the last whole packed
- * tile on runs through the general kernel; everything merges by log-sum-exp.
- * epoch_start is the host array of the call. Given at least this much
- * (256-byte aligned) the call takes that form; otherwise the one-launch form,
- * with the split workspace of quantwm_attend_workspace_bytes(cfg, n_cache +
- * n_act, n_q). Both give the same result up to fp32 rounding order. */
-size_t quantwm_attend_epochs_workspace_bytes(const quantwm_config* cfg, int32_t n_epochs,
-                                             const int64_t* epoch_start, int64_t n_cache, int64_t n_act,
-                                             int64_t n_q);
 quantwm_status quantwm_attend_active(const quantwm_config* cfg, const void* calib, const void* cache,
                                      int64_t n_cache, const void* k_act, const void* v_act, int64_t n_act,
                                      const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens,
                                      void* out, float* lse_out, void* workspace, size_t workspace_bytes,
                                      void* stream);
+
+/* Workspace bytes for quantwm_attend_active: the larger of the two-part form's
+ * (two or more fp32 partial planes; none without an active chunk or with fewer
+ * than 64 packed keys) and the split workspace of
+ * quantwm_attend_workspace_bytes(cfg, n_cache + n_act, n_q). 0 with
+ * QWM_STORE_SCALE_I8. */
+size_t quantwm_attend_active_workspace_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_act,
+                                             int64_t n_q);
 
 /* quantwm_attend_active over a cache appended in calibration epochs (the
  * streaming setting of Sec. 5: statistics and centroids are refreshed at chunk
@@ -273,6 +266,19 @@ quantwm_status quantwm_attend_epochs(const quantwm_config* cfg, const void* cali
                                      const void* k_act, const void* v_act, int64_t n_act, const void* q,
                                      int64_t n_q, int64_t q_start, int32_t frame_tokens, void* out,
                                      float* lse_out, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes for the per-epoch form of quantwm_attend_epochs (n_epochs >=
+ * 2; 0 otherwise, and 0 with QWM_STORE_SCALE_I8): each epoch's packed keys run
+ * through the plain attention kernel with that epoch's calibration block as
+ * partial results of their own; with an active chunk, the last whole packed
+ * tile on runs through the general kernel; everything merges by log-sum-exp.
+ * epoch_start is the host array of the call. Given at least this much
+ * (256-byte aligned) the call takes that form; otherwise the one-launch form,
+ * with the split workspace of quantwm_attend_workspace_bytes(cfg, n_cache +
+ * n_act, n_q). Both give the same result up to fp32 rounding order. */
+size_t quantwm_attend_epochs_workspace_bytes(const quantwm_config* cfg, int32_t n_epochs,
+                                             const int64_t* epoch_start, int64_t n_cache, int64_t n_act,
+                                             int64_t n_q);
 
 /* Test hook: the scaled logits of quantwm_attend, [B,H,n_q,n_cache] f32,
  * -inf where masked. Same tile code as quantwm_attend. */
