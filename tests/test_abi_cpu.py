@@ -133,6 +133,28 @@ def test_validation_without_a_gpu():
     assert qw.quantwm_last_error() == ""
 
 
+def test_streaming_workspace_sizes():
+    """The two-part active form holds two fp32 partial planes (the packed whole
+    tiles run unsplit at this size) and the per-epoch form one per epoch."""
+    ling = qw.make_config(1, 40, 128, 128, 32, 16, 4, 32760, "bf16")
+    rows = 40 * 4680
+
+    def planes(n):
+        return (n * rows * 128 * 4 + 255) // 256 * 256 + n * rows * 8
+
+    assert qw.quantwm_attend_active_workspace_bytes(ling, 28080, 4680, 4680) == planes(2)
+    assert qw.quantwm_attend_active_workspace_bytes(ling, 32760, 0, 4680) == 0  # no active chunk, no split
+    assert qw.quantwm_attend_active_workspace_bytes(ling, 40, 4680, 4680) == 0  # no whole packed tile
+    starts = [4680 * i for i in range(7)]
+    assert qw.quantwm_attend_epochs_workspace_bytes(ling, starts, 32760, 0, 4680) == planes(7)
+    # six epochs of packed keys, the last one cut at the last whole tile, plus the active part
+    assert qw.quantwm_attend_epochs_workspace_bytes(ling, starts[:6], 28080, 4680, 4680) == planes(7)
+    assert qw.quantwm_attend_epochs_workspace_bytes(ling, [0], 32760, 0, 4680) == 0
+    i8 = qw.make_config(1, 40, 128, 128, 32, 16, 4, 32760, "bf16", qw.STORE_SCALE_I8)
+    assert qw.quantwm_attend_epochs_workspace_bytes(i8, starts, 32760, 0, 4680) == 0
+    assert qw.quantwm_attend_active_workspace_bytes(i8, 28080, 4680, 4680) == 0
+
+
 def test_attend_workspace_sizes():
     """A launch that under-fills the GPU asks for split workspace; a full one does not."""
     # 40 heads x 7 Query blocks of 256 = 280 workgroups < 2 per CU on 256 CUs -> 4 splits
