@@ -265,7 +265,21 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   // other's registers live
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / 64), lane = tid % 64, l32 = lane % 32,
             hf = lane / 32;
-  const int h = blockIdx.y, b = blockIdx.z;
+  // XCD-aware task order: workgroup L runs on XCD L % 8, so each XCD takes a
+  // contiguous run of (Query block, head, batch) tasks, and the Query blocks
+  // of a head, which stream the same key tiles at about the same time, read
+  // them through one L2 instead of eight
+  uint32_t bx, by, bz;
+  {
+    const uint32_t gx = gridDim.x, gy = gridDim.y, n = gx * gy * gridDim.z;
+    const uint32_t L = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+    const uint32_t P = L % 8, Q = L / 8, q = n / 8, rr = n % 8;
+    const uint32_t task = P < rr ? P * (q + 1) + Q : rr * (q + 1) + (P - rr) * q + Q;
+    bx = task % gx;
+    by = (task / gx) % gy;
+    bz = task / (gx * gy);
+  }
+  const int h = int(by), b = int(bz);
   const int64_t bh = int64_t(b) * a.heads + h;
   // calibration slab of this head in epoch e
   auto epoch_slab = [&](int e) { return a.calib + int64_t(e) * a.calib_stride + bh * a.slab; };
@@ -290,12 +304,12 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   const int G = D / L.ng;
   const bool producer = wave >= NC;
 
-  // ---- key range of this workgroup: Query block blockIdx.x / n_split, and the
+  // ---- key range of this workgroup: Query block bx / n_split, and the
   // split-th of n_split equal runs of its key tiles
   // keys [0, npk) are packed; keys [npk, nc) are the exact active chunk
   const int64_t F = a.frame_tokens, qs = a.q_start, npk = a.n_cache, nc = a.n_cache + a.n_act;
-  const int split = int(blockIdx.x) % a.n_split;
-  const int64_t qa = int64_t(blockIdx.x / a.n_split) * BQ;
+  const int split = int(bx) % a.n_split;
+  const int64_t qa = int64_t(bx / a.n_split) * BQ;
   const int64_t qb = qa + BQ < a.n_q ? qa + BQ : a.n_q;
   int64_t kend = LOGITS ? nc : qs + ((qb - 1) / F + 1) * F;
   if (kend > nc) kend = nc;
