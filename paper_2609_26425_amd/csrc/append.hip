@@ -20,6 +20,8 @@
 namespace qwm {
 namespace {
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
 // Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E) step S.
 // Keeps register-array indices static where #pragma unroll gives up on large bodies.
 template <int B, int E, int S = 1, typename F>
@@ -311,28 +313,69 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
 
   // ---- Values: nearest centroid (w = 1). Both searches run before the first
   // store, so the compiler may keep their table loads on the scalar path.
-  load_row<T, D>(reinterpret_cast<const T*>(a.v) + src, x);
   int zv = 0;
   float dv = __builtin_inff();
-  for (int j = 0; j < Kc; j += 4) {
-    float acc[4];
-    int row[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      row[u] = min(j + u, Kc - 1);
-      acc[u] = bv[row[u]];
-    }
-#pragma unroll
-    for (int c = 0; c < D; ++c)
-#pragma unroll
-      for (int u = 0; u < 4; ++u) acc[u] = __builtin_fmaf(av[row[u] * D + c], x[c], acc[u]);
-    // branch-free update: a divergent branch here turns the table loads of the
-    // loop into per-lane vector loads
+  // branch-free argmin update: a divergent branch here turns the table loads of
+  // the loop into per-lane vector loads
+  auto take = [&](int j, const float (&acc)[4]) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const bool better = (j + u < Kc) & (acc[u] < dv);
       dv = better ? acc[u] : dv;
       zv = better ? j + u : zv;
+    }
+  };
+  if constexpr (sizeof(T) == 2) {
+    // BF16 Values and BF16 centroids: d'_j = b_j + sum_c mu_jc (-2 v_c), two
+    // channels per v_dot2_f32_bf16 (exact products). -2 v_c is exact in BF16
+    // for finite |v_c| < 2^127; the pairs come straight from the table.
+    uint32_t vp[D / 2];
+    {
+      const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.v) + src);
+#pragma unroll
+      for (int i = 0; i < D / 8; ++i) {
+        const uint4 u = p[i];
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t lo = __float_as_uint(__uint_as_float(w[k] << 16) * -2.0f);
+          const uint32_t hi = __float_as_uint(__uint_as_float(w[k] & 0xffff0000u) * -2.0f);
+          vp[4 * i + k] = (hi & 0xffff0000u) | (lo >> 16);
+        }
+      }
+    }
+    const uint32_t* __restrict__ mvp = reinterpret_cast<const uint32_t*>(muv);  // [Kc][D/2] BF16 pairs
+    for (int j = 0; j < Kc; j += 4) {
+      float acc[4];
+      int row[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        row[u] = min(j + u, Kc - 1);
+        acc[u] = bv[row[u]];
+      }
+#pragma unroll
+      for (int c = 0; c < D / 2; ++c)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          acc[u] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, mvp[row[u] * (D / 2) + c]),
+                                                   __builtin_bit_cast(bf16x2, vp[c]), acc[u], false);
+      take(j, acc);
+    }
+  } else {
+    load_row<T, D>(reinterpret_cast<const T*>(a.v) + src, x);
+    for (int j = 0; j < Kc; j += 4) {
+      float acc[4];
+      int row[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        row[u] = min(j + u, Kc - 1);
+        acc[u] = bv[row[u]];
+      }
+#pragma unroll
+      for (int c = 0; c < D; ++c)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[u] = __builtin_fmaf(av[row[u] * D + c], x[c], acc[u]);
+      take(j, acc);
     }
   }
   // ---- INT2 residual against mu_z, with PSAC accumulated channel by channel:
