@@ -116,7 +116,11 @@ def _run_epochs(wl, starts, n_act, rows, seed_hist=300):
              f"ws {nb} B")
         qw.quantwm_attend_epochs(cfg, calibs, list(starts), cache, n_pk, ka, va, n_act, qd, wl.n_q, wl.q_start,
                                  wl.frame_tokens, out, lse, ws)
+        out2, lse2 = torch.empty_like(out), torch.empty_like(lse)
+        qw.quantwm_attend_epochs(cfg, calibs, list(starts), cache, n_pk, ka, va, n_act, qd, wl.n_q, wl.q_start,
+                                 wl.frame_tokens, out2, lse2, ws)
         torch.cuda.synchronize()
+        assert torch.equal(out, out2) and torch.equal(lse, lse2), f"attend_epochs ({mode}) is not deterministic"
         g = out.float().cpu().numpy()[rows[:, 0], rows[:, 2], rows[:, 1], :]
         gl = lse.cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]]
         err = np.abs(g - o_out)

@@ -501,7 +501,11 @@ def _active_case(wl, max_sources, n_heads_rows, row_step):
         _say(f"[gpu] attend_active {wl.name}: {n_pk} packed + {n_act} exact keys, workspace {nb} B")
         qw.quantwm_attend_active(cfg, calib, cache, n_pk, k_act, v_act, n_act, q, wl.n_q, wl.q_start,
                                  wl.frame_tokens, out, lse, ws)
+        out2, lse2 = torch.empty_like(out), torch.empty_like(lse)
+        qw.quantwm_attend_active(cfg, calib, cache, n_pk, k_act, v_act, n_act, q, wl.n_q, wl.q_start,
+                                 wl.frame_tokens, out2, lse2, ws)
         torch.cuda.synchronize()
+        assert torch.equal(out, out2) and torch.equal(lse, lse2), f"attend_active ({mode}) is not deterministic"
         g = out.float().cpu().numpy()[rows[:, 0], rows[:, 2], rows[:, 1], :]
         gl = lse.cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]]
         err = np.abs(g - o_out)
