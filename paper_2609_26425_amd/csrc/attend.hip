@@ -1105,14 +1105,25 @@ size_t attend_lds_bytes(int d, int elem, int rank, int n_centroids, bool tables)
 
 int attend_splits(int64_t n_q, int heads, int batch, int64_t n_cache, int cus) {
   // Split the key range only when the launch gives fewer than two workgroups
-  // per compute unit: up to 4 per CU, at least 8 tiles per split, at most 16.
+  // per compute unit (one runs per CU). The split count minimises the rounds of
+  // workgroups times each one's work: its share of the key tiles plus a fixed
+  // cost of about 32 tiles (table staging, Query fragments, pipeline fill,
+  // partial write), up to 16 splits of at least 8 tiles.
   const int64_t wgs = (n_q + BQ - 1) / BQ * heads * batch;
   if (wgs <= 0 || wgs >= 2 * int64_t(cus)) return 1;
-  int64_t ns = (4 * int64_t(cus) + wgs - 1) / wgs;
-  const int64_t by_tiles = ((n_cache + KT - 1) / KT) / 8;
-  if (ns > by_tiles) ns = by_tiles;
-  if (ns > 16) ns = 16;
-  return ns < 1 ? 1 : int(ns);
+  const int64_t tiles = (n_cache + KT - 1) / KT;
+  int best = 1;
+  int64_t best_cost = -1;
+  for (int ns = 1; ns <= 16; ++ns) {
+    if (ns > 1 && tiles / ns < 8) break;
+    const int64_t rounds = (wgs * ns + cus - 1) / cus;
+    const int64_t cost = rounds * ((tiles + ns - 1) / ns + 32);
+    if (best_cost < 0 || cost < best_cost) {
+      best = ns;
+      best_cost = cost;
+    }
+  }
+  return best;
 }
 
 bool attend_tables_fit(int d, int elem, int rank, int n_centroids) {

@@ -157,11 +157,21 @@ def test_streaming_workspace_sizes():
 
 def test_attend_workspace_sizes():
     """A launch that under-fills the GPU asks for split workspace; a full one does not."""
-    # 40 heads x 7 Query blocks of 256 = 280 workgroups < 2 per CU on 256 CUs -> 4 splits
+    # 40 heads x 7 Query blocks of 256 = 280 workgroups < 2 per CU on 256 CUs. The
+    # split count minimises rounds x (tiles per split + 32): over 1,875 key tiles
+    # 7 splits (8 rounds of 268 + 32) beat 4 (5 rounds of 469 + 32); over 469
+    # tiles 4 splits (5 x 150) beat 5 (6 x 126) and 8 (9 x 91)
     roll = qw.make_config(1, 40, 128, 128, 32, 16, 4, 120000, "bf16")
-    rows = 4 * 40 * 1560
-    o_bytes = (rows * 128 * 4 + 255) // 256 * 256
-    assert qw.quantwm_attend_workspace_bytes(roll, 120000, 1560) == o_bytes + rows * 8
+
+    def split_bytes(ns, n_q, heads=40):
+        rows = ns * heads * n_q
+        return (rows * 128 * 4 + 255) // 256 * 256 + rows * 8
+
+    assert qw.quantwm_attend_workspace_bytes(roll, 120000, 1560) == split_bytes(7, 1560)
+    assert qw.quantwm_attend_workspace_bytes(roll, 30000, 1560) == split_bytes(4, 1560)
+    # 12 heads x 11 Query blocks = 132 workgroups over 207 tiles: 3 splits (2 rounds of 69 + 32)
+    mg2 = qw.make_config(1, 12, 128, 64, 32, 8, 4, 13200, "bf16")
+    assert qw.quantwm_attend_workspace_bytes(mg2, 13200, 2640) == split_bytes(3, 2640, 12)
     # 40 heads x 19 Query blocks = 760 workgroups: no split
     ling = qw.make_config(1, 40, 128, 128, 32, 16, 4, 32760, "bf16")
     assert qw.quantwm_attend_workspace_bytes(ling, 32760, 4680) == 0
