@@ -251,8 +251,9 @@ def main():
         step(i, evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    app_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    att_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    app_all = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    att_all = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    app_ms, att_ms = float(app_all.mean()), float(att_all.mean())
     ms_step = wall * 1000.0 / args.steps
     assert torch.isfinite(outs[0].float()).all(), "non-finite attention output"
 
@@ -322,6 +323,8 @@ def main():
                                f"M={wl.top_m} F={wl.frame_tokens}",
                    "global_batch": wl.batch, "seq_len": wl.n_cache, "parallelism": "single GPU"},
         "attend_ms": att_ms, "append_ms": app_ms,
+        "attend_ms_median_min": [float(np.median(att_all)), float(att_all.min())],
+        "append_ms_median_min": [float(np.median(app_all)), float(app_all.min())],
         "attend_cache_tokens_per_s": bh * wl.n_cache / (att_ms * 1e-3),
         "append_GBps": app_gbps,
         "append_hbm_frac": app_gbps / PEAK_HBM_GBPS,
