@@ -89,3 +89,42 @@ def test_coef_unpack_rejects_a_mismatched_or_truncated_record():
         assert e.value.status == qw.ERR_INVALID_ARG and msg in qw.quantwm_last_error()
     torch.cuda.synchronize()
     assert not target.any()
+
+
+@pytest.mark.timeout(600)
+def test_coef_record_full_size():
+    # The LingBot-shaped append chunk (40 heads, 4,680 tokens at slot 28,080,
+    # r = 16), encoded by the oracle, with 30% of the rows dropped as the gate
+    # leaves them: the library's record equals the oracle's, and unpacking it
+    # restores the chunk.
+    wl = synth.WORKLOADS["lingbot-40h"]
+    start, n = wl.n_cache - wl.chunk, wl.chunk
+    ocfg = oracle.cfg_from_workload(wl)
+    k = synth.round_to(synth.tensor(wl, "k", n, start=start), "bf16")
+    v = synth.round_to(synth.tensor(wl, "v", n, start=start), "bf16")
+    qh = synth.round_to(synth.tensor(wl, "qhist", 256), "bf16")  # the record does not depend on table quality
+    tables = oracle.calibrate(ocfg, qh, k, v, 1)
+    cache = oracle.new_cache(ocfg)
+    oracle.append(ocfg, tables, cache, start, k, v)
+    nbh = wl.batch * wl.heads
+    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.capacity)
+    r = np.random.default_rng(11)
+    for bh in range(nbh):
+        packed.zero_coef_rows(cache, lay, bh, start + np.nonzero(r.random(n) < 0.3)[0])
+    want = oracle.coef_pack(ocfg, cache, start, n)
+    _say(f"[case] lingbot-40h chunk [{start}, {start + n}): oracle record {want.size} B")
+    cfg = qw.make_config(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank, wl.top_m,
+                         wl.capacity, "bf16")
+    cache_d = torch.from_numpy(cache).to(DEV)
+    rec = torch.zeros(qw.quantwm_coef_record_max_bytes(cfg, n), dtype=torch.uint8, device=DEV)
+    written, layout = qw.quantwm_coef_pack(cfg, cache_d, start, n, rec)
+    torch.cuda.synchronize()
+    assert written == want.size and np.array_equal(rec.cpu().numpy()[:written], want)
+    target = torch.zeros_like(cache_d)
+    qw.quantwm_coef_unpack(cfg, rec, target, start, n, record_bytes=written)
+    torch.cuda.synchronize()
+    chunk = packed.coef_byte_mask(lay, nbh, start, n)
+    back = target.cpu().numpy()
+    assert np.array_equal(back[chunk], cache[chunk]) and not back[~chunk].any()
+    _say(f"[ok] lingbot-40h chunk: {'sparse' if layout else 'dense'} {written} B of "
+         f"{qw.quantwm_coef_record_max_bytes(cfg, n)} B")
