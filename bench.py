@@ -150,7 +150,14 @@ def cpu_baseline(wl):
     single = {"value": wl.batch * wl.heads * wl.n_cache / (t_app1 + t_att1), "cores": 1,
               "sample": f"append of one head's {wl.chunk}-token chunk; attend of {len(rows1)} Query rows of one head",
               "append_s_est": t_app1, "attend_s_est": t_att1}
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:
+        pass
     return {"value": wl.batch * wl.heads * wl.n_cache / t_step, "unit": "cache tokens/s", "cores": threads,
+            "cpu_model": cpu_model, "host_cpus": os.cpu_count(),
             "kind": "oracle",
             "sample": (f"append of one {wl.chunk}-token chunk on {nh} heads (one OpenMP thread per head), "
                        f"scaled to {wl.batch * wl.heads} heads; attend of {len(rows)} of {wl.n_q} Query rows of "
