@@ -181,8 +181,8 @@ def main():
                          "region, as the scale for FETCH_SIZE / WRITE_SIZE counter runs")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (heads shard with no exchange; "
-              "see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (heads would shard across GPUs "
+              "with no exchange). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch

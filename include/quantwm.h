@@ -36,7 +36,7 @@ extern "C" {
 typedef enum {
   QWM_OK = 0,
   QWM_ERR_INVALID_ARG = 1, /* null/misaligned pointer, negative size, bad range */
-  QWM_ERR_UNSUPPORTED = 2, /* a shape this build has no kernel for */
+  QWM_ERR_UNSUPPORTED = 2, /* a shape the library has no kernel for */
   QWM_ERR_CAPACITY = 3,    /* tokens would exceed the cache capacity */
   QWM_ERR_HIP = 4          /* a HIP runtime call or a launch failed */
 } quantwm_status;

@@ -4,7 +4,7 @@
  * Build: gcc -O2 -ffp-contract=off -fno-fast-math -fopenmp -shared -fPIC.
  * Contraction stays off so that every a*b+c below is two roundings.
  *
- * Readings of the paper that this file takes (each listed in the design doc):
+ * Readings of the paper that this file takes:
  *  - The quantiser range is extended to contain 0, so the INT2 zero-point always
  *    lies in [0, 3] and can be bit-packed (Eq. 2 with App. D.1).
  *  - The residual is quantised with the stored (FP16-rounded) scale.

@@ -19,7 +19,8 @@ BUILD = os.path.join(HERE, "_build")
 ARCH = os.environ.get("QWM_OFFLOAD_ARCH", "gfx950")
 
 # -ffp-contract=off: every a*b+c that is not an explicit fma is two roundings, as
-# the quantiser's integer decisions require. Packed FP32 is disabled.
+# the quantiser's integer decisions require. Packed FP32 arithmetic is disabled: the
+# kernels are written for non-packed fp32 vector operations.
 HIPFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=off",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall",
             "-Wno-unused-function"]

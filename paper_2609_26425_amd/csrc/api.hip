@@ -39,7 +39,7 @@ quantwm_status hip_fail(hipError_t e, const char* what) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
-// Shape support of this build; INVALID for nonsense, UNSUPPORTED for shapes
+// Shape support of the library; INVALID for nonsense, UNSUPPORTED for shapes
 // that are meaningful but have no kernel here.
 quantwm_status check_cfg(const quantwm_config* c) {
   if (!c) return fail(QWM_ERR_INVALID_ARG, "config is null");

@@ -608,7 +608,7 @@ def test_attend_masked_keys_do_not_contribute():
 
 def test_token_bytes_and_paper_compression():
     # App. D.1 storage: 4 codes per byte, uint8 ids, INT2 zero-points, FP16 group
-    # scales (this build), INT8 PSAC rows with an FP16 scale. At the paper's setting
+    # scales (the library's default), INT8 PSAC rows with an FP16 scale. At the paper's setting
     # (d = 128, G = 64, r = 8) K+V take 86 B per token-head against 512 B in BF16:
     # 5.95x, close to the reported best case of 6.20x (Sec. 5.5).
     cfg = oracle.cfg_of(1, 1, 128, 256, 64, 8, 4, 64, True)
