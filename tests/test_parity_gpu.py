@@ -241,6 +241,7 @@ _FULL = oracle.METRIC_FULL
 METRIC = [synth.scaled(synth.WORKLOADS["tiny-f32"], name="tiny-f32-fullm", metric=_FULL),
           synth.scaled(RAGGED, name="ragged-fullm", metric=_FULL),
           synth.scaled(D64, name="d64-fullm", metric=_FULL),
+          synth.scaled(RAGGED, name="ragged-fullm-i8-gate", metric=_FULL, storage=_I8 | _GATE),
           synth.scaled(synth.WORKLOADS["lingbot-40h"], name="lingbot-2h-fullm", heads=2, n_cache=1560, n_q=520,
                        q_start=1040, frame_tokens=260, chunk=780, n_hist=1560, metric=_FULL)]
 
