@@ -22,17 +22,19 @@ def _dt(wl):
     return torch.bfloat16 if wl.dtype == "bf16" else torch.float32
 
 
-def _cfg(wl):
+def _cfg(wl, metric=0):
     return qw.make_config(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank, wl.top_m,
-                          wl.n_cache, wl.dtype)
+                          wl.n_cache, wl.dtype, metric=metric)
 
 
-def test_running_statistics_equal_one_pass():
+@pytest.mark.parametrize("metric", [0, 1], ids=["diag", "full"])
+def test_running_statistics_equal_one_pass(metric):
     # Eq. 6 online: three updates give the fp64 sums of q q^T over all tokens in
     # order (numpy, fp64), and recalibrating from them gives the very block that
-    # one-pass calibration over the concatenated history gives.
+    # one-pass calibration over the concatenated history gives (with the full
+    # metric, its matrix and the Key search constants derived from it too).
     wl = synth.scaled(synth.WORKLOADS["mg2-12h"], name="stats", heads=3, n_hist=1500)
-    cfg = _cfg(wl)
+    cfg = _cfg(wl, metric)
     dt = _dt(wl)
     qh = synth.tensor(wl, "qhist", wl.n_hist)
     qd = torch.from_numpy(qh).to(DEV, dt)
