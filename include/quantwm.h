@@ -77,8 +77,9 @@ typedef struct {
  *   Query-weighted error approximated on the principal subspace,
  *   sum_k lam_k (C_k - code_k * cscale)^2 < sum_k lam_k C_k^2 (fp32, ranks in
  *   order, lam from the calibration block); otherwise the row and its scale are
- *   stored as zeros. The attention calls do not take SCALE_I8 together with an
- *   active chunk or calibration epochs (QWM_ERR_UNSUPPORTED). */
+ *   stored as zeros. With SCALE_I8, quantwm_attend_active takes no active
+ *   chunk, and quantwm_attend_epochs over several epochs needs the per-epoch
+ *   workspace and no active chunk (QWM_ERR_UNSUPPORTED otherwise). */
 #define QWM_STORE_SCALE_I8 1
 #define QWM_STORE_GATE 2
 
@@ -268,14 +269,16 @@ quantwm_status quantwm_attend_epochs(const quantwm_config* cfg, const void* cali
                                      float* lse_out, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Workspace bytes for the per-epoch form of quantwm_attend_epochs (n_epochs >=
- * 2; 0 otherwise, and 0 with QWM_STORE_SCALE_I8): each epoch's packed keys run
- * through the plain attention kernel with that epoch's calibration block as
- * partial results of their own; with an active chunk, the last whole packed
- * tile on runs through the general kernel; everything merges by log-sum-exp.
- * epoch_start is the host array of the call. Given at least this much
- * (256-byte aligned) the call takes that form; otherwise the one-launch form,
- * with the split workspace of quantwm_attend_workspace_bytes(cfg, n_cache +
- * n_act, n_q). Both give the same result up to fp32 rounding order. */
+ * 2; 0 otherwise, and 0 with QWM_STORE_SCALE_I8 and an active chunk): each
+ * epoch's packed keys run through the plain attention kernel with that epoch's
+ * calibration block as partial results of their own; with an active chunk, the
+ * last whole packed tile on runs through the general kernel; everything merges
+ * by log-sum-exp. epoch_start is the host array of the call. Given at least
+ * this much (256-byte aligned) the call takes that form; otherwise the
+ * one-launch form, with the split workspace of
+ * quantwm_attend_workspace_bytes(cfg, n_cache + n_act, n_q). Both give the same
+ * result up to fp32 rounding order. Under QWM_STORE_SCALE_I8 only the per-epoch
+ * form is available. */
 size_t quantwm_attend_epochs_workspace_bytes(const quantwm_config* cfg, int32_t n_epochs,
                                              const int64_t* epoch_start, int64_t n_cache, int64_t n_act,
                                              int64_t n_q);

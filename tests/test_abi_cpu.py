@@ -151,7 +151,8 @@ def test_streaming_workspace_sizes():
     assert qw.quantwm_attend_epochs_workspace_bytes(ling, starts[:6], 28080, 4680, 4680) == planes(7)
     assert qw.quantwm_attend_epochs_workspace_bytes(ling, [0], 32760, 0, 4680) == 0
     i8 = qw.make_config(1, 40, 128, 128, 32, 16, 4, 32760, "bf16", qw.STORE_SCALE_I8)
-    assert qw.quantwm_attend_epochs_workspace_bytes(i8, starts, 32760, 0, 4680) == 0
+    assert qw.quantwm_attend_epochs_workspace_bytes(i8, starts, 32760, 0, 4680) == planes(7)
+    assert qw.quantwm_attend_epochs_workspace_bytes(i8, starts[:6], 28080, 4680, 4680) == 0
     assert qw.quantwm_attend_active_workspace_bytes(i8, 28080, 4680, 4680) == 0
 
 
