@@ -151,6 +151,15 @@ def int2_quantise(x, mu, step):
     return codes, int(zp.value), xhat
 
 
+def coef_row(C):
+    """App. D.1 INT8 PSAC row: (codes int8 [r], FP16 scale bits)."""
+    C = _f32(C)
+    codes = np.zeros(C.shape[0], np.int8)
+    sb = ctypes.c_uint16(0)
+    lib().ora_coef_row(_p(C), C.shape[0], _p(codes, ctypes.c_int8), ctypes.byref(sb))
+    return codes, int(sb.value)
+
+
 def keep_row(C, codes, scale, lam):
     """App. D.1 retention gate for one INT8 coefficient row."""
     C, lam = _f32(C), _f32(lam)

@@ -94,8 +94,9 @@ typedef struct {
 
 static long long up256(long long x) { return (x + 255) / 256 * 256; }
 
+/* head_dim is at most 256: the per-token buffers below are sized for it. */
 static int valid_cfg(const ora_cfg* c) {
-  if (!c || c->batch < 1 || c->heads < 1 || c->head_dim < 4 || c->head_dim % 4) return 0;
+  if (!c || c->batch < 1 || c->heads < 1 || c->head_dim < 4 || c->head_dim % 4 || c->head_dim > 256) return 0;
   if (c->group_size < 1 || c->head_dim % c->group_size) return 0;
   if (c->n_centroids < 1 || c->n_centroids > 256) return 0;
   if (c->rank < 0 || c->rank > c->head_dim) return 0;
@@ -213,6 +214,22 @@ void ora_scales_i8(const float* t, int ng, uint16_t* sigma_f16, uint8_t* codes, 
     codes[g] = (uint8_t)c;
     step_out[g] = sf * (float)c; /* exact: 11-bit times 8-bit significands */
   }
+}
+
+void ora_coef_row(const float* C, int r, int8_t* codes, uint16_t* scale_f16) {
+  /* App. D.1: one INT8 PSAC row with one FP16 scale, symmetric over +-127:
+   * s = FP16(max_k |C_k| / 127) (saturating), code_k = RN(C_k / s) clamped to
+   * [-127, 127], and all codes 0 when s is 0 */
+  float amax = 0.0f;
+  for (int k = 0; k < r; ++k)
+    if (fabsf(C[k]) > amax) amax = fabsf(C[k]);
+  float s = amax / 127.0f;
+  if (s > 65504.0f) s = 65504.0f;
+  double sh = ora_round_f16((double)s);
+  float shf = (float)sh;
+  for (int k = 0; k < r; ++k)
+    codes[k] = (int8_t)(shf != 0.0f ? (int)clampf(rintf(C[k] / shf), -127.0f, 127.0f) : 0);
+  *scale_f16 = ora_f16_bits(sh);
 }
 
 int ora_keep_row(const float* C, const int8_t* codes, float scale, const float* lam, int r) {
@@ -568,28 +585,23 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
       if (cand) for (int m = 0; m < M; ++m) cand[diag * M + m] = cands[m];
       if (r > 0) {
         /* Eq. 13 and Eq. 16: C = (k - khat_0) U_r, fp64 */
-        float amax = 0.0f, Cf[256];
+        float Cf[256];
         for (int kk = 0; kk < r; ++kk) {
           double acc = 0.0;
           for (int c = 0; c < d; ++c) acc += ((double)k[c] - (double)xhat[c]) * (double)uh[(long long)kk * d + c];
           Cf[kk] = (float)acc;
-          if (fabsf(Cf[kk]) > amax) amax = fabsf(Cf[kk]);
           if (coef_f32) coef_f32[diag * r + kk] = Cf[kk];
         }
         /* INT8 row with one FP16 scale (App. D.1) */
-        float s = amax / 127.0f;
-        if (s > 65504.0f) s = 65504.0f;
-        double sh = ora_round_f16((double)s);
-        float shf = (float)sh;
         int8_t* code = (int8_t*)(cache + L.k_coef + slot * r);
-        for (int kk = 0; kk < r; ++kk)
-          code[kk] = (int8_t)(shf != 0.0f ? (int)clampf(rintf(Cf[kk] / shf), -127.0f, 127.0f) : 0);
+        uint16_t sbits;
+        ora_coef_row(Cf, r, code, &sbits);
         /* App. D.1 retention: a row that does not lower the error is zeroed */
-        if (gate && !ora_keep_row(Cf, code, shf, lam + (long long)bh * r, r)) {
+        if (gate && !ora_keep_row(Cf, code, (float)ora_f16_value(sbits), lam + (long long)bh * r, r)) {
           memset(code, 0, (size_t)r);
-          sh = 0.0;
+          sbits = 0;
         }
-        put16(cache + L.k_cscale + slot * 2, ora_f16_bits(sh));
+        put16(cache + L.k_cscale + slot * 2, sbits);
       }
       /* Values: nearest centroid, same residual path, no PSAC */
       int zv = ora_nearest(v, muv, K, d);

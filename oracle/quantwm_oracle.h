@@ -31,7 +31,7 @@ extern "C" {
 #endif
 
 typedef struct {
-  int batch, heads, head_dim;  /* B, H, d */
+  int batch, heads, head_dim;  /* B, H, d (d <= 256, a multiple of 4) */
   int n_centroids;             /* Kc <= 256 (uint8 centroid ids, App. D.1) */
   int group_size;              /* G: INT2 residual group along channels */
   int rank;                    /* r: PSAC rank (0 disables PSAC) */
@@ -82,6 +82,10 @@ void ora_int2_quantise(const float* x, const float* mu, int n, float step, uint8
 /* SCALE_I8: the fp32 step sizes t[0..ng) of one token-head -> FP16 secondary
  * scale (bits) and 8-bit codes; step_out[g] = sigma * c_g. */
 void ora_scales_i8(const float* t, int ng, uint16_t* sigma_f16, uint8_t* codes, float* step_out);
+
+/* App. D.1 INT8 PSAC row of r coefficients C: FP16 scale s = RN16(max|C|/127)
+ * (bits to *scale_f16), codes RN(C/s) clamped to [-127, 127], 0 when s is 0. */
+void ora_coef_row(const float* C, int r, int8_t* codes, uint16_t* scale_f16);
 
 /* GATE: 1 when the INT8 row chat (codes * scale) lowers the lam-weighted error
  * of the coefficients C, else 0. fp32, ranks in order. */

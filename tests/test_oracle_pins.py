@@ -985,3 +985,261 @@ def test_epochs_match_explicit_reconstruction_fp32():
         assert np.abs(got - ref).max() < 1e-5
         # and decoding the second chunk with the first epoch's tables is wrong
         assert np.abs(plain[h * wl.n_q:(h + 1) * wl.n_q] - ref).max() > 1e-3
+
+
+# ------------------------------------- INT8 PSAC rows (App. D.1, Eq. 16)
+
+def _f16(x):
+    """IEEE binary16 round-to-nearest-even of an fp32 value (numpy's cast), as a float."""
+    return float(np.float32(np.float16(np.float32(x))))
+
+
+def _row_rule(C):
+    """The App. D.1 row written from its statement (reading R10): s = RN16(max|C| / 127),
+    saturating at the largest binary16; codes RN(C / s) clamped to +-127; 0 when s = 0."""
+    C = np.asarray(C, np.float32)
+    amax = np.float32(np.abs(C).max()) if C.size else np.float32(0)
+    s = np.float32(min(np.float32(amax / np.float32(127.0)), np.float32(65504.0)))
+    s = np.float32(_f16(s))
+    if s == 0:
+        return np.zeros(C.size, np.int8), s
+    return np.clip(np.rint(C / s), -127, 127).astype(np.int8), s
+
+
+def test_coef_row_hand_examples():
+    # scale 2^-7 exactly (0.9921875 / 127); 2.5 and -2.5 steps round to even, 3.5 up
+    s = 2.0 ** -7
+    codes, sb = oracle.coef_row([127 * s, 2.5 * s, 3.5 * s, -2.5 * s, 0.0, -127 * s])
+    assert list(codes) == [127, 2, 4, -2, 0, -127]
+    assert sb == 0x2000  # binary16 2^-7
+    # a zero row stores zero codes and a zero scale
+    codes, sb = oracle.coef_row([0.0, 0.0, 0.0])
+    assert not codes.any() and sb == 0
+    # a scale below half the smallest binary16 subnormal rounds to 0: the row is zero
+    codes, sb = oracle.coef_row([1e-6, -5e-7])
+    assert not codes.any() and sb == 0
+    # saturation: max|C| / 127 above 65504 stores 65504 (0x7bff) and clamps the codes
+    codes, sb = oracle.coef_row([1e7, 3 * 65504.0, -1e7, 0.4 * 65504.0])
+    assert sb == 0x7BFF and list(codes) == [127, 3, -127, 0]
+    # the largest element lands on +-127 up to the scale's binary16 rounding
+    codes, sb = oracle.coef_row([0.3, -1.0, 0.05])
+    s16 = oracle.f16_value(sb)
+    assert s16 == _f16(1.0 / 127.0) and codes[1] == -127 and codes[0] == round(0.3 / s16)
+
+
+def test_coef_row_matches_the_rule_and_error_bound():
+    r = rng(31)
+    for n in range(600):
+        rank = int(r.integers(1, 33))
+        mag = 10.0 ** r.uniform(-6, 6)
+        C = (r.standard_normal(rank) * mag).astype(np.float32)
+        if n % 7 == 0:
+            C[r.integers(rank)] = 0.0
+        codes, sb = oracle.coef_row(C)
+        want, s = _row_rule(C)
+        np.testing.assert_array_equal(codes, want)
+        assert oracle.f16_value(sb) == float(s)
+        if s > 0:
+            inside = np.abs(C / s) <= 127.0
+            err = np.abs(C.astype(np.float64) - codes.astype(np.float64) * float(s))
+            assert np.all(err[inside] <= float(s) / 2 * (1 + 1e-6))
+
+
+def test_append_stores_int8_rows_of_its_coefficients():
+    # The cache's INT8 rows and FP16 row scales are the App. D.1 encoding of the
+    # fp32 coefficients C = (k - khat_0) U_r that append computed.
+    from packed import fields, layout
+    for dt in ("f32", "bf16"):
+        wl = _small_workload(rank=12, head_dim=32, group_size=16, dtype=dt)
+        cfg, tables, cache, k, v, q, diag = _encoded(wl)
+        lay = layout(1, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.capacity)
+        nz = 0
+        for h in range(wl.heads):
+            f = fields(cache, lay, h, 0, wl.n_cache)
+            for t in range(wl.n_cache):
+                C = diag["coef"][0, h, t]
+                want, s = _row_rule(C)
+                np.testing.assert_array_equal(f["k_coef"][t], want)
+                assert oracle.f16_value(int(f["k_cscale"][t])) == float(s)
+                nz += int(s > 0)
+        assert nz > wl.heads * wl.n_cache // 2
+
+
+# -------------------------------- BF16 operands of Eq. 17 attention (reading R15)
+
+def _bf16_f64(x):
+    """Round float64 values to BF16 (8 significant bits) once, ties to even, by
+    truncating the binary64 significand with a rounding bias."""
+    x = np.ascontiguousarray(x, np.float64)
+    bits = x.view(np.uint64)
+    lsb = (bits >> np.uint64(45)) & np.uint64(1)
+    out = (bits + np.uint64((1 << 44) - 1) + lsb) & ~np.uint64((1 << 45) - 1)
+    return out.view(np.float64)
+
+
+def _sdpa_aug(q, u, K, C, V, mask, d):
+    """fp64 SDPA over the augmented depth d + r: ([q | u] . [K | C]) / sqrt(d)."""
+    qa = np.concatenate([q, u], 1)
+    ka = np.concatenate([K, C], 1)
+    qt = torch.from_numpy(qa)[None]
+    return torch.nn.functional.scaled_dot_product_attention(
+        qt, torch.from_numpy(ka)[None], torch.from_numpy(V)[None], attn_mask=torch.from_numpy(mask)[None],
+        scale=1.0 / math.sqrt(d))[0].numpy()
+
+
+def _bf16_reference(wl, cfg, tables, cache, q, h, n_cache, rounded=True):
+    k0, ch, vh = oracle.decode(cfg, tables, cache, 0, h, n_cache)
+    U = tables[3][0, h].astype(np.float64)  # [r, d], BF16 values
+    qh = q[0, :, h, :].astype(np.float64)
+    u = qh @ U.T
+    if rounded:
+        k0, ch, vh, u = _bf16_f64(k0), _bf16_f64(ch), _bf16_f64(vh), _bf16_f64(u)
+    return qh, u, k0, ch, vh
+
+
+def test_attend_bf16_operands_are_rounded():
+    # BF16 workloads (App. D.1 keeps centroids and U_r in BF16 and attends over
+    # BF16 K/V): the oracle's Eq. 17 logits take khat_0, vhat, chat and q U_r
+    # rounded to BF16. Reference: fp64 SDPA over those operands rounded here
+    # independently; the same reference without the rounding is measurably off.
+    wl = _small_workload(rank=4, dtype="bf16")
+    cfg, tables, cache, k, v, q, _ = _encoded(wl)
+    out, lse, _ = oracle.attend(cfg, tables, cache, wl.n_cache, q, wl.q_start, wl.frame_tokens)
+    mask = _mask(wl, wl.n_cache)
+    for h in range(wl.heads):
+        got = out[h * wl.n_q:(h + 1) * wl.n_q]
+        qh, u, k0, ch, vh = _bf16_reference(wl, cfg, tables, cache, q, h, wl.n_cache)
+        ref = _sdpa_aug(qh, u, k0, ch, vh, mask, wl.head_dim)
+        assert np.abs(got - ref).max() < 1e-10
+        qh, u, k0, ch, vh = _bf16_reference(wl, cfg, tables, cache, q, h, wl.n_cache, rounded=False)
+        loose = _sdpa_aug(qh, u, k0, ch, vh, mask, wl.head_dim)
+        assert np.abs(got - loose).max() > 1e-4
+        # each rounding point on its own matters
+        qh, u, k0, ch, vh = _bf16_reference(wl, cfg, tables, cache, q, h, wl.n_cache)
+        u_raw = q[0, :, h, :].astype(np.float64) @ tables[3][0, h].astype(np.float64).T
+        assert np.abs(got - _sdpa_aug(qh, u_raw, k0, ch, vh, mask, wl.head_dim)).max() > 1e-7
+        k0_raw, _, v_raw = oracle.decode(cfg, tables, cache, 0, h, wl.n_cache)
+        assert np.abs(got - _sdpa_aug(qh, u, k0_raw, ch, vh, mask, wl.head_dim)).max() > 1e-5
+        assert np.abs(got - _sdpa_aug(qh, u, k0, ch, v_raw, mask, wl.head_dim)).max() > 1e-5
+
+
+def test_active_chunk_bf16_matches_rounded_reference():
+    # [packed | active] in BF16: the packed keys as above, the active chunk's exact
+    # tokens (BF16 already) with no PSAC term.
+    wl = _small_workload(rank=4, dtype="bf16")
+    cfg, tables, cache, k, v, q, _ = _encoded(wl)
+    n_p = wl.n_cache - 90
+    ka, va = np.ascontiguousarray(k[:, n_p:]), np.ascontiguousarray(v[:, n_p:])
+    out, _, _ = oracle.attend(cfg, tables, cache, n_p, q, wl.q_start, wl.frame_tokens, k_act=ka, v_act=va)
+    mask = _mask(wl, wl.n_cache)
+    for h in range(wl.heads):
+        qh, u, k0, ch, vh = _bf16_reference(wl, cfg, tables, cache, q, h, n_p)
+        K = np.concatenate([k0, _bf16_f64(ka[0, :, h].astype(np.float64))])
+        C = np.concatenate([ch, np.zeros((wl.n_cache - n_p, wl.rank))])
+        V = np.concatenate([vh, _bf16_f64(va[0, :, h].astype(np.float64))])
+        ref = _sdpa_aug(qh, u, K, C, V, mask, wl.head_dim)
+        assert np.abs(out[h * wl.n_q:(h + 1) * wl.n_q] - ref).max() < 1e-10
+
+
+def test_epochs_bf16_match_rounded_reference():
+    # Two calibration epochs in BF16: every key decodes with its epoch's centroids
+    # and pairs its chat with q U_r of its epoch, all operands rounded to BF16.
+    wl = _small_workload(rank=4, dtype="bf16")
+    cfg, k, v, split, t1, t2, cache = _two_epoch_cache(wl)
+    q = synth.tensor(wl, "q", wl.n_q)
+    out, _, _ = oracle.attend(cfg, None, cache, wl.n_cache, q, wl.q_start, wl.frame_tokens,
+                              epochs=[(0, t1), (split, t2)])
+    mask = _mask(wl, wl.n_cache)
+    for h in range(wl.heads):
+        parts = []
+        for (s0, s1, t) in ((0, split, t1), (split, wl.n_cache, t2)):
+            qh, u, k0, ch, vh = _bf16_reference(wl, cfg, t, cache, q, h, wl.n_cache)
+            parts.append((u, k0[s0:s1], ch[s0:s1], vh[s0:s1]))
+        # logits by hand: each epoch's keys with that epoch's u
+        L = np.concatenate([(qh @ K0.T + u @ C.T) for (u, K0, C, _) in parts], 1) / math.sqrt(wl.head_dim)
+        V = np.concatenate([p[3] for p in parts])
+        L = np.where(mask, L, -np.inf)
+        P = np.exp(L - L.max(1, keepdims=True))
+        ref = (P @ V) / P.sum(1, keepdims=True)
+        assert np.abs(out[h * wl.n_q:(h + 1) * wl.n_q] - ref).max() < 1e-10
+
+
+# ------------------------------------- K-means with an empty cluster (Eq. 3, R1)
+
+def _lloyd_reference(x, kc, iters, table):
+    """Lloyd written from reading R1: initial centroids are tokens floor(j n / Kc);
+    assignment by fp32 squared distance summed over channels in order, ties to the
+    lower index; the update is the fp64 token-order mean rounded to the table type;
+    a cluster with no token keeps its centroid."""
+    n, d = x.shape
+    rnd = (lambda a: np.asarray(a, np.float32)) if table == "f32" else (lambda a: _bf16_f64(a).astype(np.float32))
+    mu = rnd(x[[(j * n) // kc for j in range(kc)]].astype(np.float64))
+    empty = 0
+    for _ in range(iters):
+        acc = np.zeros((n, kc), np.float32)
+        for c in range(d):
+            t = (x[:, None, c] - mu[None, :, c]).astype(np.float32)
+            acc = (acc + t * t).astype(np.float32)
+        assign = np.argmin(acc, 1)  # first minimum: the lower index
+        sums = np.zeros((kc, d))
+        counts = np.zeros(kc, np.int64)
+        for t_ in range(n):
+            sums[assign[t_]] += x[t_].astype(np.float64)
+            counts[assign[t_]] += 1
+        for j in range(kc):
+            if counts[j] > 0:
+                mu[j] = rnd(sums[j] / counts[j])
+            else:
+                empty += 1
+    return mu, empty
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_kmeans_empty_cluster_keeps_its_centroid(dt):
+    # Tokens 0 and 10 (the initial picks of clusters 0 and 1) are equal, so the
+    # two starting centroids coincide and every tie goes to cluster 0: cluster 1
+    # is empty in the first iteration and must keep its initial centroid. Later
+    # iterations (cluster 0 has moved) follow the reference bit for bit.
+    r = rng(41)
+    d, kc, n = 16, 4, 40
+    x = (r.standard_normal((n, d)) * 3).astype(np.float32)
+    x = synth.round_to(x, dt)
+    x[10] = x[0]
+    wl = _small_workload(head_dim=d, n_centroids=kc, group_size=16, rank=0, heads=1, dtype=dt)
+    cfg = oracle.cfg_from_workload(wl)
+    xt = np.ascontiguousarray(x[None, :, None, :])
+    mu1, _, _, _, _ = oracle.calibrate(cfg, None, xt, xt, 1)
+    ref1, empty1 = _lloyd_reference(x, kc, 1, dt)
+    assert empty1 == 1
+    np.testing.assert_array_equal(mu1[0, 0], ref1)
+    np.testing.assert_array_equal(mu1[0, 0, 1], x[10])
+    mu6, _, _, _, _ = oracle.calibrate(cfg, None, xt, xt, 6)
+    ref6, _ = _lloyd_reference(x, kc, 6, dt)
+    np.testing.assert_array_equal(mu6[0, 0], ref6)
+
+
+def test_kmeans_matches_reference_lloyd_on_overlapping_data():
+    # Overlapping clusters (assignments change between iterations), against the
+    # same reference Lloyd, bit for bit.
+    r = rng(42)
+    d, kc, n = 8, 6, 300
+    x = (r.standard_normal((n, d)) + r.integers(0, 3, size=(n, 1))).astype(np.float32)
+    wl = _small_workload(head_dim=d, n_centroids=kc, group_size=8, rank=0, heads=1)
+    cfg = oracle.cfg_from_workload(wl)
+    xt = np.ascontiguousarray(x[None, :, None, :])
+    mu_k, _, _, _, _ = oracle.calibrate(cfg, None, xt, xt, 7)
+    ref, _ = _lloyd_reference(x, kc, 7, "f32")
+    np.testing.assert_array_equal(mu_k[0, 0], ref)
+
+
+# ---------------------------------------------------------- oracle bounds
+
+def test_oracle_rejects_head_dim_above_256():
+    # The oracle's per-token buffers hold 256 channels: larger head_dim is refused.
+    cfg = oracle.cfg_of(1, 1, 512, 4, 32, 4, 2, 64, False)
+    assert oracle.cache_bytes(cfg) == -1
+    x = np.zeros((1, 8, 1, 512), np.float32)
+    with pytest.raises(RuntimeError):
+        oracle.calibrate(cfg, None, x, x, 1)
+    ok = oracle.cfg_of(1, 1, 256, 4, 32, 4, 2, 64, False)
+    assert oracle.cache_bytes(ok) > 0
