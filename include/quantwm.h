@@ -284,9 +284,13 @@ size_t quantwm_attend_epochs_workspace_bytes(const quantwm_config* cfg, int32_t 
                                              int64_t n_q);
 
 /* Test hook: the scaled logits of quantwm_attend, [B,H,n_q,n_cache] f32,
- * -inf where masked. Same tile code as quantwm_attend. */
+ * -inf where masked. Same tile code as quantwm_attend. Query i is chunk row
+ * q_first + i (absolute position q_start + q_first + i): key j is visible iff
+ * j < q_start or (j - q_start)/F <= (q_first + i)/F, so rows of any frame can
+ * be checked without the rows before them. q_first = 0 is the Query chunk of
+ * quantwm_attend. Needs q_first >= 0. */
 quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, const void* cache,
-                              int64_t n_cache, const void* q, int64_t n_q, int64_t q_start,
+                              int64_t n_cache, const void* q, int64_t n_q, int64_t q_start, int64_t q_first,
                               int32_t frame_tokens, float* logits_out, void* stream);
 
 /* ------------------------------------------- per-chunk coefficient records */

@@ -1,8 +1,9 @@
 """Builds libquantwm.so (the gfx950 HIP kernels plus the C ABI) in-tree.
 
 Translation units compile in parallel: append.hip once per (element type,
-head_dim), attend.hip, calib.hip, coef.hip, api.hip and the host eigensolver; the objects
-link into ``paper_2609_26425_amd/libquantwm.so``.
+head_dim, group size), attend.hip once per (element type, head_dim, PSAC rank padding),
+attend_host.hip, calib.hip, coef.hip, api.hip and the host eigensolver; the
+objects link into ``paper_2609_26425_amd/libquantwm.so``.
 """
 from __future__ import annotations
 
@@ -30,12 +31,20 @@ def _units():
     units = []
     for tn, t in (("f32", "float"), ("bf16", "qwm::bf16")):
         for d in (64, 128):
-            units.append((f"append_{tn}_{d}.o", "append.hip",
-                          [f"-DQWM_APPEND_T={t}", f"-DQWM_APPEND_TN={tn}", f"-DQWM_APPEND_D={d}"]))
+            for g in (16, 32, 64):
+                units.append((f"append_{tn}_{d}_g{g}.o", "append.hip",
+                              [f"-DQWM_APPEND_T={t}", f"-DQWM_APPEND_D={d}", f"-DQWM_APPEND_G={g}"]))
     # attend: no NaN semantics, so maxima of matrix-core results are plain
     # v_max3_f32 without a quieting v_max_f32 x, x per input (its logits and
-    # running maxima are finite or -inf)
-    units.append(("attend.o", "attend.hip", ["-fno-honor-nans"]))
+    # running maxima are finite or -inf). One unit per (element type, head_dim,
+    # PSAC rank padding), so the instances compile in parallel.
+    for tn, t in (("f32", "float"), ("bf16", "qwm::bf16")):
+        for d in (64, 128):
+            for rp in (0, 16, 32):
+                units.append((f"attend_{tn}_{d}_r{rp}.o", "attend.hip",
+                              ["-fno-honor-nans", f"-DQWM_ATTEND_T={t}", f"-DQWM_ATTEND_D={d}",
+                               f"-DQWM_ATTEND_RP={rp}"]))
+    units.append(("attend_host.o", "attend_host.hip", ["-fno-honor-nans"]))
     for name in ("calib", "coef", "api"):
         units.append((f"{name}.o", f"{name}.hip", []))
     units.append(("eigh.o", "eigh.cpp", ["-x", "hip"]))
@@ -55,12 +64,25 @@ def _compile(obj, src, extra):
     return obj
 
 
-def build(jobs: int | None = None, verbose: bool = False) -> str:
+def _stale(obj, src):
+    """True when the object is missing or older than its source or a header."""
+    o = os.path.join(BUILD, obj)
+    if not os.path.exists(o):
+        return True
+    deps = [os.path.join(CSRC, src)] + [os.path.join(CSRC, h) for h in os.listdir(CSRC) if h.endswith(".h")]
+    deps.append(os.path.join(HERE, "..", "include", "quantwm.h"))
+    return any(os.path.getmtime(p) > os.path.getmtime(o) for p in deps)
+
+
+def build(jobs: int | None = None, verbose: bool = False, incremental: bool = False) -> str:
+    """Compiles every unit (or, with incremental, only those older than their
+    sources) and links the library."""
     os.makedirs(BUILD, exist_ok=True)
     units = _units()
+    todo = [u for u in units if not incremental or _stale(u[0], u[1])]
     jobs = jobs or min(len(units), max(1, min(os.cpu_count() or 1, 16)))
     with cf.ThreadPoolExecutor(jobs) as ex:
-        futs = [ex.submit(_compile, *u) for u in units]
+        futs = [ex.submit(_compile, *u) for u in todo]
         for f in cf.as_completed(futs):
             obj = f.result()
             if verbose:
@@ -74,5 +96,5 @@ def build(jobs: int | None = None, verbose: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, incremental="--incremental" in sys.argv))
     sys.exit(0)

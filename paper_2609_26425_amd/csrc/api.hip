@@ -72,6 +72,14 @@ quantwm_status check_dev(const void* p, const char* name, bool required = true) 
   return QWM_OK;
 }
 
+template <typename T, int D>
+hipError_t launch_append_td(const qwm::AppendArgs& a, int g, int batch, hipStream_t s) {
+  if (g == 16) return qwm::launch_append_g<T, D, 16>(a, batch, s);
+  if (g == 32) return qwm::launch_append_g<T, D, 32>(a, batch, s);
+  if (g == 64) return qwm::launch_append_g<T, D, 64>(a, batch, s);
+  return hipErrorInvalidValue;
+}
+
 #define QWM_TRY(x)                         \
   do {                                     \
     quantwm_status _s = (x);               \
@@ -423,10 +431,10 @@ quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   const bool bf = cfg->dtype == QWM_BF16;
-  if (cfg->head_dim == 64) e = bf ? qwm::launch_append_bf16_64(a, cfg->group_size, cfg->batch, s)
-                                  : qwm::launch_append_f32_64(a, cfg->group_size, cfg->batch, s);
-  else e = bf ? qwm::launch_append_bf16_128(a, cfg->group_size, cfg->batch, s)
-              : qwm::launch_append_f32_128(a, cfg->group_size, cfg->batch, s);
+  if (cfg->head_dim == 64) e = bf ? launch_append_td<qwm::bf16, 64>(a, cfg->group_size, cfg->batch, s)
+                                  : launch_append_td<float, 64>(a, cfg->group_size, cfg->batch, s);
+  else e = bf ? launch_append_td<qwm::bf16, 128>(a, cfg->group_size, cfg->batch, s)
+              : launch_append_td<float, 128>(a, cfg->group_size, cfg->batch, s);
   if (e != hipSuccess) return hip_fail(e, "append launch");
   return ok();
 }
@@ -532,7 +540,8 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
                                     const int64_t* epoch_start, const void* cache, int64_t n_cache,
                                     const void* k_act, const void* v_act, int64_t n_act, const void* q, int64_t n_q,
                                     int64_t q_start, int32_t frame_tokens, void* out, float* lse_out,
-                                    float* logits_out, void* workspace, size_t workspace_bytes, void* stream) {
+                                    float* logits_out, void* workspace, size_t workspace_bytes, void* stream,
+                                    int64_t q_first = 0) {
   QWM_TRY(check_cfg(cfg));
   if (n_epochs < 1 || n_epochs > qwm::kMaxEpochs) return fail(QWM_ERR_UNSUPPORTED, "n_epochs must be in [1, 64]");
   if ((cfg->storage & QWM_STORE_SCALE_I8) && n_act > 0)
@@ -603,6 +612,7 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   a.split_base = 0;
   a.partial = 0;
   a.key_lo = 0;
+  a.q_row0 = logits_out ? q_first : 0;
   hipStream_t s = static_cast<hipStream_t>(stream);
   // calibration epochs one by one through the plain kernel when the workspace
   // holds a partial plane per launch
@@ -746,11 +756,13 @@ quantwm_status quantwm_attend_epochs(const quantwm_config* cfg, const void* cali
 }
 
 quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
-                              const void* q, int64_t n_q, int64_t q_start, int32_t frame_tokens, float* logits_out,
-                              void* stream) {
+                              const void* q, int64_t n_q, int64_t q_start, int64_t q_first, int32_t frame_tokens,
+                              float* logits_out, void* stream) {
   if (!logits_out && n_q > 0) return fail(QWM_ERR_INVALID_ARG, "logits_out is null");
+  if (q_first < 0 || q_first > kMaxPositions - (n_q > 0 ? n_q : 0))
+    return fail(QWM_ERR_INVALID_ARG, "need 0 <= q_first and q_first + n_q <= %lld", (long long)kMaxPositions);
   return attend_common(cfg, calib, 1, nullptr, cache, n_cache, nullptr, nullptr, 0, q, n_q, q_start, frame_tokens,
-                       nullptr, nullptr, logits_out, nullptr, 0, stream);
+                       nullptr, nullptr, logits_out, nullptr, 0, stream, q_first);
 }
 
 }  // extern "C"

@@ -494,23 +494,15 @@ hipError_t launch_dgs(const AppendArgs& a, int batch, hipStream_t s) {
   return hipGetLastError();
 }
 
+}  // namespace
+
+// This file is compiled once per (element type, head_dim, group size):
+// QWM_APPEND_T, QWM_APPEND_D and QWM_APPEND_G select the instantiations.
 template <typename T, int D, int G>
-hipError_t launch_dg(const AppendArgs& a, int batch, hipStream_t s) {
+hipError_t launch_append_g(const AppendArgs& a, int batch, hipStream_t s) {
   return a.L.i8 ? launch_dgs<T, D, G, true>(a, batch, s) : launch_dgs<T, D, G, false>(a, batch, s);
 }
 
-}  // namespace
-
-// This file is compiled once per (element type, head_dim): QWM_APPEND_T and
-// QWM_APPEND_D select the instantiations and the launcher's name.
-#define QWM_CAT2(a, b, c) a##b##_##c
-#define QWM_CAT(a, b, c) QWM_CAT2(a, b, c)
-hipError_t QWM_CAT(launch_append_, QWM_APPEND_TN, QWM_APPEND_D)(const AppendArgs& a, int g, int batch,
-                                                                 hipStream_t s) {
-  if (g == 16) return launch_dg<QWM_APPEND_T, QWM_APPEND_D, 16>(a, batch, s);
-  if (g == 32) return launch_dg<QWM_APPEND_T, QWM_APPEND_D, 32>(a, batch, s);
-  if (g == 64) return launch_dg<QWM_APPEND_T, QWM_APPEND_D, 64>(a, batch, s);
-  return hipErrorInvalidValue;
-}
+template hipError_t launch_append_g<QWM_APPEND_T, QWM_APPEND_D, QWM_APPEND_G>(const AppendArgs&, int, hipStream_t);
 
 }  // namespace qwm

@@ -14,8 +14,9 @@
 // holds one Query column, so the exponentials feed the P.V product straight
 // from the accumulator registers and O^T = Vhat^T P^T accumulates in registers.
 // Softmax is online (running max and sum per Query, base-2 exponentials).
-#include "qwm_common.h"
+#include "attend_shape.h"
 
+#include <atomic>
 #include <type_traits>
 
 namespace qwm {
@@ -221,26 +222,6 @@ __device__ inline V pack_operand(const float* x) {
   }
 }
 
-// Workgroup: NC consumer waves (32 Queries each: logits, softmax, P.V on the
-// matrix cores) and NP producer waves (read and dequantise the packed tiles).
-// Waves w and w + 4 share a SIMD, so every SIMD runs one producer beside two
-// consumers: the producer's vector work overlaps the consumers' matrix work.
-constexpr int NC = 8, NP = 4, BQ = 32 * NC, KT = kAttendTileKeys, NT = 64 * (NC + NP), PT = 64 * NP;
-
-// LDS row strides (elements), chosen so that the matrix-core operand reads are
-// free of bank conflicts: K tile rows of 272 B (16-byte reads), V^T rows of
-// 136 B and chat rows of (r + 4) * 2 B (8-byte reads), and centroid-table rows
-// padded by 16 B so that lanes looking up different centroids spread over banks.
-template <typename T, int D, int RP>
-struct Lds {
-  static constexpr bool H = sizeof(T) == 2;
-  static constexpr int KS = D + (H ? 8 : 1);
-  static constexpr int CS = (RP > 0 ? RP : 1) + (H ? 4 : 1);
-  static constexpr int VS = KT + (H ? 4 : 1);
-  static constexpr int TS = D + (H ? 8 : 4);
-  static constexpr int tile_elems = KT * KS + KT * CS + D * VS;
-};
-
 // GEN: the launch has an exact active chunk after the packed keys and/or packed
 // keys in several calibration epochs (a separate instance, so plain launches
 // carry none of its code).
@@ -313,7 +294,9 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   const int64_t qb = qa + BQ < a.n_q ? qa + BQ : a.n_q;
   int64_t kend = LOGITS ? nc : qs + ((qb - 1) / F + 1) * F;
   if (kend > nc) kend = nc;
-  int64_t kfull = qs + (qa / F + 1) * F;  // keys below are visible to every Query of the workgroup
+  // the logits hook may start its Queries at chunk row q_row0 (the mask's frame count)
+  const int64_t qoff = LOGITS ? a.q_row0 : 0;
+  int64_t kfull = qs + ((qa + qoff) / F + 1) * F;  // keys below are visible to every Query of the workgroup
   if (kfull > nc) kfull = nc;
   const int64_t ntile_all = (kend + KT - 1) / KT;
   // this launch covers tiles [tile_lo, ntile_all) (tile_lo is 0 unless the
@@ -656,7 +639,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) oacc[cb][i] = 0.0f;
     if (qvalid) {
-      const int64_t l = qs + (qi / F + 1) * F;  // this lane's Query sees keys j < lim
+      const int64_t l = qs + ((qi + qoff) / F + 1) * F;  // this lane's Query sees keys j < lim
       lim = int(l < nc ? l : nc);
     }
   }
@@ -1003,66 +986,32 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   }
 }
 
-// Merges the n_split partial results of every Query: with M the largest running
-// max and w_s = 2^((m_s - M) log2(e) / sqrt(d)), O = sum w_s O_s / sum w_s l_s
-// and lse = M / sqrt(d) + log(sum w_s l_s). One wave per Query, D / 64 channels
-// per lane.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void attend_combine(const AttendArgs a) {
-  const int64_t qi = int64_t(blockIdx.x) * 4 + threadIdx.x / 64;
-  const int lane = threadIdx.x % 64;
-  const int h = blockIdx.y, b = blockIdx.z;
-  if (qi >= a.n_q) return;
-  const int64_t bh = int64_t(b) * a.heads + h;
-  const int64_t plane = int64_t(a.heads) * gridDim.z * a.n_q;  // rows per split
-  const float mscale = 1.4426950408889634f / sqrtf((float)D);
-  float M = -__builtin_inff();
-  for (int sp = 0; sp < a.n_split; ++sp) M = fmaxf(M, a.part_ml[2 * (sp * plane + bh * a.n_q + qi)]);
-  constexpr int PL = D / 64;
-  float o[PL];
-#pragma unroll
-  for (int j = 0; j < PL; ++j) o[j] = 0.0f;
-  float L = 0.0f;
-  for (int sp = 0; sp < a.n_split; ++sp) {
-    const int64_t row = sp * plane + bh * a.n_q + qi;
-    const float m = a.part_ml[2 * row], l = a.part_ml[2 * row + 1];
-    if (!(l > 0.0f)) continue;  // this split saw no visible key of this Query
-    const float w = __builtin_amdgcn_exp2f((m - M) * mscale);
-    L += w * l;
-#pragma unroll
-    for (int j = 0; j < PL; ++j) o[j] += w * a.part_o[row * D + j * 64 + lane];
-  }
-  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-  T* orow = reinterpret_cast<T*>(a.out) + ((int64_t(b) * a.n_q + qi) * a.heads + h) * D;
-#pragma unroll
-  for (int j = 0; j < PL; ++j) orow[j * 64 + lane] = T(o[j] * inv);
-  if (a.lse && lane == 0) a.lse[bh * a.n_q + qi] = L > 0.0f ? M / sqrtf((float)D) + logf(L) : -__builtin_inff();
-}
-
-template <typename T, int D>
-size_t lds_bytes_t(int rank, int kc, bool tables) {
-  size_t tile = 0;
-  if (rank == 0) tile = Lds<T, D, 0>::tile_elems;
-  else if (rank <= 16) tile = Lds<T, D, 16>::tile_elems;
-  else tile = Lds<T, D, 32>::tile_elems;
-  constexpr size_t TS = Lds<T, D, 0>::TS;
-  return (2 * tile + (tables ? size_t(2) * kc * TS : 0)) * sizeof(T);  // two tile buffers
-}
-
 template <typename T, int D, int RP, bool LOGITS, bool TAB, bool GEN = false, bool SI8 = false>
 hipError_t launch_k(const AttendArgs& a, const dim3& grid, size_t lds, hipStream_t s) {
-  const hipError_t e = hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, LOGITS, TAB, GEN, SI8>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  // the dynamic LDS limit is raised once per device for this instance
+  static std::atomic<uint64_t> raised{0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? uint64_t(1) << dev : 0;
+  if (!bit || !(raised.load(std::memory_order_acquire) & bit)) {
+    e = hipFuncSetAttribute((const void*)attend_kernel<T, D, RP, LOGITS, TAB, GEN, SI8>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, int(kLdsLimit));
+    if (e != hipSuccess) return e;
+    raised.fetch_or(bit, std::memory_order_release);
+  }
   hipLaunchKernelGGL((attend_kernel<T, D, RP, LOGITS, TAB, GEN, SI8>), grid, dim3(NT), lds, s, a);
   return hipGetLastError();
 }
 
+}  // namespace
+
 template <typename T, int D, int RP>
-hipError_t launch_r(const AttendArgs& a, int batch, bool logits, hipStream_t s) {
+hipError_t launch_attend_rp(const AttendArgs& a, int batch, bool logits, hipStream_t s) {
   const dim3 grid((unsigned)((a.n_q + BQ - 1) / BQ * a.n_split), (unsigned)a.heads, (unsigned)batch);
   const bool tab = a.tables_in_lds != 0;
-  const size_t lds = lds_bytes_t<T, D>(a.rank, a.n_centroids, tab);
+  const size_t lds = attend_lds_bytes_t<T, D>(a.rank, a.n_centroids, tab);
+  if (lds > kLdsLimit) return hipErrorInvalidValue;
   const bool si8 = a.L.i8 != 0;
   if (si8 && (a.n_act > 0 || a.n_epochs > 1)) return hipErrorNotSupported;
   if (logits) {
@@ -1071,90 +1020,16 @@ hipError_t launch_r(const AttendArgs& a, int batch, bool logits, hipStream_t s) 
                  : launch_k<T, D, RP, true, false, false, true>(a, grid, lds, s);
     return tab ? launch_k<T, D, RP, true, true>(a, grid, lds, s) : launch_k<T, D, RP, true, false>(a, grid, lds, s);
   }
-  hipError_t e;
   if (a.n_act > 0 || a.n_epochs > 1)
-    e = tab ? launch_k<T, D, RP, false, true, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false, true>(a, grid, lds, s);
-  else if (si8)
-    e = tab ? launch_k<T, D, RP, false, true, false, true>(a, grid, lds, s)
-            : launch_k<T, D, RP, false, false, false, true>(a, grid, lds, s);
-  else
-    e = tab ? launch_k<T, D, RP, false, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false>(a, grid, lds, s);
-  if (e != hipSuccess || a.n_split == 1 || a.partial) return e;
-  hipLaunchKernelGGL((attend_combine<T, D>), dim3((unsigned)((a.n_q + 3) / 4), (unsigned)a.heads, (unsigned)batch),
-                     dim3(256), 0, s, a);
-  return hipGetLastError();
+    return tab ? launch_k<T, D, RP, false, true, true>(a, grid, lds, s)
+               : launch_k<T, D, RP, false, false, true>(a, grid, lds, s);
+  if (si8)
+    return tab ? launch_k<T, D, RP, false, true, false, true>(a, grid, lds, s)
+               : launch_k<T, D, RP, false, false, false, true>(a, grid, lds, s);
+  return tab ? launch_k<T, D, RP, false, true>(a, grid, lds, s) : launch_k<T, D, RP, false, false>(a, grid, lds, s);
 }
 
-template <typename T, int D>
-hipError_t launch_d(const AttendArgs& a, int batch, bool logits, hipStream_t s) {
-  if (a.rank == 0) return launch_r<T, D, 0>(a, batch, logits, s);
-  if (a.rank <= 16) return launch_r<T, D, 16>(a, batch, logits, s);
-  return launch_r<T, D, 32>(a, batch, logits, s);
-}
-
-}  // namespace
-
-constexpr size_t kLdsLimit = 160 * 1024;
-
-size_t attend_lds_bytes(int d, int elem, int rank, int n_centroids, bool tables) {
-  if (elem == 2) return d == 64 ? lds_bytes_t<bf16, 64>(rank, n_centroids, tables)
-                                : lds_bytes_t<bf16, 128>(rank, n_centroids, tables);
-  return d == 64 ? lds_bytes_t<float, 64>(rank, n_centroids, tables)
-                 : lds_bytes_t<float, 128>(rank, n_centroids, tables);
-}
-
-int attend_splits(int64_t n_q, int heads, int batch, int64_t n_cache, int cus) {
-  // Split the key range only when the launch gives fewer than two workgroups
-  // per compute unit (one runs per CU). The split count minimises the rounds of
-  // workgroups times each one's work: its share of the key tiles plus a fixed
-  // cost of about 32 tiles (table staging, Query fragments, pipeline fill,
-  // partial write), up to 16 splits of at least 8 tiles.
-  const int64_t wgs = (n_q + BQ - 1) / BQ * heads * batch;
-  if (wgs <= 0 || wgs >= 2 * int64_t(cus)) return 1;
-  const int64_t tiles = (n_cache + KT - 1) / KT;
-  int best = 1;
-  int64_t best_cost = -1;
-  for (int ns = 1; ns <= 16; ++ns) {
-    if (ns > 1 && tiles / ns < 8) break;
-    const int64_t rounds = (wgs * ns + cus - 1) / cus;
-    const int64_t cost = rounds * ((tiles + ns - 1) / ns + 32);
-    if (best_cost < 0 || cost < best_cost) {
-      best = ns;
-      best_cost = cost;
-    }
-  }
-  return best;
-}
-
-bool attend_tables_fit(int d, int elem, int rank, int n_centroids) {
-  return attend_lds_bytes(d, elem, rank, n_centroids, true) <= kLdsLimit;
-}
-
-hipError_t launch_attend_f32(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s) {
-  if (d == 64) return launch_d<float, 64>(a, batch, logits, s);
-  if (d == 128) return launch_d<float, 128>(a, batch, logits, s);
-  return hipErrorInvalidValue;
-}
-
-// merges the a.n_split partial planes of a.part_o / a.part_ml into a.out and a.lse
-hipError_t launch_attend_combine(const AttendArgs& a, int d, int batch, bool is_bf16, hipStream_t s) {
-  const dim3 grid((unsigned)((a.n_q + 3) / 4), (unsigned)a.heads, (unsigned)batch);
-  if (is_bf16) {
-    if (d == 64) hipLaunchKernelGGL((attend_combine<bf16, 64>), grid, dim3(256), 0, s, a);
-    else if (d == 128) hipLaunchKernelGGL((attend_combine<bf16, 128>), grid, dim3(256), 0, s, a);
-    else return hipErrorInvalidValue;
-  } else {
-    if (d == 64) hipLaunchKernelGGL((attend_combine<float, 64>), grid, dim3(256), 0, s, a);
-    else if (d == 128) hipLaunchKernelGGL((attend_combine<float, 128>), grid, dim3(256), 0, s, a);
-    else return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-
-hipError_t launch_attend_bf16(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s) {
-  if (d == 64) return launch_d<bf16, 64>(a, batch, logits, s);
-  if (d == 128) return launch_d<bf16, 128>(a, batch, logits, s);
-  return hipErrorInvalidValue;
-}
+template hipError_t launch_attend_rp<QWM_ATTEND_T, QWM_ATTEND_D, QWM_ATTEND_RP>(const AttendArgs&, int, bool,
+                                                                                hipStream_t);
 
 }  // namespace qwm

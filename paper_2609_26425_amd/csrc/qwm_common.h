@@ -131,16 +131,15 @@ struct AttendArgs {
   int split_base;
   int partial;
   int64_t key_lo;  // keys below are masked (a launch over one calibration epoch's keys)
+  int64_t q_row0;  // logits hook only: chunk row of the first Query (frame count of the mask)
 };
 
 // keys per attention tile
 constexpr int kAttendTileKeys = 64;
 
-// Launchers (one translation unit per element type).
-hipError_t launch_append_f32_64(const AppendArgs& a, int g, int batch, hipStream_t s);
-hipError_t launch_append_f32_128(const AppendArgs& a, int g, int batch, hipStream_t s);
-hipError_t launch_append_bf16_64(const AppendArgs& a, int g, int batch, hipStream_t s);
-hipError_t launch_append_bf16_128(const AppendArgs& a, int g, int batch, hipStream_t s);
+// Launchers. Append: one translation unit per (element type, head_dim, group size).
+template <typename T, int D, int G>
+hipError_t launch_append_g(const AppendArgs& a, int batch, hipStream_t s);
 hipError_t launch_attend_f32(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s);
 hipError_t launch_attend_bf16(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s);
 size_t attend_lds_bytes(int d, int elem, int rank, int n_centroids, bool tables_in_lds);

@@ -66,7 +66,7 @@ def _load():
         "quantwm_attend_active": (I32, [C, P, P, I64, P, P, I64, P, I64, I64, I32, P, P, P, SZ, P]),
         "quantwm_attend_epochs": (I32, [C, P, I32, ctypes.POINTER(I64), P, I64, P, P, I64, P, I64, I64, I32, P, P,
                                         P, SZ, P]),
-        "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I32, P, P]),
+        "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I64, I32, P, P]),
         "quantwm_attend_active_workspace_bytes": (SZ, [C, I64, I64, I64]),
         "quantwm_attend_epochs_workspace_bytes": (SZ, [C, I32, ctypes.POINTER(I64), I64, I64, I64]),
         "quantwm_coef_record_max_bytes": (SZ, [C, I64]),
@@ -238,8 +238,8 @@ def quantwm_attend_epochs_workspace_bytes(cfg, epoch_start, n_cache, n_act, n_q)
                                                           n_act, n_q))
 
 
-def quantwm_logits(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, logits_out, stream=None):
-    _check(_lib.quantwm_logits(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cache, _ptr(q), n_q, q_start,
+def quantwm_logits(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, logits_out, stream=None, q_first=0):
+    _check(_lib.quantwm_logits(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cache, _ptr(q), n_q, q_start, q_first,
                                frame_tokens, _ptr(logits_out), _stream(stream)))
 
 

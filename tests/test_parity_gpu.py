@@ -180,20 +180,21 @@ def check_attend(case, out, lse, rows):
     return float(err.max()), float(err.mean())
 
 
-def check_logits(case, cfg, calib, cache_np, q_full, n_q_rows):
-    """Logits hook on the first n_q_rows Queries of every head (full key range)."""
+def check_logits(case, cfg, calib, cache_np, q_full, n_q_rows, first=0):
+    """Logits hook on the n_q_rows Queries from chunk row `first` on, every head
+    (full key range)."""
     wl = case.wl
     dt = cfg.torch_dtype
-    n_q = min(n_q_rows, wl.n_q)
-    q = tdev(np.ascontiguousarray(q_full[:, :n_q]), dt)
+    n_q = min(n_q_rows, wl.n_q - first)
+    q = tdev(np.ascontiguousarray(q_full[:, first:first + n_q]), dt)
     cache = torch.from_numpy(cache_np).to(DEV)
     lg = torch.empty((wl.batch, wl.heads, n_q, wl.n_cache), dtype=torch.float32, device=DEV)
-    qw.quantwm_logits(cfg, calib, cache, wl.n_cache, q, n_q, wl.q_start, wl.frame_tokens, lg)
+    qw.quantwm_logits(cfg, calib, cache, wl.n_cache, q, n_q, wl.q_start, wl.frame_tokens, lg, q_first=first)
     torch.cuda.synchronize()
     lg = lg.cpu().numpy()
-    rows = np.array([(0, s, i) for s in range(len(case.sources)) for i in range(n_q)], np.int32)
-    _, _, o_lg = oracle.attend(case.cfg, case.tables, case.cache, wl.n_cache, np.ascontiguousarray(case.q[:, :n_q]),
-                               wl.q_start, wl.frame_tokens, rows=rows, want_logits=True)
+    rows = np.array([(0, s, first + i) for s in range(len(case.sources)) for i in range(n_q)], np.int32)
+    _, _, o_lg = oracle.attend(case.cfg, case.tables, case.cache, wl.n_cache, case.q, wl.q_start, wl.frame_tokens,
+                               rows=rows, want_logits=True)
     worst = 0.0
     for bh in range(wl.batch * wl.heads):
         b, h = divmod(bh, wl.heads)
@@ -202,11 +203,21 @@ def check_logits(case, cfg, calib, cache_np, q_full, n_q_rows):
             ref = o_lg[s * n_q + i]
             got = lg[b, h, i]
             vis = np.isfinite(ref)
-            assert np.array_equal(vis, np.isfinite(got)), f"mask differs at head {bh} row {i}"
+            assert np.array_equal(vis, np.isfinite(got)), f"mask differs at head {bh} row {first + i}"
             e = np.abs(got[vis] - ref[vis]).max() / max(np.abs(ref[vis]).max(), 1e-30)
             worst = max(worst, e)
-            assert e <= 1e-3, f"logits error {e:.3g} at head {bh} row {i}"
+            assert e <= 1e-3, f"logits error {e:.3g} at head {bh} row {first + i}"
     return worst
+
+
+def frame_row_starts(wl, rows):
+    """First chunk rows of `rows`-row windows that straddle every frame boundary
+    of the Query chunk (and the chunk's first and last rows)."""
+    F = wl.frame_tokens
+    starts = {0, max(0, wl.n_q - rows)}
+    for f in range(1, (wl.n_q + F - 1) // F):
+        starts.add(min(max(0, f * F - rows // 2), max(0, wl.n_q - rows)))
+    return sorted(starts)
 
 
 # ------------------------------------------------------------------ cases
@@ -221,8 +232,17 @@ NOPSAC = synth.Workload(name="g64-r0-m1", dtype="bf16", batch=1, heads=2, head_d
                         q_start=256, frame_tokens=64, n_centroids=5, group_size=64, rank=0, top_m=1, q_rank=4,
                         n_out=2, out_scale=20.0, n_hist=300, chunk=513, seed=9)
 
-SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC]
-FULL = ["mg2-12h", "lingbot-40h", "batched-4x30h", "rollout-30k", "rollout-120k"]
+# fp32 at d = 128 (the fp32 matrix-core instances of that width, r = 16), and
+# d = 128 with G = 16: eight groups per token, so two zero-point bytes
+F32D128 = synth.Workload(name="f32-d128", dtype="f32", batch=1, heads=2, head_dim=128, n_cache=640, n_q=200,
+                         q_start=440, frame_tokens=40, n_centroids=16, group_size=32, rank=16, top_m=4, q_rank=8,
+                         n_out=4, out_scale=10.0, n_hist=400, chunk=320, seed=12)
+D128G16 = synth.Workload(name="d128-g16", dtype="bf16", batch=1, heads=3, head_dim=128, n_cache=650, n_q=190,
+                         q_start=460, frame_tokens=38, n_centroids=20, group_size=16, rank=12, top_m=4, q_rank=8,
+                         n_out=4, out_scale=10.0, n_hist=400, chunk=325, seed=13)
+
+SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC, F32D128, D128G16]
+FULL = ["mg2-12h", "lingbot-40h", "batched-4x30h", "rollout-30k", "rollout-60k", "rollout-120k"]
 
 # App. D.1 storage options: 8-bit group scales (I8), the retention gate, both.
 # D64 has r = 20 over a 32-rank stride (the unaligned coefficient load), RAGGED
@@ -232,7 +252,9 @@ STORAGE = [synth.scaled(synth.WORKLOADS["tiny-f32"], name="tiny-f32-i8", storage
            synth.scaled(RAGGED, name="ragged-i8-gate", storage=_I8 | _GATE),
            synth.scaled(D64, name="d64-i8", storage=_I8),
            synth.scaled(D64, name="d64-gate", storage=_GATE),
-           synth.scaled(NOPSAC, name="g64-r0-i8-gate", storage=_I8 | _GATE)]
+           synth.scaled(NOPSAC, name="g64-r0-i8-gate", storage=_I8 | _GATE),
+           synth.scaled(D128G16, name="d128-g16-i8-gate", storage=_I8 | _GATE),
+           synth.scaled(F32D128, name="f32-d128-i8", storage=_I8)]
 
 # The full quadratic QSAC metric (the diagonal-approximation ablation of App. C):
 # fp32 d = 64, bf16 with batch 2 and ragged tiles, M = 8 over a small Kc, and
@@ -284,8 +306,9 @@ def run_case(wl, max_sources, n_heads_rows, row_step, logits_rows):
         _say(f"[ok] attend{' split' if split else ''} {wl.name}: max-abs {mx:.3g} mean-abs {mean:.3g} "
              f"over {len(rows)} rows")
     if logits_rows:
-        worst = check_logits(case, cfg, calib, ora_full, q_full, logits_rows)
-        _say(f"[ok] logits {wl.name}: worst relative error {worst:.3g}")
+        starts = [0] if logits_rows >= wl.n_q else frame_row_starts(wl, logits_rows)
+        worst = max(check_logits(case, cfg, calib, ora_full, q_full, logits_rows, first) for first in starts)
+        _say(f"[ok] logits {wl.name}: worst relative error {worst:.3g} (rows from {starts})")
 
 
 @pytest.mark.parametrize("wl", SMALL, ids=[w.name for w in SMALL])
