@@ -12,7 +12,8 @@
  * Conventions for every entry point:
  *  - Pointers named *device* point to GPU memory that the caller allocated and
  *    owns. The library never allocates device memory and keeps no state between
- *    calls, except the per-thread message behind quantwm_last_error().
+ *    calls, except the per-thread message behind quantwm_last_error() and the
+ *    static device buffer of quantwm_attend_noalloc (held per device).
  *  - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued
  *    asynchronously on it; outputs are valid once the stream has reached that
  *    point. Calls that touch the same buffers must be ordered on one stream.
@@ -282,6 +283,28 @@ quantwm_status quantwm_attend_epochs(const quantwm_config* cfg, const void* cali
 size_t quantwm_attend_epochs_workspace_bytes(const quantwm_config* cfg, int32_t n_epochs,
                                              const int64_t* epoch_start, int64_t n_cache, int64_t n_act,
                                              int64_t n_q);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): quantwm_attend with
+ * no workspace argument. Where quantwm_attend would split the key range
+ * (launches of fewer than two workgroups per compute unit), the partial
+ * results go to a static device buffer of QWM_ATTEND_NOALLOC_SCRATCH_BYTES that
+ * the library holds on each device it runs on until the process ends; the
+ * split count is cut to what the buffer holds. The call allocates nothing
+ * (its first call on a device only looks up that device's buffer address).
+ * Arguments, layouts and results are those of quantwm_attend (equal up to fp32
+ * rounding order; bit-equal when the split count is the same). Calls on one
+ * device share the buffer: calls that overlap in time on one device (different
+ * streams, or host threads) race and give undefined results; calls ordered on
+ * one stream are safe. Nothing in the buffer needs clearing between calls.
+ * QWM_ERR_CAPACITY when even a two-way split does not fit (B*H*n_q*(d + 2)*8
+ * bytes above the buffer); quantwm_attend with a caller workspace takes such
+ * sizes. On a 256-CU device the split rule never asks for that: a launch large
+ * enough to need it has two workgroups per CU and does not split. */
+#define QWM_ATTEND_NOALLOC_SCRATCH_BYTES (128u << 20)
+quantwm_status quantwm_attend_noalloc(const quantwm_config* cfg, const void* calib, const void* cache,
+                                      int64_t n_cache, const void* q, int64_t n_q, int64_t q_start,
+                                      int32_t frame_tokens, void* out, float* lse_out, void* stream);
 
 /* Test hook: the scaled logits of quantwm_attend, [B,H,n_q,n_cache] f32,
  * -inf where masked. Same tile code as quantwm_attend. Query i is chunk row

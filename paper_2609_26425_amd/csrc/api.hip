@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -439,6 +440,33 @@ quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void
   return ok();
 }
 
+// Scratch of quantwm_attend_noalloc: the partial-result planes of its key
+// split. Each device holds its own copy while the library is loaded. Host code
+// never passes the array's name to a kernel (on the host it is only a
+// stand-in): it takes the device address from hipGetSymbolAddress, once per
+// device, and uses that.
+static __device__ __align__(256) unsigned char scratch[QWM_ATTEND_NOALLOC_SCRATCH_BYTES];
+
+static constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices];
+
+static quantwm_status noalloc_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(QWM_ERR_UNSUPPORTED, "device %d above the %d the library tracks", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "scratch address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return QWM_OK;
+}
+
 // Compute units of the current device (256 on MI355X; 256 when no device answers,
 // so that sizes agree between a host-only query and the launch).
 static int device_cus() {
@@ -536,12 +564,13 @@ size_t quantwm_attend_active_workspace_bytes(const quantwm_config* cfg, int64_t 
   return two > split ? two : split;
 }
 
+// split_cap > 0 limits the key split of the plain form to that many parts.
 static quantwm_status attend_common(const quantwm_config* cfg, const void* calib, int32_t n_epochs,
                                     const int64_t* epoch_start, const void* cache, int64_t n_cache,
                                     const void* k_act, const void* v_act, int64_t n_act, const void* q, int64_t n_q,
                                     int64_t q_start, int32_t frame_tokens, void* out, float* lse_out,
                                     float* logits_out, void* workspace, size_t workspace_bytes, void* stream,
-                                    int64_t q_first = 0) {
+                                    int split_cap = 0, int64_t q_first = 0) {
   QWM_TRY(check_cfg(cfg));
   if (n_epochs < 1 || n_epochs > qwm::kMaxEpochs) return fail(QWM_ERR_UNSUPPORTED, "n_epochs must be in [1, 64]");
   if ((cfg->storage & QWM_STORE_SCALE_I8) && n_act > 0)
@@ -600,7 +629,11 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   if (!logits_out && workspace) {
     if (reinterpret_cast<uintptr_t>(workspace) & 255) return fail(QWM_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
     int ns = 1;
-    const size_t need = attend_split_bytes(cfg, n_cache + n_act, n_q, &ns);
+    size_t need = attend_split_bytes(cfg, n_cache + n_act, n_q, &ns);
+    if (split_cap > 0 && ns > split_cap) {
+      ns = split_cap;
+      need = planes_bytes(cfg, ns, n_q);
+    }
     if (ns > 1 && workspace_bytes >= need) {
       const size_t rows = size_t(ns) * cfg->batch * cfg->heads * size_t(n_q);
       a.n_split = ns;
@@ -755,6 +788,29 @@ quantwm_status quantwm_attend_epochs(const quantwm_config* cfg, const void* cali
                        frame_tokens, out, lse_out, nullptr, workspace, workspace_bytes, stream);
 }
 
+quantwm_status quantwm_attend_noalloc(const quantwm_config* cfg, const void* calib, const void* cache,
+                                      int64_t n_cache, const void* q, int64_t n_q, int64_t q_start,
+                                      int32_t frame_tokens, void* out, float* lse_out, void* stream) {
+  QWM_TRY(check_cfg(cfg));
+  if (n_cache < 0 || n_q < 0) return fail(QWM_ERR_INVALID_ARG, "sizes must be >= 0");
+  // the key split quantwm_attend would take, cut to what the static buffer holds
+  int ns = 1;
+  if (n_q > 0) (void)attend_split_bytes(cfg, n_cache, n_q, &ns);
+  void* scratch = nullptr;
+  if (ns > 1) {
+    while (ns > 1 && planes_bytes(cfg, ns, n_q) > QWM_ATTEND_NOALLOC_SCRATCH_BYTES) --ns;
+    if (ns < 2)
+      return fail(QWM_ERR_CAPACITY,
+                  "the key split of this call needs %zu bytes of scratch for two parts; the static buffer of "
+                  "quantwm_attend_noalloc holds %zu (quantwm_attend with a workspace takes any size)",
+                  planes_bytes(cfg, 2, n_q), size_t(QWM_ATTEND_NOALLOC_SCRATCH_BYTES));
+    QWM_TRY(noalloc_scratch(&scratch));
+  }
+  return attend_common(cfg, calib, 1, nullptr, cache, n_cache, nullptr, nullptr, 0, q, n_q, q_start, frame_tokens,
+                       out, lse_out, nullptr, scratch, scratch ? size_t(QWM_ATTEND_NOALLOC_SCRATCH_BYTES) : 0, stream,
+                       ns);
+}
+
 quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,
                               const void* q, int64_t n_q, int64_t q_start, int64_t q_first, int32_t frame_tokens,
                               float* logits_out, void* stream) {
@@ -762,7 +818,7 @@ quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, cons
   if (q_first < 0 || q_first > kMaxPositions - (n_q > 0 ? n_q : 0))
     return fail(QWM_ERR_INVALID_ARG, "need 0 <= q_first and q_first + n_q <= %lld", (long long)kMaxPositions);
   return attend_common(cfg, calib, 1, nullptr, cache, n_cache, nullptr, nullptr, 0, q, n_q, q_start, frame_tokens,
-                       nullptr, nullptr, logits_out, nullptr, 0, stream, q_first);
+                       nullptr, nullptr, logits_out, nullptr, 0, stream, 0, q_first);
 }
 
 }  // extern "C"

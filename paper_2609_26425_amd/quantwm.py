@@ -66,7 +66,8 @@ def _load():
         "quantwm_attend_active": (I32, [C, P, P, I64, P, P, I64, P, I64, I64, I32, P, P, P, SZ, P]),
         "quantwm_attend_epochs": (I32, [C, P, I32, ctypes.POINTER(I64), P, I64, P, P, I64, P, I64, I64, I32, P, P,
                                         P, SZ, P]),
-        "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I64, I32, P, P]),
+        "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I32, P, P]),
+        "quantwm_attend_noalloc": (I32, [C, P, P, I64, P, I64, I64, I32, P, P, P]),
         "quantwm_attend_active_workspace_bytes": (SZ, [C, I64, I64, I64]),
         "quantwm_attend_epochs_workspace_bytes": (SZ, [C, I32, ctypes.POINTER(I64), I64, I64, I64]),
         "quantwm_coef_record_max_bytes": (SZ, [C, I64]),
@@ -86,7 +87,7 @@ EXPORTED = ("quantwm_cache_bytes", "quantwm_token_bytes", "quantwm_calib_bytes",
             "quantwm_calibrate_workspace_bytes", "quantwm_calib_pack", "quantwm_calibrate", "quantwm_stats_bytes",
             "quantwm_stats_update", "quantwm_calibrate_epoch",
             "quantwm_append", "quantwm_attend_workspace_bytes", "quantwm_attend", "quantwm_attend_active",
-            "quantwm_attend_epochs",
+            "quantwm_attend_epochs", "quantwm_attend_noalloc",
             "quantwm_logits", "quantwm_attend_active_workspace_bytes", "quantwm_attend_epochs_workspace_bytes", "quantwm_coef_record_max_bytes", "quantwm_coef_pack", "quantwm_coef_unpack",
             "quantwm_last_error")
 
@@ -236,6 +237,15 @@ def quantwm_attend_epochs_workspace_bytes(cfg, epoch_start, n_cache, n_act, n_q)
     starts = (ctypes.c_int64 * len(epoch_start))(*[int(x) for x in epoch_start])
     return int(_lib.quantwm_attend_epochs_workspace_bytes(ctypes.byref(cfg), len(epoch_start), starts, n_cache,
                                                           n_act, n_q))
+
+
+ATTEND_NOALLOC_SCRATCH_BYTES = 128 << 20  # QWM_ATTEND_NOALLOC_SCRATCH_BYTES
+
+
+def quantwm_attend_noalloc(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, out, lse_out=None,
+                           stream=None):
+    _check(_lib.quantwm_attend_noalloc(ctypes.byref(cfg), _ptr(calib), _ptr(cache), n_cache, _ptr(q), n_q, q_start,
+                                       frame_tokens, _ptr(out), _ptr(lse_out), _stream(stream)))
 
 
 def quantwm_logits(cfg, calib, cache, n_cache, q, n_q, q_start, frame_tokens, logits_out, stream=None, q_first=0):
