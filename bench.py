@@ -12,8 +12,12 @@ does identical work) and then attends.
 Prints one JSON line. `value` is cache tokens/s of the whole step
 (B * H * n_cache per step); the line also carries the per-kernel times, append
 GB/s, the roofline of the dominant kernel (attend, bf16 matrix cores) measured
-with HIP events on the launch stream, and the CPU oracle timed on a bounded
-sample on this host.
+with HIP events on the launch stream, the streaming forms (active chunk,
+calibration epochs), one record per other configuration under "workloads"
+(tiny fp32, Matrix-Game-like, batched, and the long rollout at 30k, 60k and
+120k cached tokens: the same step, timed the same way, on 4 synthetic source
+heads repeated over the launch), and the CPU oracle timed on a bounded sample
+on this host.
 """
 from __future__ import annotations
 
@@ -34,6 +38,7 @@ import synth  # noqa: E402
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix peak
 PEAK_FP32_VALU_TFLOPS = 78.6  # fp32 FMA on the vector ALUs without packed FP32
 PEAK_HBM_GBPS = 8000.0
+PEAK_FP32_MFMA_TFLOPS = 157.3  # fp32 matrix peak (the tiny fp32 workload)
 
 
 def visible_pairs(wl: synth.Workload) -> int:
@@ -65,13 +70,24 @@ def append_flops(wl, n_new) -> float:
     return wl.batch * wl.heads * n_new * (4 * wl.n_centroids * d + 2 * d * wl.rank + 28 * d)
 
 
+# the device-code sources of each kernel (their digest dates a counter summary)
+KERNEL_SOURCES = {"attend": ["attend.hip", "attend_shape.h", "qwm_common.h"],
+                  "append": ["append.hip", "qwm_common.h"]}
+
+
+def source_digest(kernel: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        h.update(open(os.path.join(ROOT, "paper_2609_26425_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
 def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch of `kernel` from the committed counter summary of this
-    workload, or None when there is none or the kernel source has changed since
-    the counters were taken (the summary records the source's SHA-256)."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", f"attend_append_{workload}_traffic.md")
-    src = os.path.join(ROOT, "paper_2609_26425_amd", "csrc", f"{kernel}.hip")
+    workload, or None when there is none or the kernel sources have changed
+    since the counters were taken (the summary records their SHA-256)."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -79,10 +95,19 @@ def measured_traffic(kernel: str, workload: str):
         if ":" in line and line.split(":")[0].strip().startswith(kernel + "_"):
             k, v = line.split(":", 1)
             fields[k.strip()] = v.strip()
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if fields.get(f"{kernel}_source_sha256") != digest or f"{kernel}_traffic_bytes_per_launch" not in fields:
+    if fields.get(f"{kernel}_source_sha256") != source_digest(kernel) or \
+            f"{kernel}_traffic_bytes_per_launch" not in fields:
         return None
     return int(fields[f"{kernel}_traffic_bytes_per_launch"])
+
+
+def attend_bytes(wl) -> float:
+    """Algorithmic HBM bytes of one attention launch: the packed cache read once,
+    the Queries read, the outputs and lse written."""
+    kb, vb = token_bytes(wl)
+    e = 2 if wl.dtype == "bf16" else 4
+    bh = wl.batch * wl.heads
+    return bh * (wl.n_cache * (kb + vb) + wl.n_q * wl.head_dim * 2 * e + wl.n_q * 4)
 
 
 def cpu_baseline(wl):
@@ -166,6 +191,136 @@ def cpu_baseline(wl):
             "append_s_est": t_app, "attend_s_est": t_att, "single_thread": single}
 
 
+def replicated_inputs(wl, what, n, sources):
+    """[B, n, H, d] float32 where head (b, h) carries synthetic head sources[(b H + h)
+    % S]: the generator's own heads, S of them, repeated over the launch (the
+    timing does not depend on which head's values a head holds)."""
+    fn = {"k": synth.keys_head, "v": synth.values_head,
+          "q": lambda w, b, h, m: synth.queries_head(w, b, h, m, False),
+          "qhist": lambda w, b, h, m: synth.queries_head(w, b, h, m, True)}[what]
+    src = [synth.round_to(fn(wl, b, h, n), wl.dtype) for (b, h) in sources]
+    out = np.empty((wl.batch, n, wl.heads, wl.head_dim), np.float32)
+    for bh in range(wl.batch * wl.heads):
+        b, h = divmod(bh, wl.heads)
+        out[b, :, h, :] = src[bh % len(sources)]
+    return out
+
+
+class Prepared:
+    """A workload's calibration block, rotated caches (prefilled by append) and
+    inputs, resident on the GPU."""
+
+    def __init__(self, wl, copies, n_sources=None):
+        import torch
+        from paper_2609_26425_amd import quantwm as qw
+        self.wl, self.qw, self.copies = wl, qw, copies
+        dev = "cuda:0"
+        dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+        self.cfg = cfg = qw.make_config(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank,
+                                        wl.top_m, wl.n_cache, wl.dtype)
+        if n_sources is None:
+            gen = lambda what, n: synth.tensor(wl, what, n)  # noqa: E731
+        else:
+            allh = [(b, h) for b in range(wl.batch) for h in range(wl.heads)]
+            srcs = allh[:n_sources]
+            gen = lambda what, n: replicated_inputs(wl, what, n, srcs)  # noqa: E731
+        k_all = torch.from_numpy(gen("k", wl.n_cache)).to(dev, dt)
+        v_all = torch.from_numpy(gen("v", wl.n_cache)).to(dev, dt)
+        qh = torch.from_numpy(gen("qhist", wl.n_hist)).to(dev, dt)
+        q = torch.from_numpy(gen("q", wl.n_q)).to(dev, dt)
+        self.calib = torch.zeros(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=dev)
+        nc = min(wl.chunk, wl.n_cache)
+        ws = torch.empty(qw.quantwm_calibrate_workspace_bytes(cfg, wl.n_hist, nc), dtype=torch.uint8, device=dev)
+        qw.quantwm_calibrate(cfg, qh, wl.n_hist, k_all[:, :nc].contiguous(), v_all[:, :nc].contiguous(), nc,
+                             wl.kmeans_iters, self.calib, ws)
+        del ws
+        self.n_new = n_new = nc
+        self.start = wl.n_cache - n_new
+        self.caches, self.k_new, self.v_new = [], [], []
+        for c in range(copies):
+            cache = torch.zeros(qw.quantwm_cache_bytes(cfg), dtype=torch.uint8, device=dev)
+            for s0, n in wl.chunks():
+                qw.quantwm_append(cfg, self.calib, cache, s0, k_all[:, s0:s0 + n].contiguous(),
+                                  v_all[:, s0:s0 + n].contiguous(), n)
+            self.caches.append(cache)
+            self.k_new.append(k_all[:, self.start:].contiguous().clone())
+            self.v_new.append(v_all[:, self.start:].contiguous().clone())
+        self.outs = [torch.empty_like(q) for _ in range(copies)]
+        self.qs = [q.clone() for _ in range(copies)]
+        self.lse = torch.empty((wl.batch, wl.heads, wl.n_q), dtype=torch.float32, device=dev)
+        self.ws_bytes = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q)
+        self.attend_ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev) if self.ws_bytes else None
+        del k_all, v_all
+        torch.cuda.synchronize()
+
+    def step(self, i, ev=None):
+        wl, qw, c = self.wl, self.qw, i % self.copies
+        if ev is not None:
+            ev[0].record()
+        qw.quantwm_append(self.cfg, self.calib, self.caches[c], self.start, self.k_new[c], self.v_new[c], self.n_new)
+        if ev is not None:
+            ev[1].record()
+        qw.quantwm_attend(self.cfg, self.calib, self.caches[c], wl.n_cache, self.qs[c], wl.n_q, wl.q_start,
+                          wl.frame_tokens, self.outs[c], self.lse, self.attend_ws)
+        if ev is not None:
+            ev[2].record()
+
+    def time(self, steps, warmup):
+        """(wall seconds of `steps` steps, append ms per step, attend ms per step),
+        the kernel times from HIP events on the launch stream."""
+        import torch
+        for i in range(warmup):
+            self.step(i)
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            self.step(i, evs[i])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        app = np.array([e[0].elapsed_time(e[1]) for e in evs])
+        att = np.array([e[1].elapsed_time(e[2]) for e in evs])
+        assert torch.isfinite(self.outs[0].float()).all(), "non-finite attention output"
+        return wall, app, att
+
+
+def kernel_record(wl, n_new, app_all, att_all, ws_bytes):
+    """Per-kernel figures of one workload: times, rates and roofline fractions.
+    ws_bytes: the attention workspace the launch took (its key-split planes)."""
+    app_ms, att_ms = float(app_all.mean()), float(att_all.mean())
+    bh = wl.batch * wl.heads
+    splits = max(1, round(ws_bytes / (bh * wl.n_q * (4 * wl.head_dim + 8)))) if ws_bytes else 1
+    fl = attend_flops(wl) / (att_ms * 1e-3) / 1e12
+    ab = attend_bytes(wl)
+    rec = {
+        "attend_ms": att_ms, "attend_ms_median_min": [float(np.median(att_all)), float(att_all.min())],
+        "append_ms": app_ms, "append_ms_median_min": [float(np.median(app_all)), float(app_all.min())],
+        "attend_cache_tokens_per_s": bh * wl.n_cache / (att_ms * 1e-3),
+        "attend_TFLOPs": fl, "attend_mfma_frac": fl / (PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS),
+        "attend_algorithmic_bytes": ab, "attend_GBps": ab / (att_ms * 1e-3) / 1e9,
+        "attend_key_splits": splits,
+        "append_tokens": bh * n_new,
+        "append_GBps": append_bytes(wl, n_new) / (app_ms * 1e-3) / 1e9,
+        "append_valu_frac": append_flops(wl, n_new) / (app_ms * 1e-3) / 1e12 / PEAK_FP32_VALU_TFLOPS,
+    }
+    rec["append_hbm_frac"] = rec["append_GBps"] / PEAK_HBM_GBPS
+    for k in ("attend", "append"):
+        t = measured_traffic(k, wl.name)
+        rec[f"{k}_traffic_bytes"] = t
+        if t is not None:
+            rec[f"{k}_traffic_GBps"] = t / ((att_ms if k == "attend" else app_ms) * 1e-3) / 1e9
+    return rec
+
+
+def workload_desc(wl, n_new):
+    return (f"{wl.name}: B={wl.batch} H={wl.heads} d={wl.head_dim} n_cache={wl.n_cache} n_q={wl.n_q} "
+            f"append={n_new} Kc={wl.n_centroids} G={wl.group_size} r={wl.rank} M={wl.top_m} F={wl.frame_tokens}")
+
+
+SUB_WORKLOADS = ["tiny-f32", "mg2-12h", "batched-4x30h", "rollout-30k", "rollout-60k", "rollout-120k"]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -176,6 +331,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-streaming", action="store_true",
                     help="skip the active-chunk and calibration-epoch timings (for kernel traces)")
+    ap.add_argument("--no-sub", action="store_true",
+                    help="skip the per-workload records of the other configurations (for kernel traces)")
+    ap.add_argument("--sub-steps", type=int, default=10)
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one plain 1 GiB device copy kernel (read 1 GiB, write 1 GiB) outside the timed "
                          "region, as the scale for FETCH_SIZE / WRITE_SIZE counter runs")
@@ -191,53 +349,9 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     dev = "cuda:0"
     torch.cuda.set_device(0)
-    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
-    cfg = qw.make_config(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank, wl.top_m,
-                         wl.n_cache, wl.dtype)
-    print(f"[bench] generating {wl.name} inputs", file=sys.stderr, flush=True)
-    k_all = torch.from_numpy(synth.tensor(wl, "k", wl.n_cache)).to(dev, dt)
-    v_all = torch.from_numpy(synth.tensor(wl, "v", wl.n_cache)).to(dev, dt)
-    qh = torch.from_numpy(synth.tensor(wl, "qhist", wl.n_hist)).to(dev, dt)
-    q = torch.from_numpy(synth.tensor(wl, "q", wl.n_q)).to(dev, dt)
-
-    print("[bench] calibrating", file=sys.stderr, flush=True)
-    calib = torch.zeros(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=dev)
-    ws = torch.empty(qw.quantwm_calibrate_workspace_bytes(cfg, wl.n_hist, wl.chunk), dtype=torch.uint8, device=dev)
-    qw.quantwm_calibrate(cfg, qh, wl.n_hist, k_all[:, :wl.chunk].contiguous(), v_all[:, :wl.chunk].contiguous(),
-                         wl.chunk, wl.kmeans_iters, calib, ws)
-    del ws
-
-    n_new = wl.chunk
-    start = wl.n_cache - n_new
-    caches, k_new, v_new = [], [], []
-    print("[bench] prefilling caches", file=sys.stderr, flush=True)
-    for c in range(args.copies):
-        cache = torch.zeros(qw.quantwm_cache_bytes(cfg), dtype=torch.uint8, device=dev)
-        for s0, n in wl.chunks():
-            qw.quantwm_append(cfg, calib, cache, s0, k_all[:, s0:s0 + n].contiguous(),
-                              v_all[:, s0:s0 + n].contiguous(), n)
-        caches.append(cache)
-        k_new.append(k_all[:, start:].contiguous().clone())
-        v_new.append(v_all[:, start:].contiguous().clone())
-    outs = [torch.empty_like(q) for _ in range(args.copies)]
-    qs = [q.clone() for _ in range(args.copies)]
-    lse = torch.empty((wl.batch, wl.heads, wl.n_q), dtype=torch.float32, device=dev)
-    ws_bytes = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q)
-    attend_ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
-    del k_all, v_all
-    torch.cuda.synchronize()
-
-    def step(i, ev=None):
-        c = i % args.copies
-        if ev is not None:
-            ev[0].record()
-        qw.quantwm_append(cfg, calib, caches[c], start, k_new[c], v_new[c], n_new)
-        if ev is not None:
-            ev[1].record()
-        qw.quantwm_attend(cfg, calib, caches[c], wl.n_cache, qs[c], wl.n_q, wl.q_start, wl.frame_tokens,
-                          outs[c], lse, attend_ws)
-        if ev is not None:
-            ev[2].record()
+    print(f"[bench] {wl.name}: inputs, calibration, prefill of {args.copies} caches", file=sys.stderr, flush=True)
+    P = Prepared(wl, args.copies)
+    cfg, calib, n_new = P.cfg, P.calib, P.n_new
 
     if args.copy_probe:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
@@ -246,76 +360,60 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(i, evs[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    app_all = np.array([e[0].elapsed_time(e[1]) for e in evs])
-    att_all = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    print(f"[bench] warmup {args.warmup}, timing {args.steps} steps", file=sys.stderr, flush=True)
+    wall, app_all, att_all = P.time(args.steps, args.warmup)
     app_ms, att_ms = float(app_all.mean()), float(att_all.mean())
     ms_step = wall * 1000.0 / args.steps
-    assert torch.isfinite(outs[0].float()).all(), "non-finite attention output"
 
     # the streaming forms, timed separately on the same inputs (skipped with
     # --no-streaming, so that a kernel trace holds the step's launches only: the
     # per-epoch and two-part forms launch the same plain attention kernel)
     act_ms = ep_ms = act_cfg = ep_cfg = None
     if not args.no_streaming:
-        # the streaming variant: the last chunk stays exact (BF16) beside the packed
-        # history of the rest, timed separately on the same inputs
-        n_pk = wl.n_cache - n_new
-        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        # the last chunk stays exact (BF16) beside the packed history of the rest;
         # with the two-part workspace: packed whole tiles through the plain kernel,
         # the rest through the general one, merged by log-sum-exp
+        n_pk = wl.n_cache - n_new
+        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         ws_act = qw.quantwm_attend_active_workspace_bytes(cfg, n_pk, n_new, wl.n_q)
         act_ws = torch.empty(ws_act, dtype=torch.uint8, device=dev) if ws_act else None
+
+        def active():
+            qw.quantwm_attend_active(cfg, calib, P.caches[0], n_pk, P.k_new[0], P.v_new[0], n_new, P.qs[0], wl.n_q,
+                                     wl.q_start, wl.frame_tokens, P.outs[0], P.lse, act_ws)
         for i in range(2):
-            qw.quantwm_attend_active(cfg, calib, caches[0], n_pk, k_new[0], v_new[0], n_new, qs[0], wl.n_q,
-                                     wl.q_start, wl.frame_tokens, outs[0], lse, act_ws)
+            active()
         ea.record()
         for i in range(5):
-            qw.quantwm_attend_active(cfg, calib, caches[0], n_pk, k_new[0], v_new[0], n_new, qs[0], wl.n_q,
-                                     wl.q_start, wl.frame_tokens, outs[0], lse, act_ws)
+            active()
         eb.record()
         torch.cuda.synchronize()
         act_ms = ea.elapsed_time(eb) / 5
 
         # calibration epochs: one per appended chunk (the timing does not depend on
-        # the tables' values, so every epoch reuses this calibration block)
+        # the tables' values, so every epoch reuses this calibration block); with
+        # the per-epoch workspace each epoch's keys go through the plain kernel
         starts = [s0 for s0, _ in wl.chunks()]
-        cb = qw.quantwm_calib_bytes(cfg)
         calibs = calib.repeat(len(starts))
-        # with the per-epoch workspace: each epoch's keys through the plain kernel,
-        # merged by log-sum-exp
         ws_ep = qw.quantwm_attend_epochs_workspace_bytes(cfg, starts, wl.n_cache, 0, wl.n_q)
-        ep_ws = torch.empty(ws_ep, dtype=torch.uint8, device=dev) if ws_ep else attend_ws
+        ep_ws = torch.empty(ws_ep, dtype=torch.uint8, device=dev) if ws_ep else P.attend_ws
+
+        def epochs():
+            qw.quantwm_attend_epochs(cfg, calibs, starts, P.caches[0], wl.n_cache, None, None, 0, P.qs[0], wl.n_q,
+                                     wl.q_start, wl.frame_tokens, P.outs[0], P.lse, ep_ws)
         for i in range(2):
-            qw.quantwm_attend_epochs(cfg, calibs, starts, caches[0], wl.n_cache, None, None, 0, qs[0], wl.n_q,
-                                     wl.q_start, wl.frame_tokens, outs[0], lse, ep_ws)
+            epochs()
         ea.record()
         for i in range(5):
-            qw.quantwm_attend_epochs(cfg, calibs, starts, caches[0], wl.n_cache, None, None, 0, qs[0], wl.n_q,
-                                     wl.q_start, wl.frame_tokens, outs[0], lse, ep_ws)
+            epochs()
         eb.record()
         torch.cuda.synchronize()
         ep_ms = ea.elapsed_time(eb) / 5
-        del calibs, cb, ep_ws
+        del calibs, ep_ws, act_ws
         act_cfg = f"{n_pk} packed + {n_new} exact BF16 keys, two-part workspace {ws_act} B"
         ep_cfg = f"{len(starts)} calibration epochs, one per {wl.chunk}-token chunk, per-epoch workspace {ws_ep} B"
 
-    flops = attend_flops(wl)
-    achieved = flops / (att_ms * 1e-3) / 1e12
-    app_bytes = append_bytes(wl, n_new)
-    app_gbps = app_bytes / (app_ms * 1e-3) / 1e9
-    app_tflops = append_flops(wl, n_new) / (app_ms * 1e-3) / 1e12
+    rec = kernel_record(wl, n_new, app_all, att_all, P.ws_bytes)
     bh = wl.batch * wl.heads
     line = {
         "metric": "cache tokens/s for quantwm_attend + append GB/s (fraction of MI355X roofline)",
@@ -325,28 +423,50 @@ def main():
         "ms_per_step": ms_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": wl.dtype, "data": "synthetic",
-        "config": {"workload": f"{wl.name}: B={wl.batch} H={wl.heads} d={wl.head_dim} n_cache={wl.n_cache} "
-                               f"n_q={wl.n_q} append={n_new} Kc={wl.n_centroids} G={wl.group_size} r={wl.rank} "
-                               f"M={wl.top_m} F={wl.frame_tokens}",
+        "config": {"workload": workload_desc(wl, n_new),
                    "global_batch": wl.batch, "seq_len": wl.n_cache, "parallelism": "single GPU"},
         "attend_ms": att_ms, "append_ms": app_ms,
-        "attend_ms_median_min": [float(np.median(att_all)), float(att_all.min())],
-        "append_ms_median_min": [float(np.median(app_all)), float(app_all.min())],
-        "attend_cache_tokens_per_s": bh * wl.n_cache / (att_ms * 1e-3),
-        "append_GBps": app_gbps,
-        "append_hbm_frac": app_gbps / PEAK_HBM_GBPS,
-        "append_valu_frac": app_tflops / PEAK_FP32_VALU_TFLOPS,
-        "roofline": {"kernel": "attend", "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": measured_traffic("attend", wl.name)},
-        "append_traffic": measured_traffic("append", wl.name),
+        "attend_ms_median_min": rec["attend_ms_median_min"],
+        "append_ms_median_min": rec["append_ms_median_min"],
+        "attend_cache_tokens_per_s": rec["attend_cache_tokens_per_s"],
+        "attend_GBps": rec["attend_GBps"],
+        "attend_key_splits": rec["attend_key_splits"],
+        "append_GBps": rec["append_GBps"],
+        "append_hbm_frac": rec["append_hbm_frac"],
+        "append_valu_frac": rec["append_valu_frac"],
+        "roofline": {"kernel": "attend", "bound": "mfma", "achieved": rec["attend_TFLOPs"], "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": rec["attend_TFLOPs"] / PEAK_BF16_TFLOPS,
+                     "traffic": rec["attend_traffic_bytes"]},
+        "append_traffic": rec["append_traffic_bytes"],
         "copies": args.copies,
-        "attend_workspace_bytes": ws_bytes,
+        "attend_workspace_bytes": P.ws_bytes,
         "attend_active_ms": act_ms,
         "attend_active_config": act_cfg,
         "attend_epochs_ms": ep_ms,
         "attend_epochs_config": ep_cfg,
     }
+    del P
+    torch.cuda.empty_cache()
+
+    # every other configuration: one append + one attend per step, as the
+    # headline, on 4 synthetic source heads repeated over the launch
+    if not args.no_sub:
+        subs = {}
+        for name in SUB_WORKLOADS:
+            if name == wl.name:
+                continue
+            w = synth.WORKLOADS[name]
+            print(f"[bench] sub-record {name}", file=sys.stderr, flush=True)
+            S = Prepared(w, args.copies, n_sources=4)
+            _, a_all, t_all = S.time(args.sub_steps, 3)
+            r = kernel_record(w, S.n_new, a_all, t_all, S.ws_bytes)
+            r["config"] = workload_desc(w, S.n_new)
+            r["attend_workspace_bytes"] = S.ws_bytes
+            r["data"] = "synthetic, 4 source heads repeated over the launch"
+            subs[name] = r
+            del S
+            torch.cuda.empty_cache()
+        line["workloads"] = subs
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(wl)

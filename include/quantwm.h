@@ -78,9 +78,10 @@ typedef struct {
  *   Query-weighted error approximated on the principal subspace,
  *   sum_k lam_k (C_k - code_k * cscale)^2 < sum_k lam_k C_k^2 (fp32, ranks in
  *   order, lam from the calibration block); otherwise the row and its scale are
- *   stored as zeros. With SCALE_I8, quantwm_attend_active takes no active
- *   chunk, and quantwm_attend_epochs over several epochs needs the per-epoch
- *   workspace and no active chunk (QWM_ERR_UNSUPPORTED otherwise). */
+ *   stored as zeros.
+ * Every attention call decodes both options, in every form (plain, key split,
+ * active chunk in one launch or two parts, calibration epochs in one launch or
+ * per epoch). */
 #define QWM_STORE_SCALE_I8 1
 #define QWM_STORE_GATE 2
 
@@ -249,8 +250,7 @@ quantwm_status quantwm_attend_active(const quantwm_config* cfg, const void* cali
 /* Workspace bytes for quantwm_attend_active: the larger of the two-part form's
  * (two or more fp32 partial planes; none without an active chunk or with fewer
  * than 64 packed keys) and the split workspace of
- * quantwm_attend_workspace_bytes(cfg, n_cache + n_act, n_q). 0 with
- * QWM_STORE_SCALE_I8. */
+ * quantwm_attend_workspace_bytes(cfg, n_cache + n_act, n_q). */
 size_t quantwm_attend_active_workspace_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_act,
                                              int64_t n_q);
 
@@ -270,7 +270,7 @@ quantwm_status quantwm_attend_epochs(const quantwm_config* cfg, const void* cali
                                      float* lse_out, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Workspace bytes for the per-epoch form of quantwm_attend_epochs (n_epochs >=
- * 2; 0 otherwise, and 0 with QWM_STORE_SCALE_I8 and an active chunk): each
+ * 2; 0 otherwise): each
  * epoch's packed keys run through the plain attention kernel with that epoch's
  * calibration block as partial results of their own; with an active chunk, the
  * last whole packed tile on runs through the general kernel; everything merges
@@ -278,8 +278,7 @@ quantwm_status quantwm_attend_epochs(const quantwm_config* cfg, const void* cali
  * this much (256-byte aligned) the call takes that form; otherwise the
  * one-launch form, with the split workspace of
  * quantwm_attend_workspace_bytes(cfg, n_cache + n_act, n_q). Both give the same
- * result up to fp32 rounding order. Under QWM_STORE_SCALE_I8 only the per-epoch
- * form is available. */
+ * result up to fp32 rounding order. */
 size_t quantwm_attend_epochs_workspace_bytes(const quantwm_config* cfg, int32_t n_epochs,
                                              const int64_t* epoch_start, int64_t n_cache, int64_t n_act,
                                              int64_t n_q);

@@ -548,7 +548,6 @@ size_t quantwm_attend_epochs_workspace_bytes(const quantwm_config* cfg, int32_t 
                                              int64_t n_cache, int64_t n_act, int64_t n_q) {
   if (check_cfg(cfg) != QWM_OK || n_cache < 0 || n_act < 0 || n_q <= 0) return 0;
   if (n_epochs < 2 || n_epochs > qwm::kMaxEpochs || !epoch_start) return 0;
-  if ((cfg->storage & QWM_STORE_SCALE_I8) && n_act > 0) return 0;
   const EpochPlan p = plan_epochs(cfg, n_epochs, epoch_start, n_cache, n_act, n_q);
   const size_t per = planes_bytes(cfg, p.planes, n_q);
   const size_t split = attend_split_bytes(cfg, n_cache + n_act, n_q, nullptr);
@@ -558,7 +557,6 @@ size_t quantwm_attend_epochs_workspace_bytes(const quantwm_config* cfg, int32_t 
 size_t quantwm_attend_active_workspace_bytes(const quantwm_config* cfg, int64_t n_cache, int64_t n_act,
                                              int64_t n_q) {
   if (check_cfg(cfg) != QWM_OK || n_cache < 0 || n_act < 0 || n_q <= 0) return 0;
-  if (cfg->storage & QWM_STORE_SCALE_I8) return 0;
   const size_t two = active_two_part_bytes(cfg, n_cache, n_act, n_q, nullptr);
   const size_t split = attend_split_bytes(cfg, n_cache + n_act, n_q, nullptr);
   return two > split ? two : split;
@@ -573,8 +571,6 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
                                     int split_cap = 0, int64_t q_first = 0) {
   QWM_TRY(check_cfg(cfg));
   if (n_epochs < 1 || n_epochs > qwm::kMaxEpochs) return fail(QWM_ERR_UNSUPPORTED, "n_epochs must be in [1, 64]");
-  if ((cfg->storage & QWM_STORE_SCALE_I8) && n_act > 0)
-    return fail(QWM_ERR_UNSUPPORTED, "8-bit group scales are not taken with an active chunk");
   if (n_epochs > 1) {
     if (!epoch_start) return fail(QWM_ERR_INVALID_ARG, "epoch_start is null");
     if (epoch_start[0] != 0) return fail(QWM_ERR_INVALID_ARG, "epoch_start[0] must be 0");
@@ -649,15 +645,6 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   hipStream_t s = static_cast<hipStream_t>(stream);
   // calibration epochs one by one through the plain kernel when the workspace
   // holds a partial plane per launch
-  const bool si8_epochs = (cfg->storage & QWM_STORE_SCALE_I8) && n_epochs > 1;
-  if (si8_epochs) {
-    // only the per-epoch form, whose launches are all plain, decodes 8-bit scales
-    const EpochPlan p = plan_epochs(cfg, n_epochs, epoch_start, n_cache, n_act, n_q);
-    if (logits_out || !workspace || p.planes == 0 || workspace_bytes < planes_bytes(cfg, p.planes, n_q))
-      return fail(QWM_ERR_UNSUPPORTED,
-                  "8-bit group scales over calibration epochs need the per-epoch workspace "
-                  "(quantwm_attend_epochs_workspace_bytes)");
-  }
   if (!logits_out && workspace && n_epochs > 1) {
     const EpochPlan p = plan_epochs(cfg, n_epochs, epoch_start, n_cache, n_act, n_q);
     const size_t need = planes_bytes(cfg, p.planes, n_q);

@@ -1013,16 +1013,19 @@ hipError_t launch_attend_rp(const AttendArgs& a, int batch, bool logits, hipStre
   const size_t lds = attend_lds_bytes_t<T, D>(a.rank, a.n_centroids, tab);
   if (lds > kLdsLimit) return hipErrorInvalidValue;
   const bool si8 = a.L.i8 != 0;
-  if (si8 && (a.n_act > 0 || a.n_epochs > 1)) return hipErrorNotSupported;
   if (logits) {
     if (si8)
       return tab ? launch_k<T, D, RP, true, true, false, true>(a, grid, lds, s)
                  : launch_k<T, D, RP, true, false, false, true>(a, grid, lds, s);
     return tab ? launch_k<T, D, RP, true, true>(a, grid, lds, s) : launch_k<T, D, RP, true, false>(a, grid, lds, s);
   }
-  if (a.n_act > 0 || a.n_epochs > 1)
+  if (a.n_act > 0 || a.n_epochs > 1) {
+    if (si8)
+      return tab ? launch_k<T, D, RP, false, true, true, true>(a, grid, lds, s)
+                 : launch_k<T, D, RP, false, false, true, true>(a, grid, lds, s);
     return tab ? launch_k<T, D, RP, false, true, true>(a, grid, lds, s)
                : launch_k<T, D, RP, false, false, true>(a, grid, lds, s);
+  }
   if (si8)
     return tab ? launch_k<T, D, RP, false, true, false, true>(a, grid, lds, s)
                : launch_k<T, D, RP, false, false, false, true>(a, grid, lds, s);

@@ -105,11 +105,12 @@ def test_validation_without_a_gpu():
     with pytest.raises(qw.QuantwmError) as e:
         qw.quantwm_token_bytes(qw.make_config(1, 2, 128, 16, 32, 8, 4, 100, "bf16", 4))
     assert e.value.status == qw.ERR_INVALID_ARG
-    # 8-bit group scales are not taken by the streaming attention forms
+    # 8-bit group scales are taken by the streaming forms: the checks that fire
+    # are those of any config (here the null calibration block)
     i8 = qw.make_config(1, 2, 128, 16, 32, 8, 4, 100, "bf16", qw.STORE_SCALE_I8)
     with pytest.raises(qw.QuantwmError) as e:
         qw.quantwm_attend_active(i8, None, None, 50, None, None, 10, None, 4, 55, 1, None)
-    assert e.value.status == qw.ERR_UNSUPPORTED
+    assert e.value.status == qw.ERR_INVALID_ARG and "calib" in qw.quantwm_last_error()
     # checks that fire before any device work
     with pytest.raises(qw.QuantwmError) as e:
         qw._check(qw.library().quantwm_append(ctypes.byref(good), None, None, 90, None, None, 20, None, None))
@@ -152,8 +153,8 @@ def test_streaming_workspace_sizes():
     assert qw.quantwm_attend_epochs_workspace_bytes(ling, [0], 32760, 0, 4680) == 0
     i8 = qw.make_config(1, 40, 128, 128, 32, 16, 4, 32760, "bf16", qw.STORE_SCALE_I8)
     assert qw.quantwm_attend_epochs_workspace_bytes(i8, starts, 32760, 0, 4680) == planes(7)
-    assert qw.quantwm_attend_epochs_workspace_bytes(i8, starts[:6], 28080, 4680, 4680) == 0
-    assert qw.quantwm_attend_active_workspace_bytes(i8, 28080, 4680, 4680) == 0
+    assert qw.quantwm_attend_epochs_workspace_bytes(i8, starts[:6], 28080, 4680, 4680) == planes(7)
+    assert qw.quantwm_attend_active_workspace_bytes(i8, 28080, 4680, 4680) == planes(2)
 
 
 def test_attend_workspace_sizes():

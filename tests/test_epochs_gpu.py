@@ -106,14 +106,7 @@ def _run_epochs(wl, starts, n_act, rows, seed_hist=300):
                                     v_act=np.ascontiguousarray(v[:, n_pk:]) if n_act else None,
                                     epochs=list(zip(starts, tables)))
     tol = 2e-2 if wl.dtype == "bf16" else 1e-4
-    i8 = bool(wl.storage & oracle.STORE_SCALE_I8)
-    if i8:
-        # 8-bit group scales: only the per-epoch form (plain kernel launches) decodes them
-        with pytest.raises(qw.QuantwmError) as e:
-            qw.quantwm_attend_epochs(cfg, calibs, list(starts), cache, n_pk, ka, va, n_act, qd, wl.n_q,
-                                     wl.q_start, wl.frame_tokens, torch.empty_like(qd))
-        assert e.value.status == qw.ERR_UNSUPPORTED and "per-epoch" in qw.quantwm_last_error()
-    for mode in (("per-epoch",) if i8 else ("none", "split", "per-epoch")):
+    for mode in ("none", "split", "per-epoch"):
         nb = {"none": 0, "split": qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q),
               "per-epoch": qw.quantwm_attend_epochs_workspace_bytes(cfg, list(starts), n_pk, n_act, wl.n_q)}[mode]
         if mode != "none" and nb == 0:
@@ -154,7 +147,9 @@ TINY_EPOCH = synth.scaled(synth.WORKLOADS["tiny-f32"], name="epochs-tiny", seed=
     (SMALL_EPOCH, [0, 333, 640], 150),    # a tile-aligned boundary, then an exact active chunk
     (TINY_EPOCH, [0, 100, 500], 0),       # fp32 path
     (synth.scaled(SMALL_EPOCH, name="epochs-small-i8", storage=1), [0, 333, 700], 0),  # 8-bit group scales
-], ids=["bf16-3epochs", "bf16-active", "f32", "bf16-i8"])
+    (synth.scaled(SMALL_EPOCH, name="epochs-small-i8-act", storage=3), [0, 333, 640], 150),  # and an active chunk
+    (synth.scaled(TINY_EPOCH, name="epochs-tiny-i8", storage=1), [0, 100, 500], 0),  # fp32 with 8-bit scales
+], ids=["bf16-3epochs", "bf16-active", "f32", "bf16-i8", "bf16-i8-gate-active", "f32-i8"])
 def test_epoch_attention_small(wl, starts, n_act):
     rows = np.array([(b, h, i) for b in range(wl.batch) for h in range(wl.heads) for i in range(wl.n_q)], np.int32)
     _run_epochs(wl, starts, n_act, rows)

@@ -546,7 +546,16 @@ def test_active_chunk_small(wl):
     _active_case(wl, 64, 64, 1)
 
 
+@pytest.mark.parametrize("wl", STORAGE, ids=[w.name for w in STORAGE])
+def test_active_chunk_storage(wl):
+    # App. D.1 storage options (8-bit group scales with their FP16 secondary
+    # scale, the retention gate) beside a BF16 active chunk, in every form
+    _active_case(wl, 64, 64, 1)
+
+
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("name", ["lingbot-40h", "rollout-30k"])
+@pytest.mark.parametrize("name", ["lingbot-40h", "rollout-30k", "lingbot-40h-i8"])
 def test_active_chunk_full(name):
-    _active_case(synth.WORKLOADS[name], 3, 6, 37)
+    wl = synth.scaled(synth.WORKLOADS["lingbot-40h"], name=name, storage=_I8) if name.endswith("-i8") \
+        else synth.WORKLOADS[name]
+    _active_case(wl, 3, 6, 37)
