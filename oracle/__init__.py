@@ -33,12 +33,13 @@ class OraCfg(ctypes.Structure):
                 ("n_centroids", ctypes.c_int), ("group_size", ctypes.c_int),
                 ("rank", ctypes.c_int), ("top_m", ctypes.c_int),
                 ("capacity", ctypes.c_longlong), ("table_bf16", ctypes.c_int), ("storage", ctypes.c_int),
-                ("metric", ctypes.c_int)]
+                ("metric", ctypes.c_int), ("coef_rows", ctypes.c_longlong), ("coef_stage", ctypes.c_longlong)]
 
 
 # App. D.1 storage options (ORA_STORE_* in quantwm_oracle.h)
 STORE_SCALE_I8 = 1
 STORE_GATE = 2
+STORE_SPARSE = 4
 # QSAC candidate metric (ORA_METRIC_*): Eq. 9 or the full quadratic form
 METRIC_DIAG = 0
 METRIC_FULL = 1
@@ -67,15 +68,16 @@ def lib():
 
 
 def cfg_of(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, bf16, storage=0,
-           metric=0) -> OraCfg:
+           metric=0, coef_rows=0, coef_stage=0) -> OraCfg:
     return OraCfg(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, int(bf16), int(storage),
-                  int(metric))
+                  int(metric), int(coef_rows), int(coef_stage))
 
 
 def cfg_from_workload(wl, capacity=None) -> OraCfg:
     return cfg_of(wl.batch, wl.heads, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank,
                   wl.top_m, wl.capacity if capacity is None else capacity, wl.dtype == "bf16",
-                  getattr(wl, "storage", 0), getattr(wl, "metric", 0))
+                  getattr(wl, "storage", 0), getattr(wl, "metric", 0), getattr(wl, "coef_rows", 0),
+                  getattr(wl, "coef_stage", 0) or getattr(wl, "chunk", 0))
 
 
 def _p(a, ct=ctypes.c_float):

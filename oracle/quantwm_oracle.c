@@ -89,6 +89,11 @@ typedef struct {
   long long k_codes, k_ids, k_zp, k_scale, k_coef, k_cscale;
   long long v_codes, v_ids, v_zp, v_scale;
   long long k_sigma, v_sigma; /* SCALE_I8: the FP16 secondary scale per token */
+  int sparse;                 /* SPARSE: rows in a pool with a tile directory */
+  long long pool;             /* rows per (b, h) in the coefficient sections */
+  long long k_dir, k_over;    /* SPARSE: directory and overflow counters */
+  long long stage;            /* SPARSE: staging rows per (b, h) */
+  long long k_st_codes, k_st_scale;
   long long total;
 } layout;
 
@@ -101,7 +106,8 @@ static int valid_cfg(const ora_cfg* c) {
   if (c->n_centroids < 1 || c->n_centroids > 256) return 0;
   if (c->rank < 0 || c->rank > c->head_dim) return 0;
   if (c->top_m < 1 || c->capacity < 0) return 0;
-  if (c->storage & ~(ORA_STORE_SCALE_I8 | ORA_STORE_GATE)) return 0;
+  if (c->storage & ~(ORA_STORE_SCALE_I8 | ORA_STORE_GATE | ORA_STORE_SPARSE)) return 0;
+  if ((c->storage & ORA_STORE_SPARSE) && (c->rank < 1 || c->coef_rows < 0 || c->coef_stage < 1)) return 0;
   if (c->metric != ORA_METRIC_DIAG && c->metric != ORA_METRIC_FULL) return 0;
   return 1;
 }
@@ -115,22 +121,31 @@ static layout make_layout(const ora_cfg* c) {
   L.slots = (c->capacity + 63) / 64 * 64;
   L.i8 = (c->storage & ORA_STORE_SCALE_I8) != 0;
   L.sb = L.i8 ? L.ng : 2 * L.ng;
+  L.sparse = (c->storage & ORA_STORE_SPARSE) != 0;
+  L.pool = L.sparse && c->coef_rows > 0 ? c->coef_rows : L.slots;
   long long bh = (long long)c->batch * c->heads, n = bh * L.slots, off = 0;
-#define SECTION(field, per_token) \
-  do { L.field = off; off = up256(off + n * (long long)(per_token)); } while (0)
+#define SECTION_N(field, rows, per_row) \
+  do { L.field = off; off = up256(off + (rows) * (long long)(per_row)); } while (0)
+#define SECTION(field, per_token) SECTION_N(field, n, per_token)
   SECTION(k_codes, L.d / 4);
   SECTION(k_ids, 1);
   SECTION(k_zp, L.zpb);
   SECTION(k_scale, L.sb);
-  SECTION(k_coef, L.r);
-  SECTION(k_cscale, L.r > 0 ? 2 : 0);
+  SECTION_N(k_coef, bh * L.pool, L.r);
+  SECTION_N(k_cscale, bh * L.pool, L.r > 0 ? 2 : 0);
   SECTION(v_codes, L.d / 4);
   SECTION(v_ids, 1);
   SECTION(v_zp, L.zpb);
   SECTION(v_scale, L.sb);
   SECTION(k_sigma, L.i8 ? 2 : 0);
   SECTION(v_sigma, L.i8 ? 2 : 0);
+  SECTION_N(k_dir, bh * (L.slots / 64), L.sparse ? 16 : 0);
+  SECTION_N(k_over, bh, L.sparse ? 4 : 0);
+  L.stage = L.sparse ? c->coef_stage : 0;
+  SECTION_N(k_st_codes, bh * L.stage, L.r);
+  SECTION_N(k_st_scale, bh * L.stage, 2);
 #undef SECTION
+#undef SECTION_N
   L.total = off;
   L.v_bytes = L.d / 4 + 1 + L.zpb + L.sb + (L.i8 ? 2 : 0);
   L.k_bytes = L.v_bytes + (L.r > 0 ? L.r + 2 : 0);
@@ -152,6 +167,82 @@ int ora_token_bytes(const ora_cfg* cfg, int* k_bytes, int* v_bytes) {
 
 static void put16(uint8_t* p, uint16_t v) { p[0] = (uint8_t)(v & 255); p[1] = (uint8_t)(v >> 8); }
 static uint16_t get16(const uint8_t* p) { return (uint16_t)(p[0] | (p[1] << 8)); }
+static void put32(uint8_t* p, uint32_t v) {
+  for (int i = 0; i < 4; ++i) p[i] = (uint8_t)(v >> (8 * i));
+}
+static uint32_t get32(const uint8_t* p) {
+  return (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16) | ((uint32_t)p[3] << 24);
+}
+static uint64_t get64(const uint8_t* p) { return (uint64_t)get32(p) | ((uint64_t)get32(p + 4) << 32); }
+static void put64(uint8_t* p, uint64_t v) { put32(p, (uint32_t)v); put32(p + 4, (uint32_t)(v >> 32)); }
+static int popcount64(uint64_t x) {
+  int c = 0;
+  for (; x; x &= x - 1) ++c;
+  return c;
+}
+
+/* ------------------------------------------- resident sparse PSAC rows */
+
+/* Directory entry of tile T of head bh: {u32 base, u32 0, u64 mask}. */
+static uint8_t* dir_entry(const layout* L, uint8_t* cache, long long bh, long long T) {
+  return cache + L->k_dir + (bh * (L->slots / 64) + T) * 16;
+}
+
+/* Pool rows used by the slots below `slot` of head bh (the rows are stored in
+ * slot order, so this is where the next row goes). */
+static long long pool_fill(const layout* L, const uint8_t* cache, long long bh, long long slot) {
+  if (slot == 0) return 0;
+  const long long T = (slot - 1) / 64;
+  const uint8_t* e = cache + L->k_dir + (bh * (L->slots / 64) + T) * 16;
+  const int used = (int)(slot - 64 * T); /* slots of tile T below `slot`: 1..64 */
+  const uint64_t below = used == 64 ? ~(uint64_t)0 : (((uint64_t)1 << used) - 1);
+  return (long long)get32(e) + popcount64(get64(e + 8) & below);
+}
+
+/* Pool row of slot t of head bh, or -1 when the slot has none. */
+static long long pool_row(const layout* L, const uint8_t* cache, long long bh, long long t) {
+  const uint8_t* e = cache + L->k_dir + (bh * (L->slots / 64) + t / 64) * 16;
+  const int i = (int)(t % 64);
+  const uint64_t mask = get64(e + 8);
+  if (!((mask >> i) & 1)) return -1;
+  return (long long)get32(e) + popcount64(mask & (((uint64_t)1 << i) - 1));
+}
+
+/* Stores one append call's rows of head bh, staged in the cache (for slots
+ * [n_cached, n_cached + n)), into the pool: the whole chunk (dense) or its
+ * non-zero-scale rows (sparse), whichever is smaller with one mask bit per slot
+ * as the sparse index (ties dense); then the directory of its tiles. */
+static void sparse_commit(const layout* L, uint8_t* cache, long long bh, long long n_cached, long long n) {
+  const int r = L->r;
+  const int8_t* codes = (const int8_t*)(cache + L->k_st_codes + bh * L->stage * r);
+  const uint8_t* sb = cache + L->k_st_scale + bh * L->stage * 2;
+  long long kept = 0;
+  for (long long t = 0; t < n; ++t) kept += get16(sb + 2 * t) != 0;
+  const int sparse = kept * (r + 2) + (n + 7) / 8 < n * (r + 2);
+  long long pos = pool_fill(L, cache, bh, n_cached), over = 0;
+  for (long long t = 0; t < n; ++t) {
+    const long long slot = n_cached + t, T = slot / 64;
+    const int i = (int)(slot % 64);
+    uint8_t* e = dir_entry(L, cache, bh, T);
+    if (i == 0 || t == 0) { /* entering tile T */
+      if (i == 0) {
+        put32(e, (uint32_t)pos);
+        put32(e + 4, 0);
+        put64(e + 8, 0);
+      } else { /* the chunk starts inside tile T: keep the rows below it */
+        put64(e + 8, get64(e + 8) & (((uint64_t)1 << i) - 1));
+      }
+    }
+    if (sparse && get16(sb + 2 * t) == 0) continue;
+    if (pos >= L->pool) { ++over; continue; }
+    memcpy(cache + L->k_coef + (bh * L->pool + pos) * r, codes + t * r, (size_t)r);
+    put16(cache + L->k_cscale + (bh * L->pool + pos) * 2, get16(sb + 2 * t));
+    put64(e + 8, get64(e + 8) | ((uint64_t)1 << i));
+    ++pos;
+  }
+  uint8_t* oc = cache + L->k_over + bh * 4;
+  put32(oc, get32(oc) + (uint32_t)over);
+}
 
 /* ----------------------------------------------------- INT2 residual (O3) */
 
@@ -549,6 +640,7 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
                float* coef_f32, int* k_ids, int* v_ids, int* cand) {
   if (!valid_cfg(cfg) || n_cached < 0 || n_new < 0) return -1;
   if (n_cached + n_new > cfg->capacity) return -3;
+  if ((cfg->storage & ORA_STORE_SPARSE) && n_new > cfg->coef_stage) return -3;
   if (n_new == 0) return 0;
   if (!mu_k || !mu_v || !w || !cache || !k_new || !v_new || (cfg->rank > 0 && !u_t)) return -1;
   const int gate = (cfg->storage & ORA_STORE_GATE) && cfg->rank > 0;
@@ -568,6 +660,9 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
     const float* uh = u_t + (long long)bh * r * d;
     float xhat[256];
     int cands[256];
+    /* SPARSE: the chunk's rows go to the staging rows, then sparse_commit */
+    int8_t* st_codes = L.sparse ? (int8_t*)(cache + L.k_st_codes + (long long)bh * L.stage * r) : NULL;
+    uint8_t* st_scale = L.sparse ? cache + L.k_st_scale + (long long)bh * L.stage * 2 : NULL;
     for (long long t = 0; t < n_new; ++t) {
       long long slot = (long long)bh * L.slots + n_cached + t;
       long long src = (((long long)b * n_new + t) * H + h) * d;
@@ -593,7 +688,7 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
           if (coef_f32) coef_f32[diag * r + kk] = Cf[kk];
         }
         /* INT8 row with one FP16 scale (App. D.1) */
-        int8_t* code = (int8_t*)(cache + L.k_coef + slot * r);
+        int8_t* code = L.sparse ? st_codes + t * r : (int8_t*)(cache + L.k_coef + slot * r);
         uint16_t sbits;
         ora_coef_row(Cf, r, code, &sbits);
         /* App. D.1 retention: a row that does not lower the error is zeroed */
@@ -601,7 +696,7 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
           memset(code, 0, (size_t)r);
           sbits = 0;
         }
-        put16(cache + L.k_cscale + slot * 2, sbits);
+        put16(L.sparse ? st_scale + 2 * t : cache + L.k_cscale + slot * 2, sbits);
       }
       /* Values: nearest centroid, same residual path, no PSAC */
       int zv = ora_nearest(v, muv, K, d);
@@ -611,6 +706,7 @@ int ora_append(const ora_cfg* cfg, const float* mu_k, const float* mu_v, const f
                      xhat);
       if (v_ids) v_ids[diag] = zv;
     }
+    if (L.sparse) sparse_commit(&L, cache, bh, n_cached, n_new);
   }
   return 0;
 }
@@ -631,15 +727,11 @@ static void load_residual(const layout* L, int G, const uint8_t* codes, const ui
 
 /* ------------------------------------------- per-chunk coefficient layout */
 
-static void put32(uint8_t* p, uint32_t v) {
-  for (int i = 0; i < 4; ++i) p[i] = (uint8_t)(v >> (8 * i));
-}
-static uint32_t get32(const uint8_t* p) {
-  return (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16) | ((uint32_t)p[3] << 24);
-}
 
+/* the chunk records read slot-addressed rows: not a SPARSE cache */
 static int coef_args_ok(const ora_cfg* cfg, long long start, long long n) {
-  return valid_cfg(cfg) && cfg->rank > 0 && start >= 0 && n >= 0 && n <= 65536 && start + n <= cfg->capacity;
+  return valid_cfg(cfg) && cfg->rank > 0 && !(cfg->storage & ORA_STORE_SPARSE) && start >= 0 && n >= 0 &&
+         n <= 65536 && start + n <= cfg->capacity;
 }
 
 /* kept rows (non-zero FP16 scale) of head bh in the chunk */
@@ -774,9 +866,19 @@ int ora_decode(const ora_cfg* cfg, const float* mu_k, const float* mu_v,
                     cache + L.v_scale + slot * L.sb, cache + L.v_sigma + slot * 2, mu_v + (bh * K + zv) * d,
                     v + t * d);
     if (chat && r > 0) {
-      float s = (float)ora_f16_value(get16(cache + L.k_cscale + slot * 2));
-      const int8_t* code = (const int8_t*)(cache + L.k_coef + slot * r);
-      for (int kk = 0; kk < r; ++kk) chat[t * r + kk] = (double)((float)code[kk] * s);
+      long long row = slot;
+      if (L.sparse) {
+        const long long pr = pool_row(&L, cache, bh, t);
+        if (pr >= L.pool) return -5; /* a directory pointing past the pool */
+        row = pr < 0 ? -1 : bh * L.pool + pr;
+      }
+      if (row < 0) {
+        for (int kk = 0; kk < r; ++kk) chat[t * r + kk] = 0.0;
+      } else {
+        float s = (float)ora_f16_value(get16(cache + L.k_cscale + row * 2));
+        const int8_t* code = (const int8_t*)(cache + L.k_coef + row * r);
+        for (int kk = 0; kk < r; ++kk) chat[t * r + kk] = (double)((float)code[kk] * s);
+      }
     }
   }
   return 0;

@@ -40,6 +40,8 @@ typedef struct {
   int table_bf16;              /* 1: centroids, U_r and attention operands are BF16 */
   int storage;                 /* ORA_STORE_* flags (App. D.1 packed-storage options) */
   int metric;                  /* ORA_METRIC_*: the distance of the QSAC candidate search */
+  long long coef_rows;         /* ORA_STORE_SPARSE: PSAC rows the pool of each (b, h) holds (0 = slots) */
+  long long coef_stage;        /* ORA_STORE_SPARSE: largest chunk (tokens) one append call takes */
 } ora_cfg;
 
 /* App. D.1 storage options. SCALE_I8: the group step sizes of a token-head are
@@ -50,6 +52,22 @@ typedef struct {
  * otherwise its codes and scale are zero. */
 #define ORA_STORE_SCALE_I8 1
 #define ORA_STORE_GATE 2
+/* SPARSE (needs rank >= 1): the PSAC rows live in a row pool per (b, h) with a
+ * directory per 64-slot tile, {u32 base, u32 0, u64 mask}: bit i of the mask
+ * says that slot 64 T + i has a row in the pool, at row base + (set bits below
+ * i). Rows are stored in slot order. Each append call (one chunk) stores, per
+ * (b, h), either every row of the chunk (dense) or only its rows with a
+ * non-zero scale (sparse), whichever is smaller counting one mask bit per slot
+ * as the sparse index: sparse iff kept (r + 2) + ceil(n / 8) < n (r + 2).
+ * A row past the pool's end is not stored (bit clear: no correction) and
+ * counted in the per-(b, h) u32 overflow counter. A slot without a row reads
+ * as a zero PSAC row. Sections: K coef and K cscale hold [B*H][coef_rows] rows;
+ * then, after the secondary scales, the directory [B*H][slots/64][16 B], the
+ * overflow counters [B*H] u32, and the staging rows of one append call,
+ * codes [B*H][coef_stage][r] and scales [B*H][coef_stage] (the chunk's rows
+ * are written there first; an append of more than coef_stage tokens is
+ * refused). */
+#define ORA_STORE_SPARSE 4
 
 /* QSAC candidate metric. DIAG: Eq. 9, the channel-weighted distance with w, the
  * diagonal of the normalised Query second moment. FULL: the full quadratic form

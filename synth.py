@@ -55,8 +55,10 @@ class Workload:
     chunk: int            # tokens per append call
     seed: int
     kmeans_iters: int = 10
-    storage: int = 0      # App. D.1 storage options: 1 = 8-bit group scales, 2 = retention gate
+    storage: int = 0      # App. D.1 storage options: 1 = 8-bit group scales, 2 = retention gate, 4 = sparse rows
     metric: int = 0       # QSAC candidate metric: 0 = Eq. 9 (diagonal), 1 = the full quadratic form
+    coef_rows: int = 0    # storage bit 2 (sparse PSAC rows): pool rows per head, 0 = one per slot
+    coef_stage: int = 0   # storage bit 2: staging rows per head (largest append chunk), 0 = the chunk size
 
     @property
     def capacity(self) -> int:

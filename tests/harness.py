@@ -71,7 +71,8 @@ def build_oracle_case(wl: synth.Workload, max_sources: int = 3, cold: bool = Fal
                               wl.kmeans_iters)
     cache = oracle.new_cache(cfg)
     diag = oracle.append(cfg, tables, cache, 0, k, v, diagnostics=True)
-    lay = packed.layout(1, S, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage)
+    lay = packed.layout(1, S, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage, wl.coef_rows,
+                         wl.coef_stage or wl.chunk)
     bh = wl.batch * wl.heads
     src_of = np.arange(bh) % S
     if S == bh:
@@ -102,7 +103,8 @@ def full_tables(case: OracleCase):
 
 def full_oracle_cache(case: OracleCase) -> np.ndarray:
     wl = case.wl
-    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage)
+    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage,
+                         wl.coef_rows, wl.coef_stage or wl.chunk)
     out = np.zeros(lay["total"], np.uint8)
     for bh in range(wl.batch * wl.heads):
         packed.copy_head(out, lay, bh, case.cache, case.lay, int(case.src_of[bh]), wl.n_cache)

@@ -1243,3 +1243,172 @@ def test_oracle_rejects_head_dim_above_256():
         oracle.calibrate(cfg, None, x, x, 1)
     ok = oracle.cfg_of(1, 1, 256, 4, 32, 4, 2, 64, False)
     assert oracle.cache_bytes(ok) > 0
+
+
+# ---------------------------- resident sparse PSAC rows (App. D.1, reading R26)
+
+def _planted(wl, drop, seed=3):
+    """Inputs whose tokens in `drop` (a set of positions) equal a centroid of
+    their head exactly: a zero residual, so E = 0, C = 0 and a zero row (App.
+    D.1 drops it). Calibration uses the unplanted first chunk."""
+    cfg0 = oracle.cfg_from_workload(synth.scaled(wl, storage=wl.storage & ~oracle.STORE_SPARSE, coef_rows=0))
+    k = synth.tensor(wl, "k", wl.n_cache)
+    v = synth.tensor(wl, "v", wl.n_cache)
+    qh = synth.tensor(wl, "qhist", wl.n_hist)
+    tables = oracle.calibrate(cfg0, qh, k[:, :wl.chunk], v[:, :wl.chunk], 5)
+    r = rng(seed)
+    for b in range(wl.batch):
+        for h in range(wl.heads):
+            for t in sorted(drop):
+                k[b, t, h] = tables[0][b, h, r.integers(wl.n_centroids)]
+    return k, v, tables
+
+
+def _append_chunks(cfg, tables, k, v, chunks):
+    cache = oracle.new_cache(cfg)
+    for s0, n in chunks:
+        oracle.append(cfg, tables, cache, s0, np.ascontiguousarray(k[:, s0:s0 + n]),
+                      np.ascontiguousarray(v[:, s0:s0 + n]))
+    return cache
+
+
+def _sparse_wl(**kw):
+    base = dict(rank=12, head_dim=32, group_size=16, n_cache=900, n_q=96, q_start=804, frame_tokens=32,
+                chunk=300, storage=oracle.STORE_GATE | oracle.STORE_SPARSE, heads=2, batch=2)
+    base.update(kw)
+    return _small_workload(**base)
+
+
+# chunk 0 drops nothing, chunk 1 drops two rows (still dense: 2 x 14 B < 38 B of
+# mask), chunk 2 drops 40% of its rows (sparse); chunk boundaries inside tiles
+_CHUNKS = [(0, 300), (300, 300), (600, 300)]
+_DROP = {310, 451} | set(range(600, 900, 5)) | set(range(601, 900, 5))
+
+
+def test_sparse_rows_decode_like_the_gated_dense_cache():
+    wl = _sparse_wl()
+    k, v, tables = _planted(wl, _DROP)
+    dense = synth.scaled(wl, storage=oracle.STORE_GATE)
+    cs = _append_chunks(oracle.cfg_from_workload(wl), tables, k, v, _CHUNKS)
+    cd = _append_chunks(oracle.cfg_from_workload(dense), tables, k, v, _CHUNKS)
+    cfg_s, cfg_d = oracle.cfg_from_workload(wl), oracle.cfg_from_workload(dense)
+    for b in range(wl.batch):
+        for h in range(wl.heads):
+            a = oracle.decode(cfg_s, tables, cs, b, h, wl.n_cache)
+            c = oracle.decode(cfg_d, tables, cd, b, h, wl.n_cache)
+            for x, y in zip(a, c):
+                np.testing.assert_array_equal(x, y)
+            assert not a[1][sorted(_DROP)].any()
+    q = synth.tensor(wl, "q", wl.n_q)
+    o1 = oracle.attend(cfg_s, tables, cs, wl.n_cache, q, wl.q_start, wl.frame_tokens)
+    o2 = oracle.attend(cfg_d, tables, cd, wl.n_cache, q, wl.q_start, wl.frame_tokens)
+    np.testing.assert_array_equal(o1[0], o2[0])
+    np.testing.assert_array_equal(o1[1], o2[1])
+
+
+def test_sparse_directory_and_pool_follow_the_chunk_rule():
+    # Read with an independent reader of the documented layout: each chunk is
+    # stored dense (all rows) or sparse (non-zero-scale rows only), whichever is
+    # smaller with one mask bit per slot; rows in slot order; bases are prefix
+    # counts; the pool rows are the rows the gated dense cache holds.
+    import packed
+    wl = _sparse_wl()
+    k, v, tables = _planted(wl, _DROP)
+    cs = _append_chunks(oracle.cfg_from_workload(wl), tables, k, v, _CHUNKS)
+    dense = synth.scaled(wl, storage=oracle.STORE_GATE)
+    cd = _append_chunks(oracle.cfg_from_workload(dense), tables, k, v, _CHUNKS)
+    ls = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.capacity, wl.storage, 0,
+                       wl.chunk)
+    ld = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.capacity, dense.storage)
+    r = wl.rank
+    modes = []
+    for bh in range(wl.batch * wl.heads):
+        fd = packed.fields(cd, ld, bh, 0, wl.n_cache)
+        base, mask = packed.directory(cs, ls, bh)
+        codes, scale = packed.pool(cs, ls, bh)
+        stored = np.zeros(wl.n_cache, bool)
+        for s0, n in _CHUNKS:
+            kept = int((fd["k_cscale"][s0:s0 + n] != 0).sum())
+            sparse = kept * (r + 2) + (n + 7) // 8 < n * (r + 2)
+            modes.append(sparse)
+            stored[s0:s0 + n] = (fd["k_cscale"][s0:s0 + n] != 0) if sparse else True
+        rows = np.cumsum(stored) - 1
+        for t in range(wl.n_cache):
+            T, i = divmod(t, 64)
+            assert bool((int(mask[T]) >> i) & 1) == stored[t]
+            if i == 0:
+                assert base[T] == stored[:t].sum()
+            if stored[t]:
+                np.testing.assert_array_equal(codes[rows[t]], fd["k_coef"][t])
+                assert scale[rows[t]] == fd["k_cscale"][t]
+        assert packed.overflow(cs, ls, bh) == 0
+        print(f"head {bh}: {stored.sum()} pool rows for {wl.n_cache} slots")
+    assert modes[:3] == [False, False, True]
+
+
+def test_sparse_pool_overflow_drops_and_counts_rows():
+    # A pool of 700 rows for 900 slots holding more: the rows past its end are not
+    # stored and are counted; they read as zero rows, so attention equals the
+    # gated dense cache with exactly those rows zeroed.
+    import packed
+    wl = _sparse_wl(coef_rows=700)
+    k, v, tables = _planted(wl, _DROP)
+    cfg_s = oracle.cfg_from_workload(wl)
+    cs = _append_chunks(cfg_s, tables, k, v, _CHUNKS)
+    dense = synth.scaled(wl, storage=oracle.STORE_GATE, coef_rows=0)
+    cfg_d = oracle.cfg_from_workload(dense)
+    cd = _append_chunks(cfg_d, tables, k, v, _CHUNKS)
+    ls = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.capacity, wl.storage, 700,
+                       wl.chunk)
+    ld = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.capacity, dense.storage)
+    for bh in range(wl.batch * wl.heads):
+        b, h = divmod(bh, wl.heads)
+        _, ch_s, _ = oracle.decode(cfg_s, tables, cs, b, h, wl.n_cache)
+        _, ch_d, _ = oracle.decode(cfg_d, tables, cd, b, h, wl.n_cache)
+        lost = np.nonzero(np.abs(ch_d).sum(1) != np.abs(ch_s).sum(1))[0]
+        assert len(lost) == packed.overflow(cs, ls, bh) > 0
+        assert not ch_s[lost].any() and lost.min() >= 600  # only the last chunk spills
+        packed.zero_coef_rows(cd, ld, bh, lost)
+    q = synth.tensor(wl, "q", wl.n_q)
+    o1 = oracle.attend(cfg_s, tables, cs, wl.n_cache, q, wl.q_start, wl.frame_tokens)
+    o2 = oracle.attend(cfg_d, tables, cd, wl.n_cache, q, wl.q_start, wl.frame_tokens)
+    np.testing.assert_array_equal(o1[0], o2[0])
+
+
+def test_sparse_reappend_over_the_same_slots_is_idempotent():
+    # Appending a chunk again into the same slots (rows in slot order, the fill
+    # read from the directory below the chunk) leaves the cache unchanged.
+    wl = _sparse_wl()
+    k, v, tables = _planted(wl, _DROP)
+    cfg = oracle.cfg_from_workload(wl)
+    cs = _append_chunks(cfg, tables, k, v, _CHUNKS)
+    again = cs.copy()
+    for s0, n in _CHUNKS[1:]:
+        oracle.append(cfg, tables, again, s0, np.ascontiguousarray(k[:, s0:s0 + n]),
+                      np.ascontiguousarray(v[:, s0:s0 + n]))
+    over_lay = __import__("packed").layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.capacity,
+                                           wl.storage, 0, wl.chunk)
+    np.testing.assert_array_equal(cs, again)
+    assert over_lay["total"] == cs.size
+
+
+def test_sparse_cache_bytes():
+    import packed
+    for rows in (0, 640, 1000):
+        wl = _sparse_wl(coef_rows=rows)
+        cfg = oracle.cfg_from_workload(wl)
+        lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.capacity, wl.storage, rows,
+                            wl.chunk)
+        assert oracle.cache_bytes(cfg) == lay["total"]
+    # an append of more tokens than the staging rows hold is refused
+    wl = _sparse_wl()
+    k, v, tables = _planted(wl, set())
+    with pytest.raises(RuntimeError):
+        oracle.append(oracle.cfg_from_workload(wl), tables, oracle.new_cache(oracle.cfg_from_workload(wl)), 0,
+                      np.ascontiguousarray(k[:, :wl.chunk + 1]), np.ascontiguousarray(v[:, :wl.chunk + 1]))
+    # sparse rows need r >= 1
+    assert oracle.cache_bytes(oracle.cfg_from_workload(_sparse_wl(rank=0))) == -1
+    # the chunk records read slot-addressed rows: refused on a sparse cache
+    wl = _sparse_wl()
+    with pytest.raises(RuntimeError):
+        oracle.coef_pack(oracle.cfg_from_workload(wl), oracle.new_cache(oracle.cfg_from_workload(wl)), 0, 10)

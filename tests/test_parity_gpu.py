@@ -68,7 +68,8 @@ def gpu_append_all(wl, cfg, calib, k_full, v_full):
 
 def check_append(case, gpu_cache, gpu_coef):
     wl = case.wl
-    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage)
+    lay = packed.layout(wl.batch, wl.heads, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage,
+                         wl.coef_rows, wl.coef_stage or wl.chunk)
     mu_k, mu_v, w = case.tables[0][0], case.tables[1][0], case.tables[2][0]
     lam = case.tables[4][0] if wl.rank > 0 else None
     mfull = case.tables[5][0] if wl.metric == oracle.METRIC_FULL else None
