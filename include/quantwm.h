@@ -56,6 +56,8 @@ typedef struct {
   int64_t capacity;    /* cache slots per (b, h), at most 2^26 */
   int32_t storage;     /* QWM_STORE_* flags, 0 for the plain format (App. D.1 options) */
   int32_t metric;      /* QWM_METRIC_*: distance of the QSAC candidate search */
+  int64_t coef_rows;   /* QWM_STORE_SPARSE: PSAC rows in each (b, h) pool, 0 = one per slot */
+  int64_t coef_stage;  /* QWM_STORE_SPARSE: staging rows, the largest n_new of one append call */
 } quantwm_config;
 
 /* QSAC candidate metric (quantwm_config.metric).
@@ -84,6 +86,23 @@ typedef struct {
  * per epoch). */
 #define QWM_STORE_SCALE_I8 1
 #define QWM_STORE_GATE 2
+/* QWM_STORE_SPARSE (needs rank >= 1 and coef_stage >= 1): the per-chunk choice
+ * of App. D.1 between dense and sparse PSAC coefficient layouts, in the cache
+ * that attention reads. The rows of each (b, h) live in a pool of coef_rows
+ * rows, found through a directory with one 16-byte entry per 64-slot tile,
+ * {u32 base, u32 0, u64 mask}: bit i of the mask says slot 64 T + i has a row,
+ * at pool row base + (set bits below i); rows are in slot order. Each append
+ * call is one chunk: per (b, h) it stores every row of the chunk (dense) or
+ * only the rows with a non-zero scale (sparse), whichever is smaller counting
+ * one mask bit per slot as the sparse index, sparse iff
+ * kept (r + 2) + ceil(n / 8) < n (r + 2). A row with no room left in the pool
+ * is not stored (it reads as a zero row, as a dropped one does) and is counted
+ * (quantwm_coef_pool_usage). The chunk's rows are first written to staging
+ * rows in the cache, so one append call takes at most coef_stage tokens
+ * (QWM_ERR_CAPACITY otherwise). Attention reads rows through the directory in
+ * every form except the logits hook and the chunk records (quantwm_coef_pack /
+ * unpack), which read slot-addressed rows and refuse such a cache. */
+#define QWM_STORE_SPARSE 4
 
 /* ------------------------------------------------------------------ sizes */
 
@@ -100,6 +119,10 @@ typedef struct {
  *   V codes, V ids, V zp, V scale: as for K (Values carry no PSAC row).
  *   K sigma, V sigma  2 bytes each, only with QWM_STORE_SCALE_I8: the binary16
  *              secondary scale of the token-head's group scales.
+ * With QWM_STORE_SPARSE the K coef and K cscale sections hold [B*H][coef_rows]
+ * rows instead of one per slot, and four sections follow: the directory
+ * [B*H][slots/64] of 16 bytes, the u32 overflow counters [B*H], and the staging
+ * rows, codes [B*H][coef_stage][r] then binary16 scales [B*H][coef_stage].
  * A token's reconstruction is centroid + scale * (code - zero_point) (Eq. 4),
  * with scale = sigma * c_g under QWM_STORE_SCALE_I8, and its coefficients are
  * code * cscale (Eq. 16, App. D.1). */
@@ -357,6 +380,13 @@ quantwm_status quantwm_coef_pack(const quantwm_config* cfg, const void* cache, i
  * and record_bytes must cover the record), which synchronises `stream`. */
 quantwm_status quantwm_coef_unpack(const quantwm_config* cfg, const void* record, size_t record_bytes,
                                    void* cache, int64_t start, int64_t n, void* stream);
+
+/* QWM_STORE_SPARSE: PSAC rows held by the pools for cache slots [0, n_cache)
+ * summed over every (b, h) (*rows_used), and rows that found no room in a pool
+ * since the cache was zeroed (*rows_dropped); host outputs. Synchronises
+ * `stream` (it reads the directory back). */
+quantwm_status quantwm_coef_pool_usage(const quantwm_config* cfg, const void* cache, int64_t n_cache,
+                                       int64_t* rows_used, int64_t* rows_dropped, void* stream);
 
 /* Message for the last non-OK status on the calling thread ("" if none). */
 const char* quantwm_last_error(void);

@@ -60,8 +60,15 @@ quantwm_status check_cfg(const quantwm_config* c) {
   if (c->top_m > 8) return fail(QWM_ERR_UNSUPPORTED, "top_m must be <= 8");
   if (c->capacity > (int64_t(1) << 26))  // kernels address a head's slots with 32-bit offsets
     return fail(QWM_ERR_UNSUPPORTED, "capacity must be <= 2^26 slots per (b, h)");
-  if (c->storage & ~(QWM_STORE_SCALE_I8 | QWM_STORE_GATE))
+  if (c->storage & ~(QWM_STORE_SCALE_I8 | QWM_STORE_GATE | QWM_STORE_SPARSE))
     return fail(QWM_ERR_INVALID_ARG, "storage has unknown flags 0x%x", unsigned(c->storage));
+  if (c->storage & QWM_STORE_SPARSE) {
+    if (c->rank < 1) return fail(QWM_ERR_INVALID_ARG, "QWM_STORE_SPARSE needs PSAC rows (rank >= 1)");
+    if (c->coef_rows < 0 || c->coef_rows > (int64_t(1) << 26))
+      return fail(QWM_ERR_INVALID_ARG, "coef_rows must be in [0, 2^26]");
+    if (c->coef_stage < 1 || c->coef_stage > (int64_t(1) << 26))
+      return fail(QWM_ERR_INVALID_ARG, "QWM_STORE_SPARSE needs coef_stage in [1, 2^26]");
+  }
   if (c->metric != QWM_METRIC_DIAG && c->metric != QWM_METRIC_FULL)
     return fail(QWM_ERR_INVALID_ARG, "metric must be QWM_METRIC_DIAG or QWM_METRIC_FULL");
   return QWM_OK;
@@ -100,6 +107,8 @@ namespace {
 quantwm_status check_coef(const quantwm_config* cfg, int64_t start, int64_t n) {
   QWM_TRY(check_cfg(cfg));
   if (cfg->rank < 1) return fail(QWM_ERR_INVALID_ARG, "the config has no PSAC rows (rank 0)");
+  if (cfg->storage & QWM_STORE_SPARSE)
+    return fail(QWM_ERR_INVALID_ARG, "chunk records read slot-addressed rows; the cache keeps sparse rows");
   if (start < 0 || n < 0 || n > 65536 || start + n > cfg->capacity)
     return fail(QWM_ERR_INVALID_ARG, "need start >= 0, 0 <= n <= 65536 and start + n <= capacity");
   return QWM_OK;
@@ -408,6 +417,9 @@ quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void
     return fail(QWM_ERR_CAPACITY, "n_cached + n_new = %lld exceeds capacity %lld", (long long)(n_cached + n_new),
                 (long long)cfg->capacity);
   if (n_new == 0) return ok();
+  if ((cfg->storage & QWM_STORE_SPARSE) && n_new > cfg->coef_stage)
+    return fail(QWM_ERR_CAPACITY, "n_new = %lld exceeds the %lld staging rows of a sparse-row cache (coef_stage)",
+                (long long)n_new, (long long)cfg->coef_stage);
   QWM_TRY(check_dev(calib, "calib"));
   QWM_TRY(check_dev(cache, "cache"));
   QWM_TRY(check_dev(k_new, "k_new"));
@@ -437,6 +449,10 @@ quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void
   else e = bf ? launch_append_td<qwm::bf16, 128>(a, cfg->group_size, cfg->batch, s)
               : launch_append_td<float, 128>(a, cfg->group_size, cfg->batch, s);
   if (e != hipSuccess) return hip_fail(e, "append launch");
+  if (cfg->storage & QWM_STORE_SPARSE) {
+    if ((e = qwm::launch_coef_commit(*cfg, cache, n_cached, n_new, s)) != hipSuccess)
+      return hip_fail(e, "sparse-row commit launch");
+  }
   return ok();
 }
 
@@ -600,6 +616,9 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
     if (lse_out && (reinterpret_cast<uintptr_t>(lse_out) & 3)) return fail(QWM_ERR_INVALID_ARG, "lse_out misaligned");
   }
   if ((n_q + 255) / 256 > 0x7fffffff) return fail(QWM_ERR_UNSUPPORTED, "n_q too large");
+  const bool sparse_rows = (cfg->storage & QWM_STORE_SPARSE) != 0;
+  if (sparse_rows && logits_out)
+    return fail(QWM_ERR_UNSUPPORTED, "the logits hook reads slot-addressed rows; the cache keeps sparse rows");
   const int elem = qwm::elem_bytes(*cfg);
   const bool tables = qwm::attend_tables_fit(cfg->head_dim, elem, cfg->rank, cfg->n_centroids);
   const quantwm_calib_layout C = qwm::calib_layout(*cfg);
@@ -645,7 +664,7 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   hipStream_t s = static_cast<hipStream_t>(stream);
   // calibration epochs one by one through the plain kernel when the workspace
   // holds a partial plane per launch
-  if (!logits_out && workspace && n_epochs > 1) {
+  if (!logits_out && workspace && n_epochs > 1 && !sparse_rows) {
     const EpochPlan p = plan_epochs(cfg, n_epochs, epoch_start, n_cache, n_act, n_q);
     const size_t need = planes_bytes(cfg, p.planes, n_q);
     if (workspace_bytes >= need && p.planes > 0) {
@@ -704,7 +723,7 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   // packed keys of whole tiles through the plain kernel, the rest through the
   // general one, merged by log-sum-exp
   int ns_a = 1;
-  const size_t two = (!logits_out && workspace && n_act > 0 && n_epochs == 1)
+  const size_t two = (!logits_out && workspace && n_act > 0 && n_epochs == 1 && !sparse_rows)
                          ? active_two_part_bytes(cfg, n_cache, n_act, n_q, &ns_a) : 0;
   const bool two_part = two > 0 && workspace_bytes >= two;
   if (two_part) {
@@ -796,6 +815,45 @@ quantwm_status quantwm_attend_noalloc(const quantwm_config* cfg, const void* cal
   return attend_common(cfg, calib, 1, nullptr, cache, n_cache, nullptr, nullptr, 0, q, n_q, q_start, frame_tokens,
                        out, lse_out, nullptr, scratch, scratch ? size_t(QWM_ATTEND_NOALLOC_SCRATCH_BYTES) : 0, stream,
                        ns);
+}
+
+quantwm_status quantwm_coef_pool_usage(const quantwm_config* cfg, const void* cache, int64_t n_cache,
+                                       int64_t* rows_used, int64_t* rows_dropped, void* stream) {
+  QWM_TRY(check_cfg(cfg));
+  if (!(cfg->storage & QWM_STORE_SPARSE)) return fail(QWM_ERR_INVALID_ARG, "the config keeps no sparse rows");
+  if (n_cache < 0 || n_cache > cfg->capacity) return fail(QWM_ERR_INVALID_ARG, "need 0 <= n_cache <= capacity");
+  if (!rows_used || !rows_dropped) return fail(QWM_ERR_INVALID_ARG, "output pointer is null");
+  QWM_TRY(check_dev(cache, "cache"));
+  const qwm::CacheLayout L = qwm::cache_layout(*cfg);
+  const int64_t nbh = int64_t(cfg->batch) * cfg->heads, tiles = L.slots / 64;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  std::vector<uint32_t> over(static_cast<size_t>(nbh));
+  std::vector<uint8_t> ent(static_cast<size_t>(nbh) * 16, 0);
+  const uint8_t* c = static_cast<const uint8_t*>(cache);
+  hipError_t e = hipMemcpyAsync(over.data(), c + L.k_over, over.size() * 4, hipMemcpyDeviceToHost, s);
+  // the directory entry of the tile holding slot n_cache - 1, for every head
+  const int64_t T = n_cache > 0 ? (n_cache - 1) / 64 : 0;
+  if (e == hipSuccess && n_cache > 0)
+    e = hipMemcpy2DAsync(ent.data(), 16, c + L.k_dir + T * 16, size_t(tiles) * 16, 16, size_t(nbh),
+                         hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "pool usage readback");
+  int64_t used = 0, dropped = 0;
+  const int u = int(n_cache - 64 * T);
+  const uint64_t below = u >= 64 ? ~uint64_t(0) : ((uint64_t(1) << u) - 1);
+  for (int64_t bh = 0; bh < nbh; ++bh) {
+    dropped += over[size_t(bh)];
+    if (n_cache == 0) continue;
+    const uint8_t* p = ent.data() + bh * 16;
+    uint32_t base, lo, hi;
+    std::memcpy(&base, p, 4);
+    std::memcpy(&lo, p + 8, 4);
+    std::memcpy(&hi, p + 12, 4);
+    used += int64_t(base) + __builtin_popcountll((uint64_t(hi) << 32 | lo) & below);
+  }
+  *rows_used = used;
+  *rows_dropped = dropped;
+  return ok();
 }
 
 quantwm_status quantwm_logits(const quantwm_config* cfg, const void* calib, const void* cache, int64_t n_cache,

@@ -447,7 +447,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
         keep = after < before;
       }
       if (active) {
-        int8_t* code = reinterpret_cast<int8_t*>(a.cache + a.L.k_coef + slot * r);
+        // with sparse rows the chunk's rows go to the staging rows (row tt of the
+        // head) and the commit kernel stores them into the pool
+        const int64_t crow = a.L.sparse ? bh * a.L.stage + tt : slot;
+        int8_t* code = reinterpret_cast<int8_t*>(a.cache + (a.L.sparse ? a.L.k_st_codes : a.L.k_coef) + crow * r);
         float* co = a.coef_out ? a.coef_out + (bh * a.n_new + tt) * r : nullptr;
 #pragma unroll
         for (int k = 0; k < RP; ++k) {
@@ -456,7 +459,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
             if (co) co[k] = C[k];
           }
         }
-        *reinterpret_cast<uint16_t*>(a.cache + a.L.k_cscale + slot * 2) = f16_bits(keep ? s : 0.0f);
+        *reinterpret_cast<uint16_t*>(a.cache + (a.L.sparse ? a.L.k_st_scale : a.L.k_cscale) + crow * 2) =
+            f16_bits(keep ? s : 0.0f);
       }
     }
   }

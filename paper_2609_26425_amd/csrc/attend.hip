@@ -385,6 +385,12 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
              r_ks = field(L.k_scale, sstride), r_vc = field(L.v_codes, D / 4), r_vi = field(L.v_ids, 1),
              r_vz = field(L.v_zp, zpb), r_vs = field(L.v_scale, sstride);
   const auto r_cc = field(L.k_coef, uint32_t(r)), r_cs = field(L.k_cscale, 2);
+  // sparse rows (general instance only): this head's row pool and tile directory
+  const auto r_pc = __builtin_amdgcn_make_buffer_rsrc((void*)(cache + L.k_coef + bh * L.pool * r), 0,
+                                                      int(uint32_t(L.pool) * uint32_t(r)), 0x00020000);
+  const auto r_ps = __builtin_amdgcn_make_buffer_rsrc((void*)(cache + L.k_cscale + bh * L.pool * 2), 0,
+                                                      int(uint32_t(L.pool) * 2u), 0x00020000);
+  const uint32_t* dir = reinterpret_cast<const uint32_t*>(cache + L.k_dir + bh * (L.slots / 64) * 16);
   const auto r_ksg = field(L.k_sigma, 2), r_vsg = field(L.v_sigma, 2);  // SI8 secondary scales
   const int o_kc = kkey * (D / 4) + kch0 / 4, o_kz = kkey * zpb, o_ks = kkey * sstride;
   const int o_cc = ckey * r + cr0, o_cs = ckey * 2;
@@ -438,7 +444,20 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       }
     }
     if constexpr (RP > 0) {
-      if (crole && (FULL || k0 + ckey < npku)) {
+      if (GEN && L.sparse && crole && (FULL || k0 + ckey < npku)) {
+        // the key's row through the directory entry of its 64-key tile: present
+        // iff its mask bit is set, at pool row base + (set bits below it)
+        const uint32_t* e = dir + (k0 / 64) * 4;
+        const uint64_t m = uint64_t(e[2]) | (uint64_t(e[3]) << 32);
+        if ((m >> ckey) & 1) {
+          const int row = int(e[0]) + __popcll(m & ((uint64_t(1) << ckey) - 1));
+          csb = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_ps, row * 2, 0, 0));
+#pragma unroll
+          for (int k = 0; k < RCH; ++k)
+            if (cr0 + k < r)
+              cw2[k / 4] |= uint32_t(__builtin_amdgcn_raw_buffer_load_b8(r_pc, row * r + cr0 + k, 0, 0)) << (8 * (k % 4));
+        }
+      } else if (crole && (FULL || k0 + ckey < npku)) {
         csb = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(r_cs, o_cs, k0i * 2, 0));
         if (aligned) {
           if constexpr (RCH == 8) {
@@ -1019,7 +1038,8 @@ hipError_t launch_attend_rp(const AttendArgs& a, int batch, bool logits, hipStre
                  : launch_k<T, D, RP, true, false, false, true>(a, grid, lds, s);
     return tab ? launch_k<T, D, RP, true, true>(a, grid, lds, s) : launch_k<T, D, RP, true, false>(a, grid, lds, s);
   }
-  if (a.n_act > 0 || a.n_epochs > 1) {
+  // the general instance: an active chunk, calibration epochs, or sparse PSAC rows
+  if (a.n_act > 0 || a.n_epochs > 1 || a.L.sparse) {
     if (si8)
       return tab ? launch_k<T, D, RP, false, true, true, true>(a, grid, lds, s)
                  : launch_k<T, D, RP, false, false, true, true>(a, grid, lds, s);

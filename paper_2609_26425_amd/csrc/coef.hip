@@ -187,4 +187,108 @@ hipError_t launch_coef_unpack(const quantwm_config& c, const void* record, int l
   return hipGetLastError();
 }
 
+
+namespace {
+
+// Stores the staged rows of one append call (slots [n_cached, n_cached + n)) of
+// head blockIdx.x into its pool: every row (dense) or the rows with a non-zero
+// scale (sparse), whichever is smaller with one mask bit per slot as the sparse
+// index (ties dense); rows in slot order after the rows of the slots below; a
+// row past the pool's end is counted and not stored. Then the directory of the
+// chunk's tiles: the tile holding n_cached keeps its rows below n_cached. One
+// wave per 64-slot tile, four tiles per pass.
+__global__ __launch_bounds__(256) void coef_commit_kernel(uint8_t* cache, CacheLayout L, int64_t n_cached, int n) {
+  const int64_t bh = blockIdx.x;
+  const int r = L.r, tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
+  const int64_t tiles = L.slots / 64;
+  uint8_t* dir = cache + L.k_dir + bh * tiles * 16;
+  const uint8_t* st_c = cache + L.k_st_codes + bh * L.stage * r;
+  const uint8_t* st_s = cache + L.k_st_scale + bh * L.stage * 2;
+  uint8_t* pc = cache + L.k_coef + bh * L.pool * r;
+  uint8_t* ps = cache + L.k_cscale + bh * L.pool * 2;
+  __shared__ uint32_t s_cnt[4];
+  __shared__ int64_t s_fill;
+  __shared__ uint32_t s_kept;
+  // pool rows used by the slots below n_cached (read before this block writes)
+  if (tid == 0) {
+    int64_t f = 0;
+    if (n_cached > 0) {
+      const int64_t T = (n_cached - 1) / 64;
+      const int used = int(n_cached - 64 * T);
+      const uint64_t below = used == 64 ? ~uint64_t(0) : ((uint64_t(1) << used) - 1);
+      const uint8_t* e = dir + T * 16;
+      const uint64_t m = uint64_t(ld32(e + 8)) | (uint64_t(ld32(e + 12)) << 32);
+      f = int64_t(ld32(e)) + __popcll(m & below);
+    }
+    s_fill = f;
+    s_kept = 0;
+  }
+  __syncthreads();
+  uint32_t c = 0;
+  for (int t = tid; t < n; t += 256) c += ld16(st_s + 2 * t) != 0;
+  atomicAdd(&s_kept, c);
+  __syncthreads();
+  const int64_t kept = s_kept, fill = s_fill;
+  const bool sparse = kept * (r + 2) + (n + 7) / 8 < int64_t(n) * (r + 2);
+  const int64_t T0 = n_cached / 64, T1 = (n_cached + n + 63) / 64;  // the chunk's tiles [T0, T1)
+  int64_t stored_before = 0;  // stored rows of the chunk before the current pass
+  uint32_t over = 0;
+  for (int64_t Tp = T0; Tp < T1; Tp += 4) {
+    const int64_t T = Tp + wave;
+    const int64_t slot = T * 64 + lane, t = slot - n_cached;
+    const bool in = T < T1 && t >= 0 && t < n;
+    const bool stored = in && (!sparse || ld16(st_s + 2 * t) != 0);
+    const uint64_t sb = __ballot(stored);
+    const int64_t rank = __popcll(sb & ((uint64_t(1) << lane) - 1));  // stored rows of this tile below the lane
+    if (lane == 0) s_cnt[wave] = __popcll(sb);
+    __syncthreads();
+    int64_t before = stored_before;  // stored rows of the chunk before tile T
+    for (int w = 0; w < wave; ++w) before += s_cnt[w];
+    const int64_t pass_total = int64_t(s_cnt[0]) + s_cnt[1] + s_cnt[2] + s_cnt[3];
+    const int64_t pos = fill + before + rank;
+    const bool fit = stored && pos < L.pool;
+    if (stored && !fit) ++over;
+    if (fit) {
+      for (int i = 0; i < r; ++i) pc[pos * r + i] = st_c[t * r + i];
+      ps[pos * 2] = st_s[2 * t];
+      ps[pos * 2 + 1] = st_s[2 * t + 1];
+    }
+    const uint64_t fb = __ballot(fit);
+    if (lane == 0 && T < T1) {
+      uint8_t* e = dir + T * 16;
+      uint64_t m = fb;
+      if (T * 64 < n_cached) {
+        // the chunk starts inside this tile: its rows below n_cached stay
+        const int i0 = int(n_cached - T * 64);
+        const uint64_t old = uint64_t(ld32(e + 8)) | (uint64_t(ld32(e + 12)) << 32);
+        m |= old & ((uint64_t(1) << i0) - 1);
+      } else {
+        const int64_t b0 = fill + before < L.pool ? fill + before : L.pool;
+        st32(e, uint32_t(b0));
+        st32(e + 4, 0);
+      }
+      st32(e + 8, uint32_t(m));
+      st32(e + 12, uint32_t(m >> 32));
+    }
+    stored_before += pass_total;
+    __syncthreads();  // s_cnt is reused by the next pass
+  }
+  // rows without room in the pool, summed over the block
+  __shared__ uint32_t s_over;
+  if (tid == 0) s_over = 0;
+  __syncthreads();
+  if (over) atomicAdd(&s_over, over);
+  __syncthreads();
+  if (tid == 0 && s_over) st32(cache + L.k_over + bh * 4, ld32(cache + L.k_over + bh * 4) + s_over);
+}
+
+}  // namespace
+
+hipError_t launch_coef_commit(const quantwm_config& c, void* cache, int64_t n_cached, int64_t n, hipStream_t s) {
+  const CacheLayout L = cache_layout(c);
+  hipLaunchKernelGGL(coef_commit_kernel, dim3(unsigned(int64_t(c.batch) * c.heads)), dim3(256), 0, s,
+                     static_cast<uint8_t*>(cache), L, n_cached, int(n));
+  return hipGetLastError();
+}
+
 }  // namespace qwm

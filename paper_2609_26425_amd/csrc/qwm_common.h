@@ -21,6 +21,9 @@ struct CacheLayout {
   int64_t k_codes, k_ids, k_zp, k_scale, k_coef, k_cscale;
   int64_t v_codes, v_ids, v_zp, v_scale;
   int64_t k_sigma, v_sigma;  // i8 only: the secondary scale per token
+  int sparse;                // PSAC rows in a pool per (b, h), found through a tile directory
+  int64_t pool, stage;       // rows per (b, h) in the coefficient sections and in the staging rows
+  int64_t k_dir, k_over, k_st_codes, k_st_scale;  // sparse only
   int64_t total;
 };
 
@@ -35,21 +38,29 @@ inline CacheLayout cache_layout(const quantwm_config& c) {
   L.slots = (c.capacity + 63) / 64 * 64;
   L.i8 = (c.storage & QWM_STORE_SCALE_I8) != 0;
   L.sb = L.i8 ? L.ng : 2 * L.ng;
-  const int64_t rows = int64_t(c.batch) * c.heads * L.slots;
+  L.sparse = (c.storage & QWM_STORE_SPARSE) != 0;
+  L.pool = L.sparse && c.coef_rows > 0 ? c.coef_rows : L.slots;
+  L.stage = L.sparse ? c.coef_stage : 0;
+  const int64_t bh = int64_t(c.batch) * c.heads, rows = bh * L.slots;
   int64_t at = 0;
-  auto take = [&](int64_t per_token) { int64_t o = at; at = align256(at + rows * per_token); return o; };
+  auto take_n = [&](int64_t n, int64_t per) { int64_t o = at; at = align256(at + n * per); return o; };
+  auto take = [&](int64_t per_token) { return take_n(rows, per_token); };
   L.k_codes = take(L.d / 4);
   L.k_ids = take(1);
   L.k_zp = take(L.zpb);
   L.k_scale = take(L.sb);
-  L.k_coef = take(L.r);
-  L.k_cscale = take(L.r > 0 ? 2 : 0);
+  L.k_coef = take_n(bh * L.pool, L.r);
+  L.k_cscale = take_n(bh * L.pool, L.r > 0 ? 2 : 0);
   L.v_codes = take(L.d / 4);
   L.v_ids = take(1);
   L.v_zp = take(L.zpb);
   L.v_scale = take(L.sb);
   L.k_sigma = take(L.i8 ? 2 : 0);
   L.v_sigma = take(L.i8 ? 2 : 0);
+  L.k_dir = take_n(bh * (L.slots / 64), L.sparse ? 16 : 0);
+  L.k_over = take_n(bh, L.sparse ? 4 : 0);
+  L.k_st_codes = take_n(bh * L.stage, L.r);
+  L.k_st_scale = take_n(bh * L.stage, 2);
   L.total = at;
   L.v_bytes = L.d / 4 + 1 + L.zpb + L.sb + (L.i8 ? 2 : 0);
   L.k_bytes = L.v_bytes + (L.r > 0 ? L.r + 2 : 0);
@@ -161,6 +172,8 @@ hipError_t launch_coef_pack(const quantwm_config& c, const void* cache, int64_t 
                             int layout, hipStream_t s);
 hipError_t launch_coef_unpack(const quantwm_config& c, const void* record, int layout, void* cache, int64_t start,
                               int n, hipStream_t s);
+// QWM_STORE_SPARSE: stores one append call's staged rows into the pools and the directory
+hipError_t launch_coef_commit(const quantwm_config& c, void* cache, int64_t n_cached, int64_t n, hipStream_t s);
 hipError_t launch_kmeans(const quantwm_config& c, const void* x, int64_t n, int iters, uint8_t* calib,
                          int64_t o_mu, int32_t* assign_ws, hipStream_t s);
 

@@ -29,7 +29,8 @@ class Config(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("n_centroids", ctypes.c_int32), ("group_size", ctypes.c_int32),
                 ("rank", ctypes.c_int32), ("top_m", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("capacity", ctypes.c_int64), ("storage", ctypes.c_int32), ("metric", ctypes.c_int32)]
+                ("capacity", ctypes.c_int64), ("storage", ctypes.c_int32), ("metric", ctypes.c_int32),
+                ("coef_rows", ctypes.c_int64), ("coef_stage", ctypes.c_int64)]
 
     @property
     def torch_dtype(self):
@@ -73,6 +74,7 @@ def _load():
         "quantwm_coef_record_max_bytes": (SZ, [C, I64]),
         "quantwm_coef_pack": (I32, [C, P, I64, I64, P, SZ, ctypes.POINTER(I64), ctypes.POINTER(I32), P]),
         "quantwm_coef_unpack": (I32, [C, P, SZ, P, I64, I64, P]),
+        "quantwm_coef_pool_usage": (I32, [C, P, I64, ctypes.POINTER(I64), ctypes.POINTER(I64), P]),
         "quantwm_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -89,6 +91,7 @@ EXPORTED = ("quantwm_cache_bytes", "quantwm_token_bytes", "quantwm_calib_bytes",
             "quantwm_append", "quantwm_attend_workspace_bytes", "quantwm_attend", "quantwm_attend_active",
             "quantwm_attend_epochs", "quantwm_attend_noalloc",
             "quantwm_logits", "quantwm_attend_active_workspace_bytes", "quantwm_attend_epochs_workspace_bytes", "quantwm_coef_record_max_bytes", "quantwm_coef_pack", "quantwm_coef_unpack",
+            "quantwm_coef_pool_usage",
             "quantwm_last_error")
 
 
@@ -99,15 +102,17 @@ def library():
 # App. D.1 storage options (QWM_STORE_* in include/quantwm.h)
 STORE_SCALE_I8 = 1
 STORE_GATE = 2
+STORE_SPARSE = 4
 # QSAC candidate metric (QWM_METRIC_*): Eq. 9 or the full quadratic form
 METRIC_DIAG = 0
 METRIC_FULL = 1
 
 
 def make_config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, capacity, dtype,
-                storage=0, metric=0) -> Config:
+                storage=0, metric=0, coef_rows=0, coef_stage=0) -> Config:
     dt = {"bf16": BF16, "f32": F32, BF16: BF16, F32: F32}[dtype]
-    return Config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, dt, capacity, storage, metric)
+    return Config(batch, heads, head_dim, n_centroids, group_size, rank, top_m, dt, capacity, storage, metric,
+                  coef_rows, coef_stage)
 
 
 def _ptr(t):
@@ -274,3 +279,11 @@ def quantwm_coef_pack(cfg, cache, start, n, record, stream=None):
 def quantwm_coef_unpack(cfg, record, cache, start, n, record_bytes=None, stream=None):
     nb = record.numel() if record_bytes is None else record_bytes
     _check(_lib.quantwm_coef_unpack(ctypes.byref(cfg), _ptr(record), nb, _ptr(cache), start, n, _stream(stream)))
+
+
+def quantwm_coef_pool_usage(cfg, cache, n_cache, stream=None):
+    """(rows used, rows dropped for lack of room) of a sparse-row cache."""
+    used, dropped = ctypes.c_int64(), ctypes.c_int64()
+    _check(_lib.quantwm_coef_pool_usage(ctypes.byref(cfg), _ptr(cache), n_cache, ctypes.byref(used),
+                                        ctypes.byref(dropped), _stream(stream)))
+    return int(used.value), int(dropped.value)

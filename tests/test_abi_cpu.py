@@ -180,3 +180,32 @@ def test_attend_workspace_sizes():
     # too few key tiles to split (fewer than 8 per split)
     assert qw.quantwm_attend_workspace_bytes(roll, 64 * 15, 1560) == 0
     assert qw.quantwm_attend_workspace_bytes(roll, 120000, 0) == 0
+
+
+@pytest.mark.parametrize("rows,stage", [(0, 300), (640, 300), (200, 4680)])
+def test_sparse_row_sizes_agree_with_the_oracle_format(rows, stage):
+    # QWM_STORE_SPARSE: pools of coef_rows rows, the tile directory, overflow
+    # counters and the staging rows, laid out as the oracle lays them out
+    for storage in (4, 5, 6, 7):
+        cfg = qw.make_config(2, 3, 128, 37, 32, 12, 3, 1000, "bf16", storage, coef_rows=rows, coef_stage=stage)
+        ocfg = oracle.cfg_of(2, 3, 128, 37, 32, 12, 3, 1000, True, storage, coef_rows=rows, coef_stage=stage)
+        assert qw.quantwm_cache_bytes(cfg) == oracle.cache_bytes(ocfg) > 0
+
+
+def test_sparse_row_argument_errors():
+    for bad in (qw.make_config(1, 2, 128, 16, 32, 0, 4, 100, "bf16", 4, coef_stage=10),   # no PSAC rows
+                qw.make_config(1, 2, 128, 16, 32, 8, 4, 100, "bf16", 4),                  # no staging rows
+                qw.make_config(1, 2, 128, 16, 32, 8, 4, 100, "bf16", 4, coef_rows=-1, coef_stage=10)):
+        with pytest.raises(qw.QuantwmError) as e:
+            qw.quantwm_token_bytes(bad)
+        assert e.value.status == qw.ERR_INVALID_ARG
+    cfg = qw.make_config(1, 2, 128, 16, 32, 8, 4, 100, "bf16", 4, coef_stage=10)
+    # an append of more tokens than the staging rows hold
+    with pytest.raises(qw.QuantwmError) as e:
+        qw._check(qw.library().quantwm_append(ctypes.byref(cfg), None, None, 0, None, None, 11, None, None))
+    assert e.value.status == qw.ERR_CAPACITY and "coef_stage" in qw.quantwm_last_error()
+    # the chunk records read slot-addressed rows
+    with pytest.raises(qw.QuantwmError) as e:
+        qw._check(qw.library().quantwm_coef_pack(ctypes.byref(cfg), None, 0, 10, None, 0, None, None, None))
+    assert e.value.status == qw.ERR_INVALID_ARG and "sparse" in qw.quantwm_last_error()
+
