@@ -16,9 +16,15 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(_HERE, "quantwm_oracle.c")
-LIB = os.path.join(_HERE, "libquantwm_oracle.so")
 CFLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC", "-shared",
           "-std=c11", "-Wall", "-Wextra"]
+# QWM_ORACLE_SANITIZE=1: a build with AddressSanitizer and UndefinedBehaviorSanitizer
+# (its own library file; the process must preload gcc's libasan, see
+# tests/test_oracle_sanitized.py), any report fatal
+SANITIZE = os.environ.get("QWM_ORACLE_SANITIZE") == "1"
+if SANITIZE:
+    CFLAGS = CFLAGS + ["-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-g"]
+LIB = os.path.join(_HERE, "libquantwm_oracle_san.so" if SANITIZE else "libquantwm_oracle.so")
 
 
 def build() -> str:

@@ -95,6 +95,38 @@ def build(jobs: int | None = None, verbose: bool = False, incremental: bool = Fa
     return OUT
 
 
+SAN_OUT = os.path.join(BUILD, "san", "libquantwm_san.so")
+
+
+def build_sanitized() -> str:
+    """libquantwm with its host-side code (the C ABI's validation and launches,
+    the host eigensolver) built with AddressSanitizer and UndefinedBehaviorSanitizer,
+    linked with the kernel objects of the normal build (built first if missing).
+    A process that loads it must preload clang's ASan runtime."""
+    units = _units()
+    if any(not os.path.exists(os.path.join(BUILD, u[0])) for u in units):
+        build()
+    san = os.path.join(BUILD, "san")
+    os.makedirs(san, exist_ok=True)
+    flags = ["-Xarch_host", "-fsanitize=address,undefined", "-Xarch_host", "-fno-sanitize-recover=all",
+             "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+    objs = []
+    for obj, src, extra in units:
+        if src in ("api.hip", "eigh.cpp"):
+            out = os.path.join(san, obj)
+            cmd = [_hipcc(), *HIPFLAGS, *extra, *flags, "-c", os.path.join(CSRC, src), "-o", out]
+            p = subprocess.run(cmd, capture_output=True, text=True)
+            if p.returncode != 0:
+                raise RuntimeError(f"hipcc failed for {src} (sanitized):\n{p.stderr}")
+            objs.append(out)
+        else:
+            objs.append(os.path.join(BUILD, obj))
+    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Xarch_host", "-fsanitize=address,undefined",
+           "-shared-libsan", "-o", SAN_OUT, *objs]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    return SAN_OUT
+
+
 if __name__ == "__main__":
     print(build(verbose=True, incremental="--incremental" in sys.argv))
     sys.exit(0)

@@ -69,14 +69,6 @@ __device__ inline uint16_t f16_bits(float exact) {
   return __builtin_bit_cast(uint16_t, (_Float16)exact);
 }
 
-// Code of one channel given its group's stored scale s and zero-point z (Eq. 1).
-// Branch-free: a zero scale divides by 1 and the result is then discarded.
-__device__ inline int quant_code(float x, float mu, float s, int z) {
-  const float sd = s != 0.0f ? s : 1.0f;
-  const int q = (int)fminf(fmaxf(rintf((x - mu) / sd) + (float)z, 0.0f), 3.0f);
-  return s != 0.0f ? q : 0;
-}
-
 // rint(x/s) for N residuals x = xv - mu with the IEEE quotient of Eq. 1, without
 // N full divisions. t = x * RN(1/s) lies within 3 * 2^-24 * |x/s| of RN(x/s);
 // every residual satisfies |x/s| <= 3.01 here (the range spans 3 steps), so the

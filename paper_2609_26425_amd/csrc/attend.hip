@@ -15,6 +15,7 @@
 // from the accumulator registers and O^T = Vhat^T P^T accumulates in registers.
 // Softmax is online (running max and sum per Query, base-2 exponentials).
 #include "attend_shape.h"
+#include "xcd_order.h"
 
 #include <atomic>
 #include <type_traits>
@@ -254,8 +255,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   {
     const uint32_t gx = gridDim.x, gy = gridDim.y, n = gx * gy * gridDim.z;
     const uint32_t L = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
-    const uint32_t P = L % 8, Q = L / 8, q = n / 8, rr = n % 8;
-    const uint32_t task = P < rr ? P * (q + 1) + Q : rr * (q + 1) + (P - rr) * q + Q;
+    const uint32_t task = qwm_xcd_task(L, n);
     bx = task % gx;
     by = (task / gx) % gy;
     bz = task / (gx * gy);

@@ -12,7 +12,9 @@ import os
 
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libquantwm.so")
+# QWM_LIB selects another build of the library (the sanitized host-side build
+# that tests/test_abi_sanitized.py loads); by default the in-tree one
+LIB_PATH = os.environ.get("QWM_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libquantwm.so")
 
 F32, BF16 = 0, 1
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_HIP = 0, 1, 2, 3, 4

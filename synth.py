@@ -59,6 +59,7 @@ class Workload:
     metric: int = 0       # QSAC candidate metric: 0 = Eq. 9 (diagonal), 1 = the full quadratic form
     coef_rows: int = 0    # storage bit 2 (sparse PSAC rows): pool rows per head, 0 = one per slot
     coef_stage: int = 0   # storage bit 2: staging rows per head (largest append chunk), 0 = the chunk size
+    q_align: float = 0.0  # > 0: the dominant Query directions load the Key outlier channels (weight in [0, 1])
 
     @property
     def capacity(self) -> int:
@@ -120,7 +121,14 @@ def _head_params(wl: Workload, b: int, h: int):
     out_ch = g.permutation(d)[: wl.n_out]
     sigma[out_ch] *= wl.out_scale
     means = sigma[None, :] * g.standard_normal((N_MIX, d))
-    a, _ = np.linalg.qr(g.standard_normal((d, wl.q_rank)))
+    raw = g.standard_normal((d, wl.q_rank))
+    if wl.q_align > 0:
+        # the first dominant directions lean on the outlier channels of the Keys
+        for i in range(min(wl.n_out, wl.q_rank)):
+            unit = np.zeros(d)
+            unit[out_ch[i]] = np.sqrt(d)
+            raw[:, i] = wl.q_align * unit + (1.0 - wl.q_align) * raw[:, i]
+    a, _ = np.linalg.qr(raw)
     return sigma, means, a
 
 

@@ -2,6 +2,7 @@
 every entry point that include/quantwm.h declares, and its size queries and
 argument validation behave as documented (no kernel is launched)."""
 import ctypes
+import subprocess
 import os
 import re
 
@@ -209,3 +210,29 @@ def test_sparse_row_argument_errors():
         qw._check(qw.library().quantwm_coef_pack(ctypes.byref(cfg), None, 0, 10, None, 0, None, None, None))
     assert e.value.status == qw.ERR_INVALID_ARG and "sparse" in qw.quantwm_last_error()
 
+
+
+def test_xcd_task_order_is_a_bijection(tmp_path):
+    # The attention kernel maps workgroup L of n to task qwm_xcd_task(L, n)
+    # (csrc/xcd_order.h, shared with the kernel); every grid size must cover
+    # every task once. Compiled here with the host C compiler.
+    src = tmp_path / "xcd.c"
+    src.write_text('#include <stdio.h>\n#include <stdlib.h>\n#include "xcd_order.h"\n'
+                   'int main(void) {\n'
+                   '  for (uint32_t n = 1; n <= 5000; ++n) {\n'
+                   '    unsigned char* seen = calloc(n, 1);\n'
+                   '    for (uint32_t L = 0; L < n; ++L) {\n'
+                   '      uint32_t t = qwm_xcd_task(L, n);\n'
+                   '      if (t >= n || seen[t]) { printf("bad %u %u\\n", n, L); return 1; }\n'
+                   '      seen[t] = 1;\n'
+                   '      /* consecutive tasks of one XCD: L and L + 8 map to t and t + 1 */\n'
+                   '      if (L + 8 < n && qwm_xcd_task(L + 8, n) != t + 1) { printf("run %u %u\\n", n, L); return 1; }\n'
+                   '    }\n'
+                   '    free(seen);\n'
+                   '  }\n'
+                   '  puts("ok");\n  return 0;\n}\n')
+    exe = tmp_path / "xcd"
+    inc = os.path.join(ROOT, "paper_2609_26425_amd", "csrc")
+    subprocess.run(["gcc", "-O2", "-std=c11", "-I", inc, str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert out.returncode == 0 and out.stdout.strip() == "ok", out.stdout

@@ -86,3 +86,19 @@ def test_quality_orderings_on_matrix_game_shape():
     assert m["both"]["logit_mse"] < m["qvg"]["logit_mse"]
     assert m["both"]["top1_shift"] <= m["qvg"]["top1_shift"]
     assert res["m_sweep"]["4"]["logit_mse"] == pytest.approx(m["both"]["logit_mse"], rel=1e-12)
+
+
+def test_qsac_ordering_with_queries_on_the_outlier_channels():
+    # Sec. 4.1: QSAC helps where the Queries load the channels whose Key residuals
+    # are hard to quantise. Here the dominant Query directions lie on the Key
+    # outlier channels (8 of them, x20): QSAC alone lowers the logit MSE below
+    # plain nearest-centroid quantisation (QVG), and PSAC, which removes the
+    # error along those same directions, lowers it most.
+    wl = synth.scaled(synth.WORKLOADS["mg2-12h"], name="mg2-4h-aligned", heads=4, n_cache=2640, n_q=880,
+                      q_start=1760, chunk=880, n_hist=1760, q_align=1.0, n_out=8, out_scale=20.0)
+    res = quality.evaluate(wl, quality.gpu_tables(wl), 128, m_sweep=(), storage=(), metric=())
+    m = res["modes"]
+    _say(f"[ok] quality {wl.name}: {m}")
+    assert m["qsac"]["logit_mse"] < m["qvg"]["logit_mse"]
+    assert m["psac"]["logit_mse"] < m["qsac"]["logit_mse"]
+    assert m["both"]["logit_mse"] < m["qsac"]["logit_mse"]
