@@ -146,10 +146,16 @@ size_t quantwm_calib_bytes(const quantwm_config* cfg);
  *   lam         [r]     f32     the matching eigenvalues (0 at cold start)
  *   u_dr        [d][rs] f32     U_r itself (the transpose of u_t), ranks zero-padded to
  *                               rs = 16 (r <= 16) or 32 (r <= 32), for per-channel use
- *   m           [d][d]  f32     Mn, only with QWM_METRIC_FULL (no bytes otherwise) */
+ *   m           [d][d]  f32     Mn, only with QWM_METRIC_FULL (no bytes otherwise)
+ *   mu_k16, mu_v16 [Kc][d] binary16  BF16 configs only (no bytes otherwise): the
+ *                               centroids times 2^-e_k (2^-e_v), e the exponent that puts
+ *                               the table's largest magnitude in [2^14, 2^15) (0 for an
+ *                               all-zero table), rounded to binary16: exact for every
+ *                               component of at least 2^-31 times that largest one
+ *   e16         [2]     int32   e_k, e_v (BF16 configs only) */
 typedef struct {
   int64_t slab_bytes;
-  int64_t mu_k, mu_v, a_k, b_k, a_v, b_v, w, wg, u_t, lam, u_dr, m;
+  int64_t mu_k, mu_v, a_k, b_k, a_v, b_v, w, wg, u_t, lam, u_dr, m, mu_k16, mu_v16, e16;
 } quantwm_calib_layout;
 quantwm_status quantwm_calib_offsets(const quantwm_config* cfg, quantwm_calib_layout* out);
 

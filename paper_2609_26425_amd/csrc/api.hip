@@ -626,6 +626,7 @@ static quantwm_status attend_common(const quantwm_config* cfg, const void* calib
   a.calib = static_cast<const uint8_t*>(calib);
   a.slab = C.slab_bytes;
   a.o_mu_k = C.mu_k; a.o_mu_v = C.mu_v; a.o_u_t = C.u_t;
+  a.o_mu_k16 = C.mu_k16; a.o_mu_v16 = C.mu_v16; a.o_e16 = C.e16;
   a.cache = static_cast<const uint8_t*>(cache);
   a.L = qwm::cache_layout(*cfg);
   a.q = q; a.out = out; a.lse = lse_out; a.logits = logits_out;

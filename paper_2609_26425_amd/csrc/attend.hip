@@ -119,6 +119,25 @@ __device__ inline uint32_t pack_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
+// N centroid components from LDS: BF16 (T), or with H16 the binary16 copy of
+// the table (scaled by a power of two), which v_fma_mix_f32 converts to fp32 as
+// an operand, so the dequant takes no separate unpack of a BF16 pair.
+template <bool H16, typename T, int N>
+__device__ inline void load_tab(const T* p, float (&out)[N]) {
+  if constexpr (H16) {
+    typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+    static_assert(N % 8 == 0, "binary16 table loads of 8 values");
+#pragma unroll
+    for (int i = 0; i < N / 8; ++i) {
+      const h8 v = reinterpret_cast<const h8*>(p)[i];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) out[8 * i + k] = (float)v[k];
+    }
+  } else {
+    load_vals<T, N>(p, out);
+  }
+}
+
 template <typename T, int N>
 __device__ inline void store_vals(T* p, const float (&x)[N]) {
   if constexpr (sizeof(T) == 2) {
@@ -181,8 +200,8 @@ __device__ inline uint32_t and_or(uint32_t x, uint32_t m, uint32_t o) {
 // SI8 (App. D.1 8-bit group scales): the step is sigma * c with s = sigma and cm
 // = (c, c); c (code - z) is an integer of magnitude <= 765, exact in binary16,
 // so the fma still rounds once.
-template <int N, bool SI8 = false>
-__device__ inline void dequant_codes(uint32_t cw, _Float16 s, uint32_t zz, const float (&mu)[N], float (&x)[N],
+template <int N, bool SI8 = false, typename S>
+__device__ inline void dequant_codes(uint32_t cw, S s, uint32_t zz, const float (&mu)[N], float (&x)[N],
                                      f16x2 cm = {}) {
   static_assert(N == 16 || N == 8, "16 or 8 channels per code word");
   const f16x2 zh = __builtin_bit_cast(f16x2, zz);
@@ -309,10 +328,16 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 
   // ---- stage the centroid tables of one epoch (App. D.1: BF16 centroids) with
   // threads [first, first + count) of the workgroup
+  // Plain BF16 instances stage the binary16 copies of the tables, which hold
+  // mu 2^-e (e per table, from the calibration block): Keys and Values then
+  // dequantise as mu 2^-e + (s 2^-e)(q - z), i.e. scaled by 2^-e exactly, and
+  // the Query fragment (times 2^e_k) and the output (times 2^e_v) undo it, so
+  // every product and sum of the attention is that of the BF16 tables.
+  constexpr bool H16 = TAB && !GEN && sizeof(T) == 2;
   auto stage_tables = [&](int e, int first, int count) {
     constexpr int PER_ROW = D * int(sizeof(T)) / 16;  // 16-byte chunks per centroid row
-    const uint4* sk = reinterpret_cast<const uint4*>(tab_of(e, a.o_mu_k));
-    const uint4* sv = reinterpret_cast<const uint4*>(tab_of(e, a.o_mu_v));
+    const uint4* sk = reinterpret_cast<const uint4*>(tab_of(e, H16 ? a.o_mu_k16 : a.o_mu_k));
+    const uint4* sv = reinterpret_cast<const uint4*>(tab_of(e, H16 ? a.o_mu_v16 : a.o_mu_v));
     for (int i = tid - first; i < Kc * PER_ROW; i += count) {
       const int row = i / PER_ROW, ch = i % PER_ROW;
       *reinterpret_cast<uint4*>(tabK + row * LY::TS + ch * (16 / int(sizeof(T)))) = sk[i];
@@ -321,6 +346,16 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   };
   // the staged epoch: that of the tile being dequantised (both roles track it)
   int se = epoch_at(t0 * KT);
+  // 2^-e of the staged binary16 tables (1 without them)
+  float sck = 1.0f, scv = 1.0f;
+  int ek = 0, ev = 0;
+  if constexpr (H16) {
+    const int32_t* e16 = reinterpret_cast<const int32_t*>(epoch_slab(se) + a.o_e16);
+    ek = e16[0];
+    ev = e16[1];
+    sck = ldexpf(1.0f, -ek);
+    scv = ldexpf(1.0f, -ev);
+  }
   if constexpr (TAB) stage_tables(se, 0, NT);
 
   // ======================= producer state (waves NC .. NC+NP-1)
@@ -519,18 +554,21 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
     // fields as the decode takes them: clamped ids, (1024 + z) pairs, binary16 scales
     const int k_id = int(p.k_idb) < Kc ? int(p.k_idb) : Kc - 1;
     uint32_t k_z[NSUB], v_z[2];
-    _Float16 k_s[NSUB], v_s[2];
+    // steps as loaded (binary16), or scaled by 2^-e (fp32) with the binary16 tables
+    std::conditional_t<H16, float, _Float16> k_s[NSUB], v_s[2];
     int v_id[2];
 #pragma unroll
     for (int u = 0; u < NSUB; ++u) {
       k_z[u] = (0x6400u + ((p.k_zb[u] >> (2 * (kgrp[u] % 4))) & 3)) * 0x00010001u;
-      k_s[u] = p.k_s[u];
+      if constexpr (H16) k_s[u] = (float)p.k_s[u] * sck;  // exact: a power of two
+      else k_s[u] = p.k_s[u];
     }
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       v_id[e] = int(p.v_idb[e]) < Kc ? int(p.v_idb[e]) : Kc - 1;
       v_z[e] = (0x6400u + ((p.v_zb[e] >> vzsh) & 3)) * 0x00010001u;
-      v_s[e] = p.v_s[e];
+      if constexpr (H16) v_s[e] = (float)p.v_s[e] * scv;
+      else v_s[e] = p.v_s[e];
     }
     const float c_s = (float)p.c_s;
     const int buf = int(t & 1);
@@ -553,7 +591,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 #pragma unroll
     for (int u = 0; u < NSUB; ++u) {
       float mu[16], x[16];
-      if (TAB && !k_e1) load_vals<T, 16>(tabK + k_id * LY::TS + kch0 + 16 * u, mu);
+      if (TAB && !k_e1) load_tab<H16, T, 16>(tabK + k_id * LY::TS + kch0 + 16 * u, mu);
       else load_vals<T, 16>((k_e1 ? gK1 : gK0) + k_id * D + kch0 + 16 * u, mu);
       if (GEN && !FULL && k_on_act) {
         uint32_t w[16 * sizeof(T) / 4];
@@ -578,9 +616,9 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       float mu0[CHV], mu1[CHV];
       const _Float16 vc0 = (_Float16)p.v_cb[0], vc1 = (_Float16)p.v_cb[1];
       const f16x2 vcm0 = {vc0, vc0}, vcm1 = {vc1, vc1};
-      if (TAB && !v_e1[0]) load_vals<T, CHV>(tabV + v_id[0] * LY::TS + vch0, mu0);
+      if (TAB && !v_e1[0]) load_tab<H16, T, CHV>(tabV + v_id[0] * LY::TS + vch0, mu0);
       else load_vals<T, CHV>((v_e1[0] ? gV1 : gV0) + v_id[0] * D + vch0, mu0);
-      if (TAB && !v_e1[1]) load_vals<T, CHV>(tabV + v_id[1] * LY::TS + vch0, mu1);
+      if (TAB && !v_e1[1]) load_tab<H16, T, CHV>(tabV + v_id[1] * LY::TS + vch0, mu1);
       else load_vals<T, CHV>((v_e1[1] ? gV1 : gV0) + v_id[1] * D + vch0, mu1);
       if (GEN && !FULL && (v_on_act[0] || v_on_act[1])) {
         uint32_t w[VW];
@@ -653,6 +691,13 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       for (int j = 0; j < KPL; ++j) vset(qreg[st], j, qvalid ? qrow[st * KSTEP + hf * KPL + j] : T(0.0f));
     }
     if constexpr (RP > 0) compute_u(se, ureg);
+    if constexpr (H16) {
+      // q 2^e_k (exact in BF16) against the Keys scaled by 2^-e_k
+#pragma unroll
+      for (int st = 0; st < D / KSTEP; ++st)
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) vset(qreg[st], j, T(ldexpf(float(vget(qreg[st], j)), ek)));
+    }
 #pragma unroll
     for (int cb = 0; cb < D / 32; ++cb)
 #pragma unroll
@@ -984,7 +1029,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
 #pragma unroll
         for (int cb = 0; cb < D / 32; ++cb)
 #pragma unroll
-          for (int i = 0; i < 16; ++i) po[cb * 32 + acc_row(i, hf)] = oacc[cb][i];
+          for (int i = 0; i < 16; ++i) po[cb * 32 + acc_row(i, hf)] = H16 ? ldexpf(oacc[cb][i], ev) : oacc[cb][i];
         if (hf == 0) {
           a.part_ml[2 * row] = m_run;
           a.part_ml[2 * row + 1] = l_tot;
@@ -992,7 +1037,8 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
       }
     } else {
       if (qvalid) {
-        const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+        // O / l; with the binary16 tables, times 2^e_v (the Values were scaled by 2^-e_v)
+        const float inv = l_tot > 0.0f ? (H16 ? ldexpf(1.0f / l_tot, ev) : 1.0f / l_tot) : 0.0f;
         T* orow = reinterpret_cast<T*>(a.out) + ((int64_t(b) * a.n_q + qi) * a.heads + h) * D;
 #pragma unroll
         for (int cb = 0; cb < D / 32; ++cb)

@@ -77,6 +77,42 @@ __global__ __launch_bounds__(256) void derive_kernel(uint8_t* calib, quantwm_cal
     bk[j] = sk;
     bv[j] = sv;
   }
+  if constexpr (sizeof(T) == 2) {
+    // binary16 copies of the BF16 tables for the attention producers, scaled by a
+    // power of two: the table's largest magnitude lands in [2^14, 2^15), so each
+    // component of at least 2^-31 of it is exact in binary16 (BF16 keeps 8
+    // significant bits) and none overflows
+    __shared__ float s_max[2][256];
+    float mxk = 0.0f, mxv = 0.0f;
+    for (int i = threadIdx.x; i < Kc * d; i += 256) {
+      mxk = fmaxf(mxk, fabsf(ldf(mk + i)));
+      mxv = fmaxf(mxv, fabsf(ldf(mv + i)));
+    }
+    s_max[0][threadIdx.x] = mxk;
+    s_max[1][threadIdx.x] = mxv;
+    __syncthreads();
+    for (int st = 128; st > 0; st /= 2) {
+      if (threadIdx.x < st) {
+        s_max[0][threadIdx.x] = fmaxf(s_max[0][threadIdx.x], s_max[0][threadIdx.x + st]);
+        s_max[1][threadIdx.x] = fmaxf(s_max[1][threadIdx.x], s_max[1][threadIdx.x + st]);
+      }
+      __syncthreads();
+    }
+    int ek = 0, ev = 0;
+    if (s_max[0][0] > 0.0f) { int x; frexpf(s_max[0][0], &x); ek = x - 15; }  // max in [2^(x-1), 2^x)
+    if (s_max[1][0] > 0.0f) { int x; frexpf(s_max[1][0], &x); ev = x - 15; }
+    _Float16* hk = reinterpret_cast<_Float16*>(slab + C.mu_k16);
+    _Float16* hv = reinterpret_cast<_Float16*>(slab + C.mu_v16);
+    for (int i = threadIdx.x; i < Kc * d; i += 256) {
+      hk[i] = (_Float16)ldexpf(ldf(mk + i), -ek);
+      hv[i] = (_Float16)ldexpf(ldf(mv + i), -ev);
+    }
+    if (threadIdx.x == 0) {
+      int32_t* e16 = reinterpret_cast<int32_t*>(slab + C.e16);
+      e16[0] = ek;
+      e16[1] = ev;
+    }
+  }
 }
 
 // Copy method-level tables into the slabs: mu [BH][Kc][d], w [BH][d],

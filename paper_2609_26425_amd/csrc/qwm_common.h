@@ -89,6 +89,10 @@ inline quantwm_calib_layout calib_layout(const quantwm_config& c) {
   L.lam = take(r * 4);
   L.u_dr = take(int64_t(rank_stride(c)) * d * 4);
   L.m = take(c.metric == QWM_METRIC_FULL ? d * d * 4 : 0);
+  const bool h16 = c.dtype == QWM_BF16;  // binary16 copies for the attention producers
+  L.mu_k16 = take(h16 ? K * d * 2 : 0);
+  L.mu_v16 = take(h16 ? K * d * 2 : 0);
+  L.e16 = take(h16 ? 8 : 0);
   L.slab_bytes = at;
   return L;
 }
@@ -116,6 +120,7 @@ struct AttendArgs {
   const uint8_t* calib;
   int64_t slab;
   int64_t o_mu_k, o_mu_v, o_u_t;
+  int64_t o_mu_k16, o_mu_v16, o_e16;  // binary16 table copies and their exponents (BF16 configs)
   const uint8_t* cache;
   CacheLayout L;
   const void* q;

@@ -42,7 +42,8 @@ class Config(ctypes.Structure):
 class CalibLayout(ctypes.Structure):
     """Mirror of quantwm_calib_layout (byte offsets inside one (b, h) slab)."""
     _fields_ = [(n, ctypes.c_int64) for n in
-                ("slab_bytes", "mu_k", "mu_v", "a_k", "b_k", "a_v", "b_v", "w", "wg", "u_t", "lam", "u_dr", "m")]
+                ("slab_bytes", "mu_k", "mu_v", "a_k", "b_k", "a_v", "b_v", "w", "wg", "u_t", "lam", "u_dr", "m",
+                 "mu_k16", "mu_v16", "e16")]
 
 
 def _load():
@@ -69,7 +70,7 @@ def _load():
         "quantwm_attend_active": (I32, [C, P, P, I64, P, P, I64, P, I64, I64, I32, P, P, P, SZ, P]),
         "quantwm_attend_epochs": (I32, [C, P, I32, ctypes.POINTER(I64), P, I64, P, P, I64, P, I64, I64, I32, P, P,
                                         P, SZ, P]),
-        "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I32, P, P]),
+        "quantwm_logits": (I32, [C, P, P, I64, P, I64, I64, I64, I32, P, P]),
         "quantwm_attend_noalloc": (I32, [C, P, P, I64, P, I64, I64, I32, P, P, P]),
         "quantwm_attend_active_workspace_bytes": (SZ, [C, I64, I64, I64]),
         "quantwm_attend_epochs_workspace_bytes": (SZ, [C, I32, ctypes.POINTER(I64), I64, I64, I64]),

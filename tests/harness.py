@@ -52,9 +52,11 @@ def _gen_sources(wl, sources, what, n):
     return out
 
 
-def build_oracle_case(wl: synth.Workload, max_sources: int = 3, cold: bool = False, transform=None) -> OracleCase:
+def build_oracle_case(wl: synth.Workload, max_sources: int = 3, cold: bool = False, transform=None,
+                      tables_edit=None) -> OracleCase:
     """transform(k, v, q) -> (k, v, q) edits the generated source inputs (for edge
-    cases); its results are rounded to the workload's dtype."""
+    cases); its results are rounded to the workload's dtype. tables_edit(tables)
+    edits the calibrated tables in place before the cache is appended."""
     sources = sources_for(wl, max_sources)
     S = len(sources)
     cfg = oracle.cfg_of(1, S, wl.head_dim, wl.n_centroids, wl.group_size, wl.rank, wl.top_m,
@@ -69,6 +71,8 @@ def build_oracle_case(wl: synth.Workload, max_sources: int = 3, cold: bool = Fal
     nc = min(wl.chunk, wl.n_cache)
     tables = oracle.calibrate(cfg, qh, np.ascontiguousarray(k[:, :nc]), np.ascontiguousarray(v[:, :nc]),
                               wl.kmeans_iters)
+    if tables_edit is not None:
+        tables_edit(tables)
     cache = oracle.new_cache(cfg)
     diag = oracle.append(cfg, tables, cache, 0, k, v, diagnostics=True)
     lay = packed.layout(1, S, wl.head_dim, wl.group_size, wl.rank, wl.n_cache, wl.storage, wl.coef_rows,

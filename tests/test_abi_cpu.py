@@ -19,6 +19,25 @@ def declared_symbols():
     return sorted(set(re.findall(r"\b(quantwm_[a-z_0-9]+)\s*\(", text)))
 
 
+def _declared_param_counts():
+    """Entry point -> number of parameters, from the declarations in quantwm.h."""
+    text = open(os.path.join(ROOT, "include", "quantwm.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    out = {}
+    for m in re.finditer(r"\b(quantwm_[a-z_0-9]+)\s*\(([^;{]*?)\)\s*;", text):
+        params = m.group(2).strip()
+        out[m.group(1)] = 0 if params in ("", "void") else params.count(",") + 1
+    return out
+
+
+def test_binding_argtypes_match_the_header():
+    # every ctypes signature in the binding has as many arguments as the C declaration
+    counts = _declared_param_counts()
+    lib = qw.library()
+    for name in qw.EXPORTED:
+        assert len(getattr(lib, name).argtypes) == counts[name], name
+
+
 def test_header_symbols_are_exported():
     names = declared_symbols()
     assert len(names) >= 10
@@ -47,14 +66,19 @@ def test_sizes_agree_with_the_oracle_format(shape, storage):
 
 @pytest.mark.parametrize("d", [64, 128])
 def test_full_metric_adds_the_matrix_to_the_calibration_block(d):
-    # QWM_METRIC_FULL keeps the cache format and appends Mn ([d][d] fp32) to the slab.
+    # QWM_METRIC_FULL keeps the cache format and adds Mn ([d][d] fp32) to the slab,
+    # after U_r and before the binary16 table copies.
     diag = qw.make_config(1, 3, d, 32, 32, 8, 4, 500, "bf16")
     full = qw.make_config(1, 3, d, 32, 32, 8, 4, 500, "bf16", metric=qw.METRIC_FULL)
     assert qw.quantwm_cache_bytes(full) == qw.quantwm_cache_bytes(diag)
     Ld, Lf = qw.quantwm_calib_offsets(diag), qw.quantwm_calib_offsets(full)
-    assert Lf.m == Ld.slab_bytes and Lf.slab_bytes == Ld.slab_bytes + d * d * 4
+    assert Lf.m == Ld.m and Lf.mu_k16 == Lf.m + d * d * 4 and Lf.slab_bytes == Ld.slab_bytes + d * d * 4
     assert all(getattr(Lf, n) == getattr(Ld, n) for n in ("mu_k", "a_k", "b_k", "w", "u_t", "lam", "u_dr"))
-    assert Ld.m == Ld.slab_bytes  # no bytes without the full metric
+    assert Ld.m == Ld.mu_k16  # no bytes without the full metric
+    # the binary16 copies of the centroid tables and their two exponents (BF16 configs)
+    assert Ld.mu_v16 - Ld.mu_k16 == (32 * d * 2 + 255) // 256 * 256 and Ld.slab_bytes == Ld.e16 + 256
+    f32 = qw.quantwm_calib_offsets(qw.make_config(1, 3, d, 32, 32, 8, 4, 500, "f32"))
+    assert f32.mu_k16 == f32.mu_v16 == f32.e16 == f32.slab_bytes  # none for fp32 tables
     with pytest.raises(qw.QuantwmError) as e:
         qw.quantwm_token_bytes(qw.make_config(1, 3, d, 32, 32, 8, 4, 500, "bf16", metric=2))
     assert e.value.status == qw.ERR_INVALID_ARG and "metric" in qw.quantwm_last_error()

@@ -49,6 +49,13 @@ CASES = [
     (_wl("kc1-i8", n_centroids=1, head_dim=64, group_size=16, rank=4, q_rank=4, storage=1), None),
     (_wl("one-partial-tile-i8-gate", n_cache=40, n_q=1, q_start=39, frame_tokens=1, chunk=40, n_hist=100,
          storage=3), None),
+    # the attention producers read binary16 copies of the centroid tables scaled by a
+    # power of two: Keys 2^11 times larger put the largest Key centroid components
+    # past binary16's range (so the scale is 2^-e with e > 0; the Value tables take
+    # e < 0 in every case), and a centroid component
+    # of 3e-12 lies below the copy's resolution (it reads as 0 there)
+    (_wl("large-keys"), "large_keys"),
+    (_wl("tiny-centroid-component"), "tiny_centroid"),
 ]
 
 
@@ -61,15 +68,35 @@ def _transform(wl, kind):
         return lambda k, v, q: (k, v, np.zeros_like(q))
     if kind == "big_q":
         return lambda k, v, q: (k, v, q * 30.0)
+    if kind == "large_keys":
+        return lambda k, v, q: (k * 2048.0, v, q)
+    if kind == "tiny_centroid":
+        return None
     raise ValueError(kind)
+
+
+def _tables_edit(kind):
+    if kind != "tiny_centroid":
+        return None
+
+    def edit(tables):
+        # one tiny component in centroid 3 of every head's Key and Value tables
+        # (a BF16 value, far below 2^-31 of the table's largest magnitude)
+        tiny = float(synth.round_to(np.array([3e-12]), "bf16")[0])
+        tables[0][..., 3, 5] = tiny
+        tables[1][..., 3, 7] = -tiny
+    return edit
 
 
 @pytest.mark.parametrize("wl,kind", CASES, ids=[c[0].name for c in CASES])
 def test_edge_case(wl, kind):
     key = (wl.name, 64)
     if key not in tp._cases:
-        tp._cases[key] = harness.build_oracle_case(wl, 64, transform=_transform(wl, kind))
+        tp._cases[key] = harness.build_oracle_case(wl, 64, transform=_transform(wl, kind),
+                                                   tables_edit=_tables_edit(kind))
     case = tp._cases[key]
+    if kind == "large_keys":
+        assert np.abs(case.tables[0]).max() > 65504.0, "the Key table should leave binary16's range"
     if kind == "zero_residual":
         import packed
         f = packed.fields(case.cache, case.lay, 0, 0, wl.n_cache)
