@@ -66,13 +66,16 @@ def append_bytes(wl, n_new) -> float:
 
 
 def append_flops(wl, n_new) -> float:
+    """Algorithmic flops of one append call: the two centroid searches (2 Kc d
+    each), PSAC (2 d r) and about 28 per channel for the Eq. 12 score and the
+    residuals."""
     d = wl.head_dim
     return wl.batch * wl.heads * n_new * (4 * wl.n_centroids * d + 2 * d * wl.rank + 28 * d)
 
 
 # the device-code sources of each kernel (their digest dates a counter summary)
-KERNEL_SOURCES = {"attend": ["attend.hip", "attend_shape.h", "qwm_common.h"],
-                  "append": ["append.hip", "qwm_common.h"]}
+KERNEL_SOURCES = {"attend": ["attend.hip", "attend_shape.h", "qwm_common.h", "xcd_order.h"],
+                  "append": ["append_bf16.hip", "append.hip", "append_common.h", "qwm_common.h", "xcd_order.h"]}
 
 
 def source_digest(kernel: str) -> str:
@@ -302,8 +305,13 @@ def kernel_record(wl, n_new, app_all, att_all, ws_bytes):
         "attend_key_splits": splits,
         "append_tokens": bh * n_new,
         "append_GBps": append_bytes(wl, n_new) / (app_ms * 1e-3) / 1e9,
-        "append_valu_frac": append_flops(wl, n_new) / (app_ms * 1e-3) / 1e12 / PEAK_FP32_VALU_TFLOPS,
+        # BF16 Keys and Values: the searches run on the matrix cores and the rest
+        # (selection, Eq. 12 score, residuals, PSAC) on the vector ALU, so no
+        # single peak bounds the kernel; fp32 ones run everything on the vector ALU
+        "append_search_on": "mfma" if wl.dtype == "bf16" else "valu",
     }
+    if wl.dtype != "bf16":
+        rec["append_valu_frac"] = append_flops(wl, n_new) / (app_ms * 1e-3) / 1e12 / PEAK_FP32_VALU_TFLOPS
     rec["append_hbm_frac"] = rec["append_GBps"] / PEAK_HBM_GBPS
     for k in ("attend", "append"):
         t = measured_traffic(k, wl.name)
@@ -334,6 +342,8 @@ def main():
     ap.add_argument("--no-sub", action="store_true",
                     help="skip the per-workload records of the other configurations (for kernel traces)")
     ap.add_argument("--sub-steps", type=int, default=10)
+    ap.add_argument("--sources", type=int, default=0,
+                    help="generate this many synthetic heads and repeat them over the launch (0: every head)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one plain 1 GiB device copy kernel (read 1 GiB, write 1 GiB) outside the timed "
                          "region, as the scale for FETCH_SIZE / WRITE_SIZE counter runs")
@@ -350,7 +360,7 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     print(f"[bench] {wl.name}: inputs, calibration, prefill of {args.copies} caches", file=sys.stderr, flush=True)
-    P = Prepared(wl, args.copies)
+    P = Prepared(wl, args.copies, n_sources=args.sources or None)
     cfg, calib, n_new = P.cfg, P.calib, P.n_new
 
     if args.copy_probe:
@@ -433,7 +443,7 @@ def main():
         "attend_key_splits": rec["attend_key_splits"],
         "append_GBps": rec["append_GBps"],
         "append_hbm_frac": rec["append_hbm_frac"],
-        "append_valu_frac": rec["append_valu_frac"],
+        "append_search_on": rec["append_search_on"],
         "roofline": {"kernel": "attend", "bound": "mfma", "achieved": rec["attend_TFLOPs"], "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": rec["attend_TFLOPs"] / PEAK_BF16_TFLOPS,
                      "traffic": rec["attend_traffic_bytes"]},

@@ -152,10 +152,14 @@ size_t quantwm_calib_bytes(const quantwm_config* cfg);
  *                               the table's largest magnitude in [2^14, 2^15) (0 for an
  *                               all-zero table), rounded to binary16: exact for every
  *                               component of at least 2^-31 times that largest one
- *   e16         [2]     int32   e_k, e_v (BF16 configs only) */
+ *   e16         [2]     int32   e_k, e_v (BF16 configs only)
+ *   a_k3        [3][Kc][d] BF16  BF16 configs only: a_k split into three BF16 planes
+ *                               whose sum is a_k exactly (the first two truncate, the
+ *                               third is the exact remainder) for the matrix-core
+ *                               Key search */
 typedef struct {
   int64_t slab_bytes;
-  int64_t mu_k, mu_v, a_k, b_k, a_v, b_v, w, wg, u_t, lam, u_dr, m, mu_k16, mu_v16, e16;
+  int64_t mu_k, mu_v, a_k, b_k, a_v, b_v, w, wg, u_t, lam, u_dr, m, mu_k16, mu_v16, e16, a_k3;
 } quantwm_calib_layout;
 quantwm_status quantwm_calib_offsets(const quantwm_config* cfg, quantwm_calib_layout* out);
 

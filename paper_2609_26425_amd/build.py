@@ -1,7 +1,7 @@
 """Builds libquantwm.so (the gfx950 HIP kernels plus the C ABI) in-tree.
 
-Translation units compile in parallel: append.hip once per (element type,
-head_dim, group size), attend.hip once per (element type, head_dim, PSAC rank padding),
+Translation units compile in parallel: append.hip (fp32) and append_bf16.hip
+once per (head_dim, group size), attend.hip once per (element type, head_dim, PSAC rank padding),
 attend_host.hip, calib.hip, coef.hip, api.hip and the host eigensolver; the
 objects link into ``paper_2609_26425_amd/libquantwm.so``.
 """
@@ -29,11 +29,13 @@ HIPFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contra
 
 def _units():
     units = []
-    for tn, t in (("f32", "float"), ("bf16", "qwm::bf16")):
+    # append_bf16: no NaN semantics either (its inputs are finite), so the group
+    # ranges are v_min/v_max rather than compare-and-select pairs
+    for tn, src, extra in (("f32", "append.hip", []), ("bf16", "append_bf16.hip", ["-fno-honor-nans"])):
         for d in (64, 128):
             for g in (16, 32, 64):
-                units.append((f"append_{tn}_{d}_g{g}.o", "append.hip",
-                              [f"-DQWM_APPEND_T={t}", f"-DQWM_APPEND_D={d}", f"-DQWM_APPEND_G={g}"]))
+                units.append((f"append_{tn}_{d}_g{g}.o", src,
+                              extra + [f"-DQWM_APPEND_D={d}", f"-DQWM_APPEND_G={g}"]))
     # attend: no NaN semantics, so maxima of matrix-core results are plain
     # v_max3_f32 without a quieting v_max_f32 x, x per input (its logits and
     # running maxima are finite or -inf). One unit per (element type, head_dim,

@@ -82,9 +82,10 @@ quantwm_status check_dev(const void* p, const char* name, bool required = true) 
 
 template <typename T, int D>
 hipError_t launch_append_td(const qwm::AppendArgs& a, int g, int batch, hipStream_t s) {
-  if (g == 16) return qwm::launch_append_g<T, D, 16>(a, batch, s);
-  if (g == 32) return qwm::launch_append_g<T, D, 32>(a, batch, s);
-  if (g == 64) return qwm::launch_append_g<T, D, 64>(a, batch, s);
+  constexpr bool bf = sizeof(T) == 2;
+  if (g == 16) return bf ? qwm::launch_append_bf16<D, 16>(a, batch, s) : qwm::launch_append_f32<D, 16>(a, batch, s);
+  if (g == 32) return bf ? qwm::launch_append_bf16<D, 32>(a, batch, s) : qwm::launch_append_f32<D, 32>(a, batch, s);
+  if (g == 64) return bf ? qwm::launch_append_bf16<D, 64>(a, batch, s) : qwm::launch_append_f32<D, 64>(a, batch, s);
   return hipErrorInvalidValue;
 }
 
@@ -427,12 +428,14 @@ quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void
   if (coef_f32_out && (reinterpret_cast<uintptr_t>(coef_f32_out) & 3))
     return fail(QWM_ERR_INVALID_ARG, "coef_f32_out is not 4-byte aligned");
   if (n_new > (int64_t(1) << 31) - 256) return fail(QWM_ERR_UNSUPPORTED, "n_new too large for one call");
+  if (cfg->dtype == QWM_BF16 && (n_new + 127) / 128 * cfg->heads * cfg->batch >= (int64_t(1) << 24))
+    return fail(QWM_ERR_UNSUPPORTED, "ceil(n_new / 128) * heads * batch must be below 2^24 (one launch)");
   const quantwm_calib_layout C = qwm::calib_layout(*cfg);
   qwm::AppendArgs a;
   a.calib = static_cast<const uint8_t*>(calib);
   a.slab = C.slab_bytes;
   a.o_mu_k = C.mu_k; a.o_mu_v = C.mu_v; a.o_a_k = C.a_k; a.o_b_k = C.b_k;
-  a.o_a_v = C.a_v; a.o_b_v = C.b_v; a.o_wg = C.wg; a.o_u_t = C.u_t; a.o_u_dr = C.u_dr;
+  a.o_a_v = C.a_v; a.o_b_v = C.b_v; a.o_wg = C.wg; a.o_u_t = C.u_t; a.o_u_dr = C.u_dr; a.o_a_k3 = C.a_k3;
   a.o_lam = C.lam;
   a.gate = (cfg->storage & QWM_STORE_GATE) && cfg->rank > 0 ? 1 : 0;
   a.cache = static_cast<uint8_t*>(cache);

@@ -1,7 +1,8 @@
-// Quantize-on-append for gfx950: QSAC centroid choice (Sec. 4.1, Eq. 9-12),
-// group-wise INT2 residual (Eq. 1-4, App. D.1) and PSAC coefficients
-// (Sec. 4.2, Eq. 13 and 16) for Keys; nearest centroid + INT2 residual for
-// Values.
+// Quantize-on-append for fp32 Keys and Values on gfx950: QSAC centroid choice
+// (Sec. 4.1, Eq. 9-12), group-wise INT2 residual (Eq. 1-4, App. D.1) and PSAC
+// coefficients (Sec. 4.2, Eq. 13 and 16) for Keys; nearest centroid + INT2
+// residual for Values. (BF16 Keys and Values: append_bf16.hip, the same outputs
+// with the searches on the matrix cores.)
 //
 // Mapping: one token-head per lane, 256 tokens of one (b, h) per workgroup. The
 // candidate search is the dominant cost (Kc * d multiply-adds per token for K
@@ -13,83 +14,19 @@
 // but FMAs in the inner loop. Everything that turns a float into an integer
 // (the Eq. 12 score, the INT2 and INT8 codes) follows the equations' operation
 // order in fp32 with IEEE division and round-to-nearest-even.
-#include "qwm_common.h"
-
-#include <type_traits>
+#include "append_common.h"
 
 namespace qwm {
 namespace {
 
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E) step S.
-// Keeps register-array indices static where #pragma unroll gives up on large bodies.
-template <int B, int E, int S = 1, typename F>
-__device__ inline void static_for(F&& f) {
-  if constexpr (B < E) {
-    f(std::integral_constant<int, B>{});
-    static_for<B + S, E, S>(f);
-  }
-}
-
-__device__ inline float ld(const float* p) { return *p; }
-__device__ inline float ld(const bf16* p) { return (float)*p; }
-
 template <typename T, int D>
 __device__ inline void load_row(const T* __restrict__ src, float (&x)[D]) {
-  if constexpr (sizeof(T) == 2) {
-    const uint4* p = reinterpret_cast<const uint4*>(src);
+  static_assert(sizeof(T) == 4, "fp32 rows");
+  const float4* p = reinterpret_cast<const float4*>(src);
 #pragma unroll
-    for (int i = 0; i < D / 8; ++i) {
-      uint4 u = p[i];
-      uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        x[8 * i + 2 * k] = __uint_as_float(w[k] << 16);
-        x[8 * i + 2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
-      }
-    }
-  } else {
-    const float4* p = reinterpret_cast<const float4*>(src);
-#pragma unroll
-    for (int i = 0; i < D / 4; ++i) {
-      float4 u = p[i];
-      x[4 * i] = u.x; x[4 * i + 1] = u.y; x[4 * i + 2] = u.z; x[4 * i + 3] = u.w;
-    }
-  }
-}
-
-__device__ inline float f16_round(float s) {
-  // FP16 storage of a scale (App. D.1): saturate, then round to nearest even.
-  s = fminf(s, 65504.0f);
-  return (float)(_Float16)s;
-}
-
-__device__ inline uint16_t f16_bits(float exact) {
-  return __builtin_bit_cast(uint16_t, (_Float16)exact);
-}
-
-// rint(x/s) for N residuals x = xv - mu with the IEEE quotient of Eq. 1, without
-// N full divisions. t = x * RN(1/s) lies within 3 * 2^-24 * |x/s| of RN(x/s);
-// every residual satisfies |x/s| <= 3.01 here (the range spans 3 steps), so the
-// two differ by less than 2^-20 and round to the same integer unless t is
-// within 2^-19 of a half-integer (or |t| > 4, out of this bound). If any lane
-// of the wave meets such a case the whole chunk takes the exact division.
-template <int N>
-__device__ inline void round_quotients(const float (&xv)[N], const float (&mu)[N], float s, float inv,
-                                       float (&t)[N]) {
-  bool near = false;
-#pragma unroll
-  for (int c = 0; c < N; ++c) {
-    const float q = (xv[c] - mu[c]) * inv;
-    const float k = rintf(q);
-    near |= fabsf(q - k) > 0.5f - 0x1p-19f || fabsf(q) > 4.0f;
-    t[c] = k;
-  }
-  if (__any(near)) {
-    const float sd = s != 0.0f ? s : 1.0f;
-#pragma unroll
-    for (int c = 0; c < N; ++c) t[c] = rintf((xv[c] - mu[c]) / sd);
+  for (int i = 0; i < D / 4; ++i) {
+    float4 u = p[i];
+    x[4 * i] = u.x; x[4 * i + 1] = u.y; x[4 * i + 2] = u.z; x[4 * i + 3] = u.w;
   }
 }
 
@@ -255,7 +192,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
   float bd[MM];
   int bi[MM];
 #pragma unroll
-  for (int p = 0; p < MM; ++p) { bd[p] = __builtin_inff(); bi[p] = 0x7fffffff; }
+  // ids start at 0, a valid row: with an infinite or NaN distance (inputs out of
+  // range) nothing enters the list, and the score below still reads real rows
+  for (int p = 0; p < MM; ++p) { bd[p] = __builtin_inff(); bi[p] = 0; }
   for (int j = 0; j < Kc; j += 4) {
     float acc[4];
     int row[4];
@@ -317,43 +256,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
       zv = better ? j + u : zv;
     }
   };
-  if constexpr (sizeof(T) == 2) {
-    // BF16 Values and BF16 centroids: d'_j = b_j + sum_c mu_jc (-2 v_c), two
-    // channels per v_dot2_f32_bf16 (exact products). -2 v_c is exact in BF16
-    // for finite |v_c| < 2^127; the pairs come straight from the table.
-    uint32_t vp[D / 2];
-    {
-      const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.v) + src);
-#pragma unroll
-      for (int i = 0; i < D / 8; ++i) {
-        const uint4 u = p[i];
-        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const uint32_t lo = __float_as_uint(__uint_as_float(w[k] << 16) * -2.0f);
-          const uint32_t hi = __float_as_uint(__uint_as_float(w[k] & 0xffff0000u) * -2.0f);
-          vp[4 * i + k] = (hi & 0xffff0000u) | (lo >> 16);
-        }
-      }
-    }
-    const uint32_t* __restrict__ mvp = reinterpret_cast<const uint32_t*>(muv);  // [Kc][D/2] BF16 pairs
-    for (int j = 0; j < Kc; j += 4) {
-      float acc[4];
-      int row[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        row[u] = min(j + u, Kc - 1);
-        acc[u] = bv[row[u]];
-      }
-#pragma unroll
-      for (int c = 0; c < D / 2; ++c)
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          acc[u] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, mvp[row[u] * (D / 2) + c]),
-                                                   __builtin_bit_cast(bf16x2, vp[c]), acc[u], false);
-      take(j, acc);
-    }
-  } else {
+  {
     load_row<T, D>(reinterpret_cast<const T*>(a.v) + src, x);
     for (int j = 0; j < Kc; j += 4) {
       float acc[4];
@@ -492,13 +395,13 @@ hipError_t launch_dgs(const AppendArgs& a, int batch, hipStream_t s) {
 
 }  // namespace
 
-// This file is compiled once per (element type, head_dim, group size):
-// QWM_APPEND_T, QWM_APPEND_D and QWM_APPEND_G select the instantiations.
-template <typename T, int D, int G>
-hipError_t launch_append_g(const AppendArgs& a, int batch, hipStream_t s) {
-  return a.L.i8 ? launch_dgs<T, D, G, true>(a, batch, s) : launch_dgs<T, D, G, false>(a, batch, s);
+// This file is compiled once per (head_dim, group size): QWM_APPEND_D and
+// QWM_APPEND_G select the instantiations.
+template <int D, int G>
+hipError_t launch_append_f32(const AppendArgs& a, int batch, hipStream_t s) {
+  return a.L.i8 ? launch_dgs<float, D, G, true>(a, batch, s) : launch_dgs<float, D, G, false>(a, batch, s);
 }
 
-template hipError_t launch_append_g<QWM_APPEND_T, QWM_APPEND_D, QWM_APPEND_G>(const AppendArgs&, int, hipStream_t);
+template hipError_t launch_append_f32<QWM_APPEND_D, QWM_APPEND_G>(const AppendArgs&, int, hipStream_t);
 
 }  // namespace qwm

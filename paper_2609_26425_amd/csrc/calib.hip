@@ -59,6 +59,23 @@ __global__ __launch_bounds__(256) void derive_kernel(uint8_t* calib, quantwm_cal
     av[i] = -2.0f * mvv;
   }
   __syncthreads();  // b_k reads the a_k rows written by other threads
+  if constexpr (sizeof(T) == 2) {
+    // a_k as three BF16 planes with an exact sum, for the matrix-core search:
+    // p0 keeps a's top 8 significant bits (truncated), p1 the top 8 of the exact
+    // remainder a - p0, and p2 = a - p0 - p1, which has at most 8 significant
+    // bits left and so is a BF16 value (for |a| above 2^-110 or so)
+    uint16_t* pl = reinterpret_cast<uint16_t*>(slab + C.a_k3);
+    for (int i = threadIdx.x; i < Kc * d; i += 256) {
+      const float av0 = ak[i];
+      const uint32_t u0 = __float_as_uint(av0) & 0xffff0000u;
+      const float r1 = av0 - __uint_as_float(u0);
+      const uint32_t u1 = __float_as_uint(r1) & 0xffff0000u;
+      const float r2 = r1 - __uint_as_float(u1);
+      pl[i] = uint16_t(u0 >> 16);
+      pl[Kc * d + i] = uint16_t(u1 >> 16);
+      pl[2 * Kc * d + i] = __builtin_bit_cast(uint16_t, bf16(r2));
+    }
+  }
   const T* ut = reinterpret_cast<const T*>(slab + C.u_t);
   float* udr = reinterpret_cast<float*>(slab + C.u_dr);
   const int rs = r == 0 ? 0 : (r <= 16 ? 16 : 32);

@@ -93,6 +93,7 @@ inline quantwm_calib_layout calib_layout(const quantwm_config& c) {
   L.mu_k16 = take(h16 ? K * d * 2 : 0);
   L.mu_v16 = take(h16 ? K * d * 2 : 0);
   L.e16 = take(h16 ? 8 : 0);
+  L.a_k3 = take(h16 ? 3 * K * d * 2 : 0);
   L.slab_bytes = at;
   return L;
 }
@@ -103,6 +104,7 @@ struct AppendArgs {
   const uint8_t* calib;
   int64_t slab;
   int64_t o_mu_k, o_mu_v, o_a_k, o_b_k, o_a_v, o_b_v, o_wg, o_u_t, o_u_dr;
+  int64_t o_a_k3;  // BF16 configs: the three BF16 planes of a_k
   uint8_t* cache;
   CacheLayout L;
   const void* k;
@@ -153,9 +155,13 @@ struct AttendArgs {
 // keys per attention tile
 constexpr int kAttendTileKeys = 64;
 
-// Launchers. Append: one translation unit per (element type, head_dim, group size).
-template <typename T, int D, int G>
-hipError_t launch_append_g(const AppendArgs& a, int batch, hipStream_t s);
+// Launchers. Append: one translation unit per (element type, head_dim, group
+// size); fp32 Keys and Values on the vector ALU, BF16 ones with the centroid
+// searches on the matrix cores.
+template <int D, int G>
+hipError_t launch_append_f32(const AppendArgs& a, int batch, hipStream_t s);
+template <int D, int G>
+hipError_t launch_append_bf16(const AppendArgs& a, int batch, hipStream_t s);
 hipError_t launch_attend_f32(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s);
 hipError_t launch_attend_bf16(const AttendArgs& a, int d, int batch, bool logits, hipStream_t s);
 size_t attend_lds_bytes(int d, int elem, int rank, int n_centroids, bool tables_in_lds);

@@ -43,7 +43,7 @@ class CalibLayout(ctypes.Structure):
     """Mirror of quantwm_calib_layout (byte offsets inside one (b, h) slab)."""
     _fields_ = [(n, ctypes.c_int64) for n in
                 ("slab_bytes", "mu_k", "mu_v", "a_k", "b_k", "a_v", "b_v", "w", "wg", "u_t", "lam", "u_dr", "m",
-                 "mu_k16", "mu_v16", "e16")]
+                 "mu_k16", "mu_v16", "e16", "a_k3")]
 
 
 def _load():

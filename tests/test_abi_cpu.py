@@ -76,9 +76,11 @@ def test_full_metric_adds_the_matrix_to_the_calibration_block(d):
     assert all(getattr(Lf, n) == getattr(Ld, n) for n in ("mu_k", "a_k", "b_k", "w", "u_t", "lam", "u_dr"))
     assert Ld.m == Ld.mu_k16  # no bytes without the full metric
     # the binary16 copies of the centroid tables and their two exponents (BF16 configs)
-    assert Ld.mu_v16 - Ld.mu_k16 == (32 * d * 2 + 255) // 256 * 256 and Ld.slab_bytes == Ld.e16 + 256
+    assert Ld.mu_v16 - Ld.mu_k16 == (32 * d * 2 + 255) // 256 * 256 and Ld.a_k3 == Ld.e16 + 256
+    # the three BF16 planes of a_k for the matrix-core search (BF16 configs)
+    assert Ld.slab_bytes == Ld.a_k3 + (3 * 32 * d * 2 + 255) // 256 * 256
     f32 = qw.quantwm_calib_offsets(qw.make_config(1, 3, d, 32, 32, 8, 4, 500, "f32"))
-    assert f32.mu_k16 == f32.mu_v16 == f32.e16 == f32.slab_bytes  # none for fp32 tables
+    assert f32.mu_k16 == f32.mu_v16 == f32.e16 == f32.a_k3 == f32.slab_bytes  # none for fp32 tables
     with pytest.raises(qw.QuantwmError) as e:
         qw.quantwm_token_bytes(qw.make_config(1, 3, d, 32, 32, 8, 4, 500, "bf16", metric=2))
     assert e.value.status == qw.ERR_INVALID_ARG and "metric" in qw.quantwm_last_error()
