@@ -309,6 +309,7 @@ def kernel_record(wl, n_new, app_all, att_all, ws_bytes):
         # (selection, Eq. 12 score, residuals, PSAC) on the vector ALU, so no
         # single peak bounds the kernel; fp32 ones run everything on the vector ALU
         "append_search_on": "mfma" if wl.dtype == "bf16" else "valu",
+        "append_algorithmic_TFLOPs": append_flops(wl, n_new) / (app_ms * 1e-3) / 1e12,
     }
     if wl.dtype != "bf16":
         rec["append_valu_frac"] = append_flops(wl, n_new) / (app_ms * 1e-3) / 1e12 / PEAK_FP32_VALU_TFLOPS
@@ -444,6 +445,7 @@ def main():
         "append_GBps": rec["append_GBps"],
         "append_hbm_frac": rec["append_hbm_frac"],
         "append_search_on": rec["append_search_on"],
+        "append_algorithmic_TFLOPs": rec["append_algorithmic_TFLOPs"],
         "roofline": {"kernel": "attend", "bound": "mfma", "achieved": rec["attend_TFLOPs"], "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": rec["attend_TFLOPs"] / PEAK_BF16_TFLOPS,
                      "traffic": rec["attend_traffic_bytes"]},

@@ -68,14 +68,6 @@ __device__ inline float bf_el(const uint4& u) {
   return (E & 1) ? bf_hi(w) : bf_lo(w);
 }
 
-template <int N>
-__device__ inline void unpack(const uint4 (&u)[N / 8], float (&x)[N]) {
-  static_for<0, N>([&](auto ci) {
-    constexpr int c = decltype(ci)::value;
-    x[c] = bf_el<c % 8>(u[c / 8]);
-  });
-}
-
 // Insert (d, j) into a list sorted by d; j exceeds every id in the list, so an
 // equal distance goes after its equals. med3(l[p - 1], d, l[p]) is the new l[p].
 template <int MM>
@@ -133,7 +125,16 @@ struct Halves {
   static __device__ inline int group(int hf, int gl) { return SPAN ? 0 : hf * GL + gl; }
 };
 
-// Residual of the lane's half-row x against the half-row mrow of centroid
+// Makes the compiler forget what the packed words hold, so that values unpacked
+// from them earlier are not kept live to be reused later (a whole unpacked
+// half-row). Emits no instruction.
+template <int N>
+__device__ inline void forget(uint4 (&u)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(u[i].x), "+v"(u[i].y), "+v"(u[i].z), "+v"(u[i].w));
+}
+
+// Residual of the lane's BF16 half-row xh against the half-row mrow of centroid
 // z (Eq. 1-2 with q_min = 0, q_max = 3, the range extended to contain 0, the
 // residual quantised with the stored scale). Fills the code words of the half
 // (16 channels per word), the zero-points, scales (SI8: 8-bit codes and the
@@ -144,12 +145,13 @@ struct Halves {
 // group's range pass precedes its code pass, and with 8-bit scales every range
 // pass comes first (the groups share the secondary scale).
 template <int D, int G, bool SI8, typename F, typename FC>
-__device__ inline void residual_half(const float (&x)[D / 2], const uint4* __restrict__ mrow, int hf,
+__device__ inline void residual_half(uint4 (&xh)[D / 16], const uint4* __restrict__ mrow, int hf,
                                      uint32_t (&cw)[D / 32], int (&zg)[Halves<D, G>::GL],
                                      float (&sg)[Halves<D, G>::GL], int (&cg)[Halves<D, G>::GL], float& sig,
                                      F each, FC chunk) {
   using H = Halves<D, G>;
   constexpr int GL = H::GL, GC = H::GC;
+  forget(xh);
   float glo[GL];
   auto range = [&](auto gi, float& lo, float& hi) {
     constexpr int gl = decltype(gi)::value;
@@ -160,7 +162,7 @@ __device__ inline void residual_half(const float (&x)[D / 2], const uint4* __res
       const uint4 mu = mrow[c0 / 8];
       static_for<0, 8>([&](auto ki) {
         constexpr int k = decltype(ki)::value;
-        const float r = x[c0 + k] - bf_el<k>(mu);
+        const float r = bf_el<k>(xh[c0 / 8]) - bf_el<k>(mu);
         lo = fminf(lo, r);
         hi = fmaxf(hi, r);
       });
@@ -172,6 +174,10 @@ __device__ inline void residual_half(const float (&x)[D / 2], const uint4* __res
   };
   auto codes = [&](auto gi) {
     constexpr int gl = decltype(gi)::value;
+    // unpack the token words and re-read the centroid words here rather than keep
+    // the range pass's unpacked values live
+    forget(xh);
+    asm volatile("" ::: "memory");
     const float s = sg[gl];
     const float sd = s != 0.0f ? s : 1.0f;
     const int z = s != 0.0f ? (int)fminf(fmaxf(rintf(0.0f - glo[gl] / sd), 0.0f), 3.0f) : 0;
@@ -183,7 +189,7 @@ __device__ inline void residual_half(const float (&x)[D / 2], const uint4* __res
       const uint4 m0 = mrow[c0 / 8];
       static_for<0, 8>([&](auto ki) {
         constexpr int k = decltype(ki)::value;
-        xv[k] = x[c0 + k];
+        xv[k] = bf_el<k>(xh[c0 / 8]);
         mu[k] = bf_el<k>(m0);
       });
       round_quotients<8>(xv, mu, s, inv, t);
@@ -297,15 +303,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
   const int64_t b = bh / a.heads, h = bh % a.heads;
   const uint8_t* slab = a.calib + bh * a.slab;
 
-  // U_r ([d][rs] fp32) in LDS: the lanes of one half read the same row
-  __shared__ float s_u[RP > 0 ? D * RP : 1];
-  __shared__ float s_err[RP > 0 ? 256 * 9 : 1];  // per thread: one chunk's 8 errors (stride 9)
-  float* my_err = s_err + threadIdx.x * 9;
-  if constexpr (RP > 0) {
-    const float4* u4 = reinterpret_cast<const float4*>(slab + a.o_u_dr);
-    for (int i = threadIdx.x; i < D * RP / 4; i += 256) reinterpret_cast<float4*>(s_u)[i] = u4[i];
-    __syncthreads();
-  }
   const int64_t t0 = tb * kBlockTokens + wv * kWaveTokens;
   if (t0 >= a.n_new) return;  // the whole wave is past the chunk
   const int64_t t = t0 + n;
@@ -338,19 +335,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[i] = bk[min(j0 + acc_row(i, hf), Kc - 1)];
       const uint4* arow = reinterpret_cast<const uint4*>(planes + int64_t(min(j0 + n, Kc - 1)) * D + hf * DH);
-      // two steps' fragments in flight: step s + 1 loads while step s multiplies
-      uint4 af[2][3];
+      // three steps' fragments in flight: steps s + 1 and s + 2 load while step s multiplies
+      uint4 af[3][3];
 #pragma unroll
       for (int pl = 0; pl < 3; ++pl) af[0][pl] = arow[pl * (KD / 8)];
+#pragma unroll
+      for (int pl = 0; pl < 3; ++pl) af[1][pl] = arow[pl * (KD / 8) + 1];
       static_for<0, NS>([&](auto si) {
         constexpr int st = decltype(si)::value;
-        if constexpr (st + 1 < NS) {
+        if constexpr (st + 2 < NS) {
 #pragma unroll
-          for (int pl = 0; pl < 3; ++pl) af[(st + 1) & 1][pl] = arow[pl * (KD / 8) + st + 1];
+          for (int pl = 0; pl < 3; ++pl) af[(st + 2) % 3][pl] = arow[pl * (KD / 8) + st + 2];
         }
 #pragma unroll
         for (int pl = 0; pl < 3; ++pl)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(af[st & 1][pl]), as_frag(xk[st]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(af[st % 3][pl]), as_frag(xk[st]), acc, 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
       });
 #pragma unroll
@@ -361,8 +360,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     }
   }
   merge_pair<MM>(bd, bi, hf);
-  float x[DH];
-  unpack<DH>(xk, x);
 
   // ---- QSAC score (Eq. 10, 12) over the M candidates; ties to the lower id
   const bf16* __restrict__ muk = reinterpret_cast<const bf16*>(slab + a.o_mu_k);
@@ -386,7 +383,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
         const uint4 mu = mrow[c0 / 8];
         static_for<0, 8>([&](auto ki) {
           constexpr int k = decltype(ki)::value;
-          const float r = x[c0 + k] - bf_el<k>(mu);
+          const float r = bf_el<k>(xk[c0 / 8]) - bf_el<k>(mu);
           mx = fmaxf(mx, r);
           mn = fminf(mn, r);
         });
@@ -415,49 +412,72 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     z = better ? j : z;
   });
 
-  // ---- Keys: INT2 residual against mu_z, PSAC accumulated channel by channel:
-  // E_c = k_c - khat_0,c (Eq. 13), C_k += E_c U_ck (Eq. 16); INT8 rows with one
-  // FP16 scale (App. D.1)
+  // ---- Keys: INT2 residual against mu_z, and PSAC (Eq. 13, 16): C = E U_r with
+  // E_c = k_c - khat_0,c, on the matrix cores. Each residual chunk is the lane's
+  // 8 channels of one k step, so its errors are the B operand as they are made:
+  // split into three BF16 parts with an exact sum (as the Key search constants)
+  // against the BF16 rows of U_r^T (rank m = lane % 32; zero rows past r), every
+  // product is exact and the fp32 accumulator holds ranks acc_row(i, hf).
+  // INT8 rows with one FP16 scale (App. D.1).
   {
     const uint4* mrow = reinterpret_cast<const uint4*>(muk + int64_t(z) * D + hf * DH);
-    float C[RP > 0 ? RP : 1];
+    const bf16* __restrict__ ut = reinterpret_cast<const bf16*>(slab + a.o_u_t);
+    const int r = a.rank;
+    const uint4* urow = reinterpret_cast<const uint4*>(ut + int64_t(min(n, r > 0 ? r - 1 : 0)) * D + hf * DH);
+    const bool urank = n < r;
+    f32x16 cacc;
 #pragma unroll
-    for (int k = 0; k < (RP > 0 ? RP : 1); ++k) C[k] = 0.0f;
+    for (int i = 0; i < 16; ++i) cacc[i] = 0.0f;
+    float ech[8];
     uint32_t cw[D / 32];
     int zg[GL], cg[GL];
     float sg[GL], sig = 0.0f;
-    // The errors of one 8-channel chunk go to this thread's LDS row, and a rolled
-    // loop over them adds e_c U_r[c, :] to C. Unrolled over the half-row, the
-    // compiler hoists the U_r loads of every channel and spills.
     residual_half<D, G, SI8>(
-        x, mrow, hf, cw, zg, sg, cg, sig,
+        xk, mrow, hf, cw, zg, sg, cg, sig,
         [&](int k, float e) {
-          if constexpr (RP > 0) my_err[k] = e;
+          if constexpr (RP > 0) ech[k] = e;
         },
         [&](int c0) {
           if constexpr (RP > 0) {
-#pragma nounroll
-            for (int k = 0; k < 8; ++k) {
-              const float e = my_err[k];
-              const float4* ur = reinterpret_cast<const float4*>(s_u + (hf * DH + c0 + k) * RP);
+            uint4 uf = urow[c0 / 8];
+            if (!urank) uf = make_uint4(0u, 0u, 0u, 0u);
+            uint32_t p0[4], p1[4], p2[4];
 #pragma unroll
-              for (int k4 = 0; k4 < RP / 4; ++k4) {
-                const float4 u = ur[k4];
-                C[4 * k4] = __builtin_fmaf(e, u.x, C[4 * k4]);
-                C[4 * k4 + 1] = __builtin_fmaf(e, u.y, C[4 * k4 + 1]);
-                C[4 * k4 + 2] = __builtin_fmaf(e, u.z, C[4 * k4 + 2]);
-                C[4 * k4 + 3] = __builtin_fmaf(e, u.w, C[4 * k4 + 3]);
+            for (int q = 0; q < 4; ++q) {
+              uint32_t w0[2], w1[2], w2[2];
+#pragma unroll
+              for (int u = 0; u < 2; ++u) {
+                const float e = ech[2 * q + u];
+                w0[u] = __float_as_uint(e) & 0xffff0000u;
+                const float r1 = e - __uint_as_float(w0[u]);
+                w1[u] = __float_as_uint(r1) & 0xffff0000u;
+                w2[u] = __float_as_uint(r1 - __uint_as_float(w1[u])) & 0xffff0000u;
               }
+              p0[q] = w0[1] | (w0[0] >> 16);
+              p1[q] = w1[1] | (w1[0] >> 16);
+              p2[q] = w2[1] | (w2[0] >> 16);
             }
+            cacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(uf), as_frag(make_uint4(p0[0], p0[1], p0[2], p0[3])),
+                                                           cacc, 0, 0, 0);
+            cacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(uf), as_frag(make_uint4(p1[0], p1[1], p1[2], p1[3])),
+                                                           cacc, 0, 0, 0);
+            cacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(uf), as_frag(make_uint4(p2[0], p2[1], p2[2], p2[3])),
+                                                           cacc, 0, 0, 0);
           }
         });
     store_half<D, G, SI8>(a.L, a.cache, a.L.k_codes, a.L.k_ids, a.L.k_zp, a.L.k_scale, a.L.k_sigma, slot, hf,
                           active, z, cw, zg, sg, cg, sig);
     if constexpr (RP > 0) {
-      // the two halves' partial sums; a + b and b + a are the same float
+      // C in rank order on both lanes: rank k sits in slot (k / 8) * 4 + k % 4 of
+      // lane half (k / 4) % 2
+      float pc[RP / 2], C[RP];
 #pragma unroll
-      for (int k = 0; k < RP; ++k) C[k] = C[k] + partner(C[k], hf);
-      const int r = a.rank;
+      for (int i = 0; i < RP / 2; ++i) pc[i] = partner(cacc[i], hf);
+#pragma unroll
+      for (int k = 0; k < RP; ++k) {
+        const int i = (k / 8) * 4 + k % 4;
+        C[k] = ((k / 4) % 2 == hf) ? cacc[i] : pc[i];
+      }
       float amax = 0.0f;
 #pragma unroll
       for (int k = 0; k < RP; ++k)
@@ -542,12 +562,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[i] = -0.5f * bv[min(j0 + acc_row(i, hf), Kc - 1)];
       const uint4* arow = reinterpret_cast<const uint4*>(muv + int64_t(min(j0 + n, Kc - 1)) * D + hf * DH);
-      uint4 af[2];
+      uint4 af[4];
       af[0] = arow[0];
+      af[1] = arow[1];
+      af[2] = arow[2];
       static_for<0, NS>([&](auto si) {
         constexpr int st = decltype(si)::value;
-        if constexpr (st + 1 < NS) af[(st + 1) & 1] = arow[st + 1];
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(af[st & 1]), as_frag(xv[st]), acc, 0, 0, 0);
+        if constexpr (st + 3 < NS) af[(st + 3) % 4] = arow[st + 3];
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(af[st % 4]), as_frag(xv[st]), acc, 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
       });
 #pragma unroll
@@ -570,8 +592,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     uint32_t cw[D / 32];
     int zg[GL], cg[GL];
     float sg[GL], sig = 0.0f;
-    unpack<DH>(xv, x);
-    residual_half<D, G, SI8>(x, mrow, hf, cw, zg, sg, cg, sig, [](int, float) {}, [](int) {});
+    residual_half<D, G, SI8>(xv, mrow, hf, cw, zg, sg, cg, sig, [](int, float) {}, [](int) {});
     store_half<D, G, SI8>(a.L, a.cache, a.L.v_codes, a.L.v_ids, a.L.v_zp, a.L.v_scale, a.L.v_sigma, slot, hf,
                           active, zv, cw, zg, sg, cg, sig);
   }
