@@ -655,6 +655,9 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
   // Query and key positions fit in 32 bits (the host rejects larger calls)
   const int qi = int(qa) + (producer ? 0 : wave) * 32 + l32;
   const bool qvalid = !producer && qi < a.n_q;
+  // a consumer wave of the last Query block whose 32 Queries all lie past n_q
+  // (wave-uniform): it keeps the barriers of every tile and computes nothing
+  const bool idle = !producer && qa + int64_t(wave) * 32 >= a.n_q;
   V qreg[D / KSTEP];
   V ureg[RP > 0 ? RP / KSTEP : 1];   // q U_r of epoch ue
   int ue = se;
@@ -822,6 +825,7 @@ __global__ __launch_bounds__(NT) void attend_kernel(const AttendArgs a) {
         }
       }
     }
+    if (idle) return;
     const T* kt = smem + tile0 + int(it & 1) * LY::tile_elems;
     const T* ct = kt + KT * LY::KS;
     const T* vt = ct + KT * LY::CS;
