@@ -242,7 +242,14 @@ D128G16 = synth.Workload(name="d128-g16", dtype="bf16", batch=1, heads=3, head_d
                          q_start=460, frame_tokens=38, n_centroids=20, group_size=16, rank=12, top_m=4, q_rank=8,
                          n_out=4, out_scale=10.0, n_hist=400, chunk=325, seed=13)
 
-SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC, F32D128, D128G16]
+# BF16 d = 64 with G = 64: the one group spans both lane halves of the BF16
+# append kernel (ranges and the 8-bit scales' maximum combined across the pair);
+# r = 16 fills the rank padding, so the coefficient rows take the word stores
+D64G64 = synth.Workload(name="d64-g64", dtype="bf16", batch=1, heads=2, head_dim=64, n_cache=600, n_q=150,
+                        q_start=450, frame_tokens=30, n_centroids=40, group_size=64, rank=16, top_m=4, q_rank=6,
+                        n_out=2, out_scale=10.0, n_hist=400, chunk=300, seed=14)
+
+SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC, F32D128, D128G16, D64G64]
 FULL = ["mg2-12h", "lingbot-40h", "batched-4x30h", "rollout-30k", "rollout-60k", "rollout-120k"]
 
 # App. D.1 storage options: 8-bit group scales (I8), the retention gate, both.
@@ -255,7 +262,8 @@ STORAGE = [synth.scaled(synth.WORKLOADS["tiny-f32"], name="tiny-f32-i8", storage
            synth.scaled(D64, name="d64-gate", storage=_GATE),
            synth.scaled(NOPSAC, name="g64-r0-i8-gate", storage=_I8 | _GATE),
            synth.scaled(D128G16, name="d128-g16-i8-gate", storage=_I8 | _GATE),
-           synth.scaled(F32D128, name="f32-d128-i8", storage=_I8)]
+           synth.scaled(F32D128, name="f32-d128-i8", storage=_I8),
+           synth.scaled(D64G64, name="d64-g64-i8-gate", storage=_I8 | _GATE)]
 
 # The full quadratic QSAC metric (the diagonal-approximation ablation of App. C):
 # fp32 d = 64, bf16 with batch 2 and ragged tiles, M = 8 over a small Kc, and
