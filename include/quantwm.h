@@ -225,9 +225,18 @@ quantwm_status quantwm_calibrate_epoch(const quantwm_config* cfg, const void* st
  *    zero-point (Eq. 1-2, range extended to contain 0); PSAC stores
  *    C = (k - khat_0) U_r (Eq. 13, 16) as INT8 with an FP16 row scale.
  *  - Values: nearest centroid and the same INT2 residual, no PSAC.
+ * The Eq. 9 search uses the expanded distance b_j + sum_c a_jc k_c in fp32.
+ * With BF16 data it and the PSAC product run on matrix cores, with each fp32
+ * operand split into three BF16 parts whose sum is exact: the products are
+ * exact and only the order of the fp32 sums differs from a channel-order
+ * evaluation, so a centroid id can differ from an exact-arithmetic choice only
+ * where two distances tie to fp32 rounding. Integer decisions after the
+ * search (Eq. 12 score, INT2 and INT8 codes) follow the equations' order in
+ * fp32 with IEEE division and round-to-nearest-even.
  * k_new, v_new: [B,n_new,H,d] dtype. coef_f32_out: optional [B,H,n_new,r] f32
  * copy of C before INT8 rounding. n_new == 0 is a no-op. Needs
- * n_cached + n_new <= capacity. */
+ * n_cached + n_new <= capacity; with BF16 data, ceil(n_new / 128) * B * H must
+ * be below 2^24 (QWM_ERR_UNSUPPORTED otherwise). */
 quantwm_status quantwm_append(const quantwm_config* cfg, const void* calib, void* cache,
                               int64_t n_cached, const void* k_new, const void* v_new,
                               int64_t n_new, float* coef_f32_out, void* stream);

@@ -149,6 +149,13 @@ def test_validation_without_a_gpu():
         qw._check(qw.library().quantwm_append(ctypes.byref(good), ctypes.c_void_p(0x1008), ctypes.c_void_p(0x2000),
                                               0, ctypes.c_void_p(0x3000), ctypes.c_void_p(0x4000), 5, None, None))
     assert "aligned" in qw.quantwm_last_error()
+    # the BF16 append launches one workgroup per 128 tokens of a (b, h): a call
+    # of 2^24 workgroups or more is refused before any device work
+    big = qw.make_config(64, 2048, 128, 16, 32, 8, 4, 1 << 14, "bf16")
+    dev = [ctypes.c_void_p(0x1000 * (i + 1)) for i in range(4)]
+    with pytest.raises(qw.QuantwmError) as e:
+        qw._check(qw.library().quantwm_append(ctypes.byref(big), dev[0], dev[1], 0, dev[2], dev[3], 1 << 14, None, None))
+    assert e.value.status == qw.ERR_UNSUPPORTED and "2^24" in qw.quantwm_last_error()
     with pytest.raises(qw.QuantwmError) as e:
         qw._check(qw.library().quantwm_attend(ctypes.byref(good), None, None, 50, None, 4, 60, 1, None, None, None, 0, None))
     assert e.value.status == qw.ERR_INVALID_ARG
