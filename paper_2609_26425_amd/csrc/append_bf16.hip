@@ -335,21 +335,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[i] = bk[min(j0 + acc_row(i, hf), Kc - 1)];
       const uint4* arow = reinterpret_cast<const uint4*>(planes + int64_t(min(j0 + n, Kc - 1)) * D + hf * DH);
-      // three steps' fragments in flight: steps s + 1 and s + 2 load while step s multiplies
-      uint4 af[3][3];
+      // five steps' fragments in flight: steps s + 1 .. s + 4 load while step s multiplies
+      constexpr int PF = 5;
+      uint4 af[PF][3];
+      static_for<0, (PF - 1 < NS ? PF - 1 : NS)>([&](auto pi) {
+        constexpr int st = decltype(pi)::value;
 #pragma unroll
-      for (int pl = 0; pl < 3; ++pl) af[0][pl] = arow[pl * (KD / 8)];
-#pragma unroll
-      for (int pl = 0; pl < 3; ++pl) af[1][pl] = arow[pl * (KD / 8) + 1];
+        for (int pl = 0; pl < 3; ++pl) af[st][pl] = arow[pl * (KD / 8) + st];
+      });
       static_for<0, NS>([&](auto si) {
         constexpr int st = decltype(si)::value;
-        if constexpr (st + 2 < NS) {
+        if constexpr (st + PF - 1 < NS) {
 #pragma unroll
-          for (int pl = 0; pl < 3; ++pl) af[(st + 2) % 3][pl] = arow[pl * (KD / 8) + st + 2];
+          for (int pl = 0; pl < 3; ++pl) af[(st + PF - 1) % PF][pl] = arow[pl * (KD / 8) + st + PF - 1];
         }
 #pragma unroll
         for (int pl = 0; pl < 3; ++pl)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(af[st % 3][pl]), as_frag(xk[st]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(af[st % PF][pl]), as_frag(xk[st]), acc, 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
       });
 #pragma unroll
@@ -562,16 +564,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[i] = -0.5f * bv[min(j0 + acc_row(i, hf), Kc - 1)];
       const uint4* arow = reinterpret_cast<const uint4*>(muv + int64_t(min(j0 + n, Kc - 1)) * D + hf * DH);
-      uint4 af[4];
-      af[0] = arow[0];
-      af[1] = arow[1];
-      af[2] = arow[2];
-      static_for<0, NS>([&](auto si) {
-        constexpr int st = decltype(si)::value;
-        if constexpr (st + 3 < NS) af[(st + 3) % 4] = arow[st + 3];
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(af[st % 4]), as_frag(xv[st]), acc, 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      });
+      // the block's fragments all load at once (one per step)
+      uint4 af[NS];
+#pragma unroll
+      for (int st = 0; st < NS; ++st) af[st] = arow[st];
+#pragma unroll
+      for (int st = 0; st < NS; ++st)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_frag(af[st]), as_frag(xv[st]), acc, 0, 0, 0);
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int j = j0 + acc_row(i, hf);
