@@ -28,11 +28,14 @@
 // its two lists, both lanes ending with the same M candidates.
 //
 // Residual and PSAC. Each lane quantises its half-row. Group ranges of a group
-// that spans both halves, the 8-bit scales' shared maximum, the Eq. 12 sum over
-// groups (added in group order) and the PSAC partial sums are combined across
-// the pair with v_permlane32_swap. Everything that turns a float into an
-// integer follows the equations' operation order in fp32 with IEEE division and
-// round-to-nearest-even, as in the fp32 kernel.
+// that spans both halves, the 8-bit scales' shared maximum and the Eq. 12 sum
+// over groups (added in group order) are combined across the pair with
+// v_permlane32_swap. The PSAC projection E U_r runs on the matrix cores as
+// well: the errors of each 8-channel residual chunk are the B operand of one k
+// step, and one exchange puts the coefficients in rank order on both lanes.
+// Everything that turns a float into an integer follows the equations'
+// operation order in fp32 with IEEE division and round-to-nearest-even, as in
+// the fp32 kernel.
 #include "append_common.h"
 #include "xcd_order.h"
 
