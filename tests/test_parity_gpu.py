@@ -379,6 +379,18 @@ def _slab_field(cfg, buf, bh, name, count, dtype):
     return np.frombuffer(buf[off:off + nbytes].tobytes(), dtype=dtype)
 
 
+def _check_search_planes(cfg, buf, bh, K, d):
+    """The BF16 planes of the Key search constants: the first two truncate, the
+    third is the remainder, and their sum is a_k exactly."""
+    a = _slab_field(cfg, buf, bh, "a_k", K * d, np.float32)
+    pl = _slab_field(cfg, buf, bh, "a_k3", 3 * K * d, np.uint16).reshape(3, K * d)
+    p = (pl.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    np.testing.assert_array_equal(p[0] + p[1] + p[2], a.astype(np.float64), err_msg=f"a_k planes head {bh}")
+    np.testing.assert_array_equal(pl[0], a.view(np.uint32) >> 16, err_msg=f"first plane head {bh}")
+    r1 = a - p[0].astype(np.float32)
+    np.testing.assert_array_equal(pl[1], r1.view(np.uint32) >> 16, err_msg=f"second plane head {bh}")
+
+
 @pytest.mark.parametrize("name", ["tiny-f32", "ragged", "mg2-12h"])
 def test_calibrate_parity(name):
     wl = {"ragged": RAGGED}.get(name) or synth.WORKLOADS[name]
@@ -399,6 +411,8 @@ def test_calibrate_parity(name):
         np.testing.assert_array_equal(mv.reshape(K, d), case.tables[1][0, s], err_msg=f"mu_v head {bh}")
         w = _slab_field(cfg, buf, bh, "w", d, np.float32)
         np.testing.assert_array_equal(w, case.tables[2][0, s], err_msg=f"w head {bh}")
+        if bf:
+            _check_search_planes(cfg, buf, bh, K, d)
         if r > 0:
             lam = _slab_field(cfg, buf, bh, "lam", r, np.float32)
             np.testing.assert_allclose(lam, case.tables[4][0, s], rtol=1e-6)
@@ -425,6 +439,8 @@ def test_calibrate_full_metric_parity():
         m = _slab_field(cfg, buf, bh, "m", d * d, np.float32).reshape(d, d)
         np.testing.assert_array_equal(m, case.tables[5][0, s], err_msg=f"m head {bh}")
         np.testing.assert_array_equal(np.diag(m), _slab_field(cfg, buf, bh, "w", d, np.float32))
+        if wl.dtype == "bf16":
+            _check_search_planes(cfg, buf, bh, wl.n_centroids, d)  # a_k = -2 Mn mu here
     k = tdev(synth.tensor(wl, "k", 64), cfg.torch_dtype)
     calib = torch.zeros(qw.quantwm_calib_bytes(cfg), dtype=torch.uint8, device=DEV)
     ws = torch.empty(qw.quantwm_calibrate_workspace_bytes(cfg, 0, 64), dtype=torch.uint8, device=DEV)
