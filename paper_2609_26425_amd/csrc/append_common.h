@@ -39,14 +39,18 @@ __device__ inline uint16_t f16_bits(float exact) {
 template <int N>
 __device__ inline void round_quotients(const float (&xv)[N], const float (&mu)[N], float s, float inv,
                                        float (&t)[N]) {
-  bool near = false;
+  // the largest |q - k| and |q| of the chunk decide it: two compares instead of
+  // two per channel, each of which fed a scalar OR chain
+  float dmax = 0.0f, qmax = 0.0f;
 #pragma unroll
   for (int c = 0; c < N; ++c) {
     const float q = (xv[c] - mu[c]) * inv;
     const float k = rintf(q);
-    near |= fabsf(q - k) > 0.5f - 0x1p-19f || fabsf(q) > 4.0f;
+    dmax = fmaxf(dmax, fabsf(q - k));
+    qmax = fmaxf(qmax, fabsf(q));
     t[c] = k;
   }
+  const bool near = dmax > 0.5f - 0x1p-19f || qmax > 4.0f;
   if (__any(near)) {
     const float sd = s != 0.0f ? s : 1.0f;
 #pragma unroll
