@@ -191,9 +191,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
   // ---- QSAC candidate search (Eq. 9, expanded form), top-M by (d', id)
   float bd[MM];
   int bi[MM];
-#pragma unroll
   // ids start at 0, a valid row: with an infinite or NaN distance (inputs out of
   // range) nothing enters the list, and the score below still reads real rows
+#pragma unroll
   for (int p = 0; p < MM; ++p) { bd[p] = __builtin_inff(); bi[p] = 0; }
   for (int j = 0; j < Kc; j += 4) {
     float acc[4];

@@ -325,9 +325,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
   }
   float bd[MM];
   int bi[MM];
-#pragma unroll
   // ids start at 0, a valid row: with an infinite or NaN distance (inputs out of
   // range) nothing enters the list, and the score below still reads real rows
+#pragma unroll
   for (int p = 0; p < MM; ++p) { bd[p] = __builtin_inff(); bi[p] = 0; }
   {
     const float* __restrict__ bk = reinterpret_cast<const float*>(slab + a.o_b_k);
