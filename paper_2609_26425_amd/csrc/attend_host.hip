@@ -8,8 +8,10 @@ namespace {
 
 // Merges the n_split partial results of every Query: with M the largest running
 // max and w_s = 2^((m_s - M) log2(e) / sqrt(d)), O = sum w_s O_s / sum w_s l_s
-// and lse = M / sqrt(d) + log(sum w_s l_s). One wave per Query, D / 64 channels
-// per lane.
+// and lse = M / sqrt(d) + log(sum w_s l_s), the sums taken in split order. One
+// wave per Query, D / 64 contiguous channels per lane. The planes are read four
+// splits per trip so that their loads are in flight together (a split count
+// known only at run time otherwise leaves one split's loads in flight at a time).
 template <typename T, int D>
 __global__ __launch_bounds__(256) void attend_combine(const AttendArgs a) {
   const int64_t qi = int64_t(blockIdx.x) * 4 + threadIdx.x / 64;
@@ -19,26 +21,39 @@ __global__ __launch_bounds__(256) void attend_combine(const AttendArgs a) {
   const int64_t bh = int64_t(b) * a.heads + h;
   const int64_t plane = int64_t(a.heads) * gridDim.z * a.n_q;  // rows per split
   const float mscale = 1.4426950408889634f / sqrtf((float)D);
-  float M = -__builtin_inff();
-  for (int sp = 0; sp < a.n_split; ++sp) M = fmaxf(M, a.part_ml[2 * (sp * plane + bh * a.n_q + qi)]);
   constexpr int PL = D / 64;
-  float o[PL];
-#pragma unroll
-  for (int j = 0; j < PL; ++j) o[j] = 0.0f;
+  typedef float vecf __attribute__((ext_vector_type(PL)));
+  const float2* ml = reinterpret_cast<const float2*>(a.part_ml);
+  float M = -__builtin_inff();
+  for (int sp = 0; sp < a.n_split; ++sp) M = fmaxf(M, ml[sp * plane + bh * a.n_q + qi].x);
+  vecf o = {};
   float L = 0.0f;
-  for (int sp = 0; sp < a.n_split; ++sp) {
-    const int64_t row = sp * plane + bh * a.n_q + qi;
-    const float m = a.part_ml[2 * row], l = a.part_ml[2 * row + 1];
-    if (!(l > 0.0f)) continue;  // this split saw no visible key of this Query
-    const float w = __builtin_amdgcn_exp2f((m - M) * mscale);
-    L += w * l;
+  auto add = [&](const float2 p, const vecf v) __attribute__((always_inline)) {
+    if (!(p.y > 0.0f)) return;  // this split saw no visible key of this Query
+    const float w = __builtin_amdgcn_exp2f((p.x - M) * mscale);
+    L += w * p.y;
 #pragma unroll
-    for (int j = 0; j < PL; ++j) o[j] += w * a.part_o[row * D + j * 64 + lane];
+    for (int j = 0; j < PL; ++j) o[j] += w * v[j];
+  };
+  auto row_of = [&](int sp) { return sp * plane + bh * a.n_q + qi; };
+  auto vals = [&](int sp) { return *reinterpret_cast<const vecf*>(a.part_o + row_of(sp) * D + lane * PL); };
+  int sp = 0;
+  for (; sp + 4 <= a.n_split; sp += 4) {
+    float2 p[4];
+    vecf v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      p[u] = ml[row_of(sp + u)];
+      v[u] = vals(sp + u);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) add(p[u], v[u]);
   }
+  for (; sp < a.n_split; ++sp) add(ml[row_of(sp)], vals(sp));
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-  T* orow = reinterpret_cast<T*>(a.out) + ((int64_t(b) * a.n_q + qi) * a.heads + h) * D;
+  T* orow = reinterpret_cast<T*>(a.out) + ((int64_t(b) * a.n_q + qi) * a.heads + h) * D + lane * PL;
 #pragma unroll
-  for (int j = 0; j < PL; ++j) orow[j * 64 + lane] = T(o[j] * inv);
+  for (int j = 0; j < PL; ++j) orow[j] = T(o[j] * inv);
   if (a.lse && lane == 0) a.lse[bh * a.n_q + qi] = L > 0.0f ? M / sqrtf((float)D) + logf(L) : -__builtin_inff();
 }
 
