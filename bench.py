@@ -74,7 +74,7 @@ def append_flops(wl, n_new) -> float:
 
 
 # the device-code sources of each kernel (their digest dates a counter summary)
-KERNEL_SOURCES = {"attend": ["attend.hip", "attend_shape.h", "qwm_common.h", "xcd_order.h"],
+KERNEL_SOURCES = {"attend": ["attend.hip", "attend_host.hip", "attend_shape.h", "qwm_common.h", "xcd_order.h"],
                   "append": ["append_bf16.hip", "append.hip", "append_common.h", "qwm_common.h", "xcd_order.h"]}
 
 
