@@ -249,7 +249,13 @@ D64G64 = synth.Workload(name="d64-g64", dtype="bf16", batch=1, heads=2, head_dim
                         q_start=450, frame_tokens=30, n_centroids=40, group_size=64, rank=16, top_m=4, q_rank=6,
                         n_out=2, out_scale=10.0, n_hist=400, chunk=300, seed=14)
 
-SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC, F32D128, D128G16, D64G64]
+# BF16 appends of 8 tokens (one partial wave per call: most lanes recompute a
+# real token and store nothing) and Kc = 16, half of a 32-centroid block
+SMALLCHUNK = synth.Workload(name="bf16-chunk8-kc16", dtype="bf16", batch=2, heads=2, head_dim=128, n_cache=200,
+                            n_q=40, q_start=160, frame_tokens=8, n_centroids=16, group_size=32, rank=8, top_m=2,
+                            q_rank=4, n_out=2, out_scale=10.0, n_hist=200, chunk=8, seed=15)
+
+SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC, F32D128, D128G16, D64G64, SMALLCHUNK]
 FULL = ["mg2-12h", "lingbot-40h", "batched-4x30h", "rollout-30k", "rollout-60k", "rollout-120k"]
 
 # App. D.1 storage options: 8-bit group scales (I8), the retention gate, both.
