@@ -255,7 +255,17 @@ SMALLCHUNK = synth.Workload(name="bf16-chunk8-kc16", dtype="bf16", batch=2, head
                             n_q=40, q_start=160, frame_tokens=8, n_centroids=16, group_size=32, rank=8, top_m=2,
                             q_rank=4, n_out=2, out_scale=10.0, n_hist=200, chunk=8, seed=15)
 
-SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC, F32D128, D128G16, D64G64, SMALLCHUNK]
+# BF16 centroid tables too large for LDS (d = 128 with Kc = 256 at r = 32 and
+# Kc = 192 at r = 12): the attention instances whose producers read the
+# centroid rows from global memory, at small sizes with ragged Query blocks
+KC256 = synth.Workload(name="d128-kc256", dtype="bf16", batch=2, heads=2, head_dim=128, n_cache=900, n_q=300,
+                       q_start=600, frame_tokens=60, n_centroids=256, group_size=64, rank=32, top_m=4, q_rank=8,
+                       n_out=8, out_scale=20.0, n_hist=600, chunk=450, seed=16)
+KC192 = synth.Workload(name="d128-kc192", dtype="bf16", batch=1, heads=3, head_dim=128, n_cache=1100, n_q=260,
+                       q_start=840, frame_tokens=52, n_centroids=192, group_size=32, rank=12, top_m=4, q_rank=6,
+                       n_out=4, out_scale=10.0, n_hist=800, chunk=550, seed=17)
+
+SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC, F32D128, D128G16, D64G64, SMALLCHUNK, KC256, KC192]
 FULL = ["mg2-12h", "lingbot-40h", "batched-4x30h", "rollout-30k", "rollout-60k", "rollout-120k"]
 
 # App. D.1 storage options: 8-bit group scales (I8), the retention gate, both.
