@@ -267,12 +267,20 @@ KC192 = synth.Workload(name="d128-kc192", dtype="bf16", batch=1, heads=3, head_d
 
 SMALL = [synth.WORKLOADS["tiny-f32"], RAGGED, D64, NOPSAC, F32D128, D128G16, D64G64, SMALLCHUNK, KC256, KC192]
 
-# two workgroups for a 320-tile key range: the launch splits the keys 16 ways
-# (the most the split rule takes), so the combine merges four full groups of
-# four partial results per Query
-MANYSPLIT = synth.Workload(name="d128-split16", dtype="bf16", batch=1, heads=2, head_dim=128, n_cache=20480,
-                           n_q=96, q_start=20384, frame_tokens=32, n_centroids=32, group_size=32, rank=8,
-                           top_m=4, q_rank=4, n_out=4, out_scale=10.0, n_hist=1024, chunk=4096, seed=18)
+# two workgroups for a key range of 200 or more tiles: the launch splits the
+# keys 16 ways (the most the split rule takes), so the combine merges four full
+# groups of four partial results per Query (d = 128 and d = 64, BF16 and fp32)
+MANYSPLIT = [
+    synth.Workload(name="d128-split16", dtype="bf16", batch=1, heads=2, head_dim=128, n_cache=20480,
+                   n_q=96, q_start=20384, frame_tokens=32, n_centroids=32, group_size=32, rank=8,
+                   top_m=4, q_rank=4, n_out=4, out_scale=10.0, n_hist=1024, chunk=4096, seed=18),
+    synth.Workload(name="d64-split16", dtype="bf16", batch=1, heads=2, head_dim=64, n_cache=12800,
+                   n_q=40, q_start=12760, frame_tokens=20, n_centroids=24, group_size=16, rank=4,
+                   top_m=4, q_rank=4, n_out=2, out_scale=10.0, n_hist=1024, chunk=3200, seed=19),
+    synth.Workload(name="f32-d64-split16", dtype="f32", batch=1, heads=2, head_dim=64, n_cache=12800,
+                   n_q=40, q_start=12760, frame_tokens=20, n_centroids=24, group_size=32, rank=4,
+                   top_m=4, q_rank=4, n_out=2, out_scale=10.0, n_hist=1024, chunk=3200, seed=20),
+]
 FULL = ["mg2-12h", "lingbot-40h", "batched-4x30h", "rollout-30k", "rollout-60k", "rollout-120k"]
 
 # App. D.1 storage options: 8-bit group scales (I8), the retention gate, both.
@@ -354,8 +362,8 @@ def test_small_parity(wl):
     run_case(wl, max_sources=64, n_heads_rows=64, row_step=1, logits_rows=wl.n_q)
 
 
-def test_many_key_splits_parity():
-    wl = MANYSPLIT
+@pytest.mark.parametrize("wl", MANYSPLIT, ids=[w.name for w in MANYSPLIT])
+def test_many_key_splits_parity(wl):
     cfg = gpu_config(wl)
     nb = qw.quantwm_attend_workspace_bytes(cfg, wl.n_cache, wl.n_q)
     splits = nb // (wl.batch * wl.heads * wl.n_q * (4 * wl.head_dim + 8))
